@@ -1,0 +1,142 @@
+/*
+ * tlc.h -- C ABI of the MI355X (gfx950) 3LC compression library.
+ *
+ * 3LC compresses one fp32 state-change tensor (a gradient push or a model
+ * delta pull) per call, as described in the paper "3LC: Lightweight and
+ * Effective Traffic Compression for Distributed Machine Learning":
+ *
+ *   encode (Section 3.1, Fig. 3; Sections 3.2 and 3.3)
+ *     acc = tensor + residual                        error accumulation
+ *     M   = max|acc| * s,  1 <= s < 2                Eq. 1
+ *     q   = round(acc / M) in {-1, 0, 1}             Eq. 2 (half to even)
+ *     residual = acc - M*q                           steps a and b
+ *     Q   = quartic encoding of q + 1                Section 3.2
+ *     C   = zero-run encoding of Q                   Section 3.3
+ *   decode
+ *     Q = zero-run expansion of C; q = quartic decoding of Q;
+ *     out = M*q (Eq. 3)  or  out += M*q (aggregation at a server).
+ *
+ * The payload of one call is the byte string C plus the fp32 scalar M.
+ *
+ * Layout conventions (bit-exact contract):
+ *   - m = ceil(n/5) quartic bytes.  The n values are padded with trit 0 to
+ *     5m and split into five CONTIGUOUS partitions p_k = [k*m, (k+1)*m);
+ *     byte j = 81*t(j) + 27*t(m+j) + 9*t(2m+j) + 3*t(3m+j) + t(4m+j).
+ *   - A run of L bytes equal to 121 becomes floor(L/14) bytes 255, then
+ *     243 + (L mod 14) - 2 if L mod 14 >= 2, or 121 if L mod 14 == 1.
+ *   - Division is IEEE fp32 and rounding is half-to-even, so results are
+ *     bit-identical to a sequential fp32 implementation.
+ *
+ * Memory: every tensor / byte pointer passed to tlc_compress and
+ * tlc_decompress is DEVICE memory owned by the caller (for example a torch
+ * tensor's data_ptr()).  The context owns its device workspace and a small
+ * pinned host buffer; nothing is allocated per call.
+ *
+ * Streams: a context is bound to one HIP stream (passed as void*; NULL is
+ * the default stream).  All work of a context is ordered on that stream.  A
+ * context must not be used by two host threads at once.
+ *
+ * Errors: functions return TLC_OK (0) or a negative TLC_E_* code; no C++
+ * exception crosses this boundary.  tlc_last_error_string() describes the
+ * most recent failure of the calling thread.
+ */
+#ifndef TLC_H
+#define TLC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TLC_OK 0
+#define TLC_E_INVALID (-1)   /* bad argument: NULL pointer, s not in [1,2), n > max_n, scale not finite */
+#define TLC_E_CAPACITY (-2)  /* bytes_cap < tlc_max_compressed_bytes(n) */
+#define TLC_E_NONFINITE (-3) /* NaN/Inf in tensor+residual, or max*s overflows */
+#define TLC_E_CORRUPT (-4)   /* compressed stream does not expand to ceil(n/5) bytes */
+#define TLC_E_DEVICE (-5)    /* HIP runtime error, or the context is unusable */
+
+/* Largest tensor one call accepts (the quartic byte count must fit the
+ * 30-bit counters of the zero-run scans). */
+#define TLC_MAX_N ((size_t)4294967295u)
+
+typedef struct tlc_ctx tlc_ctx;
+
+/* Upper bound of the compressed length for n values: ceil(n/5).  Zero-run
+ * encoding (Section 3.3) never lengthens the quartic byte string. */
+size_t tlc_max_compressed_bytes(size_t n);
+
+/* Create a context for tensors of up to max_n values (1 <= max_n <=
+ * TLC_MAX_N) whose work is issued on `hip_stream` (a hipStream_t, or NULL).
+ * Allocates about max_n/5 bytes plus max_n/1024 bytes of device workspace.
+ * On success *ctx receives the context; on failure *ctx is NULL. */
+int tlc_ctx_create(tlc_ctx** ctx, size_t max_n, void* hip_stream);
+
+/* Wait for the context's outstanding work and free it.  NULL is a no-op. */
+int tlc_ctx_destroy(tlc_ctx* ctx);
+
+/* Encode one tensor (Sections 3.1-3.3).
+ *   tensor    device fp32[n], read only (the new state change).
+ *   residual  device fp32[n], in/out: the error-accumulation buffer; on
+ *             success it holds acc - M*q.  Must not overlap tensor.
+ *   n         value count, 0 <= n <= max_n of the context.
+ *   s         sparsity multiplier, 1 <= s < 2.
+ *   bytes     device uint8[bytes_cap] receiving the zero-run encoded stream.
+ *   bytes_cap must be >= tlc_max_compressed_bytes(n).
+ *   bytes_len host out: stream length (0 on error).
+ *   scale     host out: M (0 when n == 0).
+ * Synchronous: returns after the stream length is known.  On
+ * TLC_E_NONFINITE the residual and the bytes are left unchanged. */
+int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
+                 float s, uint8_t* bytes, size_t bytes_cap, size_t* bytes_len,
+                 float* scale);
+
+/* Decode one stream (inverse of Section 3.3, Section 3.2 decoding, Eq. 3).
+ *   bytes       device uint8[bytes_len] from tlc_compress.
+ *   scale       M from tlc_compress: finite and >= 0.
+ *   n           value count of the encoded tensor, <= max_n.
+ *   out         device fp32[n]: out = M*q (accumulate == 0) or
+ *               out = out + M*q (accumulate != 0), every element written.
+ * Asynchronous on the context's stream; returns only errors detectable on
+ * the host.  If the stream does not expand to exactly ceil(n/5) bytes, out
+ * is left unchanged and the next tlc_sync() returns TLC_E_CORRUPT. */
+int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
+                   float scale, size_t n, float* out, int accumulate);
+
+/* Wait for all work of the context and return (then clear) the sticky
+ * status of asynchronous decodes: TLC_OK or TLC_E_CORRUPT. */
+int tlc_sync(tlc_ctx* ctx);
+
+/* Text of the calling thread's most recent error (never NULL). */
+const char* tlc_last_error_string(void);
+
+/* ---- per-kernel timing (HIP events on the context's stream) ----------- */
+
+#define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| */
+#define TLC_KERNEL_QUANT_PACK 1     /* Eq. 1-2, residual update, quartic pack */
+#define TLC_KERNEL_ZRE_ENCODE 2     /* zero-run encoding */
+#define TLC_KERNEL_ZRE_DECODE 3     /* zero-run expansion */
+#define TLC_KERNEL_UNPACK_DEQUANT 4 /* quartic unpack, Eq. 3, accumulate */
+#define TLC_KERNEL_COUNT 5
+
+/* Enable (on != 0) or disable recording of a start/stop event pair around
+ * every kernel launch of the context. */
+int tlc_profile_enable(tlc_ctx* ctx, int on);
+
+/* Synchronize, then report the summed device time (ms) and the number of
+ * timed launches of kernel `kernel` since the last reset. */
+int tlc_profile_get(tlc_ctx* ctx, int kernel, double* total_ms,
+                    uint64_t* launches);
+
+/* Zero the accumulated timings. */
+int tlc_profile_reset(tlc_ctx* ctx);
+
+/* Name of a kernel id (the __global__ function's name), or NULL. */
+const char* tlc_kernel_name(int kernel);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TLC_H */

@@ -1,0 +1,143 @@
+// zre_scan.hpp -- associative summary of a byte segment for parallel
+// zero-run encoding (Section 3.3).
+//
+// Zero-run encoding cuts every run of L bytes equal to 121 into
+// floor(L/14) full chunks (code 255) and a remainder chunk (code
+// 243 + rho - 2 for rho >= 2, or 121 for rho == 1).  Where a chunk's code
+// lands depends on how far into its run a byte is, and runs may cross any
+// tile boundary, so a per-tile emit count cannot be computed without the
+// prefix.  This header instead summarises a segment by
+//
+//   all : the segment is entirely 121 (or empty)
+//   ld  : (length of the leading 121 run) mod 14     (== rem when all)
+//   tr  : (length of the trailing 121 run) mod 14    (== rem when all)
+//   cnt : output bytes the segment is certain to produce on its own:
+//         floor(lead/14) + non-121 bytes + ceil(L/14) for every run closed
+//         on both sides inside the segment + floor(trail/14);
+//         for an all-121 segment of length len, floor(len/14)
+//
+// and combines two adjacent segments with an associative operator, so tile
+// prefixes can be found with a decoupled look-back.  Emission convention
+// used by the kernels: a full chunk's 255 is written at its 14th byte; the
+// remainder code of a run is written just before the non-121 byte that
+// closes it, or at the very end of the stream.
+//
+// Packed form (64 bits): cnt in bits 0..31, all in bit 32, ld in bits
+// 33..36, tr in bits 37..40.
+#pragma once
+
+#include <stdint.h>
+
+#ifndef TLC_HD
+#if defined(__HIPCC__)
+#define TLC_HD __host__ __device__ __forceinline__
+#else
+#define TLC_HD inline
+#endif
+#endif
+
+namespace tlc {
+
+constexpr uint32_t kZeroGroup = 121u;  // five zero values (Section 3.3)
+constexpr uint32_t kRunBase = 243u;    // code of a run of two
+constexpr uint32_t kRunMax = 14u;      // longest run one code covers
+constexpr uint32_t kFullChunk = 255u;  // code of a run of fourteen
+
+struct RunSum {
+  uint64_t v;
+};
+
+TLC_HD uint32_t rs_cnt(RunSum a) { return (uint32_t)a.v; }
+TLC_HD uint32_t rs_all(RunSum a) { return (uint32_t)(a.v >> 32) & 1u; }
+TLC_HD uint32_t rs_ld(RunSum a) { return (uint32_t)(a.v >> 33) & 15u; }
+TLC_HD uint32_t rs_tr(RunSum a) { return (uint32_t)(a.v >> 37) & 15u; }
+
+TLC_HD RunSum rs_make(uint32_t all, uint32_t ld, uint32_t tr, uint32_t cnt) {
+  RunSum r;
+  r.v = (uint64_t)cnt | ((uint64_t)all << 32) | ((uint64_t)ld << 33) |
+        ((uint64_t)tr << 37);
+  return r;
+}
+
+// Empty segment: the identity of rs_combine.
+TLC_HD RunSum rs_identity() { return rs_make(1u, 0u, 0u, 0u); }
+
+// Summary of one byte.
+TLC_HD RunSum rs_byte(uint32_t b) {
+  return b == kZeroGroup ? rs_make(1u, 1u, 1u, 0u) : rs_make(0u, 0u, 0u, 1u);
+}
+
+// Summary of segment a followed by segment b.
+TLC_HD RunSum rs_combine(RunSum a, RunSum b) {
+  uint32_t aall = rs_all(a), ball = rs_all(b);
+  uint32_t cnt = rs_cnt(a) + rs_cnt(b);
+  if (aall & ball) {
+    uint32_t s = rs_ld(a) + rs_ld(b);
+    return rs_make(1u, s % kRunMax, s % kRunMax, cnt + s / kRunMax);
+  }
+  if (aall) {  // the run at the end of a continues into b's leading run
+    uint32_t s = rs_ld(a) + rs_ld(b);
+    return rs_make(0u, s % kRunMax, rs_tr(b), cnt + s / kRunMax);
+  }
+  if (ball) {  // b extends a's trailing run
+    uint32_t s = rs_tr(a) + rs_ld(b);
+    return rs_make(0u, rs_ld(a), s % kRunMax, cnt + s / kRunMax);
+  }
+  // a's trailing run and b's leading run join into one run closed on both
+  // sides: its remainder costs one more code if non-empty.
+  uint32_t s = rs_tr(a) + rs_ld(b);
+  return rs_make(0u, rs_ld(a), rs_tr(b), cnt + (s + kRunMax - 1u) / kRunMax);
+}
+
+// Bytes already written by everything before a point whose prefix (from
+// the start of the stream) has summary p.  The leading run of the stream
+// is closed by the stream start, so its remainder code has been written
+// once a non-121 byte follows it.
+TLC_HD uint32_t rs_emitted(RunSum p) {
+  return rs_cnt(p) + ((!rs_all(p) && rs_ld(p) != 0u) ? 1u : 0u);
+}
+
+// Length of the open 121 run (mod 14) at the end of a prefix.
+TLC_HD uint32_t rs_phase(RunSum p) { return rs_tr(p); }
+
+// Total encoded length of a whole stream with summary t.
+TLC_HD uint32_t rs_total(RunSum t) {
+  return rs_emitted(t) + (rs_tr(t) != 0u ? 1u : 0u);
+}
+
+// Code of a run remainder of rho in [1, 14] bytes.
+TLC_HD uint32_t rs_code(uint32_t rho) {
+  return rho == 1u ? kZeroGroup : kRunBase + rho - 2u;
+}
+
+}  // namespace tlc
+
+namespace tlc {
+
+// Encode one quartic byte x arriving while the open 121 run has phi (mod
+// 14) bytes; hands output bytes to put(byte) and returns the new phase.
+template <class Put>
+TLC_HD uint32_t rs_step(uint32_t x, uint32_t phi, Put&& put) {
+  if (x == kZeroGroup) {
+    if (++phi == kRunMax) {
+      put(kFullChunk);
+      phi = 0u;
+    }
+  } else {
+    if (phi != 0u) put(rs_code(phi));
+    phi = 0u;
+    put(x);
+  }
+  return phi;
+}
+
+// rs_step over `count` bytes.  The caller writes the final remainder code
+// (rs_code) if the stream ends with a non-zero phase.
+template <class Put>
+TLC_HD uint32_t rs_walk(const uint8_t* b, uint32_t count, uint32_t phi,
+                        Put&& put) {
+  for (uint32_t i = 0; i < count; ++i) phi = rs_step(b[i], phi, put);
+  return phi;
+}
+
+}  // namespace tlc

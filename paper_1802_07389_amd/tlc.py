@@ -1,0 +1,222 @@
+"""ctypes binding of ``libtlc.so`` (declared in ``include/tlc.h``).
+
+Argument marshalling only: every step of encode and decode runs in the HIP
+kernels of the library.  The functions keep the C names; ``Context`` wraps
+them for torch tensors (torch provides device memory and the stream, nothing
+else).  Importing this module raises ImportError when the library has not
+been built -- there is no fallback.
+"""
+import ctypes
+import os
+
+import torch  # load torch's HIP runtime first so libtlc binds to the same one
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtlc.so")
+
+TLC_OK = 0
+TLC_E_INVALID = -1
+TLC_E_CAPACITY = -2
+TLC_E_NONFINITE = -3
+TLC_E_CORRUPT = -4
+TLC_E_DEVICE = -5
+
+TLC_KERNEL_ABSMAX = 0
+TLC_KERNEL_QUANT_PACK = 1
+TLC_KERNEL_ZRE_ENCODE = 2
+TLC_KERNEL_ZRE_DECODE = 3
+TLC_KERNEL_UNPACK_DEQUANT = 4
+TLC_KERNEL_COUNT = 5
+
+EXPORTS = (
+    "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_destroy",
+    "tlc_compress", "tlc_decompress", "tlc_sync", "tlc_last_error_string",
+    "tlc_profile_enable", "tlc_profile_get", "tlc_profile_reset",
+    "tlc_kernel_name",
+)
+
+
+class TLCError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{msg} (status {code})")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built: run `python -m paper_1802_07389_amd.build` "
+            "or __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    sz, vp, i, f = ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    L.tlc_max_compressed_bytes.argtypes = [sz]
+    L.tlc_max_compressed_bytes.restype = sz
+    L.tlc_ctx_create.argtypes = [ctypes.POINTER(vp), sz, vp]
+    L.tlc_ctx_create.restype = i
+    L.tlc_ctx_destroy.argtypes = [vp]
+    L.tlc_ctx_destroy.restype = i
+    L.tlc_compress.argtypes = [vp, vp, vp, sz, f, vp, sz, ctypes.POINTER(sz),
+                               ctypes.POINTER(f)]
+    L.tlc_compress.restype = i
+    L.tlc_decompress.argtypes = [vp, vp, sz, f, sz, vp, i]
+    L.tlc_decompress.restype = i
+    L.tlc_sync.argtypes = [vp]
+    L.tlc_sync.restype = i
+    L.tlc_last_error_string.argtypes = []
+    L.tlc_last_error_string.restype = ctypes.c_char_p
+    L.tlc_profile_enable.argtypes = [vp, i]
+    L.tlc_profile_enable.restype = i
+    L.tlc_profile_get.argtypes = [vp, i, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_uint64)]
+    L.tlc_profile_get.restype = i
+    L.tlc_profile_reset.argtypes = [vp]
+    L.tlc_profile_reset.restype = i
+    L.tlc_kernel_name.argtypes = [i]
+    L.tlc_kernel_name.restype = ctypes.c_char_p
+    return L
+
+
+lib = _load()
+
+
+# ----------------------------------------------------------------- C names
+def tlc_max_compressed_bytes(n):
+    return int(lib.tlc_max_compressed_bytes(n))
+
+
+def tlc_last_error_string():
+    return lib.tlc_last_error_string().decode()
+
+
+def _check(st):
+    if st != TLC_OK:
+        raise TLCError(st, tlc_last_error_string())
+    return st
+
+
+def tlc_ctx_create(max_n, hip_stream):
+    """Return a context handle (int) bound to ``hip_stream`` (int or None)."""
+    h = ctypes.c_void_p()
+    _check(lib.tlc_ctx_create(ctypes.byref(h), max_n, hip_stream))
+    return h.value
+
+
+def tlc_ctx_destroy(ctx):
+    return lib.tlc_ctx_destroy(ctx)
+
+
+def tlc_compress(ctx, tensor, residual, n, s, bytes_, bytes_cap):
+    """Device pointers in; returns (status, bytes_len, scale)."""
+    ln = ctypes.c_size_t(0)
+    sc = ctypes.c_float(0.0)
+    st = lib.tlc_compress(ctx, tensor, residual, n, s, bytes_, bytes_cap,
+                          ctypes.byref(ln), ctypes.byref(sc))
+    return st, ln.value, sc.value
+
+
+def tlc_decompress(ctx, bytes_, bytes_len, scale, n, out, accumulate):
+    return lib.tlc_decompress(ctx, bytes_, bytes_len, scale, n, out,
+                              int(bool(accumulate)))
+
+
+def tlc_sync(ctx):
+    return lib.tlc_sync(ctx)
+
+
+def tlc_profile_enable(ctx, on):
+    return lib.tlc_profile_enable(ctx, int(bool(on)))
+
+
+def tlc_profile_get(ctx, kernel):
+    """Return (status, total_ms, launches)."""
+    ms = ctypes.c_double(0.0)
+    cnt = ctypes.c_uint64(0)
+    st = lib.tlc_profile_get(ctx, kernel, ctypes.byref(ms), ctypes.byref(cnt))
+    return st, ms.value, cnt.value
+
+
+def tlc_profile_reset(ctx):
+    return lib.tlc_profile_reset(ctx)
+
+
+def tlc_kernel_name(kernel):
+    r = lib.tlc_kernel_name(kernel)
+    return r.decode() if r is not None else None
+
+
+# ----------------------------------------------------------------- torch
+def _dev_f32(t, name):
+    if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
+    return t.data_ptr()
+
+
+def _dev_u8(t, name):
+    if not (t.is_cuda and t.dtype == torch.uint8 and t.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous uint8 GPU tensor")
+    return t.data_ptr()
+
+
+class Context:
+    """One compression context (one tensor, one direction) on one stream."""
+
+    def __init__(self, max_n, stream=None, device=None):
+        self.device = torch.device(device) if device is not None else torch.device(
+            "cuda", torch.cuda.current_device())
+        with torch.cuda.device(self.device):
+            self.stream = stream if stream is not None else torch.cuda.current_stream()
+            self.max_n = int(max_n)
+            self.handle = tlc_ctx_create(self.max_n, self.stream.cuda_stream)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            tlc_ctx_destroy(self.handle)
+            self.handle = None
+
+    __del__ = close
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def max_compressed_bytes(self, n):
+        return tlc_max_compressed_bytes(n)
+
+    def compress(self, tensor, residual, s, out=None):
+        """Encode; returns (bytes view uint8[len], scale).  residual is updated."""
+        n = tensor.numel()
+        if residual.numel() != n:
+            raise ValueError("tensor and residual sizes differ")
+        cap = tlc_max_compressed_bytes(n)
+        if out is None:
+            out = torch.empty(max(cap, 1), dtype=torch.uint8, device=self.device)
+        st, ln, sc = tlc_compress(self.handle, _dev_f32(tensor, "tensor"),
+                                  _dev_f32(residual, "residual"), n, float(s),
+                                  _dev_u8(out, "out"), out.numel())
+        _check(st)
+        return out[:ln], sc
+
+    def decompress(self, data, scale, n, out, accumulate=False):
+        """Decode into out (async; check with sync())."""
+        if out.numel() != n:
+            raise ValueError("out has the wrong size")
+        ptr = _dev_u8(data, "data") if data.numel() else None
+        _check(tlc_decompress(self.handle, ptr, data.numel(), float(scale), n,
+                              _dev_f32(out, "out"), accumulate))
+
+    def sync(self):
+        _check(tlc_sync(self.handle))
+
+    # per-kernel event timing
+    def profile(self, on=True):
+        _check(tlc_profile_enable(self.handle, on))
+
+    def profile_reset(self):
+        _check(tlc_profile_reset(self.handle))
+
+    def profile_get(self, kernel):
+        st, ms, cnt = tlc_profile_get(self.handle, kernel)
+        _check(st)
+        return ms, cnt

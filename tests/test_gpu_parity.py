@@ -1,0 +1,356 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+The bar is bit-exactness: the compressed byte stream byte for byte, the
+scale M, the residual and the decoded fp32 output to 0 ULP (the method's
+fp32 operations are fixed and every product in it is exact).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_07389_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_1802_07389_amd import tlc
+    c = tlc.Context(max_n=workloads.C4_N)
+    yield c
+    c.close()
+
+
+def G():
+    import gpuutil
+    return gpuutil
+
+
+def check_encode_decode(ctx, x, r, s, out0=None, accumulate=False, offset=0, tag=""):
+    """Encode and decode x on both sides; assert bit equality; return the
+    oracle's (bytes, M, residual, decoded)."""
+    g = G()
+    r_ref = r.copy()
+    st_ref, C_ref, M_ref = oracle.compress(x, r_ref, s)
+    st, C, M, r_gpu = g.gpu_compress(ctx, x, r, s, offset=offset)
+    assert st == st_ref, (tag, st, st_ref)
+    if st != 0:
+        return None
+    assert np.array_equal(g.bits(np.array([M])), g.bits(np.array([M_ref]))), (tag, M, M_ref)
+    assert C.size == C_ref.size, (tag, C.size, C_ref.size)
+    if not np.array_equal(C, C_ref):
+        i = int(np.flatnonzero(C != C_ref)[0])
+        raise AssertionError(f"{tag}: byte {i} differs: gpu {C[i]} oracle {C_ref[i]}")
+    if not np.array_equal(g.bits(r_gpu), g.bits(r_ref)):
+        i = int(np.flatnonzero(g.bits(r_gpu) != g.bits(r_ref))[0])
+        raise AssertionError(f"{tag}: residual {i} differs: {r_gpu[i]!r} vs {r_ref[i]!r}")
+    n = x.size
+    if out0 is None:
+        out0 = np.zeros(n, F32)
+    st_ref, out_ref = oracle.decompress(C_ref, M_ref, n, out0.copy(), accumulate)
+    st, out = g.gpu_decompress(ctx, C_ref, M_ref, n, out0.copy(), accumulate, offset=offset)
+    assert st == st_ref == 0, (tag, st, st_ref)
+    if not np.array_equal(g.bits(out), g.bits(out_ref)):
+        i = int(np.flatnonzero(g.bits(out) != g.bits(out_ref))[0])
+        raise AssertionError(f"{tag}: decoded {i} differs: {out[i]!r} vs {out_ref[i]!r}")
+    return C_ref, M_ref, r_ref, out_ref
+
+
+# ------------------------------------------------------------------ small cases
+def test_worked_examples_on_gpu(ctx):
+    import json, os
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "worked_examples.json")))
+    for case in gold["cases"]:
+        if "x" not in case:
+            continue
+        x = np.array(case["x"], F32)
+        r = np.array(case["r"], F32)
+        st, C, M, r_gpu = G().gpu_compress(ctx, x, r, case["s"])
+        assert st == 0 and C.tolist() == case["bytes"] and M == case["scale"], case["name"]
+        assert r_gpu.tolist() == case["residual"], case["name"]
+        st, out = G().gpu_decompress(ctx, C, M, x.size)
+        assert st == 0 and out.tolist() == case["decoded"], case["name"]
+
+
+@pytest.mark.parametrize("s", [1.0, 1.5, 1.9])
+def test_tiny_sizes(ctx, s):
+    for n in range(1, 41):
+        x = workloads.normal([10, n], n, 1.0)
+        r = workloads.normal([11, n], n, 0.3)
+        check_encode_decode(ctx, x, r, s, tag=f"n={n}")
+        check_encode_decode(ctx, x, r, s, out0=workloads.normal([12, n], n),
+                            accumulate=True, tag=f"acc n={n}")
+
+
+def test_empty_tensor(ctx):
+    from paper_1802_07389_amd import tlc
+    st, C, M, _ = G().gpu_compress(ctx, np.zeros(0, F32), np.zeros(0, F32), 1.0)
+    assert st == 0 and C.size == 0 and M == 0.0
+    assert tlc.tlc_decompress(ctx.handle, None, 0, 0.0, 0, None, 0) == 0
+
+
+# sizes around the 4096-byte zero-run tile and the vector/scalar paths
+EDGE_N = [5 * 4096 - 1, 5 * 4096, 5 * 4096 + 1, 5 * 4096 * 2 + 7, 5 * 4096 * 3 - 5,
+          4 * 5 * 1000, 4 * 5 * 1000 + 3, 65537, 1000003]
+
+
+@pytest.mark.parametrize("n", EDGE_N)
+def test_tile_edges_dense_and_sparse(ctx, n):
+    for s, sigma_scale in [(1.0, 1.0), (1.9, 1.0)]:
+        x = workloads.normal([20, n], n, sigma_scale)
+        check_encode_decode(ctx, x, np.zeros(n, F32), s, tag=f"dense n={n} s={s}")
+    x = workloads.runs_tensor([21, n], n)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.5, tag=f"runs n={n}")
+
+
+@pytest.mark.parametrize("n", [7, 70, 71, 5 * 14 * 4096, 5 * 14 * 4096 + 3, 2 ** 20, 3 * 10 ** 6])
+def test_all_zero_tensors(ctx, n):
+    """Zero runs spanning many tiles; the 280x ceiling (Section 3.3)."""
+    x = np.zeros(n, F32)
+    res = check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"zeros n={n}")
+    C = res[0]
+    if n % 70 == 0:
+        assert 4 * n / C.size == 280
+
+
+def test_long_runs_with_sparse_spikes(ctx):
+    """Runs of every length mod 14 ending exactly at and across tile edges."""
+    rng = np.random.default_rng(30)
+    n = 5 * 4096 * 6
+    m = n // 5
+    for trial in range(8):
+        x = np.zeros(n, F32)
+        # non-zero groups at chosen quartic positions j (partition 0)
+        js = np.unique(np.concatenate([
+            np.arange(4096 - 20, 4096 + 20, int(rng.integers(1, 15))),
+            rng.integers(0, m, size=int(rng.integers(1, 30)))]))
+        x[js] = F32(1.0)
+        check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"spikes {trial}")
+
+
+@pytest.mark.parametrize("offset", [1, 2, 3])
+def test_unaligned_pointers(ctx, offset):
+    """Tensors that are not 16-byte aligned take the scalar kernels."""
+    n = 5 * 4096 + 20
+    x = workloads.normal([40, offset], n)
+    r = workloads.normal([41, offset], n, 1e-4)
+    check_encode_decode(ctx, x, r, 1.75, out0=workloads.normal([42], n), accumulate=True,
+                        offset=offset, tag=f"offset {offset}")
+
+
+def test_threshold_boundaries(ctx):
+    """Values on both sides of the q = +-1 decision (M/2 and its rounding)."""
+    for M_target in [1.0, 3.0, 1.2345678, 7.1e-39, 3 * 2.0 ** -140, 1.0e30]:
+        M = F32(M_target)
+        half = np.float64(M) * (0.5 + 2.0 ** -25)
+        c = F32(half)
+        cand = [c]
+        for _ in range(4):
+            cand.append(np.nextafter(cand[-1], F32(np.inf)))
+        d = c
+        for _ in range(4):
+            d = np.nextafter(d, F32(0))
+            cand.append(d)
+        vals = np.array(cand + [F32(M / 2)], F32)
+        x = np.concatenate([[M], vals, -vals, [F32(0.0), F32(-0.0)]]).astype(F32)
+        check_encode_decode(ctx, x, np.zeros_like(x), 1.0, tag=f"M={M_target}")
+
+
+def test_subnormals(ctx):
+    x = (workloads.normal([50], 50000, 1.0) * F32(2.0 ** -130)).astype(F32)
+    check_encode_decode(ctx, x, np.zeros_like(x), 1.0, tag="subnormal")
+    check_encode_decode(ctx, x, np.zeros_like(x), 1.75, tag="subnormal s=1.75")
+
+
+def test_negative_zero_accumulate(ctx):
+    """Dense Eq. 3: -0.0 + M*0 = +0.0 on both sides."""
+    n = 4096
+    x = workloads.normal([60], n, 1.0)
+    out0 = np.full(n, -0.0, F32)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.9, out0=out0, accumulate=True, tag="-0")
+
+
+# ------------------------------------------------------------------ error paths
+def test_nonfinite_leaves_residual_and_bytes(ctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    n = 100_000
+    for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
+        x = workloads.normal([70, pos], n)
+        x[pos] = bad
+        r = workloads.normal([71, pos], n)
+        xd, rd = torch.from_numpy(x).cuda(), torch.from_numpy(r).cuda()
+        out = torch.full((n // 5 + 1,), 7, dtype=torch.uint8, device="cuda")
+        st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, 1.0,
+                                      out.data_ptr(), out.numel())
+        assert st == tlc.TLC_E_NONFINITE and ln == 0
+        assert np.array_equal(G().bits(rd.cpu().numpy()), G().bits(r))
+        assert bool((out == 7).all())
+    # overflow of max * s
+    x = np.array([3.0e38, 1.0, 2.0, 3.0, 4.0], F32)
+    st, *_ = G().gpu_compress(ctx, x, np.zeros(5, F32), 1.5)
+    assert st == tlc.TLC_E_NONFINITE
+    # the context still works afterwards
+    check_encode_decode(ctx, workloads.normal([72], 1000), np.zeros(1000, F32), 1.0)
+
+
+def test_invalid_arguments(ctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    n = 1000
+    xd = torch.zeros(n, device="cuda")
+    rd = torch.zeros(n, device="cuda")
+    out = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    for s in (0.5, 2.0, float("nan")):
+        assert tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, s,
+                                out.data_ptr(), n)[0] == tlc.TLC_E_INVALID
+    assert tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, 1.0,
+                            out.data_ptr(), n // 5 - 1)[0] == tlc.TLC_E_CAPACITY
+    assert tlc.tlc_compress(ctx.handle, xd.data_ptr(), xd.data_ptr(), n, 1.0,
+                            out.data_ptr(), n)[0] == tlc.TLC_E_INVALID
+    assert tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), ctx.max_n + 1, 1.0,
+                            out.data_ptr(), n)[0] == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress(ctx.handle, out.data_ptr(), 10, float("inf"), n,
+                              xd.data_ptr(), 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress(ctx.handle, out.data_ptr(), 10, -1.0, n,
+                              xd.data_ptr(), 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress(ctx.handle, out.data_ptr(), n // 5 + 1, 1.0, n,
+                              xd.data_ptr(), 0) == tlc.TLC_E_CORRUPT
+    assert tlc.tlc_decompress(ctx.handle, out.data_ptr(), 0, 1.0, n,
+                              xd.data_ptr(), 0) == tlc.TLC_E_CORRUPT
+    assert tlc.tlc_sync(ctx.handle) == tlc.TLC_OK
+
+
+def test_corrupt_streams_leave_out_unchanged(ctx):
+    from paper_1802_07389_amd import tlc
+    n = 5 * 4096 * 3 + 11
+    x = workloads.runs_tensor([80], n)
+    st, C, M = oracle.compress(x, np.zeros(n, F32), 1.5)
+    out0 = workloads.normal([81], n)
+    bad_streams = [C[:-1], np.append(C, C[-1:]), C.copy()]
+    bad_streams[2][len(C) // 2] = 255 if C[len(C) // 2] != 255 else 7
+    for k, bad in enumerate(bad_streams):
+        assert oracle.decompress(bad, M, n, out0.copy(), True)[0] == oracle.E_CORRUPT
+        st, out = G().gpu_decompress(ctx, bad, M, n, out0.copy(), accumulate=True)
+        assert st == tlc.TLC_E_CORRUPT, k
+        assert np.array_equal(G().bits(out), G().bits(out0)), k
+    # sticky status is cleared by tlc_sync; a good stream decodes afterwards
+    st, out = G().gpu_decompress(ctx, C, M, n, out0.copy(), accumulate=True)
+    assert st == tlc.TLC_OK
+
+
+def test_repeated_calls_are_deterministic(ctx):
+    """The look-back scans give identical bytes on every run."""
+    n = 5 * 4096 * 40 + 3
+    x = workloads.runs_tensor([90], n)
+    first = None
+    for rep in range(25):
+        st, C, M, r = G().gpu_compress(ctx, x, np.zeros(n, F32), 1.5)
+        assert st == 0
+        if first is None:
+            first = (C, M, r)
+            st_ref, C_ref, M_ref = oracle.compress(x, np.zeros(n, F32), 1.5)
+            assert np.array_equal(C, C_ref)
+        else:
+            assert np.array_equal(C, first[0]) and M == first[1]
+            assert np.array_equal(G().bits(r), G().bits(first[2]))
+
+
+# ------------------------------------------------------------------ configs
+def test_c1_single_tensor_round_trip(ctx):
+    """2^20 values ~ N(0, 1e-3), seed 0, zero residual, s = 1; acc = 0 and 1."""
+    x = workloads.c1_tensor()
+    r = np.zeros_like(x)
+    check_encode_decode(ctx, x, r, workloads.C1_S, tag="C1")
+    check_encode_decode(ctx, x, r, workloads.C1_S, out0=np.zeros_like(x), accumulate=True,
+                        tag="C1 acc")
+
+
+def test_c2_resnet110_ten_steps(ctx):
+    """335 ResNet-110 tensors, s = 1.75, residual carried over 10 steps."""
+    g = G()
+    sizes = workloads.c2_sizes()
+    res_gpu = [np.zeros(n, F32) for n in sizes]
+    res_ref = [np.zeros(n, F32) for n in sizes]
+    for step in range(workloads.C2_STEPS):
+        for t, n in enumerate(sizes):
+            x = workloads.c2_gradient(step, t, n)
+            st_ref, C_ref, M_ref = oracle.compress(x, res_ref[t], workloads.C2_S)
+            st, C, M, r = g.gpu_compress(ctx, x, res_gpu[t], workloads.C2_S)
+            assert st == st_ref == 0
+            assert M == M_ref and np.array_equal(C, C_ref), (step, t)
+            assert np.array_equal(g.bits(r), g.bits(res_ref[t])), (step, t)
+            res_gpu[t] = r
+            if t % 37 == 0 or step == workloads.C2_STEPS - 1:
+                st, out = g.gpu_decompress(ctx, C, M, n)
+                st_ref, out_ref = oracle.decompress(C_ref, M_ref, n)
+                assert st == 0 and np.array_equal(g.bits(out), g.bits(out_ref)), (step, t)
+        g.log(f"C2 step {step} ok")
+
+
+@pytest.mark.timeout(600)
+def test_c3_runs_sweep_s(ctx):
+    """64M Laplace values, 70% zeros in geometric runs; s in {1.0, 1.5, 1.9}."""
+    x = workloads.c3_tensor()
+    for s in workloads.C3_S:
+        check_encode_decode(ctx, x, np.zeros_like(x), s, tag=f"C3 s={s}")
+        G().log(f"C3 s={s} ok")
+
+
+@pytest.mark.timeout(900)
+def test_c4_256m_five_steps(ctx):
+    """2^28 values, s = 1.75, residual carried over 5 steps; every payload
+    decoded with accumulate into a persistent model buffer."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    n = workloads.C4_N
+    r_ref = np.zeros(n, F32)
+    model_ref = np.zeros(n, F32)
+    rd = torch.zeros(n, device="cuda")
+    model = torch.zeros(n, device="cuda")
+    out = torch.empty(tlc.tlc_max_compressed_bytes(n), dtype=torch.uint8, device="cuda")
+    for step in range(workloads.C4_STEPS):
+        x = workloads.c4_tensor(step)
+        xd = torch.from_numpy(x).cuda()
+        C, M = ctx.compress(xd, rd, workloads.C4_S, out=out)
+        ctx.decompress(C, M, n, model, accumulate=True)
+        ctx.sync()
+        st, C_ref, M_ref = oracle.compress(x, r_ref, workloads.C4_S)
+        assert st == 0 and M == M_ref
+        assert np.array_equal(C.cpu().numpy(), C_ref), step
+        assert np.array_equal(g.bits(rd.cpu().numpy()), g.bits(r_ref)), step
+        st, model_ref = oracle.decompress(C_ref, M_ref, n, model_ref, accumulate=True)
+        assert np.array_equal(g.bits(model.cpu().numpy()), g.bits(model_ref)), step
+        g.log(f"C4 step {step} ok: len={C_ref.size} ratio={4 * n / (C_ref.size + 4):.1f}")
+        del xd
+
+
+@pytest.mark.timeout(900)
+def test_c5_aggregation_and_reencode(ctx):
+    """16 payloads of 25.6M values decoded into one fp32 sum, then re-encoded."""
+    import torch
+    g = G()
+    n = workloads.C5_N
+    sum_ref = np.zeros(n, F32)
+    sumd = torch.zeros(n, device="cuda")
+    payloads = []
+    for p in range(workloads.C5_PAYLOADS):
+        x = workloads.c5_tensor(p)
+        st, C, M, r = g.gpu_compress(ctx, x, np.zeros(n, F32), workloads.C5_S)
+        r_ref = np.zeros(n, F32)
+        st_ref, C_ref, M_ref = oracle.compress(x, r_ref, workloads.C5_S)
+        assert st == st_ref == 0 and M == M_ref and np.array_equal(C, C_ref), p
+        assert np.array_equal(g.bits(r), g.bits(r_ref)), p
+        payloads.append((torch.from_numpy(C).cuda(), M, C_ref))
+    for Cd, M, C_ref in payloads:
+        ctx.decompress(Cd, M, n, sumd, accumulate=True)
+        oracle.decompress(C_ref, M, n, sum_ref, accumulate=True)
+    ctx.sync()
+    assert np.array_equal(g.bits(sumd.cpu().numpy()), g.bits(sum_ref))
+    g.log("C5 aggregate ok")
+    res = check_encode_decode(ctx, sum_ref, np.zeros(n, F32), workloads.C5_S, tag="C5 re-encode")
+    g.log(f"C5 re-encode ok: len={res[0].size}")
