@@ -1,0 +1,245 @@
+"""Benchmark of the 3LC encode/decode hot path on one MI355X.
+
+One step = tlc_compress of a 2^28-value fp32 tensor (error accumulation,
+max-magnitude scale, 3-value quantization with residual write-back, quartic
+pack, zero-run encoding) followed by tlc_decompress of its payload with
+accumulation into a persistent fp32 model buffer (zero-run expansion,
+quartic unpack, dequantization, accumulate).  s = 1.75 and the residual is
+carried from step to step.  Inputs are seeded N(0, 1e-3) tensors (five of
+them, cycled), resident in HBM before timing starts.
+
+Prints ONE JSON line.  ``value`` is GB/s of fp32 input per step (4n bytes
+per round trip).  ``roofline`` is for the dominant kernel
+(tlc_quant_pack_kernel), timed with HIP events on the library's stream.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
+METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compression ratio"
+KERNEL_SRC = os.path.join(ROOT, "paper_1802_07389_amd", "csrc", "tlc_kernels.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_pack_kernel_c4_traffic.md")
+
+# Algorithmic HBM bytes per element of each kernel (m = n/5 quartic bytes,
+# c = compressed bytes, all fp32 tensors 4 B/value).
+def algorithmic_bytes(n, c):
+    m = -(-n // 5)
+    return {
+        "tlc_absmax_kernel": 8 * n,                # read x, r
+        "tlc_quant_pack_kernel": 12 * n + m,       # read x, r; write r, Q
+        "tlc_zre_encode_kernel": m + c,            # read Q; write C
+        "tlc_zre_decode_kernel": c + m,            # read C; write Q
+        "tlc_unpack_dequant_kernel": m + 8 * n,    # read Q; read+write out
+    }
+
+
+def kernel_source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(n):
+    """HBM bytes per launch of tlc_quant_pack_kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    text = open(TRAFFIC_SUMMARY).read()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    m_n = re.search(r"n:\s*(\d+)", text)
+    if not (m_hash and m_bytes and m_n):
+        return None
+    if m_hash.group(1) != kernel_source_hash() or int(m_n.group(1)) != n:
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(x, s):
+    """The CPU oracle (one thread) on one full step of the same workload."""
+    import oracle
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+    n = x.size
+    r = np.zeros(n, np.float32)
+    out = np.zeros(n, np.float32)
+    oracle.lib()
+    t0 = time.perf_counter()
+    st, C, M = oracle.compress(x, r, s)
+    t1 = time.perf_counter()
+    st2, out = oracle.decompress(C, M, n, out, accumulate=True)
+    t2 = time.perf_counter()
+    assert st == 0 and st2 == 0
+    return {
+        "value": round(4 * n / (t2 - t0) / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"one round trip (encode + decode with accumulate) of the step-0 "
+                  f"tensor, n={n}, s={s}; encode {t1 - t0:.2f} s, decode {t2 - t1:.2f} s",
+        "encode_GBps": round(4 * n / (t1 - t0) / 1e9, 4),
+        "decode_GBps": round(4 * n / (t2 - t1) / 1e9, 4),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--n", type=int, default=None, help="override the tensor size")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run 1 GiB device copies (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the 3LC path is per tensor and this build "
+              "has no multi-GPU leg (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1802_07389_amd import tlc, workloads
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": 4 << 28,
+                          "calibrate_copy_bytes_written": 4 << 28, "launches": 5}))
+        return
+
+    n = args.n or workloads.C4_N
+    s = workloads.C4_S
+    n_inputs = workloads.C4_STEPS
+    host_inputs = [workloads.c4_tensor(k, n) for k in range(n_inputs)]
+    xs = [torch.from_numpy(h).to(dev) for h in host_inputs]
+    resid = torch.zeros(n, dtype=torch.float32, device=dev)
+    model = torch.zeros(n, dtype=torch.float32, device=dev)
+    cap = tlc.tlc_max_compressed_bytes(n)
+    payload = torch.empty(cap, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ctx = tlc.Context(max_n=n, stream=stream, device=dev)
+
+    lens = []
+
+    def step(k):
+        C, M = ctx.compress(xs[k % n_inputs], resid, s, out=payload)
+        t_enc = time.perf_counter()
+        ctx.decompress(C, M, n, model, accumulate=True)
+        lens.append(C.numel())
+        return t_enc
+
+    for k in range(args.warmup):
+        step(k)
+    ctx.sync()
+    torch.cuda.synchronize()
+
+    ctx.profile(True)
+    ctx.profile_reset()
+    lens.clear()
+    enc_s = dec_s = 0.0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ta = time.perf_counter()
+        te = step(args.warmup + k)
+        ctx.sync()
+        tb = time.perf_counter()
+        enc_s += te - ta
+        dec_s += tb - te
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.profile(False)
+
+    kern = {}
+    for kid in range(tlc.TLC_KERNEL_COUNT):
+        ms, cnt = ctx.profile_get(kid)
+        kern[tlc.tlc_kernel_name(kid)] = (ms / cnt if cnt else 0.0, cnt)
+
+    elapsed = t1 - t0
+    ms_per_step = elapsed / args.steps * 1e3
+    value = 4 * n * args.steps / elapsed / 1e9
+    c_avg = float(np.mean(lens))
+    algo = algorithmic_bytes(n, c_avg)
+
+    dom = "tlc_quant_pack_kernel"
+    dom_ms = kern[dom][0]
+    achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
+    traffic = measured_traffic(n)
+
+    enc_k = ["tlc_absmax_kernel", "tlc_quant_pack_kernel", "tlc_zre_encode_kernel"]
+    dec_k = ["tlc_zre_decode_kernel", "tlc_unpack_dequant_kernel"]
+    enc_kernel_ms = sum(kern[k][0] for k in enc_k)
+    dec_kernel_ms = sum(kern[k][0] for k in dec_k)
+    enc_bytes = sum(algo[k] for k in enc_k)
+    dec_bytes = sum(algo[k] for k in dec_k)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "C4: one fp32 tensor of 2^28 values ~ N(0, 1e-3) (5 seeded inputs "
+                        "cycled), s = 1.75, residual carried across steps; step = encode + "
+                        "decode with accumulate into a persistent fp32 buffer",
+            "n": n, "s": s, "parallelism": "none (1 GPU)",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dom,
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": int(algo[dom]),
+            "avg_launch_ms": round(dom_ms, 5),
+        },
+        "encode_GBps_input": round(4 * n * args.steps / enc_s / 1e9, 2),
+        "decode_GBps_input": round(4 * n * args.steps / dec_s / 1e9, 2),
+        "encode_kernels_hbm_frac": round(enc_bytes / (enc_kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "decode_kernels_hbm_frac": round(dec_bytes / (dec_kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "encode_kernel_ms": round(enc_kernel_ms, 5),
+        "decode_kernel_ms": round(dec_kernel_ms, 5),
+        "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items()},
+        "compression_ratio": round(4 * n / (c_avg + 4), 2),
+        "compression_ratio_payload_only": round(4 * n / c_avg, 2),
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(host_inputs[0], s)
+    else:
+        result["cpu_baseline"] = None
+    ctx.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -42,12 +42,15 @@ struct StatusWord {
   __device__ static uint32_t epoch(uint64_t w) { return (uint32_t)(w >> kEpochShift); }
 };
 
+// The payload lives inside the status word, so no other memory has to be
+// made visible with it: relaxed agent-scope atomics are enough and avoid the
+// L2 write-back / invalidate that release / acquire imply on gfx950.
 __device__ __forceinline__ void status_publish(uint64_t* p, uint64_t w) {
-  __hip_atomic_store(p, w, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ uint64_t status_read(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_ACQUIRE,
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -56,44 +59,67 @@ __device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
                                 __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Single-thread look-back for tile `tile` (> 0) over an associative
-// operator op(earlier, later).  Publishes the aggregate, folds predecessor
-// words until an inclusive prefix is found, publishes the tile's inclusive
-// prefix and returns the exclusive prefix.  On a bounded-wait timeout or a
-// predecessor fault it publishes a fault word and sets *fault.
+// Wave-parallel look-back for tile `tile` (> 0), run by all 64 lanes of one
+// wave, over an associative operator op(earlier, later).  Lane l polls the
+// word of tile (base - l), so one poll covers 64 predecessors.  The words
+// from the nearest inclusive prefix up to tile - 1 are folded in order with
+// a shuffle reduction (a higher lane holds an earlier tile).  Publishes the
+// tile's aggregate first and its inclusive prefix last; returns the
+// exclusive prefix in every lane.  A bounded wait or a predecessor fault
+// publishes a fault word and sets *fault.
 template <class SW, class Op>
-__device__ uint64_t lookback_exclusive(uint64_t* status, uint32_t tile,
-                                       uint64_t agg, uint64_t identity,
-                                       uint32_t epoch, Op op, bool* fault) {
-  status_publish(&status[tile], SW::pack(agg, kFlagAgg, epoch));
+__device__ uint64_t lookback_wave(uint64_t* status, uint32_t tile, uint64_t agg,
+                                  uint64_t identity, uint32_t epoch, Op op,
+                                  bool* fault) {
+  const uint32_t lane = threadIdx.x & 63u;
+  if (lane == 0) status_publish(&status[tile], SW::pack(agg, kFlagAgg, epoch));
   uint64_t run = identity;
-  uint32_t i = tile - 1u;
+  int64_t base = (int64_t)tile - 1;
   uint32_t spins = 0;
+  bool failed = false;
   for (;;) {
-    uint64_t w = status_read(&status[i]);
-    uint32_t f = SW::flag(w);
-    if (SW::epoch(w) != epoch || f == 0u) {
+    const int64_t idx = base - (int64_t)lane;
+    uint64_t val = identity;
+    bool ready = true, is_prefix = true, is_fault = false;
+    if (idx >= 0) {  // lanes past tile 0 act as an (ignored) prefix
+      const uint64_t w = status_read(&status[idx]);
+      const uint32_t f = SW::flag(w);
+      ready = SW::epoch(w) == epoch && f != 0u;
+      is_prefix = ready && f == kFlagPrefix;
+      is_fault = ready && f == kFlagFault;
+      val = SW::payload(w);
+    }
+    const uint64_t pmask = __ballot(is_prefix);
+    const uint32_t p = pmask ? (uint32_t)(__ffsll((unsigned long long)pmask) - 1) : 64u;
+    const uint64_t need = p >= 63u ? ~0ull : ((2ull << p) - 1ull);  // lanes 0..p
+    if (__ballot(is_fault) & need) {
+      failed = true;
+      break;
+    }
+    if (__ballot(!ready) & need) {
       if (++spins > kSpinLimit) {
-        *fault = true;
+        failed = true;
         break;
       }
       __builtin_amdgcn_s_sleep(1);
       continue;
     }
-    if (f == kFlagFault) {
-      *fault = true;
-      break;
+    uint64_t v = lane <= p ? val : identity;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t o = __shfl_down(v, d, 64);
+      if (lane + d < 64u) v = op(o, v);
     }
-    run = op(SW::payload(w), run);
-    if (f == kFlagPrefix) break;
-    --i;  // an aggregate word never belongs to tile 0, so i stays >= 0
+    run = op(__shfl(v, 0, 64), run);
+    if (p < 64u) break;
+    base -= 64;
   }
-  if (*fault) {
-    status_publish(&status[tile], SW::pack(0, kFlagFault, epoch));
-    return identity;
+  *fault = failed;
+  if (lane == 0) {
+    status_publish(&status[tile], failed ? SW::pack(0, kFlagFault, epoch)
+                                         : SW::pack(op(run, agg), kFlagPrefix, epoch));
   }
-  status_publish(&status[tile], SW::pack(op(run, agg), kFlagPrefix, epoch));
-  return run;
+  return failed ? identity : run;
 }
 
 }  // namespace tlc

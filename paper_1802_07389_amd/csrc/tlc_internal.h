@@ -9,8 +9,8 @@
 namespace tlc {
 
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
-constexpr int kZreBytesPerThread = 16;    // zero-run scans: one uint4 per thread
-constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 4096 bytes per tile
+constexpr int kZreBytesPerThread = 32;    // zero-run scans: two uint4 per thread
+constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
 constexpr uint32_t kAbsmaxMaxBlocks = 512;  // partial maxima per encode
 constexpr uint32_t kQuantMaxBlocks = 4096;
 constexpr uint32_t kUnpackMaxBlocks = 1u << 16;

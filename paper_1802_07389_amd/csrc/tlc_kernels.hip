@@ -240,13 +240,23 @@ struct SumOp {
   __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
 };
 
+__device__ __forceinline__ void unpack16(uint4 v, uint8_t* b) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    b[i] = (uint8_t)(v.x >> (8 * i));
+    b[4 + i] = (uint8_t)(v.y >> (8 * i));
+    b[8 + i] = (uint8_t)(v.z >> (8 * i));
+    b[12 + i] = (uint8_t)(v.w >> (8 * i));
+  }
+}
+
 __device__ __forceinline__ RunSum shfl_up_rs(RunSum v, int d) {
   RunSum o;
   o.v = __shfl_up(v.v, d, 64);
   return o;
 }
 
-// One tile = 256 threads x 16 quartic bytes.  Each thread summarises its
+// One tile = 256 threads x 32 quartic bytes.  Each thread summarises its
 // bytes (RunSum), the block scans the summaries, the tile finds its prefix
 // by decoupled look-back, then every thread encodes its bytes from its own
 // prefix into LDS and the block copies the tile's output out contiguously.
@@ -269,19 +279,17 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_encode_kernel(
   const uint32_t cnt =
       j0 < m ? (uint32_t)min<uint64_t>(kZreBytesPerThread, m - j0) : 0u;
 
-  uint4 v = make_uint4(0u, 0u, 0u, 0u);
-  if (cnt) v = *reinterpret_cast<const uint4*>(Q + j0);  // workspace is padded
-  uint8_t b[16];
+  uint8_t b[kZreBytesPerThread];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    b[i] = (uint8_t)(v.x >> (8 * i));
-    b[4 + i] = (uint8_t)(v.y >> (8 * i));
-    b[8 + i] = (uint8_t)(v.z >> (8 * i));
-    b[12 + i] = (uint8_t)(v.w >> (8 * i));
+  for (int h = 0; h < kZreBytesPerThread / 16; ++h) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (cnt > 16u * h)  // the workspace is padded past m
+      v = *reinterpret_cast<const uint4*>(Q + j0 + 16 * h);
+    unpack16(v, b + 16 * h);
   }
   RunSum s = rs_identity();
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
+  for (int i = 0; i < kZreBytesPerThread; ++i)
     if ((uint32_t)i < cnt) s = rs_combine(s, rs_byte(b[i]));
 
   // block scan of thread summaries
@@ -303,18 +311,22 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_encode_kernel(
     agg = rs_combine(agg, s_wave[w]);
   }
 
-  if (threadIdx.x == 0) {
+  if (wid == 0) {
     bool fault = false;
     uint64_t ex = rs_to_payload(rs_identity());
     if (tile == 0) {
-      status_publish(&status[0], EncSW::pack(rs_to_payload(agg), kFlagPrefix, epoch));
+      if (lane == 0)
+        status_publish(&status[0], EncSW::pack(rs_to_payload(agg), kFlagPrefix, epoch));
     } else {
-      ex = lookback_exclusive<EncSW>(status, tile, rs_to_payload(agg), ex, epoch,
-                                     EncOp(), &fault);
+      ex = lookback_wave<EncSW>(status, tile, rs_to_payload(agg), ex, epoch, EncOp(),
+                                &fault);
     }
-    s_excl = rs_from_payload(ex);
-    s_fault = fault ? 1u : 0u;
-    if (fault) __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) {
+      s_excl = rs_from_payload(ex);
+      s_fault = fault ? 1u : 0u;
+      if (fault)
+        __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   __syncthreads();
   if (s_fault) return;
@@ -329,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_encode_kernel(
     ++o;
   };
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
+  for (int i = 0; i < kZreBytesPerThread; ++i)
     if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
   if (cnt && j0 + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
 
@@ -360,7 +372,7 @@ __device__ __forceinline__ void fill_zero_groups(uint8_t* __restrict__ Q, uint64
   while (o < end) Q[o++] = (uint8_t)kZeroGroup;
 }
 
-// One tile = 256 threads x 16 stream bytes.  Expansion lengths are scanned
+// One tile = 256 threads x 32 stream bytes.  Expansion lengths are scanned
 // in the block and across tiles (decoupled look-back), then each thread
 // writes its bytes' expansion.  Writes stop at m; the last tile flags the
 // launch's epoch as corrupt when the total is not exactly m.
@@ -381,23 +393,20 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
   const uint32_t cnt =
       j0 < c ? (uint32_t)min<uint64_t>(kZreBytesPerThread, c - j0) : 0u;
 
-  uint8_t b[16];
-  if (cnt == 16u && ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
-    const uint4 v = *reinterpret_cast<const uint4*>(C + j0);
+  uint8_t b[kZreBytesPerThread];
+  if (cnt == (uint32_t)kZreBytesPerThread &&
+      ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      b[i] = (uint8_t)(v.x >> (8 * i));
-      b[4 + i] = (uint8_t)(v.y >> (8 * i));
-      b[8 + i] = (uint8_t)(v.z >> (8 * i));
-      b[12 + i] = (uint8_t)(v.w >> (8 * i));
-    }
+    for (int h = 0; h < kZreBytesPerThread / 16; ++h)
+      unpack16(*reinterpret_cast<const uint4*>(C + j0 + 16 * h), b + 16 * h);
   } else {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
+    for (int i = 0; i < kZreBytesPerThread; ++i)
+      b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
   }
   uint32_t s = 0;
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
+  for (int i = 0; i < kZreBytesPerThread; ++i)
     if ((uint32_t)i < cnt) s += expanded_len(b[i]);
 
   uint32_t incl = s;
@@ -415,21 +424,25 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
     agg += s_wave[w];
   }
 
-  if (threadIdx.x == 0) {
+  if (wid == 0) {
     bool fault = false;
     uint64_t ex = 0;
     if (tile == 0) {
-      status_publish(&status[0], DecSW::pack(agg, kFlagPrefix, epoch));
+      if (lane == 0) status_publish(&status[0], DecSW::pack(agg, kFlagPrefix, epoch));
     } else {
-      ex = lookback_exclusive<DecSW>(status, tile, agg, 0, epoch, SumOp(), &fault);
+      ex = lookback_wave<DecSW>(status, tile, agg, 0, epoch, SumOp(), &fault);
     }
-    s_excl = ex;
-    s_fault = fault ? 1u : 0u;
-    if (fault) __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool last_tile = (uint64_t)(tile + 1) * kZreTile >= c;
-    if (last_tile && (fault || ex + agg != m)) {
-      __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&ctrl->dec_corrupt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) {
+      s_excl = ex;
+      s_fault = fault ? 1u : 0u;
+      if (fault)
+        __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const bool last_tile = (uint64_t)(tile + 1) * kZreTile >= c;
+      if (last_tile && (fault || ex + agg != m)) {
+        __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&ctrl->dec_corrupt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
   __syncthreads();
@@ -437,7 +450,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
 
   uint64_t o = s_excl + wpre + (incl - s);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < kZreBytesPerThread; ++i) {
     if ((uint32_t)i < cnt) {
       const uint32_t x = b[i];
       if (x < kRunBase) {
