@@ -10,7 +10,7 @@ them, cycled), resident in HBM before timing starts.
 
 Prints ONE JSON line.  ``value`` is GB/s of fp32 input per step (4n bytes
 per round trip).  ``roofline`` is for the dominant kernel
-(tlc_quant_pack_kernel), timed with HIP events on the library's stream.
+(tlc_quant_encode_kernel), timed with HIP events on the library's stream.
 """
 import argparse
 import hashlib
@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compression ratio"
 KERNEL_SRC = os.path.join(ROOT, "paper_1802_07389_amd", "csrc", "tlc_kernels.hip")
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_pack_kernel_c4_traffic.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_traffic.md")
 
 # Algorithmic HBM bytes per element of each kernel (m = n/5 quartic bytes,
 # c = compressed bytes, all fp32 tensors 4 B/value).
@@ -36,8 +36,7 @@ def algorithmic_bytes(n, c):
     m = -(-n // 5)
     return {
         "tlc_absmax_kernel": 8 * n,                # read x, r
-        "tlc_quant_pack_kernel": 12 * n + m,       # read x, r; write r, Q
-        "tlc_zre_encode_kernel": m + c,            # read Q; write C
+        "tlc_quant_encode_kernel": 12 * n + c,     # read x, r; write r, C
         "tlc_zre_decode_kernel": c + m,            # read C; write Q
         "tlc_unpack_dequant_kernel": m + 8 * n,    # read Q; read+write out
     }
@@ -49,7 +48,7 @@ def kernel_source_hash():
 
 
 def measured_traffic(n):
-    """HBM bytes per launch of tlc_quant_pack_kernel from the committed
+    """HBM bytes per launch of tlc_quant_encode_kernel from the committed
     rocprofv3 counter summary, if it was taken on the current kernel source."""
     if not os.path.exists(TRAFFIC_SUMMARY):
         return None
@@ -180,12 +179,12 @@ def main():
     c_avg = float(np.mean(lens))
     algo = algorithmic_bytes(n, c_avg)
 
-    dom = "tlc_quant_pack_kernel"
+    dom = "tlc_quant_encode_kernel"
     dom_ms = kern[dom][0]
     achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(n)
 
-    enc_k = ["tlc_absmax_kernel", "tlc_quant_pack_kernel", "tlc_zre_encode_kernel"]
+    enc_k = ["tlc_absmax_kernel", "tlc_quant_encode_kernel"]
     dec_k = ["tlc_zre_decode_kernel", "tlc_unpack_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
     dec_kernel_ms = sum(kern[k][0] for k in dec_k)

@@ -113,12 +113,11 @@ const char* tlc_last_error_string(void);
 
 /* ---- per-kernel timing (HIP events on the context's stream) ----------- */
 
-#define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| */
-#define TLC_KERNEL_QUANT_PACK 1     /* Eq. 1-2, residual update, quartic pack */
-#define TLC_KERNEL_ZRE_ENCODE 2     /* zero-run encoding */
-#define TLC_KERNEL_ZRE_DECODE 3     /* zero-run expansion */
-#define TLC_KERNEL_UNPACK_DEQUANT 4 /* quartic unpack, Eq. 3, accumulate */
-#define TLC_KERNEL_COUNT 5
+#define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| (Eq. 1) */
+#define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, zero-run encoding */
+#define TLC_KERNEL_ZRE_DECODE 2     /* zero-run expansion */
+#define TLC_KERNEL_UNPACK_DEQUANT 3 /* quartic unpack, Eq. 3, accumulate */
+#define TLC_KERNEL_COUNT 4
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

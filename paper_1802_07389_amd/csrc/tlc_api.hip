@@ -42,8 +42,8 @@ bool overlap(const void* a, size_t an, const void* b, size_t bn) {
 }
 
 const char* const kKernelNames[TLC_KERNEL_COUNT] = {
-    "tlc_absmax_kernel", "tlc_quant_pack_kernel", "tlc_zre_encode_kernel",
-    "tlc_zre_decode_kernel", "tlc_unpack_dequant_kernel"};
+    "tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_decode_kernel",
+    "tlc_unpack_dequant_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -64,7 +64,8 @@ struct tlc_ctx {
   uint64_t* enc_status = nullptr;
   uint64_t* dec_status = nullptr;
   uint8_t* Q = nullptr;
-  size_t status_words = 0;
+  size_t enc_status_words = 0;
+  size_t dec_status_words = 0;
   // pinned host readback
   HostReadback* rb = nullptr;
   // look-back bookkeeping
@@ -75,8 +76,8 @@ struct tlc_ctx {
   bool profiling = false;
   std::vector<hipEvent_t> free_events;
   std::vector<PendingTiming> pending;
-  double total_ms[TLC_KERNEL_COUNT] = {0, 0, 0, 0, 0};
-  uint64_t launches[TLC_KERNEL_COUNT] = {0, 0, 0, 0, 0};
+  double total_ms[TLC_KERNEL_COUNT] = {};
+  uint64_t launches[TLC_KERNEL_COUNT] = {};
 };
 
 namespace {
@@ -193,11 +194,12 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
     return hip_fail(e, "hipGetDevice");
   }
   // layout: ctrl | partials | enc status | dec status | Q
-  c->status_words = (c->max_m + kZreTile - 1) / kZreTile + 1;
+  c->enc_status_words = (c->max_m + kEncTile - 1) / kEncTile + 1;
+  c->dec_status_words = (c->max_m + kZreTile - 1) / kZreTile + 1;
   const size_t off_partials = sizeof(Ctrl);
   const size_t off_enc = round_up(off_partials + kAbsmaxMaxBlocks * sizeof(uint32_t), 256);
-  const size_t off_dec = round_up(off_enc + c->status_words * sizeof(uint64_t), 256);
-  const size_t off_q = round_up(off_dec + c->status_words * sizeof(uint64_t), 256);
+  const size_t off_dec = round_up(off_enc + c->enc_status_words * sizeof(uint64_t), 256);
+  const size_t off_q = round_up(off_dec + c->dec_status_words * sizeof(uint64_t), 256);
   const size_t total = off_q + round_up(c->max_m, 16) + 64;
   e = hipMalloc(&c->ws, total);
   if (e != hipSuccess) {
@@ -267,21 +269,17 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
-  st = timed_launch(c, TLC_KERNEL_QUANT_PACK, [&] {
-    return launch_quant_pack(tensor, residual, n, m, s, c->partials, np, c->Q, c->ctrl,
-                             c->stream);
-  });
-  if (st) return st;
   bool clear = false;
   const uint32_t epoch = next_epoch(&c->enc_epoch, kEncEpochMax, &clear);
   if (clear) {
-    hipError_t e = hipMemsetAsync(c->enc_status, 0, c->status_words * 8, c->stream);
+    hipError_t e = hipMemsetAsync(c->enc_status, 0, c->enc_status_words * 8, c->stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
   }
-  const uint32_t ntiles = (uint32_t)((m + kZreTile - 1) / kZreTile);
-  st = timed_launch(c, TLC_KERNEL_ZRE_ENCODE, [&] {
-    return launch_zre_encode(c->Q, (uint32_t)m, bytes, c->enc_status, ntiles,
-                             c->enc_ticket_base, epoch, c->ctrl, c->stream);
+  const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
+  st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
+    return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, bytes,
+                               c->enc_status, ntiles, c->enc_ticket_base, epoch, c->ctrl,
+                               c->stream);
   });
   if (st) return st;
   c->enc_ticket_base += ntiles;
@@ -321,7 +319,7 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
   bool clear = false;
   const uint32_t epoch = next_epoch(&c->dec_epoch, kDecEpochMax, &clear);
   if (clear) {
-    hipError_t e = hipMemsetAsync(c->dec_status, 0, c->status_words * 8, c->stream);
+    hipError_t e = hipMemsetAsync(c->dec_status, 0, c->dec_status_words * 8, c->stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
   }
   const uint32_t ntiles = (uint32_t)((bytes_len + kZreTile - 1) / kZreTile);

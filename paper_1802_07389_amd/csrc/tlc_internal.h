@@ -11,8 +11,8 @@ namespace tlc {
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
 constexpr int kZreBytesPerThread = 32;    // zero-run scans: two uint4 per thread
 constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
+constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr uint32_t kAbsmaxMaxBlocks = 512;  // partial maxima per encode
-constexpr uint32_t kQuantMaxBlocks = 4096;
 constexpr uint32_t kUnpackMaxBlocks = 1u << 16;
 
 // Device control block (one per context, in the workspace).  The first 16
@@ -43,14 +43,10 @@ struct HostReadback {
 hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
                          uint32_t* partials, uint32_t* nblocks,
                          hipStream_t st);
-hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint64_t m,
-                             float s, const uint32_t* partials,
-                             uint32_t npartials, uint8_t* Q, Ctrl* ctrl,
-                             hipStream_t st);
-hipError_t launch_zre_encode(const uint8_t* Q, uint32_t m, uint8_t* out,
-                             uint64_t* status, uint32_t ntiles,
-                             uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                             hipStream_t st);
+hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                              uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                              uint32_t epoch, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_decode(const uint8_t* C, uint32_t c, uint8_t* Q,
                              uint32_t m, uint64_t* status, uint32_t ntiles,
                              uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,

@@ -1,9 +1,9 @@
 // tlc_kernels.hip -- gfx950 kernels of the 3LC encode/decode path.
 //
 //   tlc_absmax_kernel          partial maxima of |tensor + residual|   (Eq. 1)
-//   tlc_quant_pack_kernel      M, 3-value quantization, residual write-back,
-//                              quartic pack                   (Eq. 1-2, 3.2)
-//   tlc_zre_encode_kernel      zero-run encoding, one pass     (Section 3.3)
+//   tlc_quant_encode_kernel    M, 3-value quantization, residual write-back,
+//                              quartic pack and zero-run encoding in one
+//                              pass              (Eq. 1-2, Sections 3.2-3.3)
 //   tlc_zre_decode_kernel      zero-run expansion, one pass
 //   tlc_unpack_dequant_kernel  quartic unpack, Eq. 3, optional accumulate
 //
@@ -141,83 +141,6 @@ __device__ __forceinline__ uint32_t quantize_one(float acc, float M, float U,
   return pos ? 2u : (neg ? 0u : 1u);
 }
 
-// One thread per 4 quartic bytes (vector path: m % 4 == 0 and 16-byte
-// aligned tensors) or per byte (scalar path).  Byte j gathers elements
-// j + k*m, k = 0..4 (contiguous partitions, p0 most significant), so each
-// wave reads and writes five coalesced streams of x and r.
-template <bool kVec>
-__global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
-    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint64_t m,
-    float s, const uint32_t* __restrict__ partials, uint32_t np,
-    uint8_t* __restrict__ Q, Ctrl* __restrict__ ctrl) {
-  __shared__ uint32_t lds[kWaves];
-  const Scale sc = finish_scale(partials, np, s, lds);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    ctrl->enc_err = sc.bad;
-    ctrl->enc_scale = sc.M;
-  }
-  if (sc.bad) return;
-  const float M = sc.M, U = sc.U;
-  const uint64_t tid = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-  if (kVec) {
-    const uint64_t groups = m >> 2;
-    for (uint64_t g = tid; g < groups; g += stride) {
-      const uint64_t j = g << 2;
-      uint32_t code[4] = {0u, 0u, 0u, 0u};
-      if (4 * m + j + 4 <= n) {  // all five partitions hold 4 real values
-        float4 a[5], b[5];
-#pragma unroll
-        for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(x + k * m + j);
-#pragma unroll
-        for (int k = 0; k < 5; ++k) b[k] = *reinterpret_cast<const float4*>(r + k * m + j);
-#pragma unroll
-        for (int k = 0; k < 5; ++k) {
-          float4 o;
-          code[0] = code[0] * 3u + quantize_one(a[k].x + b[k].x, M, U, o.x);
-          code[1] = code[1] * 3u + quantize_one(a[k].y + b[k].y, M, U, o.y);
-          code[2] = code[2] * 3u + quantize_one(a[k].z + b[k].z, M, U, o.z);
-          code[3] = code[3] * 3u + quantize_one(a[k].w + b[k].w, M, U, o.w);
-          *reinterpret_cast<float4*>(r + k * m + j) = o;
-        }
-      } else {  // the group that reaches into the zero padding of p4
-#pragma unroll
-        for (int k = 0; k < 5; ++k) {
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint64_t e = k * m + j + c;
-            uint32_t t = 0u;
-            if (e < n) {
-              float o;
-              t = quantize_one(x[e] + r[e], M, U, o);
-              r[e] = o;
-            }
-            code[c] = code[c] * 3u + t;
-          }
-        }
-      }
-      *reinterpret_cast<uint32_t*>(Q + j) =
-          code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
-    }
-  } else {
-    for (uint64_t j = tid; j < m; j += stride) {
-      uint32_t code = 0u;
-#pragma unroll
-      for (int k = 0; k < 5; ++k) {
-        const uint64_t e = k * m + j;
-        uint32_t t = 0u;
-        if (e < n) {
-          float o;
-          t = quantize_one(x[e] + r[e], M, U, o);
-          r[e] = o;
-        }
-        code = code * 3u + t;
-      }
-      Q[j] = (uint8_t)code;
-    }
-  }
-}
-
 // ---------------------------------------------------------------- Section 3.3
 using EncSW = StatusWord<39>;  // RunSum with a 30-bit count
 using DecSW = StatusWord<36>;  // expanded byte count
@@ -256,44 +179,119 @@ __device__ __forceinline__ RunSum shfl_up_rs(RunSum v, int d) {
   return o;
 }
 
-// One tile = 256 threads x 32 quartic bytes.  Each thread summarises its
-// bytes (RunSum), the block scans the summaries, the tile finds its prefix
-// by decoupled look-back, then every thread encodes its bytes from its own
-// prefix into LDS and the block copies the tile's output out contiguously.
-__global__ __launch_bounds__(kThreads) void tlc_zre_encode_kernel(
-    const uint8_t* __restrict__ Q, uint32_t m, uint8_t* __restrict__ out,
+// Quartic byte j < m: quantizes the five elements j + k*m (contiguous
+// partitions, p0 most significant; elements past n are the zero padding of
+// Section 3.2, step 4), writes their residuals and returns the byte.
+__device__ __forceinline__ uint32_t quantize_byte(const float* __restrict__ x,
+                                                  float* __restrict__ r, uint64_t n,
+                                                  uint64_t m, uint64_t j, float M, float U) {
+  uint32_t code = 0u;
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    const uint64_t e = k * m + j;
+    uint32_t t = 0u;
+    if (e < n) {
+      float o;
+      t = quantize_one(x[e] + r[e], M, U, o);
+      r[e] = o;
+    }
+    code = code * 3u + t;
+  }
+  return code;
+}
+
+// Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and 16-byte aligned x
+// and r, so every partition slice is one float4; returns the four bytes
+// packed little-endian.
+__device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
+                                                    float* __restrict__ r, uint64_t n,
+                                                    uint64_t m, uint64_t j, float M,
+                                                    float U) {
+  if (4 * m + j + 4 > n) {  // the group that reaches into the padding of p4
+    uint32_t w = 0u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) w |= quantize_byte(x, r, n, m, j + c, M, U) << (8 * c);
+    return w;
+  }
+  uint32_t code[4] = {0u, 0u, 0u, 0u};
+  float4 a[5], b[5];
+#pragma unroll
+  for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(x + k * m + j);
+#pragma unroll
+  for (int k = 0; k < 5; ++k) b[k] = *reinterpret_cast<const float4*>(r + k * m + j);
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    float4 o;
+    code[0] = code[0] * 3u + quantize_one(a[k].x + b[k].x, M, U, o.x);
+    code[1] = code[1] * 3u + quantize_one(a[k].y + b[k].y, M, U, o.y);
+    code[2] = code[2] * 3u + quantize_one(a[k].z + b[k].z, M, U, o.z);
+    code[3] = code[3] * 3u + quantize_one(a[k].w + b[k].w, M, U, o.w);
+    *reinterpret_cast<float4*>(r + k * m + j) = o;
+  }
+  return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+}
+
+// One tile = kEncTile quartic bytes (5 * kEncTile values).  Phase 1: the
+// block quantizes its values (threads take groups of 4 bytes, or single
+// bytes when the partitions are not 16-byte aligned, interleaved so every
+// load and store instruction is coalesced) and keeps the quartic bytes in
+// LDS.  Phase 2: each thread takes kEncTile/256 consecutive bytes,
+// summarises them as a RunSum, the block scans the summaries, the tile gets
+// its prefix by decoupled look-back, and every thread zero-run encodes its
+// bytes from its own prefix into LDS; the block then copies the tile's
+// output into the stream.  The quartic bytes never go to HBM.
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
     Ctrl* __restrict__ ctrl) {
+  constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
+  static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
+  __shared__ uint32_t s_max[kWaves];
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_fault;
   __shared__ RunSum s_wave[kWaves];
   __shared__ RunSum s_excl;
-  __shared__ __align__(16) uint8_t s_out[kZreTile + 16];
+  __shared__ __align__(16) uint8_t s_q[kEncTile];
+  __shared__ __align__(16) uint8_t s_out[kEncTile + 16];
 
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
-  __syncthreads();
-  if (ctrl->enc_err) return;  // quantization refused the tensor
+  const Scale sc = finish_scale(partials, np, s, s_max);  // includes a barrier
   const uint32_t tile = s_tile;
-  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  const uint64_t j0 = (uint64_t)tile * kZreTile + threadIdx.x * kZreBytesPerThread;
-  const uint32_t cnt =
-      j0 < m ? (uint32_t)min<uint64_t>(kZreBytesPerThread, m - j0) : 0u;
-
-  uint8_t b[kZreBytesPerThread];
-#pragma unroll
-  for (int h = 0; h < kZreBytesPerThread / 16; ++h) {
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (cnt > 16u * h)  // the workspace is padded past m
-      v = *reinterpret_cast<const uint4*>(Q + j0 + 16 * h);
-    unpack16(v, b + 16 * h);
+  if (tile == 0 && threadIdx.x == 0) {
+    ctrl->enc_err = sc.bad;
+    ctrl->enc_scale = sc.M;
   }
-  RunSum s = rs_identity();
-#pragma unroll
-  for (int i = 0; i < kZreBytesPerThread; ++i)
-    if ((uint32_t)i < cnt) s = rs_combine(s, rs_byte(b[i]));
+  if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
 
-  // block scan of thread summaries
-  RunSum incl = s;
+  // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
+  const uint64_t q0 = (uint64_t)tile * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  if (kVec) {  // 4 bytes per thread: float4 loads and stores
+    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
+      *reinterpret_cast<uint32_t*>(s_q + g * 4u) =
+          quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+  } else {  // 1 byte per thread: dword accesses, still contiguous per wave
+    for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
+      s_q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
+  }
+  __syncthreads();
+
+  // ---- phase 2: Section 3.3
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
+  uint8_t b[kBytes];
+#pragma unroll
+  for (int h = 0; h < kBytes / 16; ++h)
+    unpack16(*reinterpret_cast<const uint4*>(s_q + lo + 16 * h), b + 16 * h);
+  RunSum sum = rs_identity();
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum = rs_combine(sum, rs_byte(b[i]));
+
+  RunSum incl = sum;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
     RunSum o = shfl_up_rs(incl, d);
@@ -341,75 +339,90 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_encode_kernel(
     ++o;
   };
 #pragma unroll
-  for (int i = 0; i < kZreBytesPerThread; ++i)
+  for (int i = 0; i < kBytes; ++i)
     if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
-  if (cnt && j0 + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
+  if (cnt && q0 + lo + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
 
-  const bool last_tile = (uint64_t)(tile + 1) * kZreTile >= m;
+  const bool last_tile = q0 + kEncTile >= m;
   const RunSum tincl = rs_combine(tex, agg);
   const uint32_t tile_end = last_tile ? rs_total(tincl) : rs_emitted(tincl);
   __syncthreads();
-  // a tile emits at most kZreTile + 1 bytes; the clamps only keep a logic
+  // a tile emits at most kEncTile + 1 bytes; the clamps only keep a logic
   // error from writing outside the caller's m-byte buffer
   const uint32_t count =
-      tile_end >= tile_begin ? min<uint32_t>(tile_end - tile_begin, kZreTile + 1) : 0u;
+      tile_end >= tile_begin ? min<uint32_t>(tile_end - tile_begin, kEncTile + 1) : 0u;
   for (uint32_t i = threadIdx.x; i < count; i += kThreads)
     if (tile_begin + i < m) out[tile_begin + i] = s_out[i];
   if (last_tile && threadIdx.x == 0) ctrl->enc_len = tile_end;
 }
 
 // ---------------------------------------------------------------- expansion
+// Mask of the bytes of little-endian word k (bytes 4k .. 4k+3 of a 16-byte
+// chunk) that lie in [a, b).
+__device__ __forceinline__ uint32_t byte_mask(uint32_t a, uint32_t b, int k) {
+  const int lo = min(max((int)a - 4 * k, 0), 4);
+  const int hi = min(max((int)b - 4 * k, 0), 4);
+  if (hi <= lo) return 0u;
+  const uint32_t upto_hi = hi == 4 ? 0xffffffffu : ((1u << (8 * hi)) - 1u);
+  return upto_hi & ~((1u << (8 * lo)) - 1u);
+}
+
 __device__ __forceinline__ uint32_t expanded_len(uint32_t b) {
   return b < kRunBase ? 1u : b - (kRunBase - 2u);
 }
 
-// Writes k bytes of 121 at Q[o..o+k), clipped to m.
-__device__ __forceinline__ void fill_zero_groups(uint8_t* __restrict__ Q, uint64_t o,
-                                                 uint32_t k, uint64_t m) {
-  const uint64_t end = min<uint64_t>(o + k, m);
-  while (o < end && (o & 3u)) Q[o++] = (uint8_t)kZeroGroup;
-  for (; o + 4 <= end; o += 4) *reinterpret_cast<uint32_t*>(Q + o) = 0x79797979u;
-  while (o < end) Q[o++] = (uint8_t)kZeroGroup;
-}
-
 // One tile = 256 threads x 32 stream bytes.  Expansion lengths are scanned
-// in the block and across tiles (decoupled look-back), then each thread
-// writes its bytes' expansion.  Writes stop at m; the last tile flags the
-// launch's epoch as corrupt when the total is not exactly m.
+// in the block and across tiles (decoupled look-back) to place the tile's
+// output at [O, O + E) of the quartic buffer.  The output range is then cut
+// into 256 equal 16-byte aligned slices, one per thread: a thread finds the
+// stream byte covering its slice start (binary search over the per-thread
+// offsets, then a short walk) and expands forward, writing whole uint4
+// chunks (byte stores only where a chunk is shared with a neighbouring
+// tile).  Every thread gets the same amount of output whatever the run
+// structure.  Writes stop at m; the last tile flags the launch's epoch as
+// corrupt when the total is not exactly m.
 __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
     const uint8_t* __restrict__ C, uint32_t c, uint8_t* __restrict__ Q, uint32_t m,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
     Ctrl* __restrict__ ctrl) {
+  constexpr int kBytes = kZreBytesPerThread;
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_fault;
   __shared__ uint32_t s_wave[kWaves];
   __shared__ uint64_t s_excl;
+  __shared__ uint32_t s_toff[kThreads];
+  __shared__ __align__(16) uint8_t s_c[kZreTile];
 
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
   __syncthreads();
   const uint32_t tile = s_tile;
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  const uint64_t j0 = (uint64_t)tile * kZreTile + threadIdx.x * kZreBytesPerThread;
-  const uint32_t cnt =
-      j0 < c ? (uint32_t)min<uint64_t>(kZreBytesPerThread, c - j0) : 0u;
+  const uint64_t j0 = (uint64_t)tile * kZreTile + threadIdx.x * kBytes;
+  const uint32_t cnt = j0 < c ? (uint32_t)min<uint64_t>(kBytes, c - j0) : 0u;
 
-  uint8_t b[kZreBytesPerThread];
-  if (cnt == (uint32_t)kZreBytesPerThread &&
-      ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
+  uint8_t b[kBytes];
+  if (cnt == (uint32_t)kBytes && ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
 #pragma unroll
-    for (int h = 0; h < kZreBytesPerThread / 16; ++h)
+    for (int h = 0; h < kBytes / 16; ++h)
       unpack16(*reinterpret_cast<const uint4*>(C + j0 + 16 * h), b + 16 * h);
   } else {
 #pragma unroll
-    for (int i = 0; i < kZreBytesPerThread; ++i)
-      b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
+    for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
   }
-  uint32_t s = 0;
+  uint32_t sum = 0;
 #pragma unroll
-  for (int i = 0; i < kZreBytesPerThread; ++i)
-    if ((uint32_t)i < cnt) s += expanded_len(b[i]);
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+#pragma unroll
+  for (int h = 0; h < kBytes / 16; ++h) {
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int t = 0; t < 16; ++t) w[t >> 2] |= (uint32_t)b[16 * h + t] << (8 * (t & 3));
+    *reinterpret_cast<uint4*>(s_c + threadIdx.x * kBytes + 16 * h) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
 
-  uint32_t incl = s;
+  uint32_t incl = sum;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
     uint32_t o = __shfl_up(incl, d, 64);
@@ -423,6 +436,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
     if ((uint32_t)w < wid) wpre += s_wave[w];
     agg += s_wave[w];
   }
+  s_toff[threadIdx.x] = wpre + incl - sum;  // tile-relative start of this thread's output
 
   if (wid == 0) {
     bool fault = false;
@@ -448,19 +462,67 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
   __syncthreads();
   if (s_fault) return;
 
-  uint64_t o = s_excl + wpre + (incl - s);
+  const uint64_t O = s_excl;
+  const uint64_t end = min<uint64_t>(O + agg, m);
+  if (O >= end) return;
+  const uint64_t base = O & ~(uint64_t)15;
+  const uint64_t share = (((end - base) + kThreads - 1) / kThreads + 15) & ~(uint64_t)15;
+  const uint64_t g0 = max<uint64_t>(base + threadIdx.x * share, O);
+  const uint64_t g1 = min<uint64_t>(base + (threadIdx.x + 1) * share, end);
+  if (g0 >= g1) return;
+  const uint32_t rel = (uint32_t)(g0 - O);
+  // last thread whose output starts at or before rel (threads with bytes
+  // have strictly increasing starts; empty ones sit at the tile's end)
+  uint32_t th = 0;
 #pragma unroll
-  for (int i = 0; i < kZreBytesPerThread; ++i) {
-    if ((uint32_t)i < cnt) {
-      const uint32_t x = b[i];
-      if (x < kRunBase) {
-        if (o < m) Q[o] = (uint8_t)x;
-        o += 1;
-      } else {
-        const uint32_t k = x - (kRunBase - 2u);
-        fill_zero_groups(Q, o, k, m);
-        o += k;
+  for (uint32_t step = kThreads / 2; step >= 1; step >>= 1)
+    if (s_toff[th + step] <= rel) th += step;
+  uint32_t i = th * kBytes;
+  const uint32_t i_last = min<uint32_t>((th + 1) * kBytes, (uint32_t)kZreTile) - 1;
+  uint32_t pos = s_toff[th];
+  uint32_t cb = s_c[i];
+  uint32_t len = expanded_len(cb);
+  while (pos + len <= rel && i < i_last) {
+    pos += len;
+    cb = s_c[++i];
+    len = expanded_len(cb);
+  }
+  // current segment: `val` repeated `rem` more times; consecutive run codes
+  // are merged into one segment so an all-121 chunk costs one step
+  uint32_t val = cb < kRunBase ? cb : kZeroGroup;
+  uint32_t rem = pos + len - rel;
+  uint32_t nxt = i + 1;
+  for (uint64_t p0 = g0 & ~(uint64_t)15; p0 < g1; p0 += 16) {
+    const uint32_t fs = (uint32_t)(max(p0, g0) - p0);
+    const uint32_t fe = (uint32_t)(min(p0 + 16, g1) - p0);
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    for (uint32_t f = fs; f < fe;) {
+      if (rem == 0u) {
+        const uint32_t x = nxt < (uint32_t)kZreTile ? s_c[nxt] : 0u;
+        ++nxt;
+        if (x < kRunBase) {
+          val = x;
+          rem = 1u;
+        } else {
+          val = kZeroGroup;
+          rem = expanded_len(x);
+          while (rem < 64u && nxt < (uint32_t)kZreTile && s_c[nxt] >= kRunBase)
+            rem += expanded_len(s_c[nxt++]);
+        }
       }
+      const uint32_t take = min(rem, fe - f);
+      const uint32_t rep = val * 0x01010101u;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) w[k] |= rep & byte_mask(f, f + take, k);
+      f += take;
+      rem -= take;
+    }
+    if (fs == 0u && fe == 16u) {
+      *reinterpret_cast<uint4*>(Q + p0) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 16; ++t)
+        if ((uint32_t)t >= fs && (uint32_t)t < fe) Q[p0 + t] = (uint8_t)(w[t >> 2] >> (8 * (t & 3)));
     }
   }
 }
@@ -575,26 +637,17 @@ hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
   return hipGetLastError();
 }
 
-hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint64_t m,
-                             float s, const uint32_t* partials, uint32_t npartials,
-                             uint8_t* Q, Ctrl* ctrl, hipStream_t st) {
+hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                              uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                              uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
   const bool vec = (m % 4 == 0) && aligned16(x) && aligned16(r);
-  const uint64_t items = vec ? (m >> 2) : m;
-  const uint32_t blocks = blocks_for(items, kThreads, kQuantMaxBlocks);
   if (vec)
-    tlc_quant_pack_kernel<true><<<blocks, kThreads, 0, st>>>(x, r, n, m, s, partials,
-                                                             npartials, Q, ctrl);
+    tlc_quant_encode_kernel<true><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   else
-    tlc_quant_pack_kernel<false><<<blocks, kThreads, 0, st>>>(x, r, n, m, s, partials,
-                                                              npartials, Q, ctrl);
-  return hipGetLastError();
-}
-
-hipError_t launch_zre_encode(const uint8_t* Q, uint32_t m, uint8_t* out,
-                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                             uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  tlc_zre_encode_kernel<<<ntiles, kThreads, 0, st>>>(Q, m, out, status, ticket_base,
-                                                     epoch, ctrl);
+    tlc_quant_encode_kernel<false><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
 

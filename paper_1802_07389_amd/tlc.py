@@ -22,11 +22,10 @@ TLC_E_CORRUPT = -4
 TLC_E_DEVICE = -5
 
 TLC_KERNEL_ABSMAX = 0
-TLC_KERNEL_QUANT_PACK = 1
-TLC_KERNEL_ZRE_ENCODE = 2
-TLC_KERNEL_ZRE_DECODE = 3
-TLC_KERNEL_UNPACK_DEQUANT = 4
-TLC_KERNEL_COUNT = 5
+TLC_KERNEL_QUANT_ENCODE = 1
+TLC_KERNEL_ZRE_DECODE = 2
+TLC_KERNEL_UNPACK_DEQUANT = 3
+TLC_KERNEL_COUNT = 4
 
 EXPORTS = (
     "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_destroy",
