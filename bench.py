@@ -30,15 +30,14 @@ METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compress
 KERNEL_SRC = os.path.join(ROOT, "paper_1802_07389_amd", "csrc", "tlc_kernels.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_traffic.md")
 
-# Algorithmic HBM bytes per element of each kernel (m = n/5 quartic bytes,
-# c = compressed bytes, all fp32 tensors 4 B/value).
+# Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, all
+# fp32 tensors 4 B/value; the quartic bytes never leave LDS).
 def algorithmic_bytes(n, c):
-    m = -(-n // 5)
     return {
         "tlc_absmax_kernel": 8 * n,                # read x, r
         "tlc_quant_encode_kernel": 12 * n + c,     # read x, r; write r, C
-        "tlc_zre_decode_kernel": c + m,            # read C; write Q
-        "tlc_unpack_dequant_kernel": m + 8 * n,    # read Q; read+write out
+        "tlc_zre_index_kernel": c,                 # read C (writes m/4096 index words)
+        "tlc_expand_dequant_kernel": c + 8 * n,    # read C; read+write out
     }
 
 
@@ -185,7 +184,7 @@ def main():
     traffic = measured_traffic(n)
 
     enc_k = ["tlc_absmax_kernel", "tlc_quant_encode_kernel"]
-    dec_k = ["tlc_zre_decode_kernel", "tlc_unpack_dequant_kernel"]
+    dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
     dec_kernel_ms = sum(kern[k][0] for k in dec_k)
     enc_bytes = sum(algo[k] for k in enc_k)

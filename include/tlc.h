@@ -69,7 +69,8 @@ size_t tlc_max_compressed_bytes(size_t n);
 
 /* Create a context for tensors of up to max_n values (1 <= max_n <=
  * TLC_MAX_N) whose work is issued on `hip_stream` (a hipStream_t, or NULL).
- * Allocates about max_n/5 bytes plus max_n/1024 bytes of device workspace.
+ * Allocates about max_n/2000 bytes of device workspace (look-back status
+ * words and a start index for the decoder).
  * On success *ctx receives the context; on failure *ctx is NULL. */
 int tlc_ctx_create(tlc_ctx** ctx, size_t max_n, void* hip_stream);
 
@@ -115,8 +116,8 @@ const char* tlc_last_error_string(void);
 
 #define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| (Eq. 1) */
 #define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, zero-run encoding */
-#define TLC_KERNEL_ZRE_DECODE 2     /* zero-run expansion */
-#define TLC_KERNEL_UNPACK_DEQUANT 3 /* quartic unpack, Eq. 3, accumulate */
+#define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts */
+#define TLC_KERNEL_EXPAND_DEQUANT 3 /* zero-run expansion, quartic unpack, Eq. 3 */
 #define TLC_KERNEL_COUNT 4
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around

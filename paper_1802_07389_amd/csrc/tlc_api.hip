@@ -42,8 +42,8 @@ bool overlap(const void* a, size_t an, const void* b, size_t bn) {
 }
 
 const char* const kKernelNames[TLC_KERNEL_COUNT] = {
-    "tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_decode_kernel",
-    "tlc_unpack_dequant_kernel"};
+    "tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
+    "tlc_expand_dequant_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -63,7 +63,7 @@ struct tlc_ctx {
   uint32_t* partials = nullptr;
   uint64_t* enc_status = nullptr;
   uint64_t* dec_status = nullptr;
-  uint8_t* Q = nullptr;
+  uint64_t* start = nullptr;  // per kDecRange quartic bytes: (stream index, skip)
   size_t enc_status_words = 0;
   size_t dec_status_words = 0;
   // pinned host readback
@@ -193,14 +193,15 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
     delete c;
     return hip_fail(e, "hipGetDevice");
   }
-  // layout: ctrl | partials | enc status | dec status | Q
+  // layout: ctrl | partials | enc status | dec status | start index
   c->enc_status_words = (c->max_m + kEncTile - 1) / kEncTile + 1;
   c->dec_status_words = (c->max_m + kZreTile - 1) / kZreTile + 1;
   const size_t off_partials = sizeof(Ctrl);
   const size_t off_enc = round_up(off_partials + kAbsmaxMaxBlocks * sizeof(uint32_t), 256);
   const size_t off_dec = round_up(off_enc + c->enc_status_words * sizeof(uint64_t), 256);
-  const size_t off_q = round_up(off_dec + c->dec_status_words * sizeof(uint64_t), 256);
-  const size_t total = off_q + round_up(c->max_m, 16) + 64;
+  const size_t off_start = round_up(off_dec + c->dec_status_words * sizeof(uint64_t), 256);
+  const size_t start_words = (c->max_m + kDecRange - 1) / kDecRange + 1;
+  const size_t total = off_start + start_words * sizeof(uint64_t);
   e = hipMalloc(&c->ws, total);
   if (e != hipSuccess) {
     delete c;
@@ -211,8 +212,8 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
   c->partials = (uint32_t*)(base + off_partials);
   c->enc_status = (uint64_t*)(base + off_enc);
   c->dec_status = (uint64_t*)(base + off_dec);
-  c->Q = base + off_q;
-  e = hipMemset(c->ws, 0, off_q);
+  c->start = (uint64_t*)(base + off_start);
+  e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e == hipSuccess)
     e = hipHostMalloc((void**)&c->rb, sizeof(HostReadback), hipHostMallocDefault);
@@ -323,15 +324,15 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
     if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
   }
   const uint32_t ntiles = (uint32_t)((bytes_len + kZreTile - 1) / kZreTile);
-  st = timed_launch(c, TLC_KERNEL_ZRE_DECODE, [&] {
-    return launch_zre_decode(bytes, (uint32_t)bytes_len, c->Q, (uint32_t)m, c->dec_status,
-                             ntiles, c->dec_ticket_base, epoch, c->ctrl, c->stream);
+  st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
+    return launch_zre_index(bytes, (uint32_t)bytes_len, (uint32_t)m, c->start, c->dec_status,
+                            ntiles, c->dec_ticket_base, epoch, c->ctrl, c->stream);
   });
   if (st) return st;
   c->dec_ticket_base += ntiles;
-  st = timed_launch(c, TLC_KERNEL_UNPACK_DEQUANT, [&] {
-    return launch_unpack_dequant(c->Q, n, m, scale, out, accumulate, epoch, c->ctrl,
-                                 c->stream);
+  st = timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
+    return launch_expand_dequant(bytes, (uint32_t)bytes_len, c->start, n, m, scale, out,
+                                 accumulate, epoch, c->ctrl, c->stream);
   });
   return st;
 }

@@ -12,8 +12,8 @@ constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
 constexpr int kZreBytesPerThread = 32;    // zero-run scans: two uint4 per thread
 constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
+constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
 constexpr uint32_t kAbsmaxMaxBlocks = 512;  // partial maxima per encode
-constexpr uint32_t kUnpackMaxBlocks = 1u << 16;
 
 // Device control block (one per context, in the workspace).  The first 16
 // bytes are copied to pinned host memory after every encode.
@@ -47,13 +47,12 @@ hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m,
                               const uint32_t* partials, uint32_t npartials, uint8_t* out,
                               uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                               uint32_t epoch, Ctrl* ctrl, hipStream_t st);
-hipError_t launch_zre_decode(const uint8_t* C, uint32_t c, uint8_t* Q,
-                             uint32_t m, uint64_t* status, uint32_t ntiles,
-                             uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                             hipStream_t st);
-hipError_t launch_unpack_dequant(const uint8_t* Q, uint64_t n, uint64_t m,
-                                 float scale, float* out, int accumulate,
-                                 uint32_t epoch, const Ctrl* ctrl,
+hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
+                           uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                           uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
+                                 uint64_t n, uint64_t m, float scale, float* out,
+                                 int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                  hipStream_t st);
 
 // Epoch widths of the two look-back status layouts.

@@ -4,8 +4,10 @@
 //   tlc_quant_encode_kernel    M, 3-value quantization, residual write-back,
 //                              quartic pack and zero-run encoding in one
 //                              pass              (Eq. 1-2, Sections 3.2-3.3)
-//   tlc_zre_decode_kernel      zero-run expansion, one pass
-//   tlc_unpack_dequant_kernel  quartic unpack, Eq. 3, optional accumulate
+//   tlc_zre_index_kernel       zero-run scan: where each 4096-byte range of
+//                              quartic bytes starts in the stream
+//   tlc_expand_dequant_kernel  zero-run expansion into LDS, quartic unpack,
+//                              Eq. 3, optional accumulate
 //
 // All of it is HBM streaming or byte scanning; nothing is a dense
 // contraction, so there is no MFMA here.  fp32 arithmetic is exactly the
@@ -357,32 +359,20 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
 }
 
 // ---------------------------------------------------------------- expansion
-// Mask of the bytes of little-endian word k (bytes 4k .. 4k+3 of a 16-byte
-// chunk) that lie in [a, b).
-__device__ __forceinline__ uint32_t byte_mask(uint32_t a, uint32_t b, int k) {
-  const int lo = min(max((int)a - 4 * k, 0), 4);
-  const int hi = min(max((int)b - 4 * k, 0), 4);
-  if (hi <= lo) return 0u;
-  const uint32_t upto_hi = hi == 4 ? 0xffffffffu : ((1u << (8 * hi)) - 1u);
-  return upto_hi & ~((1u << (8 * lo)) - 1u);
-}
-
 __device__ __forceinline__ uint32_t expanded_len(uint32_t b) {
   return b < kRunBase ? 1u : b - (kRunBase - 2u);
 }
 
 // One tile = 256 threads x 32 stream bytes.  Expansion lengths are scanned
-// in the block and across tiles (decoupled look-back) to place the tile's
-// output at [O, O + E) of the quartic buffer.  The output range is then cut
-// into 256 equal 16-byte aligned slices, one per thread: a thread finds the
-// stream byte covering its slice start (binary search over the per-thread
-// offsets, then a short walk) and expands forward, writing whole uint4
-// chunks (byte stores only where a chunk is shared with a neighbouring
-// tile).  Every thread gets the same amount of output whatever the run
-// structure.  Writes stop at m; the last tile flags the launch's epoch as
-// corrupt when the total is not exactly m.
-__global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
-    const uint8_t* __restrict__ C, uint32_t c, uint8_t* __restrict__ Q, uint32_t m,
+// in the block and across tiles (decoupled look-back), which places every
+// stream byte's expansion in the quartic byte string.  Nothing is expanded
+// here: the byte whose expansion contains position k * kDecRange records
+// (its index, how far into its expansion that position lies) in start[k],
+// so each block of the expanding kernel can find its part of the stream
+// with one load.  The last tile flags the launch's epoch as corrupt when
+// the expansion total is not exactly m.
+__global__ __launch_bounds__(kThreads) void tlc_zre_index_kernel(
+    const uint8_t* __restrict__ C, uint32_t c, uint32_t m, uint64_t* __restrict__ start,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
     Ctrl* __restrict__ ctrl) {
   constexpr int kBytes = kZreBytesPerThread;
@@ -390,8 +380,6 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
   __shared__ uint32_t s_fault;
   __shared__ uint32_t s_wave[kWaves];
   __shared__ uint64_t s_excl;
-  __shared__ uint32_t s_toff[kThreads];
-  __shared__ __align__(16) uint8_t s_c[kZreTile];
 
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
   __syncthreads();
@@ -413,14 +401,6 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
 #pragma unroll
   for (int i = 0; i < kBytes; ++i)
     if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
-#pragma unroll
-  for (int h = 0; h < kBytes / 16; ++h) {
-    uint32_t w[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int t = 0; t < 16; ++t) w[t >> 2] |= (uint32_t)b[16 * h + t] << (8 * (t & 3));
-    *reinterpret_cast<uint4*>(s_c + threadIdx.x * kBytes + 16 * h) =
-        make_uint4(w[0], w[1], w[2], w[3]);
-  }
 
   uint32_t incl = sum;
 #pragma unroll
@@ -436,7 +416,6 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
     if ((uint32_t)w < wid) wpre += s_wave[w];
     agg += s_wave[w];
   }
-  s_toff[threadIdx.x] = wpre + incl - sum;  // tile-relative start of this thread's output
 
   if (wid == 0) {
     bool fault = false;
@@ -462,67 +441,15 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_decode_kernel(
   __syncthreads();
   if (s_fault) return;
 
-  const uint64_t O = s_excl;
-  const uint64_t end = min<uint64_t>(O + agg, m);
-  if (O >= end) return;
-  const uint64_t base = O & ~(uint64_t)15;
-  const uint64_t share = (((end - base) + kThreads - 1) / kThreads + 15) & ~(uint64_t)15;
-  const uint64_t g0 = max<uint64_t>(base + threadIdx.x * share, O);
-  const uint64_t g1 = min<uint64_t>(base + (threadIdx.x + 1) * share, end);
-  if (g0 >= g1) return;
-  const uint32_t rel = (uint32_t)(g0 - O);
-  // last thread whose output starts at or before rel (threads with bytes
-  // have strictly increasing starts; empty ones sit at the tile's end)
-  uint32_t th = 0;
+  uint64_t o = s_excl + wpre + incl - sum;  // where this thread's first byte expands
 #pragma unroll
-  for (uint32_t step = kThreads / 2; step >= 1; step >>= 1)
-    if (s_toff[th + step] <= rel) th += step;
-  uint32_t i = th * kBytes;
-  const uint32_t i_last = min<uint32_t>((th + 1) * kBytes, (uint32_t)kZreTile) - 1;
-  uint32_t pos = s_toff[th];
-  uint32_t cb = s_c[i];
-  uint32_t len = expanded_len(cb);
-  while (pos + len <= rel && i < i_last) {
-    pos += len;
-    cb = s_c[++i];
-    len = expanded_len(cb);
-  }
-  // current segment: `val` repeated `rem` more times; consecutive run codes
-  // are merged into one segment so an all-121 chunk costs one step
-  uint32_t val = cb < kRunBase ? cb : kZeroGroup;
-  uint32_t rem = pos + len - rel;
-  uint32_t nxt = i + 1;
-  for (uint64_t p0 = g0 & ~(uint64_t)15; p0 < g1; p0 += 16) {
-    const uint32_t fs = (uint32_t)(max(p0, g0) - p0);
-    const uint32_t fe = (uint32_t)(min(p0 + 16, g1) - p0);
-    uint32_t w[4] = {0u, 0u, 0u, 0u};
-    for (uint32_t f = fs; f < fe;) {
-      if (rem == 0u) {
-        const uint32_t x = nxt < (uint32_t)kZreTile ? s_c[nxt] : 0u;
-        ++nxt;
-        if (x < kRunBase) {
-          val = x;
-          rem = 1u;
-        } else {
-          val = kZeroGroup;
-          rem = expanded_len(x);
-          while (rem < 64u && nxt < (uint32_t)kZreTile && s_c[nxt] >= kRunBase)
-            rem += expanded_len(s_c[nxt++]);
-        }
-      }
-      const uint32_t take = min(rem, fe - f);
-      const uint32_t rep = val * 0x01010101u;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) w[k] |= rep & byte_mask(f, f + take, k);
-      f += take;
-      rem -= take;
-    }
-    if (fs == 0u && fe == 16u) {
-      *reinterpret_cast<uint4*>(Q + p0) = make_uint4(w[0], w[1], w[2], w[3]);
-    } else {
-#pragma unroll
-      for (int t = 0; t < 16; ++t)
-        if ((uint32_t)t >= fs && (uint32_t)t < fe) Q[p0 + t] = (uint8_t)(w[t >> 2] >> (8 * (t & 3)));
+  for (int i = 0; i < kBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t len = expanded_len(b[i]);
+      const uint64_t k = (o + kDecRange - 1) / kDecRange;  // first range start >= o
+      const uint64_t at = k * kDecRange;
+      if (at < o + len && at < m) start[k] = ((j0 + i) << 8) | (at - o);
+      o += len;
     }
   }
 }
@@ -546,21 +473,96 @@ __device__ __forceinline__ void digits5(uint32_t byte, uint32_t (&t)[5]) {
   t[4] = byte - t[3] * 3u;
 }
 
+// Writes bytes of 121 at lds[lo..hi).
+__device__ __forceinline__ void fill_zero_groups(uint8_t* lds, uint32_t lo, uint32_t hi) {
+  while (lo < hi && (lo & 3u)) lds[lo++] = (uint8_t)kZeroGroup;
+  for (; lo + 4 <= hi; lo += 4) *reinterpret_cast<uint32_t*>(lds + lo) = 0x79797979u;
+  while (lo < hi) lds[lo++] = (uint8_t)kZeroGroup;
+}
+
+// One block = quartic bytes [k*kDecRange, (k+1)*kDecRange).  Phase 1
+// expands the stream bytes that cover the range (found through start[k])
+// into LDS: the bytes are spread over the threads, a block scan of their
+// expansion lengths gives each one its position, and each thread writes
+// its expansions.  Phase 2 unpacks the base-3 digits of every quartic byte
+// (Section 3.2 decoding), dequantizes (Eq. 3) and stores or accumulates
+// into the five partitions of out, with float4 accesses when m % 4 == 0
+// and out is 16-byte aligned.
 template <bool kVec, bool kAcc>
-__global__ __launch_bounds__(kThreads) void tlc_unpack_dequant_kernel(
-    const uint8_t* __restrict__ Q, uint64_t n, uint64_t m, float M,
-    float* __restrict__ out, uint32_t epoch, const Ctrl* __restrict__ ctrl) {
+__global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
+    const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ start,
+    uint64_t n, uint64_t m, float M, float* __restrict__ out, uint32_t epoch,
+    const Ctrl* __restrict__ ctrl) {
+  constexpr int kBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
+  __shared__ uint32_t s_wave[kWaves];
+  __shared__ __align__(16) uint8_t s_q[kDecRange];
   if (ctrl->dec_bad_epoch == epoch) return;  // corrupt stream: out untouched
-  const uint64_t tid = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
+
+  // ---- phase 1: zero-run expansion of this range into LDS
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint64_t q0 = (uint64_t)blockIdx.x * kDecRange;
+  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  const uint64_t s0 = start[blockIdx.x];
+  const uint32_t i0 = (uint32_t)(s0 >> 8);
+  const uint32_t skip = (uint32_t)(s0 & 255u);
+  uint32_t i1 = c;  // one past the last stream byte that reaches into the range
+  if (q0 + kDecRange < m) {
+    const uint64_t s1 = start[blockIdx.x + 1];
+    i1 = (uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u);
+  }
+  i1 = min(i1, c);
+  const uint32_t count = i1 > i0 ? min<uint32_t>(i1 - i0, kDecRange) : 0u;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < count ? min<uint32_t>(kBytes, count - lo) : 0u;
+  uint8_t b[kBytes];
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[i0 + lo + i] : (uint8_t)0;
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+  uint32_t incl = sum;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t o = __shfl_up(incl, d, 64);
+    if (lane >= (uint32_t)d) incl += o;
+  }
+  if (lane == 63) s_wave[wid] = incl;
+  __syncthreads();
+  uint32_t wpre = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w)
+    if ((uint32_t)w < wid) wpre += s_wave[w];
+  int pos = (int)(wpre + incl - sum) - (int)skip;  // range-relative start of b[0]
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t x = b[i];
+      const int len = (int)expanded_len(x);
+      const uint32_t a = (uint32_t)max(pos, 0);
+      const uint32_t e = (uint32_t)min(pos + len, (int)qn);
+      if (a < e) {
+        if (x < kRunBase)
+          s_q[a] = (uint8_t)x;
+        else
+          fill_zero_groups(s_q, a, e);
+      }
+      pos += len;
+    }
+  }
+  __syncthreads();
+
+  // ---- phase 2: Section 3.2 decoding and Eq. 3
   if (kVec) {
-    const uint64_t groups = m >> 2;
-    for (uint64_t g = tid; g < groups; g += stride) {
-      const uint64_t j = g << 2;
-      const uint32_t w = *reinterpret_cast<const uint32_t*>(Q + j);
+#pragma unroll
+    for (int g = 0; g < kDecRange / (4 * kThreads); ++g) {
+      const uint32_t jl = 4u * (threadIdx.x + kThreads * g);
+      if (jl >= qn) break;
+      const uint64_t j = q0 + jl;
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(s_q + jl);
       uint32_t t[4][5];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) digits5((w >> (8 * c)) & 0xffu, t[c]);
+      for (int cc = 0; cc < 4; ++cc) digits5((w >> (8 * cc)) & 0xffu, t[cc]);
       if (4 * m + j + 4 <= n) {
         float4 o[5];
         if (kAcc) {
@@ -582,14 +584,14 @@ __global__ __launch_bounds__(kThreads) void tlc_unpack_dequant_kernel(
           }
           *reinterpret_cast<float4*>(out + k * m + j) = o[k];
         }
-      } else {
+      } else {  // the group whose p4 slice reaches into the padding
 #pragma unroll
         for (int k = 0; k < 5; ++k) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint64_t e = k * m + j + c;
+          for (int cc = 0; cc < 4; ++cc) {
+            const uint64_t e = k * m + j + cc;
             if (e < n) {
-              const float v = trit_value(t[c][k], M);
+              const float v = trit_value(t[cc][k], M);
               out[e] = kAcc ? out[e] + v : v;
             }
           }
@@ -597,9 +599,10 @@ __global__ __launch_bounds__(kThreads) void tlc_unpack_dequant_kernel(
       }
     }
   } else {
-    for (uint64_t j = tid; j < m; j += stride) {
+    for (uint32_t jl = threadIdx.x; jl < qn; jl += kThreads) {
+      const uint64_t j = q0 + jl;
       uint32_t t[5];
-      digits5(Q[j], t);
+      digits5(s_q[jl], t);
 #pragma unroll
       for (int k = 0; k < 5; ++k) {
         const uint64_t e = k * m + j;
@@ -651,35 +654,29 @@ hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m,
   return hipGetLastError();
 }
 
-hipError_t launch_zre_decode(const uint8_t* C, uint32_t c, uint8_t* Q, uint32_t m,
-                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                             uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  tlc_zre_decode_kernel<<<ntiles, kThreads, 0, st>>>(C, c, Q, m, status, ticket_base,
-                                                     epoch, ctrl);
+hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
+                           uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                           uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+  tlc_zre_index_kernel<<<ntiles, kThreads, 0, st>>>(C, c, m, start, status, ticket_base, epoch,
+                                                    ctrl);
   return hipGetLastError();
 }
 
-hipError_t launch_unpack_dequant(const uint8_t* Q, uint64_t n, uint64_t m, float scale,
-                                 float* out, int accumulate, uint32_t epoch,
-                                 const Ctrl* ctrl, hipStream_t st) {
+hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
+                                 uint64_t n, uint64_t m, float scale, float* out,
+                                 int accumulate, uint32_t epoch, const Ctrl* ctrl,
+                                 hipStream_t st) {
   const bool vec = (m % 4 == 0) && aligned16(out);
-  const uint64_t items = vec ? (m >> 2) : m;
-  const uint32_t blocks = blocks_for(items, kThreads, kUnpackMaxBlocks);
+  const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
+#define TLC_LAUNCH(V, A)                                                                     \
+  tlc_expand_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, out, \
+                                                               epoch, ctrl)
   if (vec) {
-    if (accumulate)
-      tlc_unpack_dequant_kernel<true, true><<<blocks, kThreads, 0, st>>>(Q, n, m, scale, out,
-                                                                         epoch, ctrl);
-    else
-      tlc_unpack_dequant_kernel<true, false><<<blocks, kThreads, 0, st>>>(Q, n, m, scale,
-                                                                          out, epoch, ctrl);
+    if (accumulate) TLC_LAUNCH(true, true); else TLC_LAUNCH(true, false);
   } else {
-    if (accumulate)
-      tlc_unpack_dequant_kernel<false, true><<<blocks, kThreads, 0, st>>>(Q, n, m, scale,
-                                                                          out, epoch, ctrl);
-    else
-      tlc_unpack_dequant_kernel<false, false><<<blocks, kThreads, 0, st>>>(Q, n, m, scale,
-                                                                           out, epoch, ctrl);
+    if (accumulate) TLC_LAUNCH(false, true); else TLC_LAUNCH(false, false);
   }
+#undef TLC_LAUNCH
   return hipGetLastError();
 }
 

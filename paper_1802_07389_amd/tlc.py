@@ -23,8 +23,8 @@ TLC_E_DEVICE = -5
 
 TLC_KERNEL_ABSMAX = 0
 TLC_KERNEL_QUANT_ENCODE = 1
-TLC_KERNEL_ZRE_DECODE = 2
-TLC_KERNEL_UNPACK_DEQUANT = 3
+TLC_KERNEL_ZRE_INDEX = 2
+TLC_KERNEL_EXPAND_DEQUANT = 3
 TLC_KERNEL_COUNT = 4
 
 EXPORTS = (

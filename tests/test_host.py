@@ -38,8 +38,8 @@ def test_host_only_entry_points():
     for n in list(range(0, 50)) + [2 ** 20, 2 ** 28, 25_600_000, 4294967295]:
         assert tlc.tlc_max_compressed_bytes(n) == -(-n // 5)
     names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
-    assert names == ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_decode_kernel",
-                     "tlc_unpack_dequant_kernel"]
+    assert names == ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
+                     "tlc_expand_dequant_kernel"]
     assert tlc.tlc_kernel_name(99) is None
 
 
