@@ -27,7 +27,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compression ratio"
-KERNEL_SRC = os.path.join(ROOT, "paper_1802_07389_amd", "csrc", "tlc_kernels.hip")
+KERNEL_SRC = [os.path.join(ROOT, "paper_1802_07389_amd", "csrc", f)
+              for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_traffic.md")
 
 # Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, all
@@ -42,8 +43,12 @@ def algorithmic_bytes(n, c):
 
 
 def kernel_source_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the sources the dominant (encoder) kernel is built from."""
+    h = hashlib.sha256()
+    for p in KERNEL_SRC:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(n):
@@ -92,6 +97,94 @@ def cpu_baseline(x, s):
     }
 
 
+def _time_config(torch, tlc, ctx, tensors, s, reps, dev, oracle_reps=1, acc=True):
+    """Encode then decode (accumulate) each tensor of a list, carrying one
+    residual per tensor; returns per-config figures and the oracle's."""
+    import oracle
+    xs = [torch.from_numpy(t).to(dev) for t in tensors]
+    rs = [torch.zeros_like(x) for x in xs]
+    outs = [torch.zeros_like(x) for x in xs]
+    bufs = [torch.empty(tlc.tlc_max_compressed_bytes(x.numel()), dtype=torch.uint8,
+                        device=dev) for x in xs]
+    total = sum(x.numel() for x in xs)
+    lens = []
+
+    def one_pass():
+        te = td = 0.0
+        lens.clear()
+        for x, r, o, b in zip(xs, rs, outs, bufs):
+            t0 = time.perf_counter()
+            C, M = ctx.compress(x, r, s, out=b)
+            t1 = time.perf_counter()
+            ctx.decompress(C, M, x.numel(), o, accumulate=acc)
+            ctx.sync()
+            t2 = time.perf_counter()
+            te += t1 - t0
+            td += t2 - t1
+            lens.append(C.numel())
+        return te, td
+
+    one_pass()
+    te = td = 0.0
+    for _ in range(reps):
+        a, b = one_pass()
+        te += a
+        td += b
+    ratio = 4 * total / (sum(lens) + 4 * len(lens))
+    # oracle: the same sequence on one core
+    r_host = [np.zeros(t.size, np.float32) for t in tensors]
+    o_host = [np.zeros(t.size, np.float32) for t in tensors]
+    oe = od = 0.0
+    for _ in range(oracle_reps):
+        for t, r, o in zip(tensors, r_host, o_host):
+            t0 = time.perf_counter()
+            st, C, M = oracle.compress(t, r, s)
+            t1 = time.perf_counter()
+            oracle.decompress(C, M, t.size, o, accumulate=acc)
+            t2 = time.perf_counter()
+            oe += t1 - t0
+            od += t2 - t1
+    gb = 4 * total * reps / 1e9
+    ogb = 4 * total * oracle_reps / 1e9
+    return {
+        "values": total, "tensors": len(tensors), "s": s,
+        "encode_GBps": round(gb / te, 2), "decode_GBps": round(gb / td, 2),
+        "round_trip_GBps": round(gb / (te + td), 2),
+        "ms_per_round_trip": round((te + td) / reps * 1e3, 4),
+        "ratio": round(ratio, 2), "ratio_payload_only": round(4 * total / sum(lens), 2),
+        "oracle_encode_GBps": round(ogb / oe, 4), "oracle_decode_GBps": round(ogb / od, 4),
+        "oracle_cores": 1,
+    }
+
+
+def report(torch, tlc, workloads, dev):
+    """One JSON line per config (C1-C5): GPU and oracle GB/s of fp32 input and
+    the compression ratio.  Each GPU figure includes the host sync of
+    tlc_compress (it returns the stream length)."""
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+    ctx = tlc.Context(max_n=workloads.C4_N, stream=torch.cuda.current_stream(dev), device=dev)
+    rows = []
+    rows.append(("C1", _time_config(torch, tlc, ctx, [workloads.c1_tensor()], workloads.C1_S,
+                                     20, dev, oracle_reps=3)))
+    sizes = workloads.c2_sizes()
+    grads = [workloads.c2_gradient(0, t, n) for t, n in enumerate(sizes)]
+    rows.append(("C2", _time_config(torch, tlc, ctx, grads, workloads.C2_S, 5, dev,
+                                     oracle_reps=3, acc=False)))
+    x3 = workloads.c3_tensor()
+    for s3 in workloads.C3_S:
+        rows.append((f"C3 s={s3}", _time_config(torch, tlc, ctx, [x3], s3, 10, dev)))
+    rows.append(("C4", _time_config(torch, tlc, ctx, [workloads.c4_tensor(0)], workloads.C4_S,
+                                     10, dev)))
+    rows.append(("C5 payload", _time_config(torch, tlc, ctx, [workloads.c5_tensor(0)],
+                                             workloads.C5_S, 10, dev)))
+    ctx.close()
+    for name, row in rows:
+        print(json.dumps({"config": name, **row}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +194,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 1 GiB device copies (counter calibration)")
+    ap.add_argument("--report", action="store_true",
+                    help="per-config report (C1-C5) instead of the headline line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -122,6 +217,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes_read": 4 << 28,
                           "calibrate_copy_bytes_written": 4 << 28, "launches": 5}))
+        return
+
+    if args.report:
+        report(torch, tlc, workloads, dev)
         return
 
     n = args.n or workloads.C4_N
@@ -226,7 +325,7 @@ def main():
         "decode_kernels_hbm_frac": round(dec_bytes / (dec_kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "encode_kernel_ms": round(enc_kernel_ms, 5),
         "decode_kernel_ms": round(dec_kernel_ms, 5),
-        "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items()},
+        "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
         "compression_ratio": round(4 * n / (c_avg + 4), 2),
         "compression_ratio_payload_only": round(4 * n / c_avg, 2),
         "kernel_source_sha256_16": kernel_source_hash(),

@@ -57,9 +57,12 @@ extern "C" {
 #define TLC_E_CORRUPT (-4)   /* compressed stream does not expand to ceil(n/5) bytes */
 #define TLC_E_DEVICE (-5)    /* HIP runtime error, or the context is unusable */
 
-/* Largest tensor one call accepts (the quartic byte count must fit the
- * 30-bit counters of the zero-run scans). */
+/* Largest number of values one call accepts, summed over a batch (the
+ * quartic byte counts must fit the 30-bit counters of the zero-run scans). */
 #define TLC_MAX_N ((size_t)4294967295u)
+
+/* Largest number of tensors (or streams) one batched call accepts. */
+#define TLC_MAX_TENSORS 65536
 
 typedef struct tlc_ctx tlc_ctx;
 
@@ -69,10 +72,20 @@ size_t tlc_max_compressed_bytes(size_t n);
 
 /* Create a context for tensors of up to max_n values (1 <= max_n <=
  * TLC_MAX_N) whose work is issued on `hip_stream` (a hipStream_t, or NULL).
- * Allocates about max_n/2000 bytes of device workspace (look-back status
- * words and a start index for the decoder).
- * On success *ctx receives the context; on failure *ctx is NULL. */
+ * Allocates about max_n/800 bytes of device workspace (partial maxima,
+ * look-back status words and a start index for the decoder).  On success
+ * *ctx receives the context; on failure *ctx is NULL.  Same as
+ * tlc_ctx_create_batch(ctx, max_n, 1, hip_stream). */
 int tlc_ctx_create(tlc_ctx** ctx, size_t max_n, void* hip_stream);
+
+/* Create a context for batched calls: at most max_tensors tensors (or
+ * streams) per call, 1 <= max_tensors <= TLC_MAX_TENSORS, and at most max_n
+ * values per call summed over the batch (for tlc_decompress_sum: count * n).
+ * Each tensor of a batch is still compressed on its own, with its own scale
+ * and error buffer (Section 3: one compression context per tensor); the
+ * batch only shares launches and the host synchronisation. */
+int tlc_ctx_create_batch(tlc_ctx** ctx, size_t max_n, size_t max_tensors,
+                         void* hip_stream);
 
 /* Wait for the context's outstanding work and free it.  NULL is a no-op. */
 int tlc_ctx_destroy(tlc_ctx* ctx);
@@ -105,6 +118,42 @@ int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
 int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
                    float scale, size_t n, float* out, int accumulate);
 
+/* Encode `count` tensors in one pass (two launches, one synchronisation):
+ * for every t, exactly tlc_compress(ctx, tensors[t], residuals[t], ns[t],
+ * s[t], bytes[t], caps[t], &bytes_len[t], &scales[t]).  All arrays are host
+ * arrays of `count` entries; the pointers in them are device pointers, and
+ * buffers of different tensors must not overlap.  Argument errors reject the
+ * whole call before any work.  status[t] receives TLC_OK or
+ * TLC_E_NONFINITE (that tensor's residual and bytes unchanged, bytes_len[t]
+ * = 0); the call returns TLC_E_NONFINITE if any tensor was refused. */
+int tlc_compress_batch(tlc_ctx* ctx, size_t count, const float* const* tensors,
+                       float* const* residuals, const size_t* ns, const float* s,
+                       uint8_t* const* bytes, const size_t* caps, size_t* bytes_len,
+                       float* scales, int* status);
+
+/* Decode `count` streams into `count` outputs in two launches: for every t,
+ * tlc_decompress(ctx, bytes[t], bytes_len[t], scales[t], ns[t], outs[t],
+ * accumulate).  Host arrays of device pointers; outputs must not overlap.
+ * Asynchronous; if any stream is corrupt no output is written and the next
+ * tlc_sync() returns TLC_E_CORRUPT. */
+int tlc_decompress_batch(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes,
+                         const size_t* bytes_len, const float* scales, const size_t* ns,
+                         float* const* outs, int accumulate);
+
+/* Server-side aggregation (Section 2, Fig. 1; Section 3, Fig. 2): decode
+ * `count` streams of the same n-value tensor and add them into one fp32
+ * output in stream order, element by element:
+ *   out = (((accumulate ? out : 0) + v_0) + v_1) + ... + v_{count-1}
+ * (with accumulate == 0 the first term is v_0 itself), bit-identical to
+ * tlc_decompress(stream 0, accumulate) followed by tlc_decompress(stream
+ * t, accumulate = 1) for t = 1 .. count-1, but reading and writing out only
+ * once.  Asynchronous; if any stream is corrupt out is left unchanged and
+ * the next tlc_sync() returns TLC_E_CORRUPT.  count * n must not exceed the
+ * context's max_n. */
+int tlc_decompress_sum(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes,
+                       const size_t* bytes_len, const float* scales, size_t n, float* out,
+                       int accumulate);
+
 /* Wait for all work of the context and return (then clear) the sticky
  * status of asynchronous decodes: TLC_OK or TLC_E_CORRUPT. */
 int tlc_sync(tlc_ctx* ctx);
@@ -118,7 +167,12 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, zero-run encoding */
 #define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts */
 #define TLC_KERNEL_EXPAND_DEQUANT 3 /* zero-run expansion, quartic unpack, Eq. 3 */
-#define TLC_KERNEL_COUNT 4
+#define TLC_KERNEL_ABSMAX_BATCH 4
+#define TLC_KERNEL_QUANT_ENCODE_BATCH 5
+#define TLC_KERNEL_ZRE_INDEX_BATCH 6
+#define TLC_KERNEL_EXPAND_DEQUANT_BATCH 7
+#define TLC_KERNEL_EXPAND_SUM 8     /* multi-stream expansion + summed dequantization */
+#define TLC_KERNEL_COUNT 9
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

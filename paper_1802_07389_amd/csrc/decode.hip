@@ -1,0 +1,447 @@
+// decode.hip -- gfx950 decode kernels of the 3LC path.
+//
+//   tlc_zre_index_kernel / _batch_kernel
+//       zero-run scan: where each kDecRange-byte range of quartic bytes
+//       starts in the stream; checks the expanded length
+//   tlc_expand_dequant_kernel / _batch_kernel
+//       zero-run expansion into LDS, quartic unpack (Section 3.2), Eq. 3,
+//       optional accumulate
+//   tlc_expand_sum_kernel
+//       the same for P streams of one tensor, summed in stream order into
+//       one output in a single pass over it (server-side aggregation)
+//
+// The quartic bytes are never stored in HBM: each block rebuilds its range
+// of them in LDS from the stream.
+#include "device_common.hpp"
+
+namespace tlc {
+
+// ---------------------------------------------------------------- index scan
+struct IdxShared {
+  uint32_t red[kWaves];
+  uint32_t fault;
+  uint64_t excl;
+};
+
+// Tile `lt` (kZreTile stream bytes) of one stream: expansion lengths are
+// scanned in the block and across tiles (decoupled look-back, status slot
+// floor + lt), which places every stream byte's expansion in the quartic
+// byte string.  The byte whose expansion contains position k * kDecRange
+// records (its index, how far into its expansion that position lies) in
+// start[k], so each expanding block finds its part of the stream with one
+// load.  The stream's last tile flags the launch's epoch as corrupt when
+// the expansion total is not exactly m.
+__device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32_t c, uint32_t m,
+                                           uint64_t* __restrict__ start,
+                                           uint64_t* __restrict__ status, uint32_t floor,
+                                           uint32_t lt, uint32_t epoch, Ctrl* __restrict__ ctrl,
+                                           IdxShared& sh) {
+  constexpr int kBytes = kZreBytesPerThread;
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint64_t j0 = (uint64_t)lt * kZreTile + threadIdx.x * kBytes;
+  const uint32_t cnt = j0 < c ? (uint32_t)min<uint64_t>(kBytes, c - j0) : 0u;
+
+  uint8_t b[kBytes];
+  if (cnt == (uint32_t)kBytes && ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
+#pragma unroll
+    for (int h = 0; h < kBytes / 16; ++h)
+      unpack16(*reinterpret_cast<const uint4*>(C + j0 + 16 * h), b + 16 * h);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
+  }
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+  const ScanU32 sc = block_scan_u32(sum, sh.red);
+  const uint32_t agg = sc.total;
+
+  if (wid == 0) {
+    bool fault = false;
+    uint64_t ex = 0;
+    if (lt == 0) {
+      if (lane == 0) status_publish(&status[floor], DecSW::pack(agg, kFlagPrefix, epoch));
+    } else {
+      ex = lookback_wave<DecSW>(status, floor, floor + lt, agg, 0, epoch, SumOp(), &fault);
+    }
+    if (lane == 0) {
+      sh.excl = ex;
+      sh.fault = fault ? 1u : 0u;
+      if (fault)
+        __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const bool last_tile = (uint64_t)(lt + 1) * kZreTile >= c;
+      if (last_tile && (fault || ex + agg != m)) {
+        __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&ctrl->dec_corrupt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+  __syncthreads();
+  if (sh.fault) return;
+
+  uint64_t o = sh.excl + sc.excl;  // where this thread's first byte expands
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t len = expanded_len(b[i]);
+      const uint64_t k = (o + kDecRange - 1) / kDecRange;  // first range start >= o
+      const uint64_t at = k * kDecRange;
+      if (at < o + len && at < m) start[k] = ((j0 + i) << 8) | (at - o);
+      o += len;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_zre_index_kernel(
+    const uint8_t* __restrict__ C, uint32_t c, uint32_t m, uint64_t* __restrict__ start,
+    uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
+    Ctrl* __restrict__ ctrl) {
+  __shared__ IdxShared sh;
+  __shared__ uint32_t s_tile;
+  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
+  __syncthreads();
+  index_tile(C, c, m, start, status, 0, s_tile, epoch, ctrl, sh);
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
+    const DecDesc* __restrict__ descs, uint32_t count, uint64_t* __restrict__ start,
+    uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
+    Ctrl* __restrict__ ctrl) {
+  __shared__ IdxShared sh;
+  __shared__ uint32_t s_tile;
+  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
+  __syncthreads();
+  const uint32_t T = s_tile;
+  const uint32_t t = find_desc(descs, count, T, [](const DecDesc& d) { return d.tile0; });
+  const DecDesc d = descs[t];
+  index_tile(d.C, d.c, d.m, start + d.range0, status, d.tile0, T - d.tile0, epoch, ctrl, sh);
+}
+
+// ---------------------------------------------------------------- expansion
+// One past the last stream byte that reaches into range k (starts: the
+// stream's start entries).
+__device__ __forceinline__ uint32_t range_end(const uint64_t* __restrict__ starts, uint32_t k,
+                                              uint64_t m, uint32_t c) {
+  if ((uint64_t)(k + 1) * kDecRange < m) {
+    const uint64_t s1 = starts[k + 1];
+    return min<uint32_t>((uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u), c);
+  }
+  return c;
+}
+
+// Expands quartic bytes [k*kDecRange, k*kDecRange + qn) of one stream into
+// s_q.  The stream bytes covering the range (found through the start
+// entries) are spread over the threads; a block scan of their expansion
+// lengths gives each one its position and each thread writes its own
+// expansions.  Ends with a barrier.
+__device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint32_t c,
+                                             const uint64_t* __restrict__ starts, uint32_t k,
+                                             uint64_t m, uint32_t qn, uint8_t* s_q,
+                                             uint32_t* red) {
+  constexpr int kBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
+  const uint64_t s0 = starts[k];
+  const uint32_t i0 = (uint32_t)(s0 >> 8);
+  const uint32_t skip = (uint32_t)(s0 & 255u);
+  const uint32_t i1 = range_end(starts, k, m, c);
+  const uint32_t count = i1 > i0 ? min<uint32_t>(i1 - i0, kDecRange) : 0u;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < count ? min<uint32_t>(kBytes, count - lo) : 0u;
+  uint8_t b[kBytes];
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[i0 + lo + i] : (uint8_t)0;
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+  const ScanU32 sc = block_scan_u32(sum, red);
+  int pos = (int)sc.excl - (int)skip;  // range-relative start of b[0]
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t x = b[i];
+      const int len = (int)expanded_len(x);
+      const uint32_t a = (uint32_t)max(pos, 0);
+      const uint32_t e = (uint32_t)min(pos + len, (int)qn);
+      if (a < e) {
+        if (x < kRunBase)
+          s_q[a] = (uint8_t)x;
+        else
+          fill_zero_groups(s_q, a, e);
+      }
+      pos += len;
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- Eq. 3
+// Unpacks the base-3 digits of quartic bytes s_q[0, qn) (global bytes
+// q0 + jl), dequantizes (Eq. 3) and stores or accumulates into the five
+// partitions of out: float4 accesses when m % 4 == 0 and out is aligned.
+template <bool kVec, bool kAcc>
+__device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, uint32_t qn,
+                                              uint64_t n, uint64_t m, float M,
+                                              float* __restrict__ out) {
+  if (kVec) {
+#pragma unroll
+    for (int g = 0; g < kDecRange / (4 * kThreads); ++g) {
+      const uint32_t jl = 4u * (threadIdx.x + kThreads * g);
+      if (jl >= qn) break;
+      const uint64_t j = q0 + jl;
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(s_q + jl);
+      uint32_t t[4][5];
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) digits5((w >> (8 * cc)) & 0xffu, t[cc]);
+      if (4 * m + j + 4 <= n) {
+        float4 o[5];
+        if (kAcc) {
+#pragma unroll
+          for (int k = 0; k < 5; ++k) o[k] = *reinterpret_cast<const float4*>(out + k * m + j);
+        }
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+          if (kAcc) {
+            o[k].x = o[k].x + trit_value(t[0][k], M);
+            o[k].y = o[k].y + trit_value(t[1][k], M);
+            o[k].z = o[k].z + trit_value(t[2][k], M);
+            o[k].w = o[k].w + trit_value(t[3][k], M);
+          } else {
+            o[k].x = trit_value(t[0][k], M);
+            o[k].y = trit_value(t[1][k], M);
+            o[k].z = trit_value(t[2][k], M);
+            o[k].w = trit_value(t[3][k], M);
+          }
+          *reinterpret_cast<float4*>(out + k * m + j) = o[k];
+        }
+      } else {  // the group whose p4 slice reaches into the padding
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const uint64_t e = k * m + j + cc;
+            if (e < n) {
+              const float v = trit_value(t[cc][k], M);
+              out[e] = kAcc ? out[e] + v : v;
+            }
+          }
+        }
+      }
+    }
+  } else {
+    for (uint32_t jl = threadIdx.x; jl < qn; jl += kThreads) {
+      const uint64_t j = q0 + jl;
+      uint32_t t[5];
+      digits5(s_q[jl], t);
+#pragma unroll
+      for (int k = 0; k < 5; ++k) {
+        const uint64_t e = k * m + j;
+        if (e < n) {
+          const float v = trit_value(t[k], M);
+          out[e] = kAcc ? out[e] + v : v;
+        }
+      }
+    }
+  }
+}
+
+// One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
+template <bool kVec, bool kAcc>
+__global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
+    const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ start,
+    uint64_t n, uint64_t m, float M, float* __restrict__ out, uint32_t epoch,
+    const Ctrl* __restrict__ ctrl) {
+  __shared__ uint32_t red[kWaves];
+  __shared__ __align__(16) uint8_t s_q[kDecRange];
+  if (ctrl->dec_bad_epoch == epoch) return;  // corrupt stream: out untouched
+  const uint32_t k = blockIdx.x;
+  const uint64_t q0 = (uint64_t)k * kDecRange;
+  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  expand_range(C, c, start, k, m, qn, s_q, red);
+  dequant_range<kVec, kAcc>(s_q, q0, qn, n, m, M, out);
+}
+
+template <bool kAcc>
+__global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
+    const DecDesc* __restrict__ descs, uint32_t count, const uint64_t* __restrict__ start,
+    uint32_t epoch, const Ctrl* __restrict__ ctrl) {
+  __shared__ uint32_t red[kWaves];
+  __shared__ __align__(16) uint8_t s_q[kDecRange];
+  if (ctrl->dec_bad_epoch == epoch) return;  // a corrupt stream: no output written
+  const uint32_t t =
+      find_desc(descs, count, blockIdx.x, [](const DecDesc& d) { return d.range0; });
+  const DecDesc d = descs[t];
+  const uint32_t k = blockIdx.x - d.range0;
+  const uint64_t q0 = (uint64_t)k * kDecRange;
+  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, (uint64_t)d.m - q0);
+  expand_range(d.C, d.c, start + d.range0, k, d.m, qn, s_q, red);
+  if (d.vec & 1u)
+    dequant_range<true, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+  else
+    dequant_range<false, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+}
+
+// ---------------------------------------------------------------- aggregation
+// Range k of `count` streams of the same n-value tensor, summed into out in
+// stream order per element (out = ((out + v0) + v1) + ..., or starting
+// from v0 without accumulate): the same fp32 additions, in the same order,
+// as decoding the streams one after another, but out is read and written
+// once.  Values stay in registers between streams.
+template <bool kVec, bool kAcc>
+__global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
+    const DecDesc* __restrict__ descs, uint32_t count, const uint64_t* __restrict__ start,
+    uint64_t n, uint64_t m, float* __restrict__ out, uint32_t epoch,
+    const Ctrl* __restrict__ ctrl) {
+  constexpr int kPer = kVec ? kDecRange / kThreads / 4 : kDecRange / kThreads;  // slots
+  constexpr int kW = kVec ? 4 : 1;                                              // bytes/slot
+  __shared__ uint32_t red[kWaves];
+  __shared__ __align__(16) uint8_t s_q[kDecRange];
+  if (ctrl->dec_bad_epoch == epoch) return;  // a corrupt stream: out untouched
+  const uint32_t k = blockIdx.x;
+  const uint64_t q0 = (uint64_t)k * kDecRange;
+  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+
+  // slot g covers quartic bytes jl(g) .. jl(g) + kW - 1 and their 5 partitions
+  float acc[kPer][5][kW];
+  auto jl_of = [&](int g) -> uint32_t {
+    return kVec ? 4u * (threadIdx.x + kThreads * g) : threadIdx.x + kThreads * g;
+  };
+  if (kAcc) {
+#pragma unroll
+    for (int g = 0; g < kPer; ++g) {
+      const uint32_t jl = jl_of(g);
+      if (jl >= qn) continue;
+      const uint64_t j = q0 + jl;
+#pragma unroll
+      for (int kk = 0; kk < 5; ++kk) {
+        if (kVec && 4 * m + j + 4 <= n) {
+          const float4 v = *reinterpret_cast<const float4*>(out + kk * m + j);
+          acc[g][kk][0] = v.x;
+          acc[g][kk][kW > 1 ? 1 : 0] = v.y;
+          acc[g][kk][kW > 2 ? 2 : 0] = v.z;
+          acc[g][kk][kW > 3 ? 3 : 0] = v.w;
+        } else {
+#pragma unroll
+          for (int cc = 0; cc < kW; ++cc) {
+            const uint64_t e = kk * m + j + cc;
+            acc[g][kk][cc] = e < n ? out[e] : 0.0f;
+          }
+        }
+      }
+    }
+  }
+
+  for (uint32_t p = 0; p < count; ++p) {
+    const DecDesc d = descs[p];
+    expand_range(d.C, d.c, start + d.range0, k, m, qn, s_q, red);
+#pragma unroll
+    for (int g = 0; g < kPer; ++g) {
+      const uint32_t jl = jl_of(g);
+      if (jl >= qn) continue;
+      uint32_t w = kVec ? *reinterpret_cast<const uint32_t*>(s_q + jl) : s_q[jl];
+#pragma unroll
+      for (int cc = 0; cc < kW; ++cc) {
+        uint32_t t[5];
+        digits5((w >> (8 * cc)) & 0xffu, t);
+#pragma unroll
+        for (int kk = 0; kk < 5; ++kk) {
+          const float v = trit_value(t[kk], d.scale);
+          acc[g][kk][cc] = (!kAcc && p == 0) ? v : acc[g][kk][cc] + v;
+        }
+      }
+    }
+    __syncthreads();  // s_q is rewritten by the next stream
+  }
+
+#pragma unroll
+  for (int g = 0; g < kPer; ++g) {
+    const uint32_t jl = jl_of(g);
+    if (jl >= qn) continue;
+    const uint64_t j = q0 + jl;
+#pragma unroll
+    for (int kk = 0; kk < 5; ++kk) {
+      if (kVec && 4 * m + j + 4 <= n) {
+        *reinterpret_cast<float4*>(out + kk * m + j) =
+            make_float4(acc[g][kk][0], acc[g][kk][kW > 1 ? 1 : 0], acc[g][kk][kW > 2 ? 2 : 0],
+                        acc[g][kk][kW > 3 ? 3 : 0]);
+      } else {
+#pragma unroll
+        for (int cc = 0; cc < kW; ++cc) {
+          const uint64_t e = kk * m + j + cc;
+          if (e < n) out[e] = acc[g][kk][cc];
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static inline bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
+}
+
+hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
+                            uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                            uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+  tlc_zre_index_kernel<<<ntiles, kThreads, 0, st>>>(C, c, m, start, status, ticket_base,
+                                                    epoch, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
+                                 uint64_t n, uint64_t m, float scale, float* out,
+                                 int accumulate, uint32_t epoch, const Ctrl* ctrl,
+                                 hipStream_t st) {
+  const bool vec = (m % 4 == 0) && aligned16(out);
+  const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
+#define TLC_LAUNCH(V, A)                                                                     \
+  tlc_expand_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, out, \
+                                                               epoch, ctrl)
+  if (vec) {
+    if (accumulate) TLC_LAUNCH(true, true); else TLC_LAUNCH(true, false);
+  } else {
+    if (accumulate) TLC_LAUNCH(false, true); else TLC_LAUNCH(false, false);
+  }
+#undef TLC_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
+                                  uint64_t* start, uint64_t* status, uint32_t ticket_base,
+                                  uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+  tlc_zre_index_batch_kernel<<<total_tiles, kThreads, 0, st>>>(descs, count, start, status,
+                                                               ticket_base, epoch, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand_dequant_batch(const DecDesc* descs, uint32_t count,
+                                       uint32_t total_ranges, const uint64_t* start,
+                                       int accumulate, uint32_t epoch, const Ctrl* ctrl,
+                                       hipStream_t st) {
+  if (accumulate)
+    tlc_expand_dequant_batch_kernel<true><<<total_ranges, kThreads, 0, st>>>(descs, count,
+                                                                             start, epoch, ctrl);
+  else
+    tlc_expand_dequant_batch_kernel<false><<<total_ranges, kThreads, 0, st>>>(
+        descs, count, start, epoch, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand_sum(const DecDesc* descs, uint32_t count, const uint64_t* start,
+                             uint64_t n, uint64_t m, float* out, int vec, int accumulate,
+                             uint32_t epoch, const Ctrl* ctrl, hipStream_t st) {
+  const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
+#define TLC_LAUNCH(V, A)                                                                 \
+  tlc_expand_sum_kernel<V, A><<<blocks, kThreads, 0, st>>>(descs, count, start, n, m, out, \
+                                                           epoch, ctrl)
+  if (vec) {
+    if (accumulate) TLC_LAUNCH(true, true); else TLC_LAUNCH(true, false);
+  } else {
+    if (accumulate) TLC_LAUNCH(false, true); else TLC_LAUNCH(false, false);
+  }
+#undef TLC_LAUNCH
+  return hipGetLastError();
+}
+
+}  // namespace tlc

@@ -1,0 +1,255 @@
+// device_common.hpp -- device helpers shared by the encode and decode
+// kernels of the 3LC path.
+#pragma once
+
+#include <float.h>
+
+#include "lookback.hpp"
+#include "tlc_internal.h"
+#include "zre_scan.hpp"
+
+namespace tlc {
+
+constexpr int kWaves = kThreads / 64;
+
+// ---------------------------------------------------------------- reductions
+__device__ __forceinline__ uint32_t abs_bits(float v) {
+  return __float_as_uint(v) & 0x7fffffffu;
+}
+
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, d, 64));
+  return v;
+}
+
+// Block-wide max; every thread gets the result.  Uses lds[kWaves] and one
+// barrier; callers that reuse lds must barrier again first.
+__device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* lds) {
+  v = wave_max(v);
+  if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = lds[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r = max(r, lds[w]);
+  return r;
+}
+
+// Block-wide exclusive prefix of u32 values: returns (exclusive prefix of
+// this thread, block total).  Uses lds[kWaves] and one barrier.
+struct ScanU32 {
+  uint32_t excl, total;
+};
+__device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = __shfl_up(incl, d, 64);
+    if (lane >= (uint32_t)d) incl += o;
+  }
+  if (lane == 63) lds[wid] = incl;
+  __syncthreads();
+  ScanU32 r;
+  r.excl = incl - v;
+  r.total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    if ((uint32_t)w < wid) r.excl += lds[w];
+    r.total += lds[w];
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------- Eq. 1-2
+struct Scale {
+  float M;       // max|acc| * s
+  float U;       // smallest fp32 u with rint(u / M) == 1
+  uint32_t bad;  // NaN/Inf input or overflowing product
+};
+
+// rint(fl(a / M)) for |a| <= M is 1 exactly when fl(a / M) > 0.5, i.e. (the
+// tie at 0.5 + 2^-25 rounds down to the even 0.5) when a > M * (0.5 +
+// 2^-25).  That product has at most 49 significant bits, so it is exact in
+// double; U is the smallest float above it.  The test a >= U therefore
+// gives the same q as an IEEE divide followed by round-half-even, and by
+// symmetry a <= -U gives q = -1.  M = 0 makes U the smallest subnormal, so
+// q = 0 for the (all-zero) tensor.
+__device__ __forceinline__ float quant_threshold(float M) {
+  const double h = 0.5000000298023223876953125;  // 0.5 + 2^-25
+  const double T = (double)M * h;
+  float f = __double2float_rn(T);
+  if ((double)f <= T) f = __uint_as_float(__float_as_uint(f) + 1u);
+  return f;
+}
+
+// M and U from the partial maxima of one tensor (all threads of the block).
+__device__ __forceinline__ Scale finish_scale(const uint32_t* __restrict__ partials,
+                                              uint32_t np, float s, uint32_t* lds) {
+  uint32_t v = 0;
+  for (uint32_t i = threadIdx.x; i < np; i += kThreads) v = max(v, partials[i]);
+  const uint32_t A = block_max(v, lds);
+  Scale sc;
+  sc.M = 0.0f;
+  sc.U = 0.0f;
+  sc.bad = 1u;
+  if (A >= 0x7f800000u) return sc;
+  const float M = __uint_as_float(A) * s;
+  if (!(M <= FLT_MAX)) return sc;
+  sc.M = M;
+  sc.U = quant_threshold(M);
+  sc.bad = 0u;
+  return sc;
+}
+
+// q = round(acc / M) in {-1, 0, 1} (returned as the trit q + 1) and the
+// residual acc - M*q.  M*q is exact, so acc - M, acc + M and acc are the
+// bit patterns of acc - M*q for q = 1, -1, 0 (acc - (+0) == acc, -0 kept).
+__device__ __forceinline__ uint32_t quantize_one(float acc, float M, float U,
+                                                 float& res) {
+  const bool pos = acc >= U;
+  const bool neg = acc <= -U;
+  res = pos ? acc - M : (neg ? acc + M : acc);
+  return pos ? 2u : (neg ? 0u : 1u);
+}
+
+// Quartic byte j < m: quantizes the five elements j + k*m (contiguous
+// partitions, p0 most significant; elements past n are the zero padding of
+// Section 3.2, step 4), writes their residuals and returns the byte.
+__device__ __forceinline__ uint32_t quantize_byte(const float* __restrict__ x,
+                                                  float* __restrict__ r, uint64_t n,
+                                                  uint64_t m, uint64_t j, float M, float U) {
+  uint32_t code = 0u;
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    const uint64_t e = k * m + j;
+    uint32_t t = 0u;
+    if (e < n) {
+      float o;
+      t = quantize_one(x[e] + r[e], M, U, o);
+      r[e] = o;
+    }
+    code = code * 3u + t;
+  }
+  return code;
+}
+
+// Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and 16-byte aligned x
+// and r, so every partition slice is one float4; returns the four bytes
+// packed little-endian.
+__device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
+                                                    float* __restrict__ r, uint64_t n,
+                                                    uint64_t m, uint64_t j, float M,
+                                                    float U) {
+  if (4 * m + j + 4 > n) {  // the group that reaches into the padding of p4
+    uint32_t w = 0u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) w |= quantize_byte(x, r, n, m, j + c, M, U) << (8 * c);
+    return w;
+  }
+  uint32_t code[4] = {0u, 0u, 0u, 0u};
+  float4 a[5], b[5];
+#pragma unroll
+  for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(x + k * m + j);
+#pragma unroll
+  for (int k = 0; k < 5; ++k) b[k] = *reinterpret_cast<const float4*>(r + k * m + j);
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    float4 o;
+    code[0] = code[0] * 3u + quantize_one(a[k].x + b[k].x, M, U, o.x);
+    code[1] = code[1] * 3u + quantize_one(a[k].y + b[k].y, M, U, o.y);
+    code[2] = code[2] * 3u + quantize_one(a[k].z + b[k].z, M, U, o.z);
+    code[3] = code[3] * 3u + quantize_one(a[k].w + b[k].w, M, U, o.w);
+    *reinterpret_cast<float4*>(r + k * m + j) = o;
+  }
+  return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+}
+
+// ---------------------------------------------------------------- Section 3.3
+using EncSW = StatusWord<39>;  // RunSum with a 30-bit count
+using DecSW = StatusWord<36>;  // expanded byte count
+
+__device__ __forceinline__ uint64_t rs_to_payload(RunSum a) {
+  return (a.v & 0x3fffffffull) | ((a.v >> 32) << 30);
+}
+__device__ __forceinline__ RunSum rs_from_payload(uint64_t p) {
+  RunSum r;
+  r.v = (p & 0x3fffffffull) | ((p >> 30) << 32);
+  return r;
+}
+
+struct EncOp {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const {
+    return rs_to_payload(rs_combine(rs_from_payload(a), rs_from_payload(b)));
+  }
+};
+struct SumOp {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
+};
+
+__device__ __forceinline__ void unpack16(uint4 v, uint8_t* b) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    b[i] = (uint8_t)(v.x >> (8 * i));
+    b[4 + i] = (uint8_t)(v.y >> (8 * i));
+    b[8 + i] = (uint8_t)(v.z >> (8 * i));
+    b[12 + i] = (uint8_t)(v.w >> (8 * i));
+  }
+}
+
+__device__ __forceinline__ RunSum shfl_up_rs(RunSum v, int d) {
+  RunSum o;
+  o.v = __shfl_up(v.v, d, 64);
+  return o;
+}
+
+// Number of quartic bytes a stream byte stands for: data bytes (< 243) one,
+// run codes 243 + (k - 2) k copies of 121.
+__device__ __forceinline__ uint32_t expanded_len(uint32_t b) {
+  return b < kRunBase ? 1u : b - (kRunBase - 2u);
+}
+
+// Writes bytes of 121 at lds[lo..hi).
+__device__ __forceinline__ void fill_zero_groups(uint8_t* lds, uint32_t lo, uint32_t hi) {
+  while (lo < hi && (lo & 3u)) lds[lo++] = (uint8_t)kZeroGroup;
+  for (; lo + 4 <= hi; lo += 4) *reinterpret_cast<uint32_t*>(lds + lo) = 0x79797979u;
+  while (lo < hi) lds[lo++] = (uint8_t)kZeroGroup;
+}
+
+// ---------------------------------------------------------------- Eq. 3
+// The dequantized value M*q for trit t = q + 1 is -M, +0 or M (M*(-1) is
+// the exact negation and M*0 is +0 for finite M >= 0).
+__device__ __forceinline__ float trit_value(uint32_t t, float M) {
+  return t == 0u ? -M : (t == 1u ? 0.0f : M);
+}
+
+// Base-3 digits of a quartic byte, most significant first (weights 81, 27,
+// 9, 3, 1): Section 3.2, decoding step 1.
+__device__ __forceinline__ void digits5(uint32_t byte, uint32_t (&t)[5]) {
+  t[0] = byte / 81u;
+  byte -= t[0] * 81u;
+  t[1] = byte / 27u;
+  byte -= t[1] * 27u;
+  t[2] = byte / 9u;
+  byte -= t[2] * 9u;
+  t[3] = byte / 3u;
+  t[4] = byte - t[3] * 3u;
+}
+
+// Index of the last descriptor whose `first` field is <= key (descriptors
+// sorted by `first`, descs[0].first == 0).
+template <class D, class F>
+__device__ __forceinline__ uint32_t find_desc(const D* __restrict__ descs, uint32_t count,
+                                              uint32_t key, F first) {
+  uint32_t lo = 0, hi = count;  // invariant: first(descs[lo]) <= key
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (first(descs[mid]) <= key)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+}  // namespace tlc

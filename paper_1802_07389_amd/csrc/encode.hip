@@ -1,0 +1,304 @@
+// encode.hip -- gfx950 encode kernels of the 3LC path.
+//
+//   tlc_absmax_kernel / _batch_kernel
+//       partial maxima of |tensor + residual|                          (Eq. 1)
+//   tlc_quant_encode_kernel / _batch_kernel
+//       M, 3-value quantization, residual write-back, quartic pack and
+//       zero-run encoding in one pass         (Eq. 1-2, Sections 3.2-3.3)
+//
+// The batch kernels run many tensors in one launch: every block maps its
+// index (absmax) or its ticket (encoder) to a tensor through the sorted
+// first-block / first-tile fields of the tensor descriptors, then runs the
+// same device code as the single-tensor kernels.  Everything is HBM
+// streaming; nothing is a dense contraction, so there is no MFMA.
+#include "device_common.hpp"
+
+namespace tlc {
+
+// ---------------------------------------------------------------- Eq. 1
+// max |x + r| is taken on the bit patterns with the sign cleared: for
+// non-negative IEEE values integer order equals numeric order, so the u32
+// max is exact and independent of reduction order, and any NaN/Inf makes
+// the result >= 0x7f800000.  Block `blk` of `nblk` strides over [0, n).
+template <bool kVec>
+__device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
+                                                const float* __restrict__ r, uint64_t n,
+                                                uint32_t blk, uint32_t nblk) {
+  uint32_t mx = 0;
+  const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
+  const uint64_t stride = (uint64_t)nblk * kThreads;
+  if (kVec) {
+    const float4* __restrict__ x4 = reinterpret_cast<const float4*>(x);
+    const float4* __restrict__ r4 = reinterpret_cast<const float4*>(r);
+    const uint64_t nv = n >> 2;
+    uint64_t i = tid;
+    for (; i + 3 * stride < nv; i += 4 * stride) {
+      float4 a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] = x4[i + u * stride];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) b[u] = r4[i + u * stride];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        mx = max(mx, abs_bits(a[u].x + b[u].x));
+        mx = max(mx, abs_bits(a[u].y + b[u].y));
+        mx = max(mx, abs_bits(a[u].z + b[u].z));
+        mx = max(mx, abs_bits(a[u].w + b[u].w));
+      }
+    }
+    for (; i < nv; i += stride) {
+      float4 a = x4[i], b = r4[i];
+      mx = max(mx, abs_bits(a.x + b.x));
+      mx = max(mx, abs_bits(a.y + b.y));
+      mx = max(mx, abs_bits(a.z + b.z));
+      mx = max(mx, abs_bits(a.w + b.w));
+    }
+    for (uint64_t e = (nv << 2) + tid; e < n; e += stride)
+      mx = max(mx, abs_bits(x[e] + r[e]));
+  } else {
+    for (uint64_t e = tid; e < n; e += stride) mx = max(mx, abs_bits(x[e] + r[e]));
+  }
+  return mx;
+}
+
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void tlc_absmax_kernel(
+    const float* __restrict__ x, const float* __restrict__ r, uint64_t n,
+    uint32_t* __restrict__ partials) {
+  __shared__ uint32_t lds[kWaves];
+  const uint32_t mx = block_max(absmax_part<kVec>(x, r, n, blockIdx.x, gridDim.x), lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = mx;
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_absmax_batch_kernel(
+    const EncDesc* __restrict__ descs, uint32_t count, uint32_t* __restrict__ partials) {
+  __shared__ uint32_t lds[kWaves];
+  const uint32_t t =
+      find_desc(descs, count, blockIdx.x, [](const EncDesc& d) { return d.blk0; });
+  const EncDesc& d = descs[t];
+  const uint32_t blk = blockIdx.x - d.blk0;
+  const uint32_t mx = (d.vec & 2u) ? absmax_part<true>(d.x, d.r, d.n, blk, d.nblk)
+                                   : absmax_part<false>(d.x, d.r, d.n, blk, d.nblk);
+  const uint32_t bm = block_max(mx, lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = bm;
+}
+
+// ---------------------------------------------------------------- Eq. 2, 3.2, 3.3
+struct EncShared {
+  uint32_t red[kWaves];
+  uint32_t fault;
+  RunSum wave[kWaves];
+  RunSum excl;
+  __align__(16) uint8_t q[kEncTile];
+  __align__(16) uint8_t out[kEncTile + 16];
+};
+
+// Encodes tile `lt` (kEncTile quartic bytes) of one tensor whose scale is
+// sc.  Phase 1: the block quantizes its 5 * kEncTile values (threads take
+// groups of 4 bytes, or single bytes when the partitions are not 16-byte
+// aligned, interleaved so every load and store instruction is coalesced)
+// and keeps the quartic bytes in LDS.  Phase 2: each thread takes
+// kEncTile/256 consecutive bytes and summarises them as a RunSum; the block
+// scans the summaries, the tile gets its prefix by decoupled look-back
+// (status slot floor + lt; slot floor is the tensor's first tile), and
+// every thread zero-run encodes its bytes from its own prefix into LDS; the
+// block then copies the tile's output into the stream.  The last tile
+// stores the stream length in res->len.
+template <bool kVec>
+__device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* __restrict__ r,
+                                            uint64_t n, uint32_t m, const Scale& sc,
+                                            uint32_t lt, uint32_t floor,
+                                            uint8_t* __restrict__ out,
+                                            uint64_t* __restrict__ status, uint32_t epoch,
+                                            Ctrl* __restrict__ ctrl, EncResult* res,
+                                            EncShared& sh) {
+  constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
+  static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
+
+  // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
+  const uint64_t q0 = (uint64_t)lt * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  if (kVec) {  // 4 bytes per thread: float4 loads and stores
+    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
+      *reinterpret_cast<uint32_t*>(sh.q + g * 4u) =
+          quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+  } else {  // 1 byte per thread: dword accesses, still contiguous per wave
+    for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
+      sh.q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
+  }
+  __syncthreads();
+
+  // ---- phase 2: Section 3.3
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
+  uint8_t b[kBytes];
+#pragma unroll
+  for (int h = 0; h < kBytes / 16; ++h)
+    unpack16(*reinterpret_cast<const uint4*>(sh.q + lo + 16 * h), b + 16 * h);
+  RunSum sum = rs_identity();
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) sum = rs_combine(sum, rs_byte(b[i]));
+
+  RunSum incl = sum;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    RunSum o = shfl_up_rs(incl, d);
+    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
+  }
+  RunSum excl_lane = shfl_up_rs(incl, 1);
+  if (lane == 0) excl_lane = rs_identity();
+  if (lane == 63) sh.wave[wid] = incl;
+  __syncthreads();
+  RunSum wpre = rs_identity();
+  RunSum agg = rs_identity();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    if ((uint32_t)w < wid) wpre = rs_combine(wpre, sh.wave[w]);
+    agg = rs_combine(agg, sh.wave[w]);
+  }
+
+  if (wid == 0) {
+    bool fault = false;
+    uint64_t ex = rs_to_payload(rs_identity());
+    if (lt == 0) {
+      if (lane == 0)
+        status_publish(&status[floor], EncSW::pack(rs_to_payload(agg), kFlagPrefix, epoch));
+    } else {
+      ex = lookback_wave<EncSW>(status, floor, floor + lt, rs_to_payload(agg), ex, epoch,
+                                EncOp(), &fault);
+    }
+    if (lane == 0) {
+      sh.excl = rs_from_payload(ex);
+      sh.fault = fault ? 1u : 0u;
+      if (fault)
+        __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __syncthreads();
+  if (sh.fault) return;
+
+  const RunSum tex = sh.excl;
+  const RunSum P = rs_combine(rs_combine(tex, wpre), excl_lane);
+  const uint32_t tile_begin = rs_emitted(tex);
+  uint32_t o = rs_emitted(P) - tile_begin;
+  uint32_t phi = rs_phase(P);
+  auto put = [&](uint32_t c) {
+    if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
+    ++o;
+  };
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
+  if (cnt && q0 + lo + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
+
+  const bool last_tile = q0 + kEncTile >= m;
+  const RunSum tincl = rs_combine(tex, agg);
+  const uint32_t tile_end = last_tile ? rs_total(tincl) : rs_emitted(tincl);
+  __syncthreads();
+  // a tile emits at most kEncTile + 1 bytes; the clamps only keep a logic
+  // error from writing outside the m-byte output buffer
+  const uint32_t count =
+      tile_end >= tile_begin ? min<uint32_t>(tile_end - tile_begin, kEncTile + 1) : 0u;
+  for (uint32_t i = threadIdx.x; i < count; i += kThreads)
+    if (tile_begin + i < m) out[tile_begin + i] = sh.out[i];
+  if (last_tile && threadIdx.x == 0) res->len = tile_end;
+}
+
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
+    uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
+    Ctrl* __restrict__ ctrl) {
+  __shared__ EncShared sh;
+  __shared__ uint32_t s_tile;
+  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
+  const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+  const uint32_t tile = s_tile;
+  if (tile == 0 && threadIdx.x == 0) {
+    ctrl->enc.err = sc.bad;
+    ctrl->enc.scale = sc.M;
+  }
+  if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
+  encode_tile<kVec>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
+    const EncDesc* __restrict__ descs, uint32_t count, const uint32_t* __restrict__ partials,
+    EncResult* __restrict__ results, uint64_t* __restrict__ status, uint32_t ticket_base,
+    uint32_t epoch, Ctrl* __restrict__ ctrl) {
+  __shared__ EncShared sh;
+  __shared__ uint32_t s_tile;
+  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
+  __syncthreads();
+  const uint32_t T = s_tile;
+  const uint32_t t = find_desc(descs, count, T, [](const EncDesc& d) { return d.tile0; });
+  const EncDesc d = descs[t];
+  const Scale sc = finish_scale(partials + d.blk0, d.nblk, d.s, sh.red);
+  const uint32_t lt = T - d.tile0;
+  if (lt == 0 && threadIdx.x == 0) {
+    results[t].err = sc.bad;
+    results[t].scale = sc.M;
+    if (sc.bad) results[t].len = 0u;
+  }
+  if (sc.bad) return;  // this tensor is refused; the others go on
+  if (d.vec & 1u)
+    encode_tile<true>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                      &results[t], sh);
+  else
+    encode_tile<false>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                       &results[t], sh);
+}
+
+// ---------------------------------------------------------------- launchers
+static inline bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
+}
+
+hipError_t launch_absmax(const float* x, const float* r, uint64_t n, uint32_t* partials,
+                         uint32_t* nblocks, hipStream_t st) {
+  const bool vec = aligned16(x) && aligned16(r);
+  const uint64_t items = vec ? (n >> 2) : n;
+  uint64_t blocks = (items + kThreads * 4 - 1) / (kThreads * 4);
+  blocks = blocks < 1 ? 1 : (blocks > kAbsmaxMaxBlocks ? kAbsmaxMaxBlocks : blocks);
+  *nblocks = (uint32_t)blocks;
+  if (vec)
+    tlc_absmax_kernel<true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  else
+    tlc_absmax_kernel<false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                               const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                               uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                               uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+  const bool vec = (m % 4 == 0) && aligned16(x) && aligned16(r);
+  if (vec)
+    tlc_quant_encode_kernel<true><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+  else
+    tlc_quant_encode_kernel<false><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
+                               uint32_t* partials, hipStream_t st) {
+  tlc_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_tiles, const uint32_t* partials,
+                                     EncResult* results, uint64_t* status,
+                                     uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
+                                     hipStream_t st) {
+  tlc_quant_encode_batch_kernel<<<total_tiles, kThreads, 0, st>>>(
+      descs, count, partials, results, status, ticket_base, epoch, ctrl);
+  return hipGetLastError();
+}
+
+}  // namespace tlc

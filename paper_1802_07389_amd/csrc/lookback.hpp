@@ -59,17 +59,19 @@ __device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
                                 __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wave-parallel look-back for tile `tile` (> 0), run by all 64 lanes of one
-// wave, over an associative operator op(earlier, later).  Lane l polls the
-// word of tile (base - l), so one poll covers 64 predecessors.  The words
+// Wave-parallel look-back for tile `tile` (> floor), run by all 64 lanes of
+// one wave, over an associative operator op(earlier, later).  Tiles
+// [floor, tile) belong to the same scan (a batch keeps several scans in one
+// status array); tile `floor` always publishes its inclusive prefix.  Lane l
+// polls the word of tile (base - l), so one poll covers 64 predecessors.  The words
 // from the nearest inclusive prefix up to tile - 1 are folded in order with
 // a shuffle reduction (a higher lane holds an earlier tile).  Publishes the
 // tile's aggregate first and its inclusive prefix last; returns the
 // exclusive prefix in every lane.  A bounded wait or a predecessor fault
 // publishes a fault word and sets *fault.
 template <class SW, class Op>
-__device__ uint64_t lookback_wave(uint64_t* status, uint32_t tile, uint64_t agg,
-                                  uint64_t identity, uint32_t epoch, Op op,
+__device__ uint64_t lookback_wave(uint64_t* status, uint32_t floor, uint32_t tile,
+                                  uint64_t agg, uint64_t identity, uint32_t epoch, Op op,
                                   bool* fault) {
   const uint32_t lane = threadIdx.x & 63u;
   if (lane == 0) status_publish(&status[tile], SW::pack(agg, kFlagAgg, epoch));
@@ -81,7 +83,7 @@ __device__ uint64_t lookback_wave(uint64_t* status, uint32_t tile, uint64_t agg,
     const int64_t idx = base - (int64_t)lane;
     uint64_t val = identity;
     bool ready = true, is_prefix = true, is_fault = false;
-    if (idx >= 0) {  // lanes past tile 0 act as an (ignored) prefix
+    if (idx >= (int64_t)floor) {  // lanes before the scan's first tile act as an (ignored) prefix
       const uint64_t w = status_read(&status[idx]);
       const uint32_t f = SW::flag(w);
       ready = SW::epoch(w) == epoch && f != 0u;

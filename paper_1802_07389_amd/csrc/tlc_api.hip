@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -36,38 +37,57 @@ size_t quartic_len(size_t n) { return n / 5 + (n % 5 ? 1 : 0); }
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+size_t ceil_div(size_t a, size_t b) { return (a + b - 1) / b; }
+
 bool overlap(const void* a, size_t an, const void* b, size_t bn) {
   const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
   return an && bn && pa < pb + bn && pb < pa + an;
 }
 
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0u; }
+
 const char* const kKernelNames[TLC_KERNEL_COUNT] = {
-    "tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
-    "tlc_expand_dequant_kernel"};
+    "tlc_absmax_kernel",           "tlc_quant_encode_kernel",
+    "tlc_zre_index_kernel",        "tlc_expand_dequant_kernel",
+    "tlc_absmax_batch_kernel",     "tlc_quant_encode_batch_kernel",
+    "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
+    "tlc_expand_sum_kernel"};
 
 struct PendingTiming {
   int kernel;
   hipEvent_t start, stop;
 };
 
+constexpr int kStagingSlots = 4;
+
 }  // namespace
 
 struct tlc_ctx {
   hipStream_t stream = nullptr;
   int device = 0;
-  size_t max_n = 0;
-  size_t max_m = 0;
+  size_t max_n = 0;        // values per call (summed over a batch)
+  size_t max_tensors = 0;  // tensors or streams per call
   // device workspace (one allocation)
   void* ws = nullptr;
   Ctrl* ctrl = nullptr;
   uint32_t* partials = nullptr;
+  size_t partials_cap = 0;
   uint64_t* enc_status = nullptr;
-  uint64_t* dec_status = nullptr;
-  uint64_t* start = nullptr;  // per kDecRange quartic bytes: (stream index, skip)
   size_t enc_status_words = 0;
+  uint64_t* dec_status = nullptr;
   size_t dec_status_words = 0;
-  // pinned host readback
+  uint64_t* start = nullptr;  // per kDecRange quartic bytes: (stream index, skip)
+  size_t start_words = 0;
+  EncDesc* enc_descs = nullptr;
+  DecDesc* dec_descs = nullptr;
+  EncResult* enc_results = nullptr;
+  // pinned host memory: status readback, batch results, descriptor staging
   HostReadback* rb = nullptr;
+  EncResult* host_results = nullptr;
+  uint8_t* staging = nullptr;  // kStagingSlots slots of max_tensors * 64 bytes
+  hipEvent_t staging_done[kStagingSlots] = {};
+  bool staging_used[kStagingSlots] = {};
+  int staging_next = 0;
   // look-back bookkeeping
   uint32_t enc_ticket_base = 0, dec_ticket_base = 0;
   uint32_t enc_epoch = 0, dec_epoch = 0;
@@ -149,12 +169,40 @@ int timed_launch(tlc_ctx* c, int kernel, F&& launch) {
   return TLC_OK;
 }
 
-// Next look-back epoch (never 0, the value of cleared status words).  When
-// the counter wraps, the caller clears the status array first.
-uint32_t next_epoch(uint32_t* epoch, uint32_t max_epoch, bool* need_clear) {
-  *need_clear = *epoch >= max_epoch;
-  if (*need_clear) *epoch = 0;
-  return ++*epoch;
+// Next look-back epoch (never 0, the value of cleared status words); when
+// the counter wraps the status array is cleared on the stream first.
+int next_epoch(tlc_ctx* c, uint32_t* epoch, uint32_t max_epoch, uint64_t* status,
+               size_t words, uint32_t* out) {
+  if (*epoch >= max_epoch) {
+    *epoch = 0;
+    hipError_t e = hipMemsetAsync(status, 0, words * sizeof(uint64_t), c->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
+  }
+  *out = ++*epoch;
+  return TLC_OK;
+}
+
+// Copies `bytes` of host descriptors to `dst` on the stream through a
+// pinned staging slot.  A slot is reused only after its previous copy has
+// executed, so back-to-back asynchronous calls cannot overwrite a
+// descriptor table that is still in flight.
+int upload(tlc_ctx* c, void* dst, const void* src, size_t bytes) {
+  const int slot = c->staging_next;
+  c->staging_next = (slot + 1) % kStagingSlots;
+  if (c->staging_used[slot]) {
+    hipError_t e = hipEventSynchronize(c->staging_done[slot]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging)");
+  }
+  uint8_t* host = c->staging + (size_t)slot * c->max_tensors * 64;
+  memcpy(host, src, bytes);
+  hipError_t e = hipMemcpyAsync(dst, host, bytes, hipMemcpyHostToDevice, c->stream);
+  if (e == hipSuccess) e = hipEventRecord(c->staging_done[slot], c->stream);
+  if (e != hipSuccess) {
+    c->broken = true;
+    return hip_fail(e, "descriptor upload");
+  }
+  c->staging_used[slot] = true;
+  return TLC_OK;
 }
 
 int sync_and_read(tlc_ctx* c) {
@@ -167,6 +215,19 @@ int sync_and_read(tlc_ctx* c) {
   return TLC_OK;
 }
 
+int check_usable(tlc_ctx* c, const char* fn) {
+  if (!c) return fail(TLC_E_INVALID, "%s: NULL context", fn);
+  if (c->broken) return fail(TLC_E_DEVICE, "%s: context unusable after a device error", fn);
+  return TLC_OK;
+}
+
+// Absmax blocks given to one tensor of a batch (proportional to its size,
+// `items` float4 pairs or single values).
+uint32_t batch_absmax_blocks(size_t items) {
+  size_t b = ceil_div(items, (size_t)kThreads * 4);
+  return (uint32_t)std::max<size_t>(1, std::min<size_t>(b, kAbsmaxMaxBlocks));
+}
+
 }  // namespace
 
 TLC_API size_t tlc_max_compressed_bytes(size_t n) { return quartic_len(n); }
@@ -177,31 +238,51 @@ TLC_API const char* tlc_kernel_name(int kernel) {
   return (kernel >= 0 && kernel < TLC_KERNEL_COUNT) ? kKernelNames[kernel] : nullptr;
 }
 
-TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
+TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors,
+                                 void* hip_stream) {
   if (!out) return fail(TLC_E_INVALID, "tlc_ctx_create: ctx pointer is NULL");
   *out = nullptr;
   if (max_n == 0 || max_n > TLC_MAX_N)
     return fail(TLC_E_INVALID, "tlc_ctx_create: max_n %zu not in [1, %zu]", max_n,
                 (size_t)TLC_MAX_N);
+  if (max_tensors == 0 || max_tensors > TLC_MAX_TENSORS)
+    return fail(TLC_E_INVALID, "tlc_ctx_create: max_tensors %zu not in [1, %d]", max_tensors,
+                TLC_MAX_TENSORS);
   tlc_ctx* c = new (std::nothrow) tlc_ctx();
   if (!c) return fail(TLC_E_DEVICE, "tlc_ctx_create: out of host memory");
   c->stream = (hipStream_t)hip_stream;
   c->max_n = max_n;
-  c->max_m = quartic_len(max_n);
+  c->max_tensors = max_tensors;
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) {
     delete c;
     return hip_fail(e, "hipGetDevice");
   }
-  // layout: ctrl | partials | enc status | dec status | start index
-  c->enc_status_words = (c->max_m + kEncTile - 1) / kEncTile + 1;
-  c->dec_status_words = (c->max_m + kZreTile - 1) / kZreTile + 1;
-  const size_t off_partials = sizeof(Ctrl);
-  const size_t off_enc = round_up(off_partials + kAbsmaxMaxBlocks * sizeof(uint32_t), 256);
-  const size_t off_dec = round_up(off_enc + c->enc_status_words * sizeof(uint64_t), 256);
-  const size_t off_start = round_up(off_dec + c->dec_status_words * sizeof(uint64_t), 256);
-  const size_t start_words = (c->max_m + kDecRange - 1) / kDecRange + 1;
-  const size_t total = off_start + start_words * sizeof(uint64_t);
+  // Bounds over any call: the sum of m_t is at most max_n/5 + tensors, and a
+  // tensor has at most m_t/tile + 1 tiles.
+  const size_t mm = max_n / 5 + max_tensors;
+  c->partials_cap =
+      std::max<size_t>(kAbsmaxMaxBlocks, max_n / ((size_t)kThreads * 4) + max_tensors + 1);
+  c->enc_status_words = mm / kEncTile + max_tensors + 2;
+  c->dec_status_words = mm / kZreTile + max_tensors + 2;
+  c->start_words = mm / kDecRange + max_tensors + 2;
+  // layout: ctrl | partials | enc status | dec status | start | enc descs |
+  //         dec descs | enc results
+  size_t off = sizeof(Ctrl);
+  const size_t off_partials = off;
+  off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
+  const size_t off_enc = off;
+  off = round_up(off + c->enc_status_words * sizeof(uint64_t), 256);
+  const size_t off_dec = off;
+  off = round_up(off + c->dec_status_words * sizeof(uint64_t), 256);
+  const size_t off_start = off;
+  off = round_up(off + c->start_words * sizeof(uint64_t), 256);
+  const size_t off_edesc = off;
+  off = round_up(off + max_tensors * sizeof(EncDesc), 256);
+  const size_t off_ddesc = off;
+  off = round_up(off + max_tensors * sizeof(DecDesc), 256);
+  const size_t off_res = off;
+  const size_t total = round_up(off + max_tensors * sizeof(EncResult), 256);
   e = hipMalloc(&c->ws, total);
   if (e != hipSuccess) {
     delete c;
@@ -213,11 +294,27 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
   c->enc_status = (uint64_t*)(base + off_enc);
   c->dec_status = (uint64_t*)(base + off_dec);
   c->start = (uint64_t*)(base + off_start);
+  c->enc_descs = (EncDesc*)(base + off_edesc);
+  c->dec_descs = (DecDesc*)(base + off_ddesc);
+  c->enc_results = (EncResult*)(base + off_res);
   e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e == hipSuccess)
     e = hipHostMalloc((void**)&c->rb, sizeof(HostReadback), hipHostMallocDefault);
+  if (e == hipSuccess)
+    e = hipHostMalloc((void**)&c->host_results, max_tensors * sizeof(EncResult),
+                      hipHostMallocDefault);
+  if (e == hipSuccess)
+    e = hipHostMalloc((void**)&c->staging, kStagingSlots * max_tensors * 64,
+                      hipHostMallocDefault);
+  for (int i = 0; i < kStagingSlots && e == hipSuccess; ++i)
+    e = hipEventCreateWithFlags(&c->staging_done[i], hipEventDisableTiming);
   if (e != hipSuccess) {
+    for (int i = 0; i < kStagingSlots; ++i)
+      if (c->staging_done[i]) (void)hipEventDestroy(c->staging_done[i]);
+    if (c->staging) (void)hipHostFree(c->staging);
+    if (c->host_results) (void)hipHostFree(c->host_results);
+    if (c->rb) (void)hipHostFree(c->rb);
     (void)hipFree(c->ws);
     delete c;
     return hip_fail(e, "tlc_ctx_create: workspace init");
@@ -227,24 +324,34 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
   return TLC_OK;
 }
 
+TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
+  return tlc_ctx_create_batch(out, max_n, 1, hip_stream);
+}
+
 TLC_API int tlc_ctx_destroy(tlc_ctx* c) {
   if (!c) return TLC_OK;
   ensure_device(c);
   (void)hipStreamSynchronize(c->stream);
   collect_timings(c);
   for (hipEvent_t ev : c->free_events) (void)hipEventDestroy(ev);
+  for (int i = 0; i < kStagingSlots; ++i)
+    if (c->staging_done[i]) (void)hipEventDestroy(c->staging_done[i]);
+  if (c->staging) (void)hipHostFree(c->staging);
+  if (c->host_results) (void)hipHostFree(c->host_results);
   if (c->rb) (void)hipHostFree(c->rb);
   if (c->ws) (void)hipFree(c->ws);
   delete c;
   return TLC_OK;
 }
 
+// ---------------------------------------------------------------- encode
 TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_t n,
                          float s, uint8_t* bytes, size_t bytes_cap, size_t* bytes_len,
                          float* scale) {
   if (bytes_len) *bytes_len = 0;
-  if (!c || !bytes_len || !scale) return fail(TLC_E_INVALID, "tlc_compress: NULL argument");
-  if (c->broken) return fail(TLC_E_DEVICE, "tlc_compress: context unusable after a device error");
+  int st = check_usable(c, "tlc_compress");
+  if (st) return st;
+  if (!bytes_len || !scale) return fail(TLC_E_INVALID, "tlc_compress: NULL argument");
   if (!(s >= 1.0f && s < 2.0f))
     return fail(TLC_E_INVALID, "tlc_compress: s = %g not in [1, 2)", (double)s);
   if (n > c->max_n)
@@ -262,7 +369,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (overlap(tensor, n * 4, residual, n * 4) || overlap(tensor, n * 4, bytes, m) ||
       overlap(residual, n * 4, bytes, m))
     return fail(TLC_E_INVALID, "tlc_compress: tensor, residual and bytes overlap");
-  int st = ensure_device(c);
+  st = ensure_device(c);
   if (st) return st;
 
   uint32_t np = 0;
@@ -270,13 +377,10 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
-  bool clear = false;
-  const uint32_t epoch = next_epoch(&c->enc_epoch, kEncEpochMax, &clear);
-  if (clear) {
-    hipError_t e = hipMemsetAsync(c->enc_status, 0, c->enc_status_words * 8, c->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
-  }
-  const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
+  uint32_t epoch = 0;
+  st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
+  if (st) return st;
+  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, bytes,
                                c->enc_status, ntiles, c->enc_ticket_base, epoch, c->ctrl,
@@ -290,51 +394,301 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     c->broken = true;
     return fail(TLC_E_DEVICE, "tlc_compress: look-back wait timed out");
   }
-  if (c->rb->enc_err)
+  if (c->rb->enc.err)
     return fail(TLC_E_NONFINITE, "tlc_compress: NaN/Inf in tensor+residual or max*s overflow");
-  *bytes_len = c->rb->enc_len;
-  *scale = c->rb->enc_scale;
+  *bytes_len = c->rb->enc.len;
+  *scale = c->rb->enc.scale;
   return TLC_OK;
 }
 
+TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* tensors,
+                               float* const* residuals, const size_t* ns, const float* s,
+                               uint8_t* const* bytes, const size_t* caps, size_t* bytes_len,
+                               float* scales, int* status) {
+  int st = check_usable(c, "tlc_compress_batch");
+  if (st) return st;
+  if (count == 0) return TLC_OK;
+  if (!tensors || !residuals || !ns || !s || !bytes || !caps || !bytes_len || !scales ||
+      !status)
+    return fail(TLC_E_INVALID, "tlc_compress_batch: NULL argument");
+  if (count > c->max_tensors)
+    return fail(TLC_E_INVALID, "tlc_compress_batch: %zu tensors exceed the context's %zu",
+                count, c->max_tensors);
+  size_t total_n = 0;
+  for (size_t t = 0; t < count; ++t) {
+    bytes_len[t] = 0;
+    scales[t] = 0.0f;
+    status[t] = TLC_OK;
+  }
+  for (size_t t = 0; t < count; ++t) {
+    if (!(s[t] >= 1.0f && s[t] < 2.0f))
+      return fail(TLC_E_INVALID, "tlc_compress_batch: tensor %zu: s = %g not in [1, 2)", t,
+                  (double)s[t]);
+    if (ns[t] > c->max_n)
+      return fail(TLC_E_INVALID, "tlc_compress_batch: tensor %zu: n = %zu too large", t, ns[t]);
+    total_n += ns[t];
+    if (ns[t] == 0) continue;
+    const size_t m = quartic_len(ns[t]);
+    if (!tensors[t] || !residuals[t] || !bytes[t])
+      return fail(TLC_E_INVALID, "tlc_compress_batch: tensor %zu: NULL device pointer", t);
+    if (caps[t] < m)
+      return fail(TLC_E_CAPACITY, "tlc_compress_batch: tensor %zu: capacity %zu < %zu", t,
+                  caps[t], m);
+    if (overlap(tensors[t], ns[t] * 4, residuals[t], ns[t] * 4) ||
+        overlap(tensors[t], ns[t] * 4, bytes[t], m) ||
+        overlap(residuals[t], ns[t] * 4, bytes[t], m))
+      return fail(TLC_E_INVALID, "tlc_compress_batch: tensor %zu: buffers overlap", t);
+  }
+  if (total_n > c->max_n)
+    return fail(TLC_E_INVALID, "tlc_compress_batch: %zu values exceed the context's max_n %zu",
+                total_n, c->max_n);
+  std::vector<EncDesc> d;
+  std::vector<size_t> which;  // batch position of each launched tensor
+  d.reserve(count);
+  uint32_t blocks = 0, tiles = 0;
+  for (size_t t = 0; t < count; ++t) {
+    if (ns[t] == 0) continue;
+    EncDesc e = {};
+    e.x = tensors[t];
+    e.r = residuals[t];
+    e.out = bytes[t];
+    e.n = ns[t];
+    e.m = (uint32_t)quartic_len(ns[t]);
+    e.s = s[t];
+    e.tile0 = tiles;
+    e.blk0 = blocks;
+    const bool al = aligned16(tensors[t]) && aligned16(residuals[t]);
+    e.nblk = batch_absmax_blocks(al ? ns[t] / 4 : ns[t]);
+    e.vec = ((e.m % 4 == 0 && al) ? 1u : 0u) | (al ? 2u : 0u);
+    blocks += e.nblk;
+    tiles += (uint32_t)ceil_div(e.m, kEncTile);
+    d.push_back(e);
+    which.push_back(t);
+  }
+  if (d.empty()) return TLC_OK;
+  if (blocks > c->partials_cap || tiles > c->enc_status_words)
+    return fail(TLC_E_INVALID, "tlc_compress_batch: batch exceeds the context's workspace");
+  st = ensure_device(c);
+  if (st) return st;
+  const uint32_t cnt = (uint32_t)d.size();
+  st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_ABSMAX_BATCH, [&] {
+    return launch_absmax_batch(c->enc_descs, cnt, blocks, c->partials, c->stream);
+  });
+  if (st) return st;
+  uint32_t epoch = 0;
+  st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_BATCH, [&] {
+    return launch_quant_encode_batch(c->enc_descs, cnt, tiles, c->partials, c->enc_results,
+                                     c->enc_status, c->enc_ticket_base, epoch, c->ctrl,
+                                     c->stream);
+  });
+  if (st) return st;
+  c->enc_ticket_base += tiles;
+  hipError_t e = hipMemcpyAsync(c->host_results, c->enc_results, cnt * sizeof(EncResult),
+                                hipMemcpyDeviceToHost, c->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(results)");
+  st = sync_and_read(c);
+  if (st) return st;
+  if (c->rb->fault) {
+    c->broken = true;
+    return fail(TLC_E_DEVICE, "tlc_compress_batch: look-back wait timed out");
+  }
+  int worst = TLC_OK;
+  for (uint32_t i = 0; i < cnt; ++i) {
+    const size_t t = which[i];
+    const EncResult& r = c->host_results[i];
+    if (r.err) {
+      status[t] = TLC_E_NONFINITE;
+      worst = TLC_E_NONFINITE;
+    } else {
+      bytes_len[t] = r.len;
+      scales[t] = r.scale;
+    }
+  }
+  if (worst) fail(worst, "tlc_compress_batch: NaN/Inf or overflow in at least one tensor");
+  return worst;
+}
+
+// ---------------------------------------------------------------- decode
+namespace {
+
+// Shared checks of one stream; *skip is set for an empty tensor.
+int check_stream(const char* fn, size_t t, const uint8_t* bytes, size_t len, float scale,
+                 size_t n, const float* out, bool* skip) {
+  *skip = false;
+  if (!isfinite(scale) || scale < 0.0f)
+    return fail(TLC_E_INVALID, "%s: stream %zu: scale %g is not finite and >= 0", fn, t,
+                (double)scale);
+  if (n == 0) {
+    if (len != 0) return fail(TLC_E_CORRUPT, "%s: stream %zu: bytes for an empty tensor", fn, t);
+    *skip = true;
+    return TLC_OK;
+  }
+  if (!out || (len && !bytes)) return fail(TLC_E_INVALID, "%s: stream %zu: NULL pointer", fn, t);
+  if (len == 0 || len > quartic_len(n))
+    return fail(TLC_E_CORRUPT, "%s: stream %zu: length %zu impossible for n = %zu", fn, t, len,
+                n);
+  return TLC_OK;
+}
+
+}  // namespace
+
 TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, float scale,
                            size_t n, float* out, int accumulate) {
-  if (!c) return fail(TLC_E_INVALID, "tlc_decompress: NULL context");
-  if (c->broken) return fail(TLC_E_DEVICE, "tlc_decompress: context unusable after a device error");
-  if (!isfinite(scale) || scale < 0.0f)
-    return fail(TLC_E_INVALID, "tlc_decompress: scale %g is not finite and >= 0", (double)scale);
+  int st = check_usable(c, "tlc_decompress");
+  if (st) return st;
   if (n > c->max_n)
     return fail(TLC_E_INVALID, "tlc_decompress: n = %zu exceeds the context's max_n %zu", n,
                 c->max_n);
-  if (n == 0) {
-    if (bytes_len != 0) return fail(TLC_E_CORRUPT, "tlc_decompress: bytes for an empty tensor");
-    return TLC_OK;
-  }
-  if (!out || (bytes_len && !bytes)) return fail(TLC_E_INVALID, "tlc_decompress: NULL device pointer");
+  bool skip = false;
+  st = check_stream("tlc_decompress", 0, bytes, bytes_len, scale, n, out, &skip);
+  if (st || skip) return st;
   const size_t m = quartic_len(n);
-  if (bytes_len == 0 || bytes_len > m)
-    return fail(TLC_E_CORRUPT, "tlc_decompress: stream length %zu impossible for n = %zu",
-                bytes_len, n);
-  int st = ensure_device(c);
+  st = ensure_device(c);
   if (st) return st;
-  bool clear = false;
-  const uint32_t epoch = next_epoch(&c->dec_epoch, kDecEpochMax, &clear);
-  if (clear) {
-    hipError_t e = hipMemsetAsync(c->dec_status, 0, c->dec_status_words * 8, c->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
-  }
-  const uint32_t ntiles = (uint32_t)((bytes_len + kZreTile - 1) / kZreTile);
+  uint32_t epoch = 0;
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  if (st) return st;
+  const uint32_t ntiles = (uint32_t)ceil_div(bytes_len, kZreTile);
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
     return launch_zre_index(bytes, (uint32_t)bytes_len, (uint32_t)m, c->start, c->dec_status,
                             ntiles, c->dec_ticket_base, epoch, c->ctrl, c->stream);
   });
   if (st) return st;
   c->dec_ticket_base += ntiles;
-  st = timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
+  return timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
     return launch_expand_dequant(bytes, (uint32_t)bytes_len, c->start, n, m, scale, out,
                                  accumulate, epoch, c->ctrl, c->stream);
   });
-  return st;
+}
+
+TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const* bytes,
+                                 const size_t* bytes_len, const float* scales, const size_t* ns,
+                                 float* const* outs, int accumulate) {
+  int st = check_usable(c, "tlc_decompress_batch");
+  if (st) return st;
+  if (count == 0) return TLC_OK;
+  if (!bytes || !bytes_len || !scales || !ns || !outs)
+    return fail(TLC_E_INVALID, "tlc_decompress_batch: NULL argument");
+  if (count > c->max_tensors)
+    return fail(TLC_E_INVALID, "tlc_decompress_batch: %zu streams exceed the context's %zu",
+                count, c->max_tensors);
+  size_t total_n = 0;
+  std::vector<DecDesc> d;
+  d.reserve(count);
+  uint32_t tiles = 0, ranges = 0;
+  for (size_t t = 0; t < count; ++t) {
+    if (ns[t] > c->max_n)
+      return fail(TLC_E_INVALID, "tlc_decompress_batch: stream %zu: n = %zu too large", t,
+                  ns[t]);
+    bool skip = false;
+    st = check_stream("tlc_decompress_batch", t, bytes[t], bytes_len[t], scales[t], ns[t],
+                      outs[t], &skip);
+    if (st) return st;
+    total_n += ns[t];
+    if (skip) continue;
+    DecDesc e = {};
+    e.C = bytes[t];
+    e.out = outs[t];
+    e.n = ns[t];
+    e.c = (uint32_t)bytes_len[t];
+    e.m = (uint32_t)quartic_len(ns[t]);
+    e.scale = scales[t];
+    e.tile0 = tiles;
+    e.range0 = ranges;
+    e.vec = (e.m % 4 == 0 && aligned16(outs[t])) ? 1u : 0u;
+    tiles += (uint32_t)ceil_div(e.c, kZreTile);
+    ranges += (uint32_t)ceil_div(e.m, kDecRange);
+    d.push_back(e);
+  }
+  if (total_n > c->max_n)
+    return fail(TLC_E_INVALID, "tlc_decompress_batch: %zu values exceed the context's max_n %zu",
+                total_n, c->max_n);
+  if (d.empty()) return TLC_OK;
+  if (tiles > c->dec_status_words || ranges > c->start_words)
+    return fail(TLC_E_INVALID, "tlc_decompress_batch: batch exceeds the context's workspace");
+  st = ensure_device(c);
+  if (st) return st;
+  const uint32_t cnt = (uint32_t)d.size();
+  st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
+  if (st) return st;
+  uint32_t epoch = 0;
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
+    return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
+                                  c->dec_ticket_base, epoch, c->ctrl, c->stream);
+  });
+  if (st) return st;
+  c->dec_ticket_base += tiles;
+  return timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT_BATCH, [&] {
+    return launch_expand_dequant_batch(c->dec_descs, cnt, ranges, c->start, accumulate, epoch,
+                                       c->ctrl, c->stream);
+  });
+}
+
+TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* bytes,
+                               const size_t* bytes_len, const float* scales, size_t n,
+                               float* out, int accumulate) {
+  int st = check_usable(c, "tlc_decompress_sum");
+  if (st) return st;
+  if (count == 0) return fail(TLC_E_INVALID, "tlc_decompress_sum: no streams");
+  if (!bytes || !bytes_len || !scales)
+    return fail(TLC_E_INVALID, "tlc_decompress_sum: NULL argument");
+  if (count > c->max_tensors)
+    return fail(TLC_E_INVALID, "tlc_decompress_sum: %zu streams exceed the context's %zu",
+                count, c->max_tensors);
+  if (n > c->max_n / count)
+    return fail(TLC_E_INVALID,
+                "tlc_decompress_sum: %zu streams of %zu values exceed the context's max_n %zu",
+                count, n, c->max_n);
+  const size_t m = quartic_len(n);
+  const uint32_t nranges = (uint32_t)ceil_div(m, kDecRange);
+  std::vector<DecDesc> d;
+  d.reserve(count);
+  uint32_t tiles = 0;
+  for (size_t t = 0; t < count; ++t) {
+    bool skip = false;
+    st = check_stream("tlc_decompress_sum", t, bytes[t], bytes_len[t], scales[t], n, out, &skip);
+    if (st) return st;
+    if (skip) continue;  // n == 0: nothing to do for any stream
+    DecDesc e = {};
+    e.C = bytes[t];
+    e.out = out;
+    e.n = n;
+    e.c = (uint32_t)bytes_len[t];
+    e.m = (uint32_t)m;
+    e.scale = scales[t];
+    e.tile0 = tiles;
+    e.range0 = (uint32_t)t * nranges;
+    tiles += (uint32_t)ceil_div(e.c, kZreTile);
+    d.push_back(e);
+  }
+  if (d.empty()) return TLC_OK;
+  if (tiles > c->dec_status_words || (size_t)count * nranges > c->start_words)
+    return fail(TLC_E_INVALID, "tlc_decompress_sum: streams exceed the context's workspace");
+  st = ensure_device(c);
+  if (st) return st;
+  const uint32_t cnt = (uint32_t)d.size();
+  st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
+  if (st) return st;
+  uint32_t epoch = 0;
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
+    return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
+                                  c->dec_ticket_base, epoch, c->ctrl, c->stream);
+  });
+  if (st) return st;
+  c->dec_ticket_base += tiles;
+  const int vec = (m % 4 == 0 && aligned16(out)) ? 1 : 0;
+  return timed_launch(c, TLC_KERNEL_EXPAND_SUM, [&] {
+    return launch_expand_sum(c->dec_descs, cnt, c->start, n, m, out, vec, accumulate, epoch,
+                             c->ctrl, c->stream);
+  });
 }
 
 TLC_API int tlc_sync(tlc_ctx* c) {
@@ -356,6 +710,7 @@ TLC_API int tlc_sync(tlc_ctx* c) {
   return TLC_OK;
 }
 
+// ---------------------------------------------------------------- profiling
 TLC_API int tlc_profile_enable(tlc_ctx* c, int on) {
   if (!c) return fail(TLC_E_INVALID, "tlc_profile_enable: NULL context");
   c->profiling = on != 0;

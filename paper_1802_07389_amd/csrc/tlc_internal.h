@@ -15,45 +15,98 @@ constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
 constexpr uint32_t kAbsmaxMaxBlocks = 512;  // partial maxima per encode
 
-// Device control block (one per context, in the workspace).  The first 16
-// bytes are copied to pinned host memory after every encode.
+// Per-tensor encode result (device), written by the encoder's tiles.
+struct EncResult {
+  uint32_t err;    // 1: NaN/Inf in tensor + residual, or max*s overflow
+  uint32_t len;    // zero-run stream length
+  float scale;     // M
+  uint32_t reserved;
+};
+
+// Device control block (one per context, in the workspace).  The first 32
+// bytes are copied to pinned host memory after every encode and by
+// tlc_sync.
 struct Ctrl {
-  uint32_t enc_err;        // 1 if the last encode saw NaN/Inf or overflow
-  uint32_t enc_len;        // zero-run stream length of the last encode
-  float enc_scale;         // M of the last encode
+  EncResult enc;           // single-tensor encode result
   uint32_t fault;          // sticky: a look-back wait timed out
   uint32_t dec_corrupt;    // sticky: a decoded stream had the wrong length
-  uint32_t dec_bad_epoch;  // epoch of the last decode whose stream was bad
-  uint32_t enc_ticket;     // tile tickets of the zero-run encoder
-  uint32_t dec_ticket;     // tile tickets of the zero-run decoder
-  uint32_t pad[56];
+  uint32_t dec_bad_epoch;  // epoch of the last decode launch with a bad stream
+  uint32_t enc_ticket;     // tile tickets of the encoder
+  uint32_t dec_ticket;     // tile tickets of the zero-run index scan
+  uint32_t pad[55];
 };
 static_assert(sizeof(Ctrl) == 256, "Ctrl is one 256-byte slot");
 
 struct HostReadback {
-  uint32_t enc_err;
-  uint32_t enc_len;
-  float enc_scale;
+  EncResult enc;
   uint32_t fault;
   uint32_t dec_corrupt;
-  uint32_t pad[3];
+  uint32_t pad[2];
 };
 
-// Launchers (tlc_kernels.hip).  All return the hipError_t of the launch.
+// One tensor of a batched encode (device copy of the host's description).
+struct EncDesc {
+  const float* x;
+  float* r;
+  uint8_t* out;
+  uint64_t n;
+  uint32_t m;
+  float s;
+  uint32_t tile0;  // first encoder tile (global tile numbering of the launch)
+  uint32_t blk0;   // first absmax block / partial maximum of this tensor
+  uint32_t nblk;   // absmax blocks of this tensor
+  uint32_t vec;    // 1: m % 4 == 0 and x, r 16-byte aligned
+  uint32_t pad[2];
+};
+static_assert(sizeof(EncDesc) == 64, "EncDesc is 64 bytes");
+
+// One stream of a batched decode or of a decode-sum.
+struct DecDesc {
+  const uint8_t* C;
+  float* out;      // batched decode: this stream's output (decode-sum: unused)
+  uint64_t n;
+  uint32_t c;
+  uint32_t m;
+  float scale;
+  uint32_t tile0;   // first index-scan tile (global numbering of the launch)
+  uint32_t range0;  // first start-index entry / expand block of this stream
+  uint32_t vec;     // 1: m % 4 == 0 and out 16-byte aligned
+  uint32_t pad[4];
+};
+static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
+
+// Launchers (encode.hip, decode.hip).  All return the hipError_t of the
+// launch.
 hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
-                         uint32_t* partials, uint32_t* nblocks,
-                         hipStream_t st);
+                         uint32_t* partials, uint32_t* nblocks, hipStream_t st);
 hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
-                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
-                              uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                              uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+                               const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                               uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                               uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
+                               uint32_t* partials, hipStream_t st);
+hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_tiles, const uint32_t* partials,
+                                     EncResult* results, uint64_t* status,
+                                     uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
+                                     hipStream_t st);
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
-                           uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                           uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+                            uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                            uint32_t epoch, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
                                  uint64_t n, uint64_t m, float scale, float* out,
                                  int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                  hipStream_t st);
+hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
+                                  uint64_t* start, uint64_t* status, uint32_t ticket_base,
+                                  uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_expand_dequant_batch(const DecDesc* descs, uint32_t count,
+                                       uint32_t total_ranges, const uint64_t* start,
+                                       int accumulate, uint32_t epoch, const Ctrl* ctrl,
+                                       hipStream_t st);
+hipError_t launch_expand_sum(const DecDesc* descs, uint32_t count, const uint64_t* start,
+                             uint64_t n, uint64_t m, float* out, int vec, int accumulate,
+                             uint32_t epoch, const Ctrl* ctrl, hipStream_t st);
 
 // Epoch widths of the two look-back status layouts.
 constexpr uint32_t kEncEpochMax = (1u << 23) - 1u;

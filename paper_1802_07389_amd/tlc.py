@@ -25,13 +25,19 @@ TLC_KERNEL_ABSMAX = 0
 TLC_KERNEL_QUANT_ENCODE = 1
 TLC_KERNEL_ZRE_INDEX = 2
 TLC_KERNEL_EXPAND_DEQUANT = 3
-TLC_KERNEL_COUNT = 4
+TLC_KERNEL_ABSMAX_BATCH = 4
+TLC_KERNEL_QUANT_ENCODE_BATCH = 5
+TLC_KERNEL_ZRE_INDEX_BATCH = 6
+TLC_KERNEL_EXPAND_DEQUANT_BATCH = 7
+TLC_KERNEL_EXPAND_SUM = 8
+TLC_KERNEL_COUNT = 9
 
 EXPORTS = (
-    "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_destroy",
-    "tlc_compress", "tlc_decompress", "tlc_sync", "tlc_last_error_string",
-    "tlc_profile_enable", "tlc_profile_get", "tlc_profile_reset",
-    "tlc_kernel_name",
+    "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_create_batch",
+    "tlc_ctx_destroy", "tlc_compress", "tlc_compress_batch", "tlc_decompress",
+    "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
+    "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_get",
+    "tlc_profile_reset", "tlc_kernel_name",
 )
 
 
@@ -52,6 +58,16 @@ def _load():
     L.tlc_max_compressed_bytes.restype = sz
     L.tlc_ctx_create.argtypes = [ctypes.POINTER(vp), sz, vp]
     L.tlc_ctx_create.restype = i
+    L.tlc_ctx_create_batch.argtypes = [ctypes.POINTER(vp), sz, sz, vp]
+    L.tlc_ctx_create_batch.restype = i
+    P = ctypes.POINTER
+    L.tlc_compress_batch.argtypes = [vp, sz, P(vp), P(vp), P(sz), P(f), P(vp), P(sz),
+                                     P(sz), P(f), P(i)]
+    L.tlc_compress_batch.restype = i
+    L.tlc_decompress_batch.argtypes = [vp, sz, P(vp), P(sz), P(f), P(sz), P(vp), i]
+    L.tlc_decompress_batch.restype = i
+    L.tlc_decompress_sum.argtypes = [vp, sz, P(vp), P(sz), P(f), sz, vp, i]
+    L.tlc_decompress_sum.restype = i
     L.tlc_ctx_destroy.argtypes = [vp]
     L.tlc_ctx_destroy.restype = i
     L.tlc_compress.argtypes = [vp, vp, vp, sz, f, vp, sz, ctypes.POINTER(sz),
@@ -98,6 +114,46 @@ def tlc_ctx_create(max_n, hip_stream):
     h = ctypes.c_void_p()
     _check(lib.tlc_ctx_create(ctypes.byref(h), max_n, hip_stream))
     return h.value
+
+
+def tlc_ctx_create_batch(max_n, max_tensors, hip_stream):
+    """Return a context handle for batched calls."""
+    h = ctypes.c_void_p()
+    _check(lib.tlc_ctx_create_batch(ctypes.byref(h), max_n, max_tensors, hip_stream))
+    return h.value
+
+
+def _arr(ctype, values):
+    return (ctype * len(values))(*values)
+
+
+def tlc_compress_batch(ctx, tensors, residuals, ns, s, bytes_, caps):
+    """Device pointer lists in; returns (status, bytes_len list, scales list,
+    per-tensor status list)."""
+    k = len(tensors)
+    lens = (ctypes.c_size_t * k)()
+    scales = (ctypes.c_float * k)()
+    stat = (ctypes.c_int * k)()
+    st = lib.tlc_compress_batch(
+        ctx, k, _arr(ctypes.c_void_p, tensors), _arr(ctypes.c_void_p, residuals),
+        _arr(ctypes.c_size_t, ns), _arr(ctypes.c_float, s), _arr(ctypes.c_void_p, bytes_),
+        _arr(ctypes.c_size_t, caps), lens, scales, stat)
+    return st, list(lens), list(scales), list(stat)
+
+
+def tlc_decompress_batch(ctx, bytes_, bytes_len, scales, ns, outs, accumulate):
+    k = len(bytes_)
+    return lib.tlc_decompress_batch(
+        ctx, k, _arr(ctypes.c_void_p, bytes_), _arr(ctypes.c_size_t, bytes_len),
+        _arr(ctypes.c_float, scales), _arr(ctypes.c_size_t, ns), _arr(ctypes.c_void_p, outs),
+        int(bool(accumulate)))
+
+
+def tlc_decompress_sum(ctx, bytes_, bytes_len, scales, n, out, accumulate):
+    k = len(bytes_)
+    return lib.tlc_decompress_sum(
+        ctx, k, _arr(ctypes.c_void_p, bytes_), _arr(ctypes.c_size_t, bytes_len),
+        _arr(ctypes.c_float, scales), n, out, int(bool(accumulate)))
 
 
 def tlc_ctx_destroy(ctx):
@@ -159,13 +215,15 @@ def _dev_u8(t, name):
 class Context:
     """One compression context (one tensor, one direction) on one stream."""
 
-    def __init__(self, max_n, stream=None, device=None):
+    def __init__(self, max_n, stream=None, device=None, max_tensors=1):
         self.device = torch.device(device) if device is not None else torch.device(
             "cuda", torch.cuda.current_device())
         with torch.cuda.device(self.device):
             self.stream = stream if stream is not None else torch.cuda.current_stream()
             self.max_n = int(max_n)
-            self.handle = tlc_ctx_create(self.max_n, self.stream.cuda_stream)
+            self.max_tensors = int(max_tensors)
+            self.handle = tlc_ctx_create_batch(self.max_n, self.max_tensors,
+                                               self.stream.cuda_stream)
 
     def close(self):
         if getattr(self, "handle", None):
@@ -204,6 +262,35 @@ class Context:
         ptr = _dev_u8(data, "data") if data.numel() else None
         _check(tlc_decompress(self.handle, ptr, data.numel(), float(scale), n,
                               _dev_f32(out, "out"), accumulate))
+
+    def compress_batch(self, tensors, residuals, s, outs=None):
+        """Encode a list of tensors in one pass.  Returns a list of
+        (bytes view, scale); raises TLCError if any tensor is refused (the
+        others are still encoded: see per-tensor status via the C call)."""
+        if outs is None:
+            outs = [torch.empty(max(tlc_max_compressed_bytes(t.numel()), 1),
+                                dtype=torch.uint8, device=self.device) for t in tensors]
+        ss = list(s) if isinstance(s, (list, tuple)) else [float(s)] * len(tensors)
+        st, lens, scales, _ = tlc_compress_batch(
+            self.handle, [_dev_f32(t, "tensor") for t in tensors],
+            [_dev_f32(r, "residual") for r in residuals], [t.numel() for t in tensors], ss,
+            [_dev_u8(o, "out") for o in outs], [o.numel() for o in outs])
+        _check(st)
+        return [(o[:ln], sc) for o, ln, sc in zip(outs, lens, scales)]
+
+    def decompress_batch(self, datas, scales, outs, accumulate=False):
+        """Decode a list of streams into a list of outputs (async)."""
+        _check(tlc_decompress_batch(
+            self.handle, [_dev_u8(d, "data") if d.numel() else None for d in datas],
+            [d.numel() for d in datas], [float(x) for x in scales],
+            [o.numel() for o in outs], [_dev_f32(o, "out") for o in outs], accumulate))
+
+    def decompress_sum(self, datas, scales, out, accumulate=False):
+        """Decode streams of one tensor and add them into out in order (async)."""
+        _check(tlc_decompress_sum(
+            self.handle, [_dev_u8(d, "data") if d.numel() else None for d in datas],
+            [d.numel() for d in datas], [float(x) for x in scales], out.numel(),
+            _dev_f32(out, "out"), accumulate))
 
     def sync(self):
         _check(tlc_sync(self.handle))

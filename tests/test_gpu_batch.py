@@ -1,0 +1,236 @@
+"""GPU parity of the batched entry points (tlc_compress_batch,
+tlc_decompress_batch, tlc_decompress_sum) against the CPU oracle applied
+tensor by tensor / stream by stream.  Bar: bit-exact."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_07389_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+def G():
+    import gpuutil
+    return gpuutil
+
+
+@pytest.fixture(scope="module")
+def bctx():
+    from paper_1802_07389_amd import tlc
+    c = tlc.Context(max_n=16 * workloads.C5_N, max_tensors=400)
+    yield c
+    c.close()
+
+
+def batch_encode(ctx, xs, rs, ss, offsets=None):
+    """Run tlc_compress_batch; return (status, per-tensor status, [(bytes,
+    scale, residual)])."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    offsets = offsets or [0] * len(xs)
+    xd = [g.to_dev(x, o) for x, o in zip(xs, offsets)]
+    rd = [g.to_dev(r, o) for r, o in zip(rs, offsets)]
+    outs = [torch.full((max(tlc.tlc_max_compressed_bytes(x.size), 1),), 0xAB,
+                       dtype=torch.uint8, device="cuda") for x in xs]
+    ptr = lambda t, n: t.data_ptr() if n else None
+    st, lens, scales, stat = tlc.tlc_compress_batch(
+        ctx.handle, [ptr(t, x.size) for t, x in zip(xd, xs)],
+        [ptr(t, x.size) for t, x in zip(rd, xs)], [x.size for x in xs], ss,
+        [o.data_ptr() for o in outs], [o.numel() for o in outs])
+    torch.cuda.synchronize()
+    res = [(o[:ln].cpu().numpy(), sc, r.cpu().numpy(), o.cpu().numpy())
+           for o, ln, sc, r in zip(outs, lens, scales, rd)]
+    return st, stat, res
+
+
+def check_against_oracle(xs, rs, ss, res, tag):
+    g = G()
+    for t, (x, r, s) in enumerate(zip(xs, rs, ss)):
+        r_ref = r.copy()
+        st, C_ref, M_ref = oracle.compress(x, r_ref, s)
+        C, M, r_gpu, _ = res[t]
+        assert st == 0, (tag, t)
+        assert M == M_ref, (tag, t, M, M_ref)
+        assert np.array_equal(C, C_ref), (tag, t, C.size, C_ref.size)
+        assert np.array_equal(g.bits(r_gpu), g.bits(r_ref)), (tag, t)
+
+
+def test_batch_mixed_sizes_and_alignment(bctx):
+    sizes = [0, 1, 5, 7, 13, 4096 * 5, 4096 * 5 + 3, 100003, 0, 5 * 14 * 4096 + 9, 262144]
+    offs = [0, 0, 1, 0, 3, 0, 2, 0, 0, 1, 0]
+    xs, rs, ss = [], [], []
+    for t, n in enumerate(sizes):
+        x = workloads.runs_tensor([700, t], n) if t % 2 else workloads.normal([701, t], n, 1.0)
+        xs.append(x)
+        rs.append(workloads.normal([702, t], n, 1e-4))
+        ss.append([1.0, 1.5, 1.75, 1.9][t % 4])
+    st, stat, res = batch_encode(bctx, xs, rs, ss, offs)
+    assert st == 0 and all(v == 0 for v in stat)
+    check_against_oracle(xs, rs, ss, res, "mixed")
+
+
+def test_batch_nonfinite_tensor_is_refused_alone(bctx):
+    from paper_1802_07389_amd import tlc
+    g = G()
+    sizes = [1000, 5000, 20481, 7]
+    xs = [workloads.normal([710, t], n, 1.0) for t, n in enumerate(sizes)]
+    rs = [workloads.normal([711, t], n, 1e-3) for t, n in enumerate(sizes)]
+    xs[2][123] = np.nan
+    ss = [1.0] * 4
+    st, stat, res = batch_encode(bctx, xs, rs, ss)
+    assert st == tlc.TLC_E_NONFINITE
+    assert stat == [0, 0, tlc.TLC_E_NONFINITE, 0]
+    C, M, r_gpu, raw = res[2]
+    assert C.size == 0
+    assert np.array_equal(g.bits(r_gpu), g.bits(rs[2]))  # residual untouched
+    assert bool((raw == 0xAB).all())  # bytes untouched
+    keep = [0, 1, 3]
+    check_against_oracle([xs[i] for i in keep], [rs[i] for i in keep], [ss[i] for i in keep],
+                         [res[i] for i in keep], "nonfinite-others")
+
+
+def test_batch_argument_errors(bctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    x = torch.zeros(100, device="cuda")
+    r = torch.zeros(100, device="cuda")
+    o = torch.zeros(100, dtype=torch.uint8, device="cuda")
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [x.data_ptr()], [r.data_ptr()], [100], [1.0],
+                                    [o.data_ptr()], [19])
+    assert st == tlc.TLC_E_CAPACITY
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [x.data_ptr()], [r.data_ptr()], [100], [2.0],
+                                    [o.data_ptr()], [20])
+    assert st == tlc.TLC_E_INVALID
+    k = bctx.max_tensors + 1
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [x.data_ptr()] * k, [r.data_ptr()] * k,
+                                    [0] * k, [1.0] * k, [o.data_ptr()] * k, [20] * k)
+    assert st == tlc.TLC_E_INVALID
+    assert tlc.tlc_sync(bctx.handle) == tlc.TLC_OK
+
+
+def test_batch_c2_ten_steps_and_batch_decode(bctx):
+    """C2 through the batched calls: 335 tensors, 10 steps, residuals carried."""
+    import torch
+    g = G()
+    sizes = workloads.c2_sizes()
+    rs_gpu = [torch.zeros(n, device="cuda") for n in sizes]
+    rs_ref = [np.zeros(n, F32) for n in sizes]
+    outs = [torch.full((n,), -0.0, device="cuda") for n in sizes]
+    for step in range(workloads.C2_STEPS):
+        xs = [workloads.c2_gradient(step, t, n) for t, n in enumerate(sizes)]
+        xd = [torch.from_numpy(x).cuda() for x in xs]
+        pays = bctx.compress_batch(xd, rs_gpu, workloads.C2_S)
+        for t, x in enumerate(xs):
+            st, C_ref, M_ref = oracle.compress(x, rs_ref[t], workloads.C2_S)
+            C, M = pays[t]
+            assert st == 0 and M == M_ref, (step, t)
+            assert np.array_equal(C.cpu().numpy(), C_ref), (step, t)
+        acc = step % 2 == 1
+        bctx.decompress_batch([p[0] for p in pays], [p[1] for p in pays], outs, accumulate=acc)
+        bctx.sync()
+        for t in range(0, len(sizes), 7):
+            assert np.array_equal(g.bits(rs_gpu[t].cpu().numpy()), g.bits(rs_ref[t])), (step, t)
+        g.log(f"batched C2 step {step} ok")
+    # the last decode was accumulate=True on top of step 8's values: check a few
+    # tensors end to end against the oracle
+    for t in range(0, len(sizes), 41):
+        n = sizes[t]
+        out_ref = np.full(n, -0.0, F32)
+        rr = np.zeros(n, F32)
+        for step in range(workloads.C2_STEPS):
+            x = workloads.c2_gradient(step, t, n)
+            st, C, M = oracle.compress(x, rr, workloads.C2_S)
+            st, out_ref = oracle.decompress(C, M, n, out_ref, accumulate=(step % 2 == 1))
+        assert np.array_equal(g.bits(outs[t].cpu().numpy()), g.bits(out_ref)), t
+
+
+def test_batch_decode_corrupt_writes_nothing(bctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    sizes = [5000, 20481, 300]
+    xs = [workloads.runs_tensor([720, t], n) for t, n in enumerate(sizes)]
+    pays = []
+    for x in xs:
+        st, C, M = oracle.compress(x, np.zeros(x.size, F32), 1.5)
+        pays.append((C, M))
+    bad = pays[1][0].copy()
+    bad[len(bad) // 2] = 7 if bad[len(bad) // 2] >= 243 else 255
+    streams = [pays[0][0], bad, pays[2][0]]
+    outs0 = [workloads.normal([721, t], n) for t, n in enumerate(sizes)]
+    outs = [torch.from_numpy(o.copy()).cuda() for o in outs0]
+    cd = [torch.from_numpy(c).cuda() for c in streams]
+    bctx.decompress_batch(cd, [p[1] for p in pays], outs, accumulate=True)
+    assert tlc.tlc_sync(bctx.handle) == tlc.TLC_E_CORRUPT
+    for o, o0 in zip(outs, outs0):
+        assert np.array_equal(g.bits(o.cpu().numpy()), g.bits(o0))
+
+
+@pytest.mark.parametrize("n,count,offset", [(1, 3, 0), (7, 2, 0), (4096 * 5 + 13, 3, 0),
+                                            (4096 * 5 * 3, 5, 1), (100003, 4, 0),
+                                            (262144, 2, 2)])
+def test_decompress_sum_small(bctx, n, count, offset):
+    """Streams summed in order equal sequential decode-accumulate, bit for bit."""
+    g = G()
+    import torch
+    pays = []
+    for p in range(count):
+        x = workloads.runs_tensor([730, n, p], n) if p % 2 else workloads.normal([731, n, p], n)
+        st, C, M = oracle.compress(x, np.zeros(n, F32), [1.0, 1.75, 1.5][p % 3])
+        pays.append((C, M))
+    out0 = workloads.normal([732, n], n, 1e-3)
+    for acc in (False, True):
+        ref = out0.copy()
+        for p, (C, M) in enumerate(pays):
+            st, ref = oracle.decompress(C, M, n, ref, accumulate=(acc or p > 0))
+        od = g.to_dev(out0, offset)
+        bctx.decompress_sum([torch.from_numpy(C).cuda() for C, _ in pays],
+                            [M for _, M in pays], od, accumulate=acc)
+        bctx.sync()
+        assert np.array_equal(g.bits(od.cpu().numpy()), g.bits(ref)), (n, count, acc)
+
+
+def test_decompress_sum_corrupt_leaves_out(bctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    n = 5 * 4096 * 2 + 3
+    pays = []
+    for p in range(3):
+        x = workloads.runs_tensor([740, p], n)
+        st, C, M = oracle.compress(x, np.zeros(n, F32), 1.5)
+        pays.append((C, M))
+    bad = pays[2][0][:-1]
+    out0 = workloads.normal([741], n)
+    od = torch.from_numpy(out0.copy()).cuda()
+    bctx.decompress_sum([torch.from_numpy(c).cuda() for c in (pays[0][0], pays[1][0], bad)],
+                        [M for _, M in pays], od, accumulate=True)
+    assert tlc.tlc_sync(bctx.handle) == tlc.TLC_E_CORRUPT
+    assert np.array_equal(g.bits(od.cpu().numpy()), g.bits(out0))
+
+
+@pytest.mark.timeout(900)
+def test_c5_aggregation_fused(bctx):
+    """C5 with the fused aggregation: 16 payloads of 25.6M values summed in one
+    pass; then the aggregate is re-encoded."""
+    import torch
+    g = G()
+    n = workloads.C5_N
+    payloads = []
+    sum_ref = np.zeros(n, F32)
+    for p in range(workloads.C5_PAYLOADS):
+        x = workloads.c5_tensor(p)
+        st, C, M = oracle.compress(x, np.zeros(n, F32), workloads.C5_S)
+        assert st == 0
+        st, sum_ref = oracle.decompress(C, M, n, sum_ref, accumulate=True)
+        payloads.append((torch.from_numpy(C).cuda(), M))
+    sumd = torch.zeros(n, device="cuda")
+    bctx.decompress_sum([c for c, _ in payloads], [M for _, M in payloads], sumd,
+                        accumulate=True)
+    bctx.sync()
+    assert np.array_equal(g.bits(sumd.cpu().numpy()), g.bits(sum_ref))
+    g.log("C5 fused aggregation ok")
