@@ -97,92 +97,221 @@ def cpu_baseline(x, s):
     }
 
 
-def _time_config(torch, tlc, ctx, tensors, s, reps, dev, oracle_reps=1, acc=True):
-    """Encode then decode (accumulate) each tensor of a list, carrying one
-    residual per tensor; returns per-config figures and the oracle's."""
-    import oracle
-    xs = [torch.from_numpy(t).to(dev) for t in tensors]
-    rs = [torch.zeros_like(x) for x in xs]
-    outs = [torch.zeros_like(x) for x in xs]
-    bufs = [torch.empty(tlc.tlc_max_compressed_bytes(x.numel()), dtype=torch.uint8,
-                        device=dev) for x in xs]
-    total = sum(x.numel() for x in xs)
-    lens = []
-
-    def one_pass():
-        te = td = 0.0
-        lens.clear()
-        for x, r, o, b in zip(xs, rs, outs, bufs):
-            t0 = time.perf_counter()
-            C, M = ctx.compress(x, r, s, out=b)
-            t1 = time.perf_counter()
-            ctx.decompress(C, M, x.numel(), o, accumulate=acc)
-            ctx.sync()
-            t2 = time.perf_counter()
-            te += t1 - t0
-            td += t2 - t1
-            lens.append(C.numel())
-        return te, td
-
-    one_pass()
+def _gpu_round_trips(torch, ctx, steps, s, dev, acc=True, carry=True):
+    """Encode + decode each single-tensor step (host arrays) in turn; the
+    residual is carried between steps (or reset to zero when carry is
+    False).  Returns (encode s, decode s, payload bytes, values)."""
+    xs = [torch.from_numpy(t).to(dev) for t in steps]
+    r = torch.zeros_like(xs[0])
+    out = torch.zeros_like(xs[0])
+    buf = torch.empty(-(-xs[0].numel() // 5), dtype=torch.uint8, device=dev)
     te = td = 0.0
-    for _ in range(reps):
-        a, b = one_pass()
-        te += a
-        td += b
-    ratio = 4 * total / (sum(lens) + 4 * len(lens))
-    # oracle: the same sequence on one core
-    r_host = [np.zeros(t.size, np.float32) for t in tensors]
-    o_host = [np.zeros(t.size, np.float32) for t in tensors]
-    oe = od = 0.0
-    for _ in range(oracle_reps):
-        for t, r, o in zip(tensors, r_host, o_host):
-            t0 = time.perf_counter()
-            st, C, M = oracle.compress(t, r, s)
-            t1 = time.perf_counter()
-            oracle.decompress(C, M, t.size, o, accumulate=acc)
-            t2 = time.perf_counter()
-            oe += t1 - t0
-            od += t2 - t1
-    gb = 4 * total * reps / 1e9
-    ogb = 4 * total * oracle_reps / 1e9
-    return {
-        "values": total, "tensors": len(tensors), "s": s,
-        "encode_GBps": round(gb / te, 2), "decode_GBps": round(gb / td, 2),
-        "round_trip_GBps": round(gb / (te + td), 2),
-        "ms_per_round_trip": round((te + td) / reps * 1e3, 4),
-        "ratio": round(ratio, 2), "ratio_payload_only": round(4 * total / sum(lens), 2),
-        "oracle_encode_GBps": round(ogb / oe, 4), "oracle_decode_GBps": round(ogb / od, 4),
-        "oracle_cores": 1,
-    }
+    nbytes = 0
+    for x in xs:
+        if not carry:
+            r.zero_()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        C, M = ctx.compress(x, r, s, out=buf)
+        t1 = time.perf_counter()
+        ctx.decompress(C, M, x.numel(), out, accumulate=acc)
+        ctx.sync()
+        t2 = time.perf_counter()
+        te += t1 - t0
+        td += t2 - t1
+        nbytes += C.numel() + 4
+    return te, td, nbytes, sum(x.numel() for x in xs)
+
+
+def _oracle_round_trips(steps, s, acc=True, carry=True):
+    import oracle
+    r = np.zeros(steps[0].size, np.float32)
+    out = np.zeros(steps[0].size, np.float32)
+    te = td = 0.0
+    for x in steps:
+        if not carry:
+            r[:] = 0
+        t0 = time.perf_counter()
+        st, C, M = oracle.compress(x, r, s)
+        t1 = time.perf_counter()
+        oracle.decompress(C, M, x.size, out, accumulate=acc)
+        t2 = time.perf_counter()
+        te += t1 - t0
+        td += t2 - t1
+    return te, td
+
+
+def _row(name, values, s, te, td, nbytes, ote=None, otd=None, ovalues=None, **extra):
+    gb = 4 * values / 1e9
+    row = {"config": name, "values": values, "s": s,
+           "encode_GBps": round(gb / te, 2), "decode_GBps": round(gb / td, 2),
+           "round_trip_GBps": round(gb / (te + td), 2),
+           "ratio": round(4 * values / nbytes, 2)}
+    if ote is not None:
+        ogb = 4 * ovalues / 1e9
+        row.update({"oracle_encode_GBps": round(ogb / ote, 4),
+                    "oracle_decode_GBps": round(ogb / otd, 4), "oracle_cores": 1})
+    row.update(extra)
+    return row
 
 
 def report(torch, tlc, workloads, dev):
-    """One JSON line per config (C1-C5): GPU and oracle GB/s of fp32 input and
-    the compression ratio.  Each GPU figure includes the host sync of
-    tlc_compress (it returns the stream length)."""
+    """One JSON line per config (C1-C5): GPU and oracle GB/s of fp32 input
+    and the compression ratio 4n / (payload + 4-byte scale).  GPU encode
+    times include the host synchronisation of tlc_compress (it returns the
+    stream length)."""
     try:
         os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
     except (AttributeError, OSError):
         pass
-    ctx = tlc.Context(max_n=workloads.C4_N, stream=torch.cuda.current_stream(dev), device=dev)
+    stream = torch.cuda.current_stream(dev)
     rows = []
-    rows.append(("C1", _time_config(torch, tlc, ctx, [workloads.c1_tensor()], workloads.C1_S,
-                                     20, dev, oracle_reps=3)))
-    sizes = workloads.c2_sizes()
-    grads = [workloads.c2_gradient(0, t, n) for t, n in enumerate(sizes)]
-    rows.append(("C2", _time_config(torch, tlc, ctx, grads, workloads.C2_S, 5, dev,
-                                     oracle_reps=3, acc=False)))
+    ctx = tlc.Context(max_n=workloads.C4_N, stream=stream, device=dev)
+
+    # C1: one 2^20 tensor, s = 1, zero residual each time
+    x1 = workloads.c1_tensor()
+    _gpu_round_trips(torch, ctx, [x1], workloads.C1_S, dev, carry=False)
+    te, td, nb, v = _gpu_round_trips(torch, ctx, [x1] * 50, workloads.C1_S, dev, carry=False)
+    ote, otd = _oracle_round_trips([x1] * 5, workloads.C1_S, carry=False)
+    rows.append(_row("C1", v, workloads.C1_S, te, td, nb, ote, otd, 5 * x1.size))
+
+    # C3: 2^26 values with zero runs, each s from a zero residual
     x3 = workloads.c3_tensor()
     for s3 in workloads.C3_S:
-        rows.append((f"C3 s={s3}", _time_config(torch, tlc, ctx, [x3], s3, 10, dev)))
-    rows.append(("C4", _time_config(torch, tlc, ctx, [workloads.c4_tensor(0)], workloads.C4_S,
-                                     10, dev)))
-    rows.append(("C5 payload", _time_config(torch, tlc, ctx, [workloads.c5_tensor(0)],
-                                             workloads.C5_S, 10, dev)))
+        _gpu_round_trips(torch, ctx, [x3], s3, dev, carry=False)
+        te, td, nb, v = _gpu_round_trips(torch, ctx, [x3] * 10, s3, dev, carry=False)
+        ote, otd = _oracle_round_trips([x3], s3, carry=False)
+        rows.append(_row(f"C3 s={s3}", v, s3, te, td, nb, ote, otd, x3.size))
+
+    # C4: 5 steps of 2^28 values, residual carried, decode-accumulate
+    x4 = [workloads.c4_tensor(k) for k in range(workloads.C4_STEPS)]
+    _gpu_round_trips(torch, ctx, x4[:1], workloads.C4_S, dev)
+    te, td, nb, v = _gpu_round_trips(torch, ctx, x4, workloads.C4_S, dev)
+    ote, otd = _oracle_round_trips(x4, workloads.C4_S)
+    rows.append(_row("C4 (5 steps)", v, workloads.C4_S, te, td, nb, ote, otd, v))
+    del x4
     ctx.close()
-    for name, row in rows:
-        print(json.dumps({"config": name, **row}), flush=True)
+
+    # C2: 335 ResNet-110 tensors x 10 steps through the batched calls.  The
+    # pointer arrays are built once (a training loop keeps its gradient and
+    # residual buffers), so the timed region is the library calls.
+    import ctypes
+    sizes = workloads.c2_sizes()
+    T = len(sizes)
+    bctx = tlc.Context(max_n=sum(sizes), stream=stream, device=dev, max_tensors=T)
+    rs = [torch.zeros(n, device=dev) for n in sizes]
+    outs = [torch.zeros(n, device=dev) for n in sizes]
+    bufs = [torch.empty(-(-n // 5), dtype=torch.uint8, device=dev) for n in sizes]
+    grads = [[torch.from_numpy(workloads.c2_gradient(k, t, n)).to(dev)
+              for t, n in enumerate(sizes)] for k in range(workloads.C2_STEPS)]
+    A = lambda ct, vals: (ct * T)(*vals)
+    vp, sz, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+    g_ptrs = [A(vp, [g.data_ptr() for g in gs]) for gs in grads]
+    r_ptrs = A(vp, [r.data_ptr() for r in rs])
+    b_ptrs = A(vp, [b.data_ptr() for b in bufs])
+    o_ptrs = A(vp, [o.data_ptr() for o in outs])
+    ns_a = A(sz, sizes)
+    caps_a = A(sz, [b.numel() for b in bufs])
+    s_a = A(f32, [workloads.C2_S] * T)
+    lens_a, sc_a, st_a = (sz * T)(), (f32 * T)(), (ctypes.c_int * T)()
+    te = td = 0.0
+    nb = 0
+    for k in range(workloads.C2_STEPS + 1):  # the first pass warms up
+        if k == 1:
+            bctx.profile(True)
+            bctx.profile_reset()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st = tlc.lib.tlc_compress_batch(bctx.handle, T, g_ptrs[k % workloads.C2_STEPS], r_ptrs,
+                                        ns_a, s_a, b_ptrs, caps_a, lens_a, sc_a, st_a)
+        t1 = time.perf_counter()
+        st2 = tlc.lib.tlc_decompress_batch(bctx.handle, T, b_ptrs, lens_a, sc_a, ns_a, o_ptrs, 0)
+        st3 = tlc.lib.tlc_sync(bctx.handle)
+        t2 = time.perf_counter()
+        assert st == 0 and st2 == 0 and st3 == 0
+        if k:
+            te += t1 - t0
+            td += t2 - t1
+            nb += sum(lens_a) + 4 * T
+    kms = {}
+    for kid in (tlc.TLC_KERNEL_ABSMAX_BATCH, tlc.TLC_KERNEL_QUANT_ENCODE_BATCH,
+                tlc.TLC_KERNEL_ZRE_INDEX_BATCH, tlc.TLC_KERNEL_EXPAND_DEQUANT_BATCH):
+        ms, cnt = bctx.profile_get(kid)
+        kms[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
+    bctx.close()
+    # oracle: the same 10 steps tensor by tensor on one core
+    import oracle
+    r_h = [np.zeros(n, np.float32) for n in sizes]
+    ote = otd = 0.0
+    nb_bn = 0
+    for k in range(workloads.C2_STEPS):
+        for t, n in enumerate(sizes):
+            g = workloads.c2_gradient(k, t, n)
+            t0 = time.perf_counter()
+            st, C, M = oracle.compress(g, r_h[t], workloads.C2_S)
+            t1 = time.perf_counter()
+            oracle.decompress(C, M, n)
+            t2 = time.perf_counter()
+            ote += t1 - t0
+            otd += t2 - t1
+            if workloads.resnet110_cifar_shapes()[t][2] != "bn":
+                nb_bn += C.size + 4
+    v2 = sum(sizes) * workloads.C2_STEPS
+    bn_vals = sum(n for (_, _, kind), n in zip(workloads.resnet110_cifar_shapes(), sizes)
+                  if kind == "bn") * workloads.C2_STEPS
+    rows.append(_row("C2 (batched, 10 steps)", v2, workloads.C2_S, te, td, nb, ote, otd, v2,
+                     ms_per_step=round((te + td) / workloads.C2_STEPS * 1e3, 4),
+                     ratio_without_bn=round(4 * (v2 - bn_vals) / nb_bn, 2),
+                     kernel_us_per_step=kms))
+
+    # C5: 16 payloads encoded (batched), summed by the fused aggregation,
+    # then the sum re-encoded
+    n5 = workloads.C5_N
+    P = workloads.C5_PAYLOADS
+    actx = tlc.Context(max_n=P * n5, stream=stream, device=dev, max_tensors=P)
+    xs5 = [torch.from_numpy(workloads.c5_tensor(p)).to(dev) for p in range(P)]
+    rs5 = [torch.zeros(n5, device=dev) for _ in range(P)]
+    pays = actx.compress_batch(xs5, rs5, workloads.C5_S)
+    total = torch.zeros(n5, device=dev)
+    reps = 10
+    actx.decompress_sum([p[0] for p in pays], [p[1] for p in pays], total)
+    actx.sync()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        actx.decompress_sum([p[0] for p in pays], [p[1] for p in pays], total)
+    actx.sync()
+    t1 = time.perf_counter()
+    r_srv = torch.zeros(n5, device=dev)
+    out = torch.empty(-(-n5 // 5), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(reps):  # same work every rep (the residual's values do not matter)
+        C, M = actx.compress(total, r_srv, workloads.C5_S, out=out)
+    t3 = time.perf_counter()
+    actx.close()
+    agg_gb = 4 * n5 * P * reps / 1e9
+    # oracle: 16 decode-accumulates + one re-encode
+    s5 = [workloads.c5_tensor(p) for p in range(2)]
+    o_pay = [oracle.compress(x, np.zeros(n5, np.float32), workloads.C5_S) for x in s5]
+    acc5 = np.zeros(n5, np.float32)
+    ta = time.perf_counter()
+    for st, C5, M5 in o_pay:
+        oracle.decompress(C5, M5, n5, acc5, accumulate=True)
+    tb = time.perf_counter()
+    oracle.compress(acc5, np.zeros(n5, np.float32), workloads.C5_S)
+    tc = time.perf_counter()
+    rows.append({"config": "C5 (16-stream aggregation + re-encode)", "values": n5,
+                 "streams": P, "s": workloads.C5_S,
+                 "aggregate_GBps_of_stream_values": round(agg_gb / (t1 - t0), 2),
+                 "aggregate_ms": round((t1 - t0) / reps * 1e3, 4),
+                 "reencode_GBps": round(4 * n5 * reps / 1e9 / (t3 - t2), 2),
+                 "reencode_ms": round((t3 - t2) / reps * 1e3, 4),
+                 "oracle_aggregate_GBps": round(4 * n5 * len(s5) / 1e9 / (tb - ta), 4),
+                 "oracle_reencode_GBps": round(4 * n5 / 1e9 / (tc - tb), 4),
+                 "oracle_cores": 1})
+    for row in rows:
+        print(json.dumps(row), flush=True)
 
 
 def main():
