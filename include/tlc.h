@@ -118,6 +118,30 @@ int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
 int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
                    float scale, size_t n, float* out, int accumulate);
 
+/* ---- comparison encodings (decoded by tlc_decompress like any stream) --- */
+
+#define TLC_MODE_3LC 0        /* Sections 3.1-3.3: same as tlc_compress */
+#define TLC_MODE_NO_ZRE 1     /* 3-value quantization with error feedback and
+                                 quartic encoding, no zero-run encoding
+                                 (Table 2, row "No ZRE"): ceil(n/5) bytes */
+#define TLC_MODE_STOCHASTIC 2 /* stochastic 3-value quantization + quartic
+                                 encoding, no error feedback (the "Stoch
+                                 3-value + QE" design of Section 5.1, TernGrad
+                                 without clipping; Section 3.1) */
+
+/* Encode with a comparison mode.  TLC_MODE_3LC forwards to tlc_compress
+ * (seed and step unused).  TLC_MODE_NO_ZRE: as tlc_compress but the payload
+ * is the ceil(n/5) quartic bytes.  TLC_MODE_STOCHASTIC: M = max|tensor| * s;
+ * value i becomes sign(tensor[i]) with probability |tensor[i]|/M, else 0,
+ * decided by u < |tensor[i]|/M with u = (w >> 8) * 2^-24 and w word (i mod
+ * 4) of Philox4x32-10 (Salmon et al., SC 2011) at counter (i/4 low, i/4
+ * high, step low, step high) and key (seed low, seed high); residual is not
+ * used (may be NULL).  Both return *bytes_len = ceil(n/5); the bytes are
+ * 0..242, so tlc_decompress decodes them unchanged. */
+int tlc_compress_ex(tlc_ctx* ctx, int mode, const float* tensor, float* residual, size_t n,
+                    float s, uint64_t seed, uint64_t step, uint8_t* bytes, size_t bytes_cap,
+                    size_t* bytes_len, float* scale);
+
 /* Encode `count` tensors in one pass (two launches, one synchronisation):
  * for every t, exactly tlc_compress(ctx, tensors[t], residuals[t], ns[t],
  * s[t], bytes[t], caps[t], &bytes_len[t], &scales[t]).  All arrays are host
@@ -172,7 +196,8 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_ZRE_INDEX_BATCH 6
 #define TLC_KERNEL_EXPAND_DEQUANT_BATCH 7
 #define TLC_KERNEL_EXPAND_SUM 8     /* multi-stream expansion + summed dequantization */
-#define TLC_KERNEL_COUNT 9
+#define TLC_KERNEL_QUANT_PACK 9     /* comparison modes: quantize + quartic pack */
+#define TLC_KERNEL_COUNT 10
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

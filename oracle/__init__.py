@@ -59,6 +59,15 @@ def lib():
     L.tlc_ref_compress.restype = c_i
     L.tlc_ref_decompress.argtypes = [vp, c_sz, c_f, c_sz, vp, c_i]
     L.tlc_ref_decompress.restype = c_i
+    L.tlc_ref_philox4x32_10.argtypes = [vp, vp, vp]
+    L.tlc_ref_philox4x32_10.restype = None
+    L.tlc_ref_compress_nozre.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
+                                         ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+    L.tlc_ref_compress_nozre.restype = c_i
+    u64 = ctypes.c_uint64
+    L.tlc_ref_compress_stochastic.argtypes = [vp, c_sz, c_f, u64, u64, vp, c_sz,
+                                              ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+    L.tlc_ref_compress_stochastic.restype = c_i
     _lib = L
     return L
 
@@ -166,3 +175,39 @@ def decompress(C, M, n, out=None, accumulate=False):
     st = lib().tlc_ref_decompress(_ptr(C), C.size, M, n, _ptr(out),
                                   int(accumulate))
     return st, out
+
+
+def philox4x32_10(ctr, key):
+    """Four 32-bit words of Philox4x32-10 for a 4-word counter and 2-word key."""
+    c = np.array(ctr, dtype=np.uint32)
+    k = np.array(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().tlc_ref_philox4x32_10(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return [int(v) for v in out]
+
+
+def compress_nozre(x, r, s):
+    """Quantize + quartic encode without zero-run encoding; r updated in place.
+    Return (status, bytes, M)."""
+    x = _f32(x)
+    assert r.dtype == np.float32 and r.flags.c_contiguous and r.size == x.size
+    m = quartic_len(x.size)
+    out = np.zeros(max(m, 1), dtype=np.uint8)
+    ln = ctypes.c_size_t(0)
+    M = ctypes.c_float(0.0)
+    st = lib().tlc_ref_compress_nozre(_ptr(x), _ptr(r), x.size, s, out.ctypes.data, m,
+                                      ctypes.byref(ln), ctypes.byref(M))
+    return st, out[:ln.value].copy(), M.value
+
+
+def compress_stochastic(x, s, seed, step):
+    """Stochastic 3-value quantization + quartic encoding.  Return (status,
+    bytes, M)."""
+    x = _f32(x)
+    m = quartic_len(x.size)
+    out = np.zeros(max(m, 1), dtype=np.uint8)
+    ln = ctypes.c_size_t(0)
+    M = ctypes.c_float(0.0)
+    st = lib().tlc_ref_compress_stochastic(_ptr(x), x.size, s, seed, step, out.ctypes.data,
+                                           m, ctypes.byref(ln), ctypes.byref(M))
+    return st, out[:ln.value].copy(), M.value

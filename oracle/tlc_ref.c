@@ -216,3 +216,105 @@ int tlc_ref_decompress(const uint8_t* bytes, size_t len, float scale,
   free(Q);
   return TLC_REF_OK;
 }
+
+/* ---- comparison modes -------------------------------------------------- */
+
+static void ref_mulhilo(uint32_t a, uint32_t b, uint32_t* hi, uint32_t* lo) {
+  uint64_t p = (uint64_t)a * (uint64_t)b;
+  *hi = (uint32_t)(p >> 32);
+  *lo = (uint32_t)p;
+}
+
+void tlc_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) { /* key schedule: bump the key between rounds */
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    uint32_t hi0, lo0, hi1, lo1;
+    ref_mulhilo(0xD2511F53u, c0, &hi0, &lo0);
+    ref_mulhilo(0xCD9E8D57u, c2, &hi1, &lo1);
+    uint32_t n0 = hi1 ^ c1 ^ k0;
+    uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  out[0] = c0;
+  out[1] = c1;
+  out[2] = c2;
+  out[3] = c3;
+}
+
+int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t* bytes,
+                           size_t cap, size_t* len, float* scale) {
+  if (len) *len = 0;
+  if (!len || !scale) return TLC_REF_E_INVALID;
+  if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
+  if (n == 0) {
+    *scale = 0.0f;
+    return TLC_REF_OK;
+  }
+  if (!x || !r || !bytes) return TLC_REF_E_INVALID;
+  size_t m = tlc_ref_quartic_len(n);
+  if (cap < m) return TLC_REF_E_CAPACITY;
+  float* acc = (float*)ref_alloc(n * sizeof(float));
+  tlc_ref_accumulate(x, r, n, acc);
+  float M = 0.0f;
+  int st = tlc_ref_absmax_scale(acc, n, s, &M);
+  if (st != TLC_REF_OK) {
+    free(acc);
+    return st;
+  }
+  int8_t* q = (int8_t*)ref_alloc(n);
+  float* resid = (float*)ref_alloc(n * sizeof(float));
+  tlc_ref_quantize(acc, n, M, q, resid);
+  tlc_ref_quartic_encode(q, n, bytes); /* the quartic bytes are the payload */
+  memcpy(r, resid, n * sizeof(float));
+  *len = m;
+  *scale = M;
+  free(resid);
+  free(q);
+  free(acc);
+  return TLC_REF_OK;
+}
+
+int tlc_ref_compress_stochastic(const float* x, size_t n, float s, uint64_t seed,
+                                uint64_t step, uint8_t* bytes, size_t cap, size_t* len,
+                                float* scale) {
+  if (len) *len = 0;
+  if (!len || !scale) return TLC_REF_E_INVALID;
+  if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
+  if (n == 0) {
+    *scale = 0.0f;
+    return TLC_REF_OK;
+  }
+  if (!x || !bytes) return TLC_REF_E_INVALID;
+  size_t m = tlc_ref_quartic_len(n);
+  if (cap < m) return TLC_REF_E_CAPACITY;
+  float M = 0.0f;
+  int st = tlc_ref_absmax_scale(x, n, s, &M); /* no error accumulation */
+  if (st != TLC_REF_OK) return st;
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  int8_t* q = (int8_t*)ref_alloc(n);
+  for (size_t i = 0; i < n; ++i) {
+    const uint64_t blk = i / 4;
+    const uint32_t ctr[4] = {(uint32_t)blk, (uint32_t)(blk >> 32), (uint32_t)step,
+                             (uint32_t)(step >> 32)};
+    uint32_t w[4];
+    tlc_ref_philox4x32_10(ctr, key, w);
+    const double u = (double)(w[i % 4] >> 8) / 16777216.0; /* uniform on [0, 1), 24 bits */
+    const double a = fabs((double)x[i]);
+    /* keep with probability |x|/M: u < |x|/M, i.e. u*M < |x| (exact in double) */
+    const int keep = (M > 0.0f) && (u * (double)M < a);
+    q[i] = keep ? (x[i] > 0.0f ? 1 : -1) : 0;
+  }
+  tlc_ref_quartic_encode(q, n, bytes);
+  *len = m;
+  *scale = M;
+  free(q);
+  return TLC_REF_OK;
+}

@@ -83,6 +83,30 @@ int tlc_ref_compress(const float* x, float* r, size_t n, float s,
 int tlc_ref_decompress(const uint8_t* bytes, size_t len, float scale,
                        size_t n, float* out, int accumulate);
 
+/* ---- comparison modes -------------------------------------------------- */
+
+/* Philox4x32-10 counter-based generator (Salmon, Moraes, Dror and Shaw,
+ * "Parallel random numbers: as easy as 1, 2, 3", SC 2011): ten rounds of
+ * two 32x32->64 multiplications with multipliers 0xD2511F53, 0xCD9E8D57 and
+ * a Weyl key schedule 0x9E3779B9, 0xBB67AE85. */
+void tlc_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Quantization + quartic encoding without zero-run encoding (Table 2, row
+ * "No ZRE"): bytes receives the ceil(n/5) quartic bytes, error feedback as in
+ * tlc_ref_compress. */
+int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t* bytes,
+                           size_t cap, size_t* len, float* scale);
+
+/* Stochastic 3-value quantization + quartic encoding, no error feedback
+ * (the "Stoch 3-value + QE" comparator of Section 5.1, described in Section
+ * 3.1): M = max|x| * s; element i keeps sign(x_i) with probability |x_i|/M,
+ * decided by u_i < |x_i|/M with u_i = (w >> 8) * 2^-24, w the 32-bit Philox
+ * word (i mod 4) of counter (i/4 low, i/4 high, step low, step high) and key
+ * (seed low, seed high).  bytes receives ceil(n/5) quartic bytes. */
+int tlc_ref_compress_stochastic(const float* x, size_t n, float s, uint64_t seed,
+                                uint64_t step, uint8_t* bytes, size_t cap, size_t* len,
+                                float* scale);
+
 #ifdef __cplusplus
 }
 #endif

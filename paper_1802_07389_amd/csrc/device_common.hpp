@@ -165,6 +165,53 @@ __device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
   return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
 }
 
+// ---------------------------------------------------------------- stochastic mode
+// Philox4x32-10 (Salmon et al., SC 2011): ten rounds, each multiplying two
+// counter words by 0xD2511F53 and 0xCD9E8D57 (high halves XORed with the
+// other two words and the key), the key advancing by 0x9E3779B9 /
+// 0xBB67AE85 between rounds.
+struct Philox4 {
+  uint32_t v[4];
+};
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                 uint32_t c3, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  Philox4 r;
+  r.v[0] = c0;
+  r.v[1] = c1;
+  r.v[2] = c2;
+  r.v[3] = c3;
+  return r;
+}
+
+// Random words for elements 4b .. 4b+3 of a tensor: counter (b, step),
+// key = seed.
+__device__ __forceinline__ Philox4 element_words(uint64_t b, uint64_t step, uint64_t seed) {
+  return philox4x32_10((uint32_t)b, (uint32_t)(b >> 32), (uint32_t)step,
+                       (uint32_t)(step >> 32), (uint32_t)seed, (uint32_t)(seed >> 32));
+}
+
+// Stochastic 3-value quantization of one value: sign(x) kept with
+// probability |x|/M, i.e. when u*M < |x| for u = (w >> 8) * 2^-24; the
+// product of a 24-bit integer and an fp32 is exact in double, so the
+// decision is exact.  Returns the trit q + 1.
+__device__ __forceinline__ uint32_t stochastic_trit(float x, float M, uint32_t w) {
+  const double u = (double)(w >> 8) * (1.0 / 16777216.0);
+  const bool keep = (M > 0.0f) && (u * (double)M < fabs((double)x));
+  return keep ? (x > 0.0f ? 2u : 0u) : 1u;
+}
+
 // ---------------------------------------------------------------- Section 3.3
 using EncSW = StatusWord<39>;  // RunSum with a 30-bit count
 using DecSW = StatusWord<36>;  // expanded byte count

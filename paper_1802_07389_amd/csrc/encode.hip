@@ -20,7 +20,7 @@ namespace tlc {
 // non-negative IEEE values integer order equals numeric order, so the u32
 // max is exact and independent of reduction order, and any NaN/Inf makes
 // the result >= 0x7f800000.  Block `blk` of `nblk` strides over [0, n).
-template <bool kVec>
+template <bool kVec, bool kResid = true>
 __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
                                                 const float* __restrict__ r, uint64_t n,
                                                 uint32_t blk, uint32_t nblk) {
@@ -37,7 +37,7 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
 #pragma unroll
       for (int u = 0; u < 4; ++u) a[u] = x4[i + u * stride];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) b[u] = r4[i + u * stride];
+      for (int u = 0; u < 4; ++u) b[u] = kResid ? r4[i + u * stride] : make_float4(0, 0, 0, 0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         mx = max(mx, abs_bits(a[u].x + b[u].x));
@@ -47,26 +47,28 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       }
     }
     for (; i < nv; i += stride) {
-      float4 a = x4[i], b = r4[i];
+      float4 a = x4[i], b = kResid ? r4[i] : make_float4(0, 0, 0, 0);
       mx = max(mx, abs_bits(a.x + b.x));
       mx = max(mx, abs_bits(a.y + b.y));
       mx = max(mx, abs_bits(a.z + b.z));
       mx = max(mx, abs_bits(a.w + b.w));
     }
     for (uint64_t e = (nv << 2) + tid; e < n; e += stride)
-      mx = max(mx, abs_bits(x[e] + r[e]));
+      mx = max(mx, abs_bits(kResid ? x[e] + r[e] : x[e]));
   } else {
-    for (uint64_t e = tid; e < n; e += stride) mx = max(mx, abs_bits(x[e] + r[e]));
+    for (uint64_t e = tid; e < n; e += stride)
+      mx = max(mx, abs_bits(kResid ? x[e] + r[e] : x[e]));
   }
   return mx;
 }
 
-template <bool kVec>
+template <bool kVec, bool kResid>
 __global__ __launch_bounds__(kThreads) void tlc_absmax_kernel(
     const float* __restrict__ x, const float* __restrict__ r, uint64_t n,
     uint32_t* __restrict__ partials) {
   __shared__ uint32_t lds[kWaves];
-  const uint32_t mx = block_max(absmax_part<kVec>(x, r, n, blockIdx.x, gridDim.x), lds);
+  const uint32_t mx =
+      block_max(absmax_part<kVec, kResid>(x, r, n, blockIdx.x, gridDim.x), lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = mx;
 }
 
@@ -252,6 +254,78 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
                        &results[t], sh);
 }
 
+// ---------------------------------------------------------------- comparison modes
+// Quantization + quartic pack without zero-run encoding: the quartic bytes
+// are the payload (m bytes), so tiles are independent and need no
+// look-back.  kStoch selects stochastic 3-value quantization with Philox
+// random words (no error feedback: r is not read or written); otherwise
+// Eq. 2 with the residual write-back, exactly as in tlc_quant_encode_kernel.
+template <bool kVec, bool kStoch>
+__global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    uint64_t seed, uint64_t step, const uint32_t* __restrict__ partials, uint32_t np,
+    uint8_t* __restrict__ out, Ctrl* __restrict__ ctrl) {
+  __shared__ uint32_t red[kWaves];
+  const Scale sc = finish_scale(partials, np, s, red);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctrl->enc.err = sc.bad;
+    ctrl->enc.scale = sc.M;
+    ctrl->enc.len = sc.bad ? 0u : m;
+  }
+  if (sc.bad) return;
+  const uint64_t q0 = (uint64_t)blockIdx.x * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  if (kVec) {
+    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads) {
+      const uint64_t j = q0 + g * 4u;
+      uint32_t w;
+      if (!kStoch) {
+        w = quantize_group4(x, r, n, m, j, sc.M, sc.U);
+      } else {
+        uint32_t code[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+          const uint64_t e = k * m + j;  // a multiple of 4: one Philox call per slice
+          const Philox4 rw = element_words(e >> 2, step, seed);
+          if (e + 4 <= n) {
+            const float4 a = *reinterpret_cast<const float4*>(x + e);
+            code[0] = code[0] * 3u + stochastic_trit(a.x, sc.M, rw.v[0]);
+            code[1] = code[1] * 3u + stochastic_trit(a.y, sc.M, rw.v[1]);
+            code[2] = code[2] * 3u + stochastic_trit(a.z, sc.M, rw.v[2]);
+            code[3] = code[3] * 3u + stochastic_trit(a.w, sc.M, rw.v[3]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              code[c] = code[c] * 3u +
+                        (e + c < n ? stochastic_trit(x[e + c], sc.M, rw.v[c]) : 0u);
+          }
+        }
+        w = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) out[j + c] = (uint8_t)(w >> (8 * c));
+    }
+  } else {
+    for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads) {
+      const uint64_t j = q0 + lj;
+      uint32_t code;
+      if (!kStoch) {
+        code = quantize_byte(x, r, n, m, j, sc.M, sc.U);
+      } else {
+        code = 0u;
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+          const uint64_t e = k * m + j;
+          uint32_t t = 0u;
+          if (e < n) t = stochastic_trit(x[e], sc.M, element_words(e >> 2, step, seed).v[e & 3]);
+          code = code * 3u + t;
+        }
+      }
+      out[j] = (uint8_t)code;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 static inline bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
@@ -259,15 +333,21 @@ static inline bool aligned16(const void* p) {
 
 hipError_t launch_absmax(const float* x, const float* r, uint64_t n, uint32_t* partials,
                          uint32_t* nblocks, hipStream_t st) {
-  const bool vec = aligned16(x) && aligned16(r);
+  const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
   const uint64_t items = vec ? (n >> 2) : n;
   uint64_t blocks = (items + kThreads * 4 - 1) / (kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > kAbsmaxMaxBlocks ? kAbsmaxMaxBlocks : blocks);
   *nblocks = (uint32_t)blocks;
-  if (vec)
-    tlc_absmax_kernel<true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
-  else
-    tlc_absmax_kernel<false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  if (r == nullptr) {  // no error buffer: max |x|
+    if (aligned16(x))
+      tlc_absmax_kernel<true, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+    else
+      tlc_absmax_kernel<false, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  } else if (vec) {
+    tlc_absmax_kernel<true, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  } else {
+    tlc_absmax_kernel<false, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+  }
   return hipGetLastError();
 }
 
@@ -298,6 +378,29 @@ hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      hipStream_t st) {
   tlc_quant_encode_batch_kernel<<<total_tiles, kThreads, 0, st>>>(
       descs, count, partials, results, status, ticket_base, epoch, ctrl);
+  return hipGetLastError();
+}
+
+}  // namespace tlc
+
+namespace tlc {
+
+hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                             int stochastic, uint64_t seed, uint64_t step,
+                             const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                             Ctrl* ctrl, hipStream_t st) {
+  const uint32_t blocks = (uint32_t)((m + kEncTile - 1) / kEncTile);
+  const bool al = aligned16(x) && (stochastic || aligned16(r));
+  const bool vec = (m % 4 == 0) && al;
+#define TLC_LAUNCH(V, S)                                                                      \
+  tlc_quant_pack_kernel<V, S><<<blocks, kThreads, 0, st>>>(x, r, n, m, s, seed, step, partials, \
+                                                           npartials, out, ctrl)
+  if (stochastic) {
+    if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);
+  } else {
+    if (vec) TLC_LAUNCH(true, false); else TLC_LAUNCH(false, false);
+  }
+#undef TLC_LAUNCH
   return hipGetLastError();
 }
 

@@ -51,7 +51,7 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_zre_index_kernel",        "tlc_expand_dequant_kernel",
     "tlc_absmax_batch_kernel",     "tlc_quant_encode_batch_kernel",
     "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
-    "tlc_expand_sum_kernel"};
+    "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -396,6 +396,57 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   }
   if (c->rb->enc.err)
     return fail(TLC_E_NONFINITE, "tlc_compress: NaN/Inf in tensor+residual or max*s overflow");
+  *bytes_len = c->rb->enc.len;
+  *scale = c->rb->enc.scale;
+  return TLC_OK;
+}
+
+TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* residual,
+                            size_t n, float s, uint64_t seed, uint64_t step, uint8_t* bytes,
+                            size_t bytes_cap, size_t* bytes_len, float* scale) {
+  if (mode == TLC_MODE_3LC)
+    return tlc_compress(c, tensor, residual, n, s, bytes, bytes_cap, bytes_len, scale);
+  if (bytes_len) *bytes_len = 0;
+  int st = check_usable(c, "tlc_compress_ex");
+  if (st) return st;
+  if (mode != TLC_MODE_NO_ZRE && mode != TLC_MODE_STOCHASTIC)
+    return fail(TLC_E_INVALID, "tlc_compress_ex: unknown mode %d", mode);
+  const bool stoch = mode == TLC_MODE_STOCHASTIC;
+  if (!bytes_len || !scale) return fail(TLC_E_INVALID, "tlc_compress_ex: NULL argument");
+  if (!(s >= 1.0f && s < 2.0f))
+    return fail(TLC_E_INVALID, "tlc_compress_ex: s = %g not in [1, 2)", (double)s);
+  if (n > c->max_n)
+    return fail(TLC_E_INVALID, "tlc_compress_ex: n = %zu exceeds the context's max_n %zu", n,
+                c->max_n);
+  if (n == 0) {
+    *scale = 0.0f;
+    return TLC_OK;
+  }
+  if (!tensor || !bytes || (!stoch && !residual))
+    return fail(TLC_E_INVALID, "tlc_compress_ex: NULL device pointer");
+  const size_t m = quartic_len(n);
+  if (bytes_cap < m)
+    return fail(TLC_E_CAPACITY, "tlc_compress_ex: bytes_cap %zu < %zu", bytes_cap, m);
+  if (overlap(tensor, n * 4, bytes, m) ||
+      (!stoch && (overlap(tensor, n * 4, residual, n * 4) || overlap(residual, n * 4, bytes, m))))
+    return fail(TLC_E_INVALID, "tlc_compress_ex: tensor, residual and bytes overlap");
+  st = ensure_device(c);
+  if (st) return st;
+  float* r = stoch ? nullptr : residual;  // the stochastic mode has no error feedback
+  uint32_t np = 0;
+  st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
+    return launch_absmax(tensor, r, n, c->partials, &np, c->stream);
+  });
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_QUANT_PACK, [&] {
+    return launch_quant_pack(tensor, r, n, (uint32_t)m, s, stoch ? 1 : 0, seed, step,
+                             c->partials, np, bytes, c->ctrl, c->stream);
+  });
+  if (st) return st;
+  st = sync_and_read(c);
+  if (st) return st;
+  if (c->rb->enc.err)
+    return fail(TLC_E_NONFINITE, "tlc_compress_ex: NaN/Inf in the input or max*s overflow");
   *bytes_len = c->rb->enc.len;
   *scale = c->rb->enc.scale;
   return TLC_OK;

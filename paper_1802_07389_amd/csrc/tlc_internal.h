@@ -83,6 +83,10 @@ hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m,
                                const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                                uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                             int stochastic, uint64_t seed, uint64_t step,
+                             const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                             Ctrl* ctrl, hipStream_t st);
 hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
                                uint32_t* partials, hipStream_t st);
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,

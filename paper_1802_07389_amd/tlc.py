@@ -30,11 +30,17 @@ TLC_KERNEL_QUANT_ENCODE_BATCH = 5
 TLC_KERNEL_ZRE_INDEX_BATCH = 6
 TLC_KERNEL_EXPAND_DEQUANT_BATCH = 7
 TLC_KERNEL_EXPAND_SUM = 8
-TLC_KERNEL_COUNT = 9
+TLC_KERNEL_QUANT_PACK = 9
+TLC_KERNEL_COUNT = 10
+
+TLC_MODE_3LC = 0
+TLC_MODE_NO_ZRE = 1
+TLC_MODE_STOCHASTIC = 2
 
 EXPORTS = (
     "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_create_batch",
-    "tlc_ctx_destroy", "tlc_compress", "tlc_compress_batch", "tlc_decompress",
+    "tlc_ctx_destroy", "tlc_compress", "tlc_compress_ex", "tlc_compress_batch",
+    "tlc_decompress",
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
     "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_get",
     "tlc_profile_reset", "tlc_kernel_name",
@@ -68,6 +74,9 @@ def _load():
     L.tlc_decompress_batch.restype = i
     L.tlc_decompress_sum.argtypes = [vp, sz, P(vp), P(sz), P(f), sz, vp, i]
     L.tlc_decompress_sum.restype = i
+    L.tlc_compress_ex.argtypes = [vp, i, vp, vp, sz, f, ctypes.c_uint64, ctypes.c_uint64, vp,
+                                  sz, P(sz), P(f)]
+    L.tlc_compress_ex.restype = i
     L.tlc_ctx_destroy.argtypes = [vp]
     L.tlc_ctx_destroy.restype = i
     L.tlc_compress.argtypes = [vp, vp, vp, sz, f, vp, sz, ctypes.POINTER(sz),
@@ -169,6 +178,15 @@ def tlc_compress(ctx, tensor, residual, n, s, bytes_, bytes_cap):
     return st, ln.value, sc.value
 
 
+def tlc_compress_ex(ctx, mode, tensor, residual, n, s, seed, step, bytes_, bytes_cap):
+    """Device pointers in; returns (status, bytes_len, scale)."""
+    ln = ctypes.c_size_t(0)
+    sc = ctypes.c_float(0.0)
+    st = lib.tlc_compress_ex(ctx, mode, tensor, residual, n, s, seed, step, bytes_, bytes_cap,
+                             ctypes.byref(ln), ctypes.byref(sc))
+    return st, ln.value, sc.value
+
+
 def tlc_decompress(ctx, bytes_, bytes_len, scale, n, out, accumulate):
     return lib.tlc_decompress(ctx, bytes_, bytes_len, scale, n, out,
                               int(bool(accumulate)))
@@ -262,6 +280,20 @@ class Context:
         ptr = _dev_u8(data, "data") if data.numel() else None
         _check(tlc_decompress(self.handle, ptr, data.numel(), float(scale), n,
                               _dev_f32(out, "out"), accumulate))
+
+    def compress_mode(self, mode, tensor, residual, s, seed=0, step=0, out=None):
+        """Encode with TLC_MODE_NO_ZRE or TLC_MODE_STOCHASTIC (residual may be
+        None for the stochastic mode).  Returns (bytes view, scale)."""
+        n = tensor.numel()
+        cap = tlc_max_compressed_bytes(n)
+        if out is None:
+            out = torch.empty(max(cap, 1), dtype=torch.uint8, device=self.device)
+        rp = _dev_f32(residual, "residual") if residual is not None else None
+        st, ln, sc = tlc_compress_ex(self.handle, mode, _dev_f32(tensor, "tensor"), rp, n,
+                                     float(s), int(seed), int(step), _dev_u8(out, "out"),
+                                     out.numel())
+        _check(st)
+        return out[:ln], sc
 
     def compress_batch(self, tensors, residuals, s, outs=None):
         """Encode a list of tensors in one pass.  Returns a list of

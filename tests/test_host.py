@@ -23,7 +23,7 @@ def test_library_exports_every_declared_function():
     from paper_1802_07389_amd import build, tlc
     assert os.path.exists(build.LIB)
     declared = header_functions()
-    assert len(declared) >= 15
+    assert len(declared) >= 16
     out = subprocess.run(["nm", "-D", "--defined-only", build.LIB], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\sT\s(tlc_\w+)$", out, flags=re.M))
@@ -41,7 +41,8 @@ def test_host_only_entry_points():
     assert names == ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
                      "tlc_expand_dequant_kernel", "tlc_absmax_batch_kernel",
                      "tlc_quant_encode_batch_kernel", "tlc_zre_index_batch_kernel",
-                     "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel"]
+                     "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel",
+                     "tlc_quant_pack_kernel"]
     assert tlc.tlc_kernel_name(99) is None
 
 
