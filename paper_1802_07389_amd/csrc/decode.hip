@@ -177,14 +177,78 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
 }
 
 // ---------------------------------------------------------------- Eq. 3
+// Partition K of quartic bytes s_q[0, qn) (global bytes q0 + jl) when
+// m % 4 != 0 and out is 16-byte aligned: the partition starts a =
+// (K*m + q0) mod 4 values past a float4 boundary, and cell f of its aligned
+// float4 grid takes digit K of bytes 4f - a .. 4f + 3 - a (two LDS words).
+// Cells shared with a neighbouring range or partition, or reaching past n,
+// are written value by value.
+template <int K, bool kAcc>
+__device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, uint64_t q0,
+                                                          uint32_t qn, uint64_t n, uint64_t m,
+                                                          float M, float* __restrict__ out) {
+  constexpr uint32_t kPlace = K == 0 ? 81u : (K == 1 ? 27u : (K == 2 ? 9u : (K == 3 ? 3u : 1u)));
+  constexpr int kCells = (kDecRange + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
+  const uint32_t* qw = reinterpret_cast<const uint32_t*>(s_q);
+  const uint64_t base = (uint64_t)K * m + q0;
+  const uint32_t a = (uint32_t)(base & 3u);
+  const uint64_t e0 = base - a;
+  const uint32_t nf = (qn + a + 3u) >> 2;
+  float4 o[kCells];
+  bool full[kCells];
+#pragma unroll
+  for (int i = 0; i < kCells; ++i) {
+    const uint32_t f = threadIdx.x + kThreads * i;
+    full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= qn + a && e0 + 4ull * f + 4u <= n;
+    if (kAcc && full[i]) o[i] = *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
+  }
+#pragma unroll
+  for (int i = 0; i < kCells; ++i) {
+    const uint32_t f = threadIdx.x + kThreads * i;
+    if (f >= nf) break;
+    const uint64_t e = e0 + 4ull * f;
+    // bytes 4f - a .. 4f + 3 - a: the top a bytes of word f - 1, then word f
+    const uint32_t lo = (a != 0u && f >= 1u) ? qw[f - 1] : 0u;
+    const uint32_t hi = 4u * f < qn ? qw[f] : 0u;
+    const uint32_t w4 = a ? (uint32_t)((((uint64_t)hi << 32) | lo) >> (8u * (4u - a))) : hi;
+    float v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = trit_value((((w4 >> (8 * c)) & 0xffu) / kPlace) % 3u, M);
+    if (full[i]) {
+      if (kAcc) {
+        o[i].x = o[i].x + v[0];
+        o[i].y = o[i].y + v[1];
+        o[i].z = o[i].z + v[2];
+        o[i].w = o[i].w + v[3];
+      } else {
+        o[i] = make_float4(v[0], v[1], v[2], v[3]);
+      }
+      *reinterpret_cast<float4*>(out + e) = o[i];
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t p = 4u * f + c;
+        if (p >= a && p - a < qn && e + c < n) out[e + c] = kAcc ? out[e + c] + v[c] : v[c];
+      }
+    }
+  }
+}
+
 // Unpacks the base-3 digits of quartic bytes s_q[0, qn) (global bytes
 // q0 + jl), dequantizes (Eq. 3) and stores or accumulates into the five
-// partitions of out: float4 accesses when m % 4 == 0 and out is aligned.
-template <bool kVec, bool kAcc>
+// partitions of out: float4 slices when m % 4 == 0 and out is aligned,
+// shifted float4 cells when only out is aligned, else scalar accesses.
+template <int kPath, bool kAcc>
 __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, uint32_t qn,
                                               uint64_t n, uint64_t m, float M,
                                               float* __restrict__ out) {
-  if (kVec) {
+  if (kPath == kPathShift) {
+    dequant_partition_shifted<0, kAcc>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<1, kAcc>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<2, kAcc>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<3, kAcc>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<4, kAcc>(s_q, q0, qn, n, m, M, out);
+  } else if (kPath == kPathVec) {
 #pragma unroll
     for (int g = 0; g < kDecRange / (4 * kThreads); ++g) {
       const uint32_t jl = 4u * (threadIdx.x + kThreads * g);
@@ -247,7 +311,7 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 }
 
 // One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
-template <bool kVec, bool kAcc>
+template <int kPath, bool kAcc>
 __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
     const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ start,
     uint64_t n, uint64_t m, float M, float* __restrict__ out, uint32_t epoch,
@@ -259,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
   expand_range(C, c, start, k, m, qn, s_q, red);
-  dequant_range<kVec, kAcc>(s_q, q0, qn, n, m, M, out);
+  dequant_range<kPath, kAcc>(s_q, q0, qn, n, m, M, out);
 }
 
 template <bool kAcc>
@@ -277,9 +341,11 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, (uint64_t)d.m - q0);
   expand_range(d.C, d.c, start + d.range0, k, d.m, qn, s_q, red);
   if (d.vec & 1u)
-    dequant_range<true, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+    dequant_range<kPathVec, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+  else if (d.vec & 2u)
+    dequant_range<kPathShift, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
   else
-    dequant_range<false, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+    dequant_range<kPathByte, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
 }
 
 // ---------------------------------------------------------------- aggregation
@@ -393,15 +459,17 @@ hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* s
                                  uint64_t n, uint64_t m, float scale, float* out,
                                  int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                  hipStream_t st) {
-  const bool vec = (m % 4 == 0) && aligned16(out);
+  const bool al = aligned16(out);
   const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
 #define TLC_LAUNCH(V, A)                                                                     \
   tlc_expand_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, out, \
                                                                epoch, ctrl)
-  if (vec) {
-    if (accumulate) TLC_LAUNCH(true, true); else TLC_LAUNCH(true, false);
+  if (al && m % 4 == 0) {
+    if (accumulate) TLC_LAUNCH(kPathVec, true); else TLC_LAUNCH(kPathVec, false);
+  } else if (al) {
+    if (accumulate) TLC_LAUNCH(kPathShift, true); else TLC_LAUNCH(kPathShift, false);
   } else {
-    if (accumulate) TLC_LAUNCH(false, true); else TLC_LAUNCH(false, false);
+    if (accumulate) TLC_LAUNCH(kPathByte, true); else TLC_LAUNCH(kPathByte, false);
   }
 #undef TLC_LAUNCH
   return hipGetLastError();

@@ -61,6 +61,19 @@ __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
   return r;
 }
 
+// How a kernel reaches the five partitions of a tile: one float4 per
+// partition slice (m % 4 == 0, 16-byte aligned tensors), aligned float4
+// cells off the slice grid (aligned tensors, m % 4 != 0), or one quartic
+// byte per lane with scalar accesses (unaligned tensors).
+constexpr int kPathVec = 0;
+constexpr int kPathShift = 1;
+constexpr int kPathByte = 2;
+
+// Place value of partition k's trit in a quartic byte (p0 most significant).
+__device__ __forceinline__ uint32_t trit_weight(int k) {
+  return k == 0 ? 81u : (k == 1 ? 27u : (k == 2 ? 9u : (k == 3 ? 3u : 1u)));
+}
+
 // ---------------------------------------------------------------- Eq. 1-2
 struct Scale {
   float M;       // max|acc| * s

@@ -85,6 +85,86 @@ __global__ __launch_bounds__(kThreads) void tlc_absmax_batch_kernel(
   if (threadIdx.x == 0) partials[blockIdx.x] = bm;
 }
 
+// ---------------------------------------------------------------- Eq. 2, 3.2
+// Phase 1 of a tile (quartic bytes [q0, q0 + T), T <= kEncTile) when
+// m % 4 != 0 but x and r are 16-byte aligned.  Partition k of the tile
+// starts a = (k*m + q0) mod 4 values past a float4 boundary, so the block
+// sweeps it in aligned float4 cells: cell f holds the values of tile bytes
+// 4f - a .. 4f + 3 - a.  A cell shared with a neighbouring tile or
+// partition, or reaching past n, is read and written value by value, so
+// every value's residual has one writer.  Partition 0 (a = 0, as q0 is a
+// multiple of 4) stores the bytes; partitions 1-4 add their weighted trits
+// with LDS atomics on the two words a cell straddles: a byte's total stays
+// below 243, so no carry crosses into the next byte.
+__device__ __forceinline__ void quantize_tile_shifted(const float* __restrict__ x,
+                                                      float* __restrict__ r, uint64_t n,
+                                                      uint64_t m, uint64_t q0, uint32_t T,
+                                                      float M, float U, uint32_t* qw) {
+  constexpr int kCells = (kEncTile + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
+#pragma unroll 1
+  for (int k = 0; k < 5; ++k) {
+    const uint64_t base = (uint64_t)k * m + q0;
+    const uint32_t a = (uint32_t)(base & 3u);
+    const uint64_t e0 = base - a;  // first value of cell 0
+    const uint32_t nf = (T + a + 3u) >> 2;
+    const uint32_t w = trit_weight(k);
+    float4 xa[kCells], ra[kCells];
+    bool full[kCells];
+#pragma unroll
+    for (int i = 0; i < kCells; ++i) {
+      const uint32_t f = threadIdx.x + kThreads * i;
+      const uint64_t e = e0 + 4ull * f;
+      full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= T + a && e + 4u <= n;
+      if (full[i]) {
+        xa[i] = *reinterpret_cast<const float4*>(x + e);
+        ra[i] = *reinterpret_cast<const float4*>(r + e);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCells; ++i) {
+      const uint32_t f = threadIdx.x + kThreads * i;
+      if (f >= nf) break;
+      const uint64_t e = e0 + 4ull * f;
+      uint32_t t[4] = {0u, 0u, 0u, 0u};  // padding and other tiles' values add nothing
+      if (full[i]) {
+        float4 o;
+        t[0] = quantize_one(xa[i].x + ra[i].x, M, U, o.x);
+        t[1] = quantize_one(xa[i].y + ra[i].y, M, U, o.y);
+        t[2] = quantize_one(xa[i].z + ra[i].z, M, U, o.z);
+        t[3] = quantize_one(xa[i].w + ra[i].w, M, U, o.w);
+        *reinterpret_cast<float4*>(r + e) = o;
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t p = 4u * f + c;  // position in the partition's cell grid
+          if (p >= a && p - a < T && e + c < n) {
+            float o;
+            t[c] = quantize_one(x[e + c] + r[e + c], M, U, o);
+            r[e + c] = o;
+          }
+        }
+      }
+      // byte 4f + c - a: word f - 1 for c < a, word f otherwise
+      uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t v = t[c] * w;
+        if ((uint32_t)c < a)
+          lo |= v << (8u * (4u + c - a));
+        else
+          hi |= v << (8u * (c - a));
+      }
+      if (k == 0) {
+        qw[f] = hi;  // a == 0: the cell is word f
+      } else {
+        if (lo) atomicAdd(&qw[f - 1], lo);  // lo != 0 only when f >= 1
+        if (hi) atomicAdd(&qw[f], hi);
+      }
+    }
+    if (k == 0) __syncthreads();  // partition 0 has stored every word
+  }
+}
+
 // ---------------------------------------------------------------- Eq. 2, 3.2, 3.3
 struct EncShared {
   uint32_t red[kWaves];
@@ -96,17 +176,17 @@ struct EncShared {
 };
 
 // Encodes tile `lt` (kEncTile quartic bytes) of one tensor whose scale is
-// sc.  Phase 1: the block quantizes its 5 * kEncTile values (threads take
-// groups of 4 bytes, or single bytes when the partitions are not 16-byte
-// aligned, interleaved so every load and store instruction is coalesced)
-// and keeps the quartic bytes in LDS.  Phase 2: each thread takes
+// sc.  Phase 1: the block quantizes its 5 * kEncTile values (kPath: threads
+// take groups of 4 bytes, aligned float4 cells of one partition at a time,
+// or single bytes, interleaved so every load and store instruction is
+// coalesced) and keeps the quartic bytes in LDS.  Phase 2: each thread takes
 // kEncTile/256 consecutive bytes and summarises them as a RunSum; the block
 // scans the summaries, the tile gets its prefix by decoupled look-back
 // (status slot floor + lt; slot floor is the tensor's first tile), and
 // every thread zero-run encodes its bytes from its own prefix into LDS; the
 // block then copies the tile's output into the stream.  The last tile
 // stores the stream length in res->len.
-template <bool kVec>
+template <int kPath>
 __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* __restrict__ r,
                                             uint64_t n, uint32_t m, const Scale& sc,
                                             uint32_t lt, uint32_t floor,
@@ -120,10 +200,13 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  if (kVec) {  // 4 bytes per thread: float4 loads and stores
+  if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
     for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
       *reinterpret_cast<uint32_t*>(sh.q + g * 4u) =
           quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+  } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
+    quantize_tile_shifted(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
+                          reinterpret_cast<uint32_t*>(sh.q));
   } else {  // 1 byte per thread: dword accesses, still contiguous per wave
     for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
       sh.q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
@@ -208,7 +291,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   if (last_tile && threadIdx.x == 0) res->len = tile_end;
 }
 
-template <bool kVec>
+template <int kPath>
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
@@ -224,7 +307,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
     ctrl->enc.scale = sc.M;
   }
   if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
-  encode_tile<kVec>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+  encode_tile<kPath>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
@@ -247,11 +330,14 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
   }
   if (sc.bad) return;  // this tensor is refused; the others go on
   if (d.vec & 1u)
-    encode_tile<true>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                      &results[t], sh);
+    encode_tile<kPathVec>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                          &results[t], sh);
+  else if (d.vec & 2u)
+    encode_tile<kPathShift>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                            &results[t], sh);
   else
-    encode_tile<false>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                       &results[t], sh);
+    encode_tile<kPathByte>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                           &results[t], sh);
 }
 
 // ---------------------------------------------------------------- comparison modes
@@ -355,12 +441,15 @@ hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m,
                                const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                                uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  const bool vec = (m % 4 == 0) && aligned16(x) && aligned16(r);
-  if (vec)
-    tlc_quant_encode_kernel<true><<<ntiles, kThreads, 0, st>>>(
+  const bool al = aligned16(x) && aligned16(r);
+  if (al && m % 4 == 0)
+    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+  else if (al)
+    tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
         x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   else
-    tlc_quant_encode_kernel<false><<<ntiles, kThreads, 0, st>>>(
+    tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
         x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }

@@ -650,7 +650,7 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
     e.scale = scales[t];
     e.tile0 = tiles;
     e.range0 = ranges;
-    e.vec = (e.m % 4 == 0 && aligned16(outs[t])) ? 1u : 0u;
+    e.vec = aligned16(outs[t]) ? (e.m % 4 == 0 ? 1u : 2u) : 0u;
     tiles += (uint32_t)ceil_div(e.c, kZreTile);
     ranges += (uint32_t)ceil_div(e.m, kDecRange);
     d.push_back(e);

@@ -55,7 +55,7 @@ struct EncDesc {
   uint32_t tile0;  // first encoder tile (global tile numbering of the launch)
   uint32_t blk0;   // first absmax block / partial maximum of this tensor
   uint32_t nblk;   // absmax blocks of this tensor
-  uint32_t vec;    // 1: m % 4 == 0 and x, r 16-byte aligned
+  uint32_t vec;    // bit 0: m % 4 == 0 and x, r 16-byte aligned; bit 1: x, r aligned
   uint32_t pad[2];
 };
 static_assert(sizeof(EncDesc) == 64, "EncDesc is 64 bytes");
@@ -70,7 +70,7 @@ struct DecDesc {
   float scale;
   uint32_t tile0;   // first index-scan tile (global numbering of the launch)
   uint32_t range0;  // first start-index entry / expand block of this stream
-  uint32_t vec;     // 1: m % 4 == 0 and out 16-byte aligned
+  uint32_t vec;     // 1: m % 4 == 0 and out 16-byte aligned; 2: only out aligned
   uint32_t pad[4];
 };
 static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");

@@ -131,6 +131,25 @@ def test_long_runs_with_sparse_spikes(ctx):
         check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"spikes {trial}")
 
 
+# m = ceil(n/5) with m % 4 = 1, 2, 3 spanning several 4096-byte tiles and a
+# ragged tail: every partition but p0 starts off the float4 grid
+SHIFT_N = [5 * (4 * 4096 + 1), 5 * (4 * 4096 + 2) - 3, 5 * (4 * 4096 + 3) - 1,
+           5 * (3 * 4096 + 1001) - 4, 5 * 4097 + 2]
+
+
+@pytest.mark.parametrize("n", SHIFT_N)
+@pytest.mark.parametrize("offset", [0, 4])
+def test_partitions_off_float4_grid(ctx, n, offset):
+    """16-byte aligned tensors whose partition boundaries k*m are not."""
+    assert ((n + 4) // 5) % 4 != 0
+    x = workloads.runs_tensor([45, n], n)
+    r = workloads.normal([46, n], n, 1e-4)
+    check_encode_decode(ctx, x, r, 1.75, out0=workloads.normal([47, n], n), accumulate=True,
+                        offset=offset, tag=f"shift n={n}")
+    x = workloads.normal([48, n], n, 1.0)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, offset=offset, tag=f"shift dense n={n}")
+
+
 @pytest.mark.parametrize("offset", [1, 2, 3])
 def test_unaligned_pointers(ctx, offset):
     """Tensors that are not 16-byte aligned take the scalar kernels."""
