@@ -68,6 +68,15 @@ def lib():
     L.tlc_ref_compress_stochastic.argtypes = [vp, c_sz, c_f, u64, u64, vp, c_sz,
                                               ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
     L.tlc_ref_compress_stochastic.restype = c_i
+    L.tlc_ref_int8_step.argtypes = [c_f]
+    L.tlc_ref_int8_step.restype = c_f
+    L.tlc_ref_int8_quantize.argtypes = [vp, c_sz, c_f, vp, vp]
+    L.tlc_ref_int8_quantize.restype = None
+    L.tlc_ref_compress_int8.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
+                                        ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+    L.tlc_ref_compress_int8.restype = c_i
+    L.tlc_ref_decompress_int8.argtypes = [vp, c_sz, c_f, c_sz, vp, c_i]
+    L.tlc_ref_decompress_int8.restype = c_i
     _lib = L
     return L
 
@@ -211,3 +220,42 @@ def compress_stochastic(x, s, seed, step):
     st = lib().tlc_ref_compress_stochastic(_ptr(x), x.size, s, seed, step, out.ctypes.data,
                                            m, ctypes.byref(ln), ctypes.byref(M))
     return st, out[:ln.value].copy(), M.value
+
+
+def int8_step(M):
+    """The 8-bit comparator's quantization step fl(M / 127)."""
+    return lib().tlc_ref_int8_step(M)
+
+
+def int8_quantize(acc, M, residual=True):
+    """8-bit codes of acc at scale M.  Return (q int8, residual or None)."""
+    acc = _f32(acc)
+    q = np.zeros(acc.size, dtype=np.int8)
+    res = np.zeros(acc.size, dtype=np.float32) if residual else None
+    lib().tlc_ref_int8_quantize(_ptr(acc), acc.size, M, _ptr(q),
+                                _ptr(res) if residual else None)
+    return q, res
+
+
+def compress_int8(x, r, s):
+    """8-bit encode; r (float32, updated in place) or None for no error
+    feedback.  Return (status, bytes, M)."""
+    x = _f32(x)
+    if r is not None:
+        assert r.dtype == np.float32 and r.flags.c_contiguous and r.size == x.size
+    out = np.zeros(max(x.size, 1), dtype=np.uint8)
+    ln = ctypes.c_size_t(0)
+    M = ctypes.c_float(0.0)
+    st = lib().tlc_ref_compress_int8(_ptr(x), _ptr(r) if r is not None else None, x.size, s,
+                                     out.ctypes.data, x.size, ctypes.byref(ln), ctypes.byref(M))
+    return st, out[:ln.value].copy(), M.value
+
+
+def decompress_int8(C, M, n, out=None, accumulate=False):
+    """8-bit decode into out (float32, zeros if None).  Return (status, out)."""
+    C = np.ascontiguousarray(C, dtype=np.uint8)
+    if out is None:
+        out = np.zeros(n, dtype=np.float32)
+    assert out.dtype == np.float32 and out.flags.c_contiguous and out.size == n
+    st = lib().tlc_ref_decompress_int8(_ptr(C), C.size, M, n, _ptr(out), int(accumulate))
+    return st, out

@@ -318,3 +318,75 @@ int tlc_ref_compress_stochastic(const float* x, size_t n, float s, uint64_t seed
   free(q);
   return TLC_REF_OK;
 }
+
+/* ---- 8-bit integer comparator (Section 5.1, "8-bit int") ----------------
+ * The paper fixes the code set (255 levels, -127..127, -128 unused) and
+ * nothing else.  Reading: M as in Eq. 1, one step D = fl(M / 127) per
+ * tensor, q = rint(fl(acc / D)) (round half to even) clamped to
+ * [-127, 127], dequantized value fl(q * D).  The clamp only acts when D is
+ * subnormal (its rounding can leave M / D above 127.5); D == 0 (M below
+ * 127 * 2^-150) quantizes everything to 0. */
+float tlc_ref_int8_step(float M) { return M / 127.0f; }
+
+void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float* resid) {
+  const float D = tlc_ref_int8_step(M);
+  for (size_t i = 0; i < n; ++i) {
+    float v = 0.0f;
+    if (D > 0.0f) {
+      v = rintf(acc[i] / D);
+      if (v > 127.0f) v = 127.0f;
+      if (v < -127.0f) v = -127.0f;
+    }
+    q[i] = (int8_t)v;
+    if (resid) resid[i] = acc[i] - (float)q[i] * D;
+  }
+}
+
+int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
+                          size_t cap, size_t* len, float* scale) {
+  if (len) *len = 0;
+  if (!len || !scale) return TLC_REF_E_INVALID;
+  if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
+  if (n == 0) {
+    *scale = 0.0f;
+    return TLC_REF_OK;
+  }
+  if (!x || !bytes) return TLC_REF_E_INVALID;
+  if (cap < n) return TLC_REF_E_CAPACITY;
+  float* acc = (float*)ref_alloc(n * sizeof(float));
+  if (r)
+    tlc_ref_accumulate(x, r, n, acc); /* error feedback on */
+  else
+    memcpy(acc, x, n * sizeof(float));
+  float M = 0.0f;
+  int st = tlc_ref_absmax_scale(acc, n, s, &M);
+  if (st != TLC_REF_OK) {
+    free(acc);
+    return st;
+  }
+  int8_t* q = (int8_t*)ref_alloc(n);
+  float* resid = r ? (float*)ref_alloc(n * sizeof(float)) : NULL;
+  tlc_ref_int8_quantize(acc, n, M, q, resid);
+  for (size_t i = 0; i < n; ++i) bytes[i] = (uint8_t)q[i]; /* two's complement */
+  if (r) memcpy(r, resid, n * sizeof(float));
+  *len = n;
+  *scale = M;
+  free(resid);
+  free(q);
+  free(acc);
+  return TLC_REF_OK;
+}
+
+int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_t n,
+                            float* out, int accumulate) {
+  if (!(scale >= 0.0f) || !isfinite(scale)) return TLC_REF_E_INVALID;
+  if (n == 0) return len == 0 ? TLC_REF_OK : TLC_REF_E_CORRUPT;
+  if (!bytes || !out) return TLC_REF_E_INVALID;
+  if (len != n) return TLC_REF_E_CORRUPT;
+  const float D = tlc_ref_int8_step(scale);
+  for (size_t i = 0; i < n; ++i) {
+    const float v = (float)(int8_t)bytes[i] * D;
+    out[i] = accumulate ? out[i] + v : v;
+  }
+  return TLC_REF_OK;
+}

@@ -107,6 +107,25 @@ int tlc_ref_compress_stochastic(const float* x, size_t n, float s, uint64_t seed
                                 uint64_t step, uint8_t* bytes, size_t cap, size_t* len,
                                 float* scale);
 
+/* 8-bit integer quantization (the "8-bit int" comparator of Section 5.1):
+ * 255 codes -127..127.  Step D = fl(M / 127) with M = fl(max|acc| * s);
+ * q_i = rint(fl(acc_i / D)) clamped to [-127, 127] (q = 0 when D == 0);
+ * residual fl(acc_i - fl(q_i * D)).  tlc_ref_int8_quantize writes resid
+ * only when it is not NULL. */
+float tlc_ref_int8_step(float M);
+void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float* resid);
+
+/* Encoder: acc = x + r when r != NULL (error feedback, r updated), else acc
+ * = x.  bytes receives the n codes as two's-complement int8 (cap >= n). */
+int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
+                          size_t cap, size_t* len, float* scale);
+
+/* Decoder: out_i = fl(q_i * D) or fl(out_i + fl(q_i * D)), D = fl(scale /
+ * 127), every int8 code accepted; len != n is TLC_REF_E_CORRUPT with out
+ * unchanged. */
+int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_t n,
+                            float* out, int accumulate);
+
 #ifdef __cplusplus
 }
 #endif
