@@ -190,6 +190,64 @@ def report(torch, tlc, workloads, dev):
     ote, otd = _oracle_round_trips(x4, workloads.C4_S)
     rows.append(_row("C4 (5 steps)", v, workloads.C4_S, te, td, nb, ote, otd, v))
     del x4
+
+    # The comparison encodings of Section 5.1 on the C4 step-0 tensor: one
+    # encode + decode-accumulate per rep, kernel averages from the library's
+    # timers, and the oracle on the same tensor
+    import oracle
+    xh = workloads.c4_tensor(0)
+    x = torch.from_numpy(xh).to(dev)
+    r = torch.zeros_like(x)
+    out = torch.zeros_like(x)
+    buf = torch.empty(x.numel(), dtype=torch.uint8, device=dev)
+    modes = [("No ZRE", tlc.TLC_MODE_NO_ZRE, (tlc.TLC_KERNEL_QUANT_PACK,
+                                              tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+             ("Stoch 3-value + QE", tlc.TLC_MODE_STOCHASTIC, (tlc.TLC_KERNEL_QUANT_PACK,
+                                                              tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+             ("8-bit int", tlc.TLC_MODE_INT8, (tlc.TLC_KERNEL_INT8_QUANT,
+                                               tlc.TLC_KERNEL_INT8_DEQUANT))]
+    for name, mode, kids in modes:
+        rr = None if mode == tlc.TLC_MODE_STOCHASTIC else r
+        C, M = ctx.compress_mode(mode, x, rr, workloads.C4_S, seed=7, step=0, out=buf)
+        ctx.decompress_mode(mode, C, M, out, accumulate=True)
+        ctx.sync()
+        ctx.profile(True)
+        ctx.profile_reset()
+        reps = 5
+        te = td = 0.0
+        for k in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            C, M = ctx.compress_mode(mode, x, rr, workloads.C4_S, seed=7, step=k, out=buf)
+            t1 = time.perf_counter()
+            ctx.decompress_mode(mode, C, M, out, accumulate=True)
+            ctx.sync()
+            t2 = time.perf_counter()
+            te += t1 - t0
+            td += t2 - t1
+        kus = {}
+        for kid in (tlc.TLC_KERNEL_ABSMAX,) + kids:
+            ms, cnt = ctx.profile_get(kid)
+            kus[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
+        ctx.profile(False)
+        rh = np.zeros(xh.size, np.float32)
+        t0 = time.perf_counter()
+        if mode == tlc.TLC_MODE_NO_ZRE:
+            st, Ch, Mh = oracle.compress_nozre(xh, rh, workloads.C4_S)
+        elif mode == tlc.TLC_MODE_STOCHASTIC:
+            st, Ch, Mh = oracle.compress_stochastic(xh, workloads.C4_S, 7, 0)
+        else:
+            st, Ch, Mh = oracle.compress_int8(xh, rh, workloads.C4_S)
+        t1 = time.perf_counter()
+        if mode == tlc.TLC_MODE_INT8:
+            oracle.decompress_int8(Ch, Mh, xh.size, rh, accumulate=True)
+        else:
+            oracle.decompress(Ch, Mh, xh.size, rh, accumulate=True)
+        t2 = time.perf_counter()
+        rows.append(_row(f"C4 step 0, {name}", reps * x.numel(), workloads.C4_S, te, td,
+                         reps * (C.numel() + 4), t1 - t0, t2 - t1, x.numel(),
+                         kernel_us=kus))
+    del x, r, out, buf, xh, rh
     ctx.close()
 
     # C2: 335 ResNet-110 tensors x 10 steps through the batched calls.  The

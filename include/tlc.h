@@ -128,6 +128,9 @@ int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
                                  encoding, no error feedback (the "Stoch
                                  3-value + QE" design of Section 5.1, TernGrad
                                  without clipping; Section 3.1) */
+#define TLC_MODE_INT8 3       /* 8-bit integer quantization, codes -127..127
+                                 (the "8-bit int" design of Section 5.1): n
+                                 bytes, decoded by tlc_decompress_ex */
 
 /* Encode with a comparison mode.  TLC_MODE_3LC forwards to tlc_compress
  * (seed and step unused).  TLC_MODE_NO_ZRE: as tlc_compress but the payload
@@ -137,10 +140,25 @@ int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
  * 4) of Philox4x32-10 (Salmon et al., SC 2011) at counter (i/4 low, i/4
  * high, step low, step high) and key (seed low, seed high); residual is not
  * used (may be NULL).  Both return *bytes_len = ceil(n/5); the bytes are
- * 0..242, so tlc_decompress decodes them unchanged. */
+ * 0..242, so tlc_decompress decodes them unchanged.
+ * TLC_MODE_INT8: acc = tensor + residual (error feedback, residual
+ * rewritten) or, with residual == NULL, acc = tensor; M = max|acc| * s
+ * (Eq. 1), step D = fl(M / 127); byte i is the two's-complement int8 code
+ * rint(fl(acc_i / D)) clamped to [-127, 127] (0 when D == 0) and the
+ * residual becomes fl(acc_i - fl(code * D)).  bytes_cap >= n; *bytes_len =
+ * n.  Synchronous; on TLC_E_NONFINITE the residual and bytes are unchanged. */
 int tlc_compress_ex(tlc_ctx* ctx, int mode, const float* tensor, float* residual, size_t n,
                     float s, uint64_t seed, uint64_t step, uint8_t* bytes, size_t bytes_cap,
                     size_t* bytes_len, float* scale);
+
+/* Decode a stream of any mode.  TLC_MODE_3LC, TLC_MODE_NO_ZRE and
+ * TLC_MODE_STOCHASTIC forward to tlc_decompress.  TLC_MODE_INT8: bytes is
+ * device uint8[n] of int8 codes (every code accepted), out = fl(code * D)
+ * or out + fl(code * D) with D = fl(scale / 127); bytes_len != n returns
+ * TLC_E_CORRUPT at once with out unchanged.  Asynchronous on the context's
+ * stream. */
+int tlc_decompress_ex(tlc_ctx* ctx, int mode, const uint8_t* bytes, size_t bytes_len,
+                      float scale, size_t n, float* out, int accumulate);
 
 /* Encode `count` tensors in one pass (two launches, one synchronisation):
  * for every t, exactly tlc_compress(ctx, tensors[t], residuals[t], ns[t],
@@ -197,7 +215,9 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_EXPAND_DEQUANT_BATCH 7
 #define TLC_KERNEL_EXPAND_SUM 8     /* multi-stream expansion + summed dequantization */
 #define TLC_KERNEL_QUANT_PACK 9     /* comparison modes: quantize + quartic pack */
-#define TLC_KERNEL_COUNT 10
+#define TLC_KERNEL_INT8_QUANT 10    /* 8-bit comparator: codes and residual */
+#define TLC_KERNEL_INT8_DEQUANT 11  /* 8-bit comparator: decode */
+#define TLC_KERNEL_COUNT 12
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

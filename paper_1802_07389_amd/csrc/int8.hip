@@ -1,0 +1,216 @@
+// int8.hip -- gfx950 kernels of the 8-bit integer comparator (the "8-bit
+// int" design of Section 5.1): 255 codes -127..127 at one step D = M / 127
+// per tensor, M from Eq. 1.
+//
+//   tlc_int8_quant_kernel    code = rint(acc / D) clamped to [-127, 127]
+//                            (0 when D == 0), residual acc - code * D,
+//                            one int8 byte per value
+//   tlc_int8_dequant_kernel  out = code * D, or out + code * D
+//
+// Both are elementwise streams: a block covers kI8Rows rows of 1024 values;
+// in a row lane t owns values 4t .. 4t + 3 (one float4 per tensor and one
+// 32-bit word of codes), so every load and store instruction of a wave is
+// one contiguous span.  Divides, products and sums use the _rn intrinsics,
+// so each is one IEEE operation rounded to nearest even, as in the
+// definition.
+#include "device_common.hpp"
+
+namespace tlc {
+
+constexpr int kI8Rows = 16;                    // rows per block
+constexpr uint32_t kI8Row = kThreads * 4u;     // values per row
+constexpr int kI8Batch = 4;                    // rows whose loads are in flight together
+
+__device__ __forceinline__ float int8_step(float M) { return __fdiv_rn(M, 127.0f); }
+
+// Code of one accumulated value, as a float holding an integer in
+// [-127, 127].
+__device__ __forceinline__ float int8_code(float acc, float D) {
+  if (!(D > 0.0f)) return 0.0f;
+  const float v = rintf(__fdiv_rn(acc, D));
+  return fminf(fmaxf(v, -127.0f), 127.0f);
+}
+
+__device__ __forceinline__ uint32_t int8_byte(float code) {
+  return (uint32_t)(int32_t)code & 0xffu;
+}
+
+// Value of one byte: fl(code * D) (code 0 gives +0).
+__device__ __forceinline__ float int8_value(uint32_t byte, float D) {
+  return __fmul_rn((float)(int32_t)(int8_t)(uint8_t)byte, D);
+}
+
+// One value: code byte and (kResid) residual acc - fl(code * D).
+template <bool kResid>
+__device__ __forceinline__ uint32_t int8_one(float x, float r, float D, float& res) {
+  const float acc = kResid ? __fadd_rn(x, r) : x;
+  const float code = int8_code(acc, D);
+  if (kResid) res = __fsub_rn(acc, __fmul_rn(code, D));
+  return int8_byte(code);
+}
+
+// kVec: x (and r) 16-byte aligned, out 4-byte aligned.  kResid: error
+// feedback (acc = x + r, r rewritten); otherwise acc = x and r is unused.
+template <bool kVec, bool kResid>
+__global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, float s,
+    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
+    Ctrl* __restrict__ ctrl) {
+  __shared__ uint32_t red[kWaves];
+  const Scale sc = finish_scale(partials, np, s, red);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctrl->enc.err = sc.bad;
+    ctrl->enc.scale = sc.M;
+    ctrl->enc.len = sc.bad ? 0u : (uint32_t)n;
+  }
+  if (sc.bad) return;  // NaN/Inf or overflow: residual and bytes untouched
+  const float D = int8_step(sc.M);
+  const uint64_t base = (uint64_t)blockIdx.x * kI8Row * kI8Rows;
+  if (kVec) {
+#pragma unroll 1
+    for (int h = 0; h < kI8Rows; h += kI8Batch) {
+      float4 xa[kI8Batch], ra[kI8Batch];
+      bool full[kI8Batch];
+#pragma unroll
+      for (int i = 0; i < kI8Batch; ++i) {
+        const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
+        full[i] = e + 4u <= n;
+        if (full[i]) {
+          xa[i] = *reinterpret_cast<const float4*>(x + e);
+          if (kResid) ra[i] = *reinterpret_cast<const float4*>(r + e);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kI8Batch; ++i) {
+        const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
+        if (full[i]) {
+          float4 o;
+          const float4 rr = kResid ? ra[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+          const uint32_t w = int8_one<kResid>(xa[i].x, rr.x, D, o.x) |
+                             int8_one<kResid>(xa[i].y, rr.y, D, o.y) << 8 |
+                             int8_one<kResid>(xa[i].z, rr.z, D, o.z) << 16 |
+                             int8_one<kResid>(xa[i].w, rr.w, D, o.w) << 24;
+          if (kResid) *reinterpret_cast<float4*>(r + e) = o;
+          *reinterpret_cast<uint32_t*>(out + e) = w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            if (e + c < n) {
+              float o = 0.0f;
+              out[e + c] = (uint8_t)int8_one<kResid>(x[e + c], kResid ? r[e + c] : 0.0f, D, o);
+              if (kResid) r[e + c] = o;
+            }
+          }
+        }
+      }
+    }
+  } else {
+    for (uint32_t k = threadIdx.x; k < kI8Row * kI8Rows; k += kThreads) {
+      const uint64_t e = base + k;
+      if (e >= n) break;
+      float o = 0.0f;
+      out[e] = (uint8_t)int8_one<kResid>(x[e], kResid ? r[e] : 0.0f, D, o);
+      if (kResid) r[e] = o;
+    }
+  }
+}
+
+// kVec: C 4-byte aligned, out 16-byte aligned.
+template <bool kVec, bool kAcc>
+__global__ __launch_bounds__(kThreads) void tlc_int8_dequant_kernel(
+    const uint8_t* __restrict__ C, uint64_t n, float M, float* __restrict__ out) {
+  const float D = int8_step(M);
+  const uint64_t base = (uint64_t)blockIdx.x * kI8Row * kI8Rows;
+  if (kVec) {
+#pragma unroll 1
+    for (int h = 0; h < kI8Rows; h += kI8Batch) {
+      uint32_t w[kI8Batch];
+      float4 o[kI8Batch];
+      bool full[kI8Batch];
+#pragma unroll
+      for (int i = 0; i < kI8Batch; ++i) {
+        const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
+        full[i] = e + 4u <= n;
+        if (full[i]) {
+          w[i] = *reinterpret_cast<const uint32_t*>(C + e);
+          if (kAcc) o[i] = *reinterpret_cast<const float4*>(out + e);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kI8Batch; ++i) {
+        const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
+        if (full[i]) {
+          const float v0 = int8_value(w[i], D), v1 = int8_value(w[i] >> 8, D);
+          const float v2 = int8_value(w[i] >> 16, D), v3 = int8_value(w[i] >> 24, D);
+          float4 res;
+          if (kAcc) {
+            res = make_float4(__fadd_rn(o[i].x, v0), __fadd_rn(o[i].y, v1),
+                              __fadd_rn(o[i].z, v2), __fadd_rn(o[i].w, v3));
+          } else {
+            res = make_float4(v0, v1, v2, v3);
+          }
+          *reinterpret_cast<float4*>(out + e) = res;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            if (e + c < n) {
+              const float v = int8_value(C[e + c], D);
+              out[e + c] = kAcc ? __fadd_rn(out[e + c], v) : v;
+            }
+          }
+        }
+      }
+    }
+  } else {
+    for (uint32_t k = threadIdx.x; k < kI8Row * kI8Rows; k += kThreads) {
+      const uint64_t e = base + k;
+      if (e >= n) break;
+      const float v = int8_value(C[e], D);
+      out[e] = kAcc ? __fadd_rn(out[e], v) : v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+namespace {
+inline bool aligned(const void* p, uintptr_t a) {
+  return (reinterpret_cast<uintptr_t>(p) & (a - 1u)) == 0u;
+}
+inline uint32_t int8_blocks(uint64_t n) {
+  const uint64_t per = (uint64_t)kI8Row * kI8Rows;
+  return (uint32_t)((n + per - 1) / per);
+}
+}  // namespace
+
+hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
+                             const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                             Ctrl* ctrl, hipStream_t st) {
+  const uint32_t blocks = int8_blocks(n);
+  const bool vec = aligned(x, 16) && (r == nullptr || aligned(r, 16)) && aligned(out, 4);
+#define TLC_LAUNCH(V, R)                                                                 \
+  tlc_int8_quant_kernel<V, R><<<blocks, kThreads, 0, st>>>(x, r, n, s, partials, npartials, \
+                                                           out, ctrl)
+  if (r) {
+    if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);
+  } else {
+    if (vec) TLC_LAUNCH(true, false); else TLC_LAUNCH(false, false);
+  }
+#undef TLC_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_int8_dequant(const uint8_t* C, uint64_t n, float M, float* out,
+                               int accumulate, hipStream_t st) {
+  const uint32_t blocks = int8_blocks(n);
+  const bool vec = aligned(C, 4) && aligned(out, 16);
+#define TLC_LAUNCH(V, A) tlc_int8_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, n, M, out)
+  if (accumulate) {
+    if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);
+  } else {
+    if (vec) TLC_LAUNCH(true, false); else TLC_LAUNCH(false, false);
+  }
+#undef TLC_LAUNCH
+  return hipGetLastError();
+}
+
+}  // namespace tlc

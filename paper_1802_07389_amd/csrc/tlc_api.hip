@@ -51,7 +51,8 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_zre_index_kernel",        "tlc_expand_dequant_kernel",
     "tlc_absmax_batch_kernel",     "tlc_quant_encode_batch_kernel",
     "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
-    "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel"};
+    "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel",
+    "tlc_int8_quant_kernel",       "tlc_int8_dequant_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -401,6 +402,50 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   return TLC_OK;
 }
 
+namespace {
+
+// TLC_MODE_INT8 of tlc_compress_ex (residual may be NULL: no error feedback).
+int compress_int8(tlc_ctx* c, const float* tensor, float* residual, size_t n, float s,
+                  uint8_t* bytes, size_t bytes_cap, size_t* bytes_len, float* scale) {
+  if (!bytes_len || !scale) return fail(TLC_E_INVALID, "tlc_compress_ex: NULL argument");
+  if (!(s >= 1.0f && s < 2.0f))
+    return fail(TLC_E_INVALID, "tlc_compress_ex: s = %g not in [1, 2)", (double)s);
+  if (n > c->max_n)
+    return fail(TLC_E_INVALID, "tlc_compress_ex: n = %zu exceeds the context's max_n %zu", n,
+                c->max_n);
+  if (n == 0) {
+    *scale = 0.0f;
+    return TLC_OK;
+  }
+  if (!tensor || !bytes) return fail(TLC_E_INVALID, "tlc_compress_ex: NULL device pointer");
+  if (bytes_cap < n)
+    return fail(TLC_E_CAPACITY, "tlc_compress_ex: bytes_cap %zu < n = %zu", bytes_cap, n);
+  if (overlap(tensor, n * 4, bytes, n) ||
+      (residual && (overlap(tensor, n * 4, residual, n * 4) || overlap(residual, n * 4, bytes, n))))
+    return fail(TLC_E_INVALID, "tlc_compress_ex: tensor, residual and bytes overlap");
+  int st = ensure_device(c);
+  if (st) return st;
+  uint32_t np = 0;
+  st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
+    return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
+  });
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_INT8_QUANT, [&] {
+    return launch_int8_quant(tensor, residual, n, s, c->partials, np, bytes, c->ctrl,
+                             c->stream);
+  });
+  if (st) return st;
+  st = sync_and_read(c);
+  if (st) return st;
+  if (c->rb->enc.err)
+    return fail(TLC_E_NONFINITE, "tlc_compress_ex: NaN/Inf in the input or max*s overflow");
+  *bytes_len = c->rb->enc.len;
+  *scale = c->rb->enc.scale;
+  return TLC_OK;
+}
+
+}  // namespace
+
 TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* residual,
                             size_t n, float s, uint64_t seed, uint64_t step, uint8_t* bytes,
                             size_t bytes_cap, size_t* bytes_len, float* scale) {
@@ -409,6 +454,8 @@ TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* re
   if (bytes_len) *bytes_len = 0;
   int st = check_usable(c, "tlc_compress_ex");
   if (st) return st;
+  if (mode == TLC_MODE_INT8)
+    return compress_int8(c, tensor, residual, n, s, bytes, bytes_cap, bytes_len, scale);
   if (mode != TLC_MODE_NO_ZRE && mode != TLC_MODE_STOCHASTIC)
     return fail(TLC_E_INVALID, "tlc_compress_ex: unknown mode %d", mode);
   const bool stoch = mode == TLC_MODE_STOCHASTIC;
@@ -613,6 +660,32 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
   return timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
     return launch_expand_dequant(bytes, (uint32_t)bytes_len, c->start, n, m, scale, out,
                                  accumulate, epoch, c->ctrl, c->stream);
+  });
+}
+
+TLC_API int tlc_decompress_ex(tlc_ctx* c, int mode, const uint8_t* bytes, size_t bytes_len,
+                              float scale, size_t n, float* out, int accumulate) {
+  if (mode == TLC_MODE_3LC || mode == TLC_MODE_NO_ZRE || mode == TLC_MODE_STOCHASTIC)
+    return tlc_decompress(c, bytes, bytes_len, scale, n, out, accumulate);
+  int st = check_usable(c, "tlc_decompress_ex");
+  if (st) return st;
+  if (mode != TLC_MODE_INT8)
+    return fail(TLC_E_INVALID, "tlc_decompress_ex: unknown mode %d", mode);
+  if (!isfinite(scale) || scale < 0.0f)
+    return fail(TLC_E_INVALID, "tlc_decompress_ex: scale %g is not finite and >= 0",
+                (double)scale);
+  if (n > c->max_n)
+    return fail(TLC_E_INVALID, "tlc_decompress_ex: n = %zu exceeds the context's max_n %zu", n,
+                c->max_n);
+  if (bytes_len != n)
+    return fail(TLC_E_CORRUPT, "tlc_decompress_ex: %zu bytes for n = %zu int8 codes",
+                bytes_len, n);
+  if (n == 0) return TLC_OK;
+  if (!bytes || !out) return fail(TLC_E_INVALID, "tlc_decompress_ex: NULL pointer");
+  st = ensure_device(c);
+  if (st) return st;
+  return timed_launch(c, TLC_KERNEL_INT8_DEQUANT, [&] {
+    return launch_int8_dequant(bytes, n, scale, out, accumulate, c->stream);
   });
 }
 

@@ -75,7 +75,7 @@ struct DecDesc {
 };
 static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
 
-// Launchers (encode.hip, decode.hip).  All return the hipError_t of the
+// Launchers (encode.hip, decode.hip, int8.hip).  All return the hipError_t of the
 // launch.
 hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
                          uint32_t* partials, uint32_t* nblocks, hipStream_t st);
@@ -87,6 +87,11 @@ hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, f
                              int stochastic, uint64_t seed, uint64_t step,
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
                              Ctrl* ctrl, hipStream_t st);
+hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
+                             const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                             Ctrl* ctrl, hipStream_t st);
+hipError_t launch_int8_dequant(const uint8_t* C, uint64_t n, float M, float* out,
+                               int accumulate, hipStream_t st);
 hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
                                uint32_t* partials, hipStream_t st);
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,

@@ -21,6 +21,9 @@ TLC_E_NONFINITE = -3
 TLC_E_CORRUPT = -4
 TLC_E_DEVICE = -5
 
+TLC_MAX_N = 4294967295
+TLC_MAX_TENSORS = 65536
+
 TLC_KERNEL_ABSMAX = 0
 TLC_KERNEL_QUANT_ENCODE = 1
 TLC_KERNEL_ZRE_INDEX = 2
@@ -31,16 +34,19 @@ TLC_KERNEL_ZRE_INDEX_BATCH = 6
 TLC_KERNEL_EXPAND_DEQUANT_BATCH = 7
 TLC_KERNEL_EXPAND_SUM = 8
 TLC_KERNEL_QUANT_PACK = 9
-TLC_KERNEL_COUNT = 10
+TLC_KERNEL_INT8_QUANT = 10
+TLC_KERNEL_INT8_DEQUANT = 11
+TLC_KERNEL_COUNT = 12
 
 TLC_MODE_3LC = 0
 TLC_MODE_NO_ZRE = 1
 TLC_MODE_STOCHASTIC = 2
+TLC_MODE_INT8 = 3
 
 EXPORTS = (
     "tlc_max_compressed_bytes", "tlc_ctx_create", "tlc_ctx_create_batch",
     "tlc_ctx_destroy", "tlc_compress", "tlc_compress_ex", "tlc_compress_batch",
-    "tlc_decompress",
+    "tlc_decompress", "tlc_decompress_ex",
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
     "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_get",
     "tlc_profile_reset", "tlc_kernel_name",
@@ -84,6 +90,8 @@ def _load():
     L.tlc_compress.restype = i
     L.tlc_decompress.argtypes = [vp, vp, sz, f, sz, vp, i]
     L.tlc_decompress.restype = i
+    L.tlc_decompress_ex.argtypes = [vp, i, vp, sz, f, sz, vp, i]
+    L.tlc_decompress_ex.restype = i
     L.tlc_sync.argtypes = [vp]
     L.tlc_sync.restype = i
     L.tlc_last_error_string.argtypes = []
@@ -192,6 +200,11 @@ def tlc_decompress(ctx, bytes_, bytes_len, scale, n, out, accumulate):
                               int(bool(accumulate)))
 
 
+def tlc_decompress_ex(ctx, mode, bytes_, bytes_len, scale, n, out, accumulate):
+    return lib.tlc_decompress_ex(ctx, mode, bytes_, bytes_len, scale, n, out,
+                                 int(bool(accumulate)))
+
+
 def tlc_sync(ctx):
     return lib.tlc_sync(ctx)
 
@@ -282,10 +295,11 @@ class Context:
                               _dev_f32(out, "out"), accumulate))
 
     def compress_mode(self, mode, tensor, residual, s, seed=0, step=0, out=None):
-        """Encode with TLC_MODE_NO_ZRE or TLC_MODE_STOCHASTIC (residual may be
-        None for the stochastic mode).  Returns (bytes view, scale)."""
+        """Encode with TLC_MODE_NO_ZRE, TLC_MODE_STOCHASTIC or TLC_MODE_INT8
+        (residual may be None for the stochastic mode, and for the 8-bit mode
+        without error feedback).  Returns (bytes view, scale)."""
         n = tensor.numel()
-        cap = tlc_max_compressed_bytes(n)
+        cap = n if mode == TLC_MODE_INT8 else tlc_max_compressed_bytes(n)
         if out is None:
             out = torch.empty(max(cap, 1), dtype=torch.uint8, device=self.device)
         rp = _dev_f32(residual, "residual") if residual is not None else None
@@ -309,6 +323,12 @@ class Context:
             [_dev_u8(o, "out") for o in outs], [o.numel() for o in outs])
         _check(st)
         return [(o[:ln], sc) for o, ln, sc in zip(outs, lens, scales)]
+
+    def decompress_mode(self, mode, data, scale, out, accumulate=False):
+        """Decode a stream of any mode into out (async)."""
+        _check(tlc_decompress_ex(self.handle, mode, _dev_u8(data, "data") if data.numel() else None,
+                                 data.numel(), float(scale), out.numel(),
+                                 _dev_f32(out, "out") if out.numel() else None, accumulate))
 
     def decompress_batch(self, datas, scales, outs, accumulate=False):
         """Decode a list of streams into a list of outputs (async)."""

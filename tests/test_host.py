@@ -33,6 +33,18 @@ def test_library_exports_every_declared_function():
         getattr(tlc.lib, name)
 
 
+def test_binding_constants_match_header():
+    """Every TLC_* integer #define of the C header has the same value in the
+    Python binding."""
+    from paper_1802_07389_amd import tlc
+    text = open(os.path.join(ROOT, "include", "tlc.h")).read()
+    defs = dict(re.findall(r"^#define\s+(TLC_\w+)\s+\(?(-?\d+)[uU]?L*L*\)?", text, flags=re.M))
+    defs.update(re.findall(r"^#define\s+(TLC_MAX_N)\s+\(\(size_t\)(\d+)u\)", text, flags=re.M))
+    assert len(defs) >= 25 and "TLC_MAX_N" in defs
+    for name, val in defs.items():
+        assert getattr(tlc, name) == int(val), name
+
+
 def test_host_only_entry_points():
     from paper_1802_07389_amd import tlc
     for n in list(range(0, 50)) + [2 ** 20, 2 ** 28, 25_600_000, 4294967295]:
@@ -42,7 +54,8 @@ def test_host_only_entry_points():
                      "tlc_expand_dequant_kernel", "tlc_absmax_batch_kernel",
                      "tlc_quant_encode_batch_kernel", "tlc_zre_index_batch_kernel",
                      "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel",
-                     "tlc_quant_pack_kernel"]
+                     "tlc_quant_pack_kernel", "tlc_int8_quant_kernel",
+                     "tlc_int8_dequant_kernel"]
     assert tlc.tlc_kernel_name(99) is None
 
 
