@@ -28,7 +28,8 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compression ratio"
 KERNEL_SRC = [os.path.join(ROOT, "paper_1802_07389_amd", "csrc", f)
-              for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp")]
+              for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp",
+                        "tlc_internal.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_traffic.md")
 
 # Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, all

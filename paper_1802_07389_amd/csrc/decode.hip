@@ -238,6 +238,7 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
 // q0 + jl), dequantizes (Eq. 3) and stores or accumulates into the five
 // partitions of out: float4 slices when m % 4 == 0 and out is aligned,
 // shifted float4 cells when only out is aligned, else scalar accesses.
+// These read-modify-write streams use plain (cached) accesses.
 template <int kPath, bool kAcc>
 __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, uint32_t qn,
                                               uint64_t n, uint64_t m, float M,

@@ -28,16 +28,15 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
   const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
   const uint64_t stride = (uint64_t)nblk * kThreads;
   if (kVec) {
-    const float4* __restrict__ x4 = reinterpret_cast<const float4*>(x);
-    const float4* __restrict__ r4 = reinterpret_cast<const float4*>(r);
     const uint64_t nv = n >> 2;
     uint64_t i = tid;
     for (; i + 3 * stride < nv; i += 4 * stride) {
       float4 a[4], b[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) a[u] = x4[i + u * stride];
+      for (int u = 0; u < 4; ++u) a[u] = ld_stream(x + 4 * (i + u * stride));
 #pragma unroll
-      for (int u = 0; u < 4; ++u) b[u] = kResid ? r4[i + u * stride] : make_float4(0, 0, 0, 0);
+      for (int u = 0; u < 4; ++u)
+        b[u] = kResid ? ld_stream(r + 4 * (i + u * stride)) : make_float4(0, 0, 0, 0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         mx = max(mx, abs_bits(a[u].x + b[u].x));
@@ -47,7 +46,7 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       }
     }
     for (; i < nv; i += stride) {
-      float4 a = x4[i], b = kResid ? r4[i] : make_float4(0, 0, 0, 0);
+      float4 a = ld_stream(x + 4 * i), b = kResid ? ld_stream(r + 4 * i) : make_float4(0, 0, 0, 0);
       mx = max(mx, abs_bits(a.x + b.x));
       mx = max(mx, abs_bits(a.y + b.y));
       mx = max(mx, abs_bits(a.z + b.z));
@@ -374,7 +373,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
           const uint64_t e = k * m + j;  // a multiple of 4: one Philox call per slice
           const Philox4 rw = element_words(e >> 2, step, seed);
           if (e + 4 <= n) {
-            const float4 a = *reinterpret_cast<const float4*>(x + e);
+            const float4 a = ld_stream(x + e);
             code[0] = code[0] * 3u + stochastic_trit(a.x, sc.M, rw.v[0]);
             code[1] = code[1] * 3u + stochastic_trit(a.y, sc.M, rw.v[1]);
             code[2] = code[2] * 3u + stochastic_trit(a.z, sc.M, rw.v[2]);

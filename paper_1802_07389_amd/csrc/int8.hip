@@ -76,8 +76,8 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
         const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
         full[i] = e + 4u <= n;
         if (full[i]) {
-          xa[i] = *reinterpret_cast<const float4*>(x + e);
-          if (kResid) ra[i] = *reinterpret_cast<const float4*>(r + e);
+          xa[i] = ld_stream(x + e);
+          if (kResid) ra[i] = ld_stream(r + e);
         }
       }
 #pragma unroll
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
                              int8_one<kResid>(xa[i].y, rr.y, D, o.y) << 8 |
                              int8_one<kResid>(xa[i].z, rr.z, D, o.z) << 16 |
                              int8_one<kResid>(xa[i].w, rr.w, D, o.w) << 24;
-          if (kResid) *reinterpret_cast<float4*>(r + e) = o;
+          if (kResid) st_stream(r + e, o);
           *reinterpret_cast<uint32_t*>(out + e) = w;
         } else {
 #pragma unroll
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_dequant_kernel(
         full[i] = e + 4u <= n;
         if (full[i]) {
           w[i] = *reinterpret_cast<const uint32_t*>(C + e);
-          if (kAcc) o[i] = *reinterpret_cast<const float4*>(out + e);
+          if (kAcc) o[i] = ld_stream(out + e);
         }
       }
 #pragma unroll
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_dequant_kernel(
           } else {
             res = make_float4(v0, v1, v2, v3);
           }
-          *reinterpret_cast<float4*>(out + e) = res;
+          st_stream(out + e, res);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) {

@@ -13,7 +13,7 @@ constexpr int kZreBytesPerThread = 32;    // zero-run scans: two uint4 per threa
 constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
-constexpr uint32_t kAbsmaxMaxBlocks = 512;  // partial maxima per encode
+constexpr uint32_t kAbsmaxMaxBlocks = 256;  // partial maxima per encode (one block per CU)
 
 // Per-tensor encode result (device), written by the encoder's tiles.
 struct EncResult {
