@@ -217,13 +217,21 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   const uint32_t lo = threadIdx.x * kBytes;
   const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
   uint8_t b[kBytes];
+  bool zero = cnt == (uint32_t)kBytes;  // a full chunk of five-zero groups (byte 121)
 #pragma unroll
-  for (int h = 0; h < kBytes / 16; ++h)
-    unpack16(*reinterpret_cast<const uint4*>(sh.q + lo + 16 * h), b + 16 * h);
-  RunSum sum = rs_identity();
+  for (int h = 0; h < kBytes / 16; ++h) {
+    const uint4 w = *reinterpret_cast<const uint4*>(sh.q + lo + 16 * h);
+    zero = zero && w.x == 0x79797979u && w.y == 0x79797979u && w.z == 0x79797979u &&
+           w.w == 0x79797979u;
+    unpack16(w, b + 16 * h);
+  }
+  RunSum sum = rs_zero_run(kBytes);
+  if (!zero) {
+    sum = rs_identity();
 #pragma unroll
-  for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt) sum = rs_combine(sum, rs_byte(b[i]));
+    for (int i = 0; i < kBytes; ++i)
+      if ((uint32_t)i < cnt) sum = rs_combine(sum, rs_byte(b[i]));
+  }
 
   RunSum incl = sum;
 #pragma unroll
@@ -272,9 +280,13 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
+  if (zero) {
+    phi = rs_zero_walk(kBytes, phi, put);
+  } else {
 #pragma unroll
-  for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
+    for (int i = 0; i < kBytes; ++i)
+      if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
+  }
   if (cnt && q0 + lo + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
 
   const bool last_tile = q0 + kEncTile >= m;

@@ -131,6 +131,21 @@ TLC_HD uint32_t rs_step(uint32_t x, uint32_t phi, Put&& put) {
   return phi;
 }
 
+// Closed forms for a segment of len bytes that are all 121 (the common
+// case: most groups of five values quantize to zero).  Its summary is
+// (all, len mod 14, len mod 14, len / 14); encoding it after phase phi
+// writes one 255 for every 14th byte of the grown run.
+TLC_HD RunSum rs_zero_run(uint32_t len) {
+  return rs_make(1u, len % kRunMax, len % kRunMax, len / kRunMax);
+}
+
+template <class Put>
+TLC_HD uint32_t rs_zero_walk(uint32_t len, uint32_t phi, Put&& put) {
+  const uint32_t t = phi + len;
+  for (uint32_t e = 0; e < t / kRunMax; ++e) put(kFullChunk);
+  return t % kRunMax;
+}
+
 // rs_step over `count` bytes.  The caller writes the final remainder code
 // (rs_code) if the stream ends with a non-zero phase.
 template <class Put>

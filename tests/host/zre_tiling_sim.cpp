@@ -2,8 +2,10 @@
 // tiles of `tile` bytes and threads of `per` bytes; thread summaries are
 // scanned inside a tile, tile prefixes are folded in order (what the
 // decoupled look-back computes), and every thread encodes its bytes from its
-// own prefix.  Reads raw bytes on stdin and writes the encoded stream on
-// stdout.  Usage: zre_tiling_sim TILE PER < in > out
+// own prefix.  As in the kernel, a thread whose `per` bytes are all 121 uses
+// the closed forms rs_zero_run / rs_zero_walk instead of the byte loop.
+// Reads raw bytes on stdin and writes the encoded stream on stdout.
+// Usage: zre_tiling_sim TILE PER < in > out
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
@@ -38,14 +40,18 @@ int main(int argc, char** argv) {
     RunSum thr = excl;
     for (size_t p = t * tile; p < (t + 1) * tile && p < m; p += per) {
       size_t cnt = (p + per <= m) ? per : m - p;
+      bool zero = cnt == per;
+      for (size_t j = p; j < p + cnt; ++j) zero = zero && q[j] == kZeroGroup;
       uint32_t o = rs_emitted(thr);
       uint32_t phi = rs_phase(thr);
-      phi = rs_walk(&q[p], (uint32_t)cnt, phi, [&](uint32_t b) {
-        out[o++] = (uint8_t)b;
-      });
+      auto put = [&](uint32_t b) { out[o++] = (uint8_t)b; };
+      phi = zero ? rs_zero_walk((uint32_t)cnt, phi, put) : rs_walk(&q[p], (uint32_t)cnt, phi, put);
       if (p + cnt == m && phi) out[o++] = (uint8_t)rs_code(phi);
       RunSum s = rs_identity();
-      for (size_t j = p; j < p + cnt; ++j) s = rs_combine(s, rs_byte(q[j]));
+      if (zero)
+        s = rs_zero_run((uint32_t)cnt);
+      else
+        for (size_t j = p; j < p + cnt; ++j) s = rs_combine(s, rs_byte(q[j]));
       thr = rs_combine(thr, s);
       if (p + cnt == m) total_written = o;
     }
