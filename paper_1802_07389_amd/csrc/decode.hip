@@ -177,13 +177,18 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
 }
 
 // ---------------------------------------------------------------- Eq. 3
-// Partition K of quartic bytes s_q[0, qn) (global bytes q0 + jl) when
-// m % 4 != 0 and out is 16-byte aligned: the partition starts a =
-// (K*m + q0) mod 4 values past a float4 boundary, and cell f of its aligned
+// Partition K of quartic bytes s_q[0, qn) (global bytes q0 + jl) when out
+// is 16-byte aligned: the partition starts a = (K*m + q0) mod 4 values past
+// a float4 boundary (a = 0 when m % 4 == 0), and cell f of its aligned
 // float4 grid takes digit K of bytes 4f - a .. 4f + 3 - a (two LDS words).
 // Cells shared with a neighbouring range or partition, or reaching past n,
-// are written value by value.
-template <int K, bool kAcc>
+// are written value by value.  The block sweeps one partition at a time.
+// kNT: the full cells use nontemporal loads and stores.  That pays when out
+// is far larger than the 256 MB last-level cache: on gfx950 the hinted
+// sweep then beat the plain one and five-partition float4 groups, and its
+// stores leave no dirty lines for the next encode to write back.  Outputs
+// that fit the cache decode faster with plain accesses.
+template <int K, bool kAcc, bool kNT>
 __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, uint64_t q0,
                                                           uint32_t qn, uint64_t n, uint64_t m,
                                                           float M, float* __restrict__ out) {
@@ -200,7 +205,9 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
   for (int i = 0; i < kCells; ++i) {
     const uint32_t f = threadIdx.x + kThreads * i;
     full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= qn + a && e0 + 4ull * f + 4u <= n;
-    if (kAcc && full[i]) o[i] = *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
+    if (kAcc && full[i])
+      o[i] = kNT ? ld_stream(out + e0 + 4ull * f)
+                 : *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
   }
 #pragma unroll
   for (int i = 0; i < kCells; ++i) {
@@ -223,7 +230,10 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
       } else {
         o[i] = make_float4(v[0], v[1], v[2], v[3]);
       }
-      *reinterpret_cast<float4*>(out + e) = o[i];
+      if (kNT)
+        st_stream(out + e, o[i]);
+      else
+        *reinterpret_cast<float4*>(out + e) = o[i];
     } else {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
@@ -236,19 +246,22 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
 
 // Unpacks the base-3 digits of quartic bytes s_q[0, qn) (global bytes
 // q0 + jl), dequantizes (Eq. 3) and stores or accumulates into the five
-// partitions of out: float4 slices when m % 4 == 0 and out is aligned,
-// shifted float4 cells when only out is aligned, else scalar accesses.
-// These read-modify-write streams use plain (cached) accesses.
-template <int kPath, bool kAcc>
+// partitions of out.  kPathShift: aligned float4 cells partition by
+// partition (aligned out; the large outputs also take the nontemporal
+// hint).  kPathVec: each lane takes 4 bytes and their five float4 slices
+// at once (aligned out, m % 4 == 0; fewer dependent memory round trips per
+// block, which is what outputs that fit the cache are bound by).
+// kPathByte: one quartic byte per lane with scalar accesses.
+template <int kPath, bool kAcc, bool kNT = false>
 __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, uint32_t qn,
                                               uint64_t n, uint64_t m, float M,
                                               float* __restrict__ out) {
   if (kPath == kPathShift) {
-    dequant_partition_shifted<0, kAcc>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<1, kAcc>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<2, kAcc>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<3, kAcc>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<4, kAcc>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<0, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<1, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
   } else if (kPath == kPathVec) {
 #pragma unroll
     for (int g = 0; g < kDecRange / (4 * kThreads); ++g) {
@@ -312,7 +325,7 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 }
 
 // One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
-template <int kPath, bool kAcc>
+template <int kPath, bool kAcc, bool kNT>
 __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
     const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ start,
     uint64_t n, uint64_t m, float M, float* __restrict__ out, uint32_t epoch,
@@ -324,7 +337,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
   expand_range(C, c, start, k, m, qn, s_q, red);
-  dequant_range<kPath, kAcc>(s_q, q0, qn, n, m, M, out);
+  dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
 }
 
 template <bool kAcc>
@@ -444,6 +457,10 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
 }
 
 // ---------------------------------------------------------------- launchers
+// Outputs of at least this size decode with nontemporal hints (twice the
+// 256 MB last-level cache of the part).
+constexpr uint64_t kNtMinBytes = 512ull << 20;
+
 static inline bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
 }
@@ -461,16 +478,19 @@ hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* s
                                  int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                  hipStream_t st) {
   const bool al = aligned16(out);
+  const bool nt = al && n * sizeof(float) >= kNtMinBytes;
   const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
-#define TLC_LAUNCH(V, A)                                                                     \
-  tlc_expand_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, out, \
-                                                               epoch, ctrl)
-  if (al && m % 4 == 0) {
-    if (accumulate) TLC_LAUNCH(kPathVec, true); else TLC_LAUNCH(kPathVec, false);
+#define TLC_LAUNCH(V, A, N)                                                                 \
+  tlc_expand_dequant_kernel<V, A, N><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, \
+                                                                  out, epoch, ctrl)
+  if (nt) {
+    if (accumulate) TLC_LAUNCH(kPathShift, true, true); else TLC_LAUNCH(kPathShift, false, true);
+  } else if (al && m % 4 == 0) {
+    if (accumulate) TLC_LAUNCH(kPathVec, true, false); else TLC_LAUNCH(kPathVec, false, false);
   } else if (al) {
-    if (accumulate) TLC_LAUNCH(kPathShift, true); else TLC_LAUNCH(kPathShift, false);
+    if (accumulate) TLC_LAUNCH(kPathShift, true, false); else TLC_LAUNCH(kPathShift, false, false);
   } else {
-    if (accumulate) TLC_LAUNCH(kPathByte, true); else TLC_LAUNCH(kPathByte, false);
+    if (accumulate) TLC_LAUNCH(kPathByte, true, false); else TLC_LAUNCH(kPathByte, false, false);
   }
 #undef TLC_LAUNCH
   return hipGetLastError();

@@ -72,12 +72,13 @@ constexpr int kPathByte = 2;
 // Streaming float4 accesses (16-byte aligned addresses) with the
 // nontemporal hint, for tensors read or written once per kernel and far
 // larger than the caches.  Measured on gfx950: the max reduction reads
-// 25 % faster with it, and the 8-bit kernels (contiguous read/write
-// streams, both sides hinted) 10-15 % faster.  The 3LC encoder and decoder,
-// whose blocks each stream five partitions, stay with plain accesses: there
-// the hint slowed the decoder by 10 %, and hinted encoder stores slowed the
-// decode that follows by more than they saved.  The hint changes neither
-// values nor visibility: the next kernel on the stream sees the stores.
+// 25 % faster with it, the 8-bit kernels (contiguous read/write streams,
+// both sides hinted) 10-15 % faster, and the decoder's partition-by-
+// partition sweep gains too (its hinted stores leave no dirty lines for the
+// next encode).  The 3LC encoder keeps plain accesses: its hinted stores
+// slowed the decode that follows by more than they saved.  The hint
+// changes neither values nor visibility: the next kernel on the stream
+// sees the stores.
 typedef float tlc_f4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float4 ld_stream(const float* p) {
   const tlc_f4 v = __builtin_nontemporal_load(reinterpret_cast<const tlc_f4*>(p));
