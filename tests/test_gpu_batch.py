@@ -234,3 +234,24 @@ def test_c5_aggregation_fused(bctx):
     bctx.sync()
     assert np.array_equal(g.bits(sumd.cpu().numpy()), g.bits(sum_ref))
     g.log("C5 fused aggregation ok")
+
+
+def test_shared_pull_one_payload_many_receivers(bctx):
+    """Section 3 (shared compression of a pull): the server encodes one
+    model delta once and every worker decodes the same payload into its own
+    model replica.  One batched call with the stream repeated gives every
+    replica exactly the oracle's decode-accumulate."""
+    import torch
+    g = G()
+    n = 4096 * 5 * 3 + 7
+    delta = workloads.runs_tensor([730], n)
+    st, C, M = oracle.compress(delta, np.zeros(n, F32), 1.5)
+    assert st == 0
+    Cd = torch.from_numpy(C).cuda()
+    replicas0 = [workloads.normal([731, w], n) for w in range(6)]
+    outs = [torch.from_numpy(r.copy()).cuda() for r in replicas0]
+    bctx.decompress_batch([Cd] * len(outs), [M] * len(outs), outs, accumulate=True)
+    bctx.sync()
+    for w, (o, r0) in enumerate(zip(outs, replicas0)):
+        st, ref = oracle.decompress(C, M, n, r0.copy(), accumulate=True)
+        assert st == 0 and np.array_equal(g.bits(o.cpu().numpy()), g.bits(ref)), w
