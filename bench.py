@@ -35,11 +35,17 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_tra
 # Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, all
 # fp32 tensors 4 B/value; the quartic bytes never leave LDS).
 def algorithmic_bytes(n, c):
+    tiles = -(-(-(-n // 5)) // 4096)  # 4096-byte quartic tiles
     return {
-        "tlc_absmax_kernel": 8 * n,                # read x, r
-        "tlc_quant_encode_kernel": 12 * n + c,     # read x, r; write r, C
-        "tlc_zre_index_kernel": c,                 # read C (writes m/4096 index words)
-        "tlc_expand_dequant_kernel": c + 8 * n,    # read C; read+write out
+        "tlc_absmax_kernel": 8 * n,                      # read x, r
+        # read x, r; write r, each tile's own stream bytes (c in all) and record
+        "tlc_quant_encode_kernel": 12 * n + c + 16 * tiles,
+        # tile records in, tile prefixes and chunk summaries out
+        "tlc_zre_chunk_kernel": 24 * tiles,
+        # records, prefixes and slot bytes in, the stream out
+        "tlc_zre_compact_kernel": 2 * c + 32 * tiles,
+        "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
+        "tlc_expand_dequant_kernel": c + 8 * n,          # read C; read+write out
     }
 
 
@@ -467,7 +473,8 @@ def main():
     achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(n)
 
-    enc_k = ["tlc_absmax_kernel", "tlc_quant_encode_kernel"]
+    enc_k = ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_chunk_kernel",
+             "tlc_zre_compact_kernel"]
     dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
     dec_kernel_ms = sum(kern[k][0] for k in dec_k)

@@ -206,7 +206,8 @@ const char* tlc_last_error_string(void);
 /* ---- per-kernel timing (HIP events on the context's stream) ----------- */
 
 #define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| (Eq. 1) */
-#define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, zero-run encoding */
+#define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, each tile's own
+                                       zero-run encoding */
 #define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts */
 #define TLC_KERNEL_EXPAND_DEQUANT 3 /* zero-run expansion, quartic unpack, Eq. 3 */
 #define TLC_KERNEL_ABSMAX_BATCH 4
@@ -217,7 +218,9 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_QUANT_PACK 9     /* comparison modes: quantize + quartic pack */
 #define TLC_KERNEL_INT8_QUANT 10    /* 8-bit comparator: codes and residual */
 #define TLC_KERNEL_INT8_DEQUANT 11  /* 8-bit comparator: decode */
-#define TLC_KERNEL_COUNT 12
+#define TLC_KERNEL_ZRE_CHUNKS 12    /* zero-run encoding: summaries of tile chunks */
+#define TLC_KERNEL_ZRE_COMPACT 13   /* zero-run encoding: tiles compacted into the stream */
+#define TLC_KERNEL_COUNT 14
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

@@ -2,15 +2,20 @@
 //
 //   tlc_absmax_kernel / _batch_kernel
 //       partial maxima of |tensor + residual|                          (Eq. 1)
-//   tlc_quant_encode_kernel / _batch_kernel
-//       M, 3-value quantization, residual write-back, quartic pack and
-//       zero-run encoding in one pass         (Eq. 1-2, Sections 3.2-3.3)
+//   tlc_quant_encode_kernel, tlc_zre_chunk(_scan)_kernel, tlc_zre_compact_kernel
+//       one tensor: M, 3-value quantization, residual write-back, quartic
+//       pack and each tile's own zero-run encoding; then a scan of the tile
+//       summaries and the compaction into one stream
+//                                             (Eq. 1-2, Sections 3.2-3.3)
+//   tlc_quant_encode_batch_kernel
+//       many tensors in one pass, tiles chained by decoupled look-back
 //
 // The batch kernels run many tensors in one launch: every block maps its
 // index (absmax) or its ticket (encoder) to a tensor through the sorted
 // first-block / first-tile fields of the tensor descriptors, then runs the
-// same device code as the single-tensor kernels.  Everything is HBM
-// streaming; nothing is a dense contraction, so there is no MFMA.
+// same max reduction and tile quantization as the single-tensor kernels.
+// Everything is HBM streaming; nothing is a dense contraction, so there is
+// no MFMA.
 #include "device_common.hpp"
 
 namespace tlc {
@@ -174,11 +179,32 @@ struct EncShared {
   __align__(16) uint8_t out[kEncTile + 16];
 };
 
-// Encodes tile `lt` (kEncTile quartic bytes) of one tensor whose scale is
-// sc.  Phase 1: the block quantizes its 5 * kEncTile values (kPath: threads
-// take groups of 4 bytes, aligned float4 cells of one partition at a time,
-// or single bytes, interleaved so every load and store instruction is
-// coalesced) and keeps the quartic bytes in LDS.  Phase 2: each thread takes
+// Phase 1 of a tile (Eq. 1-2, residual write-back, quartic pack): the block
+// quantizes the 5 * tile_bytes values of quartic bytes [q0, q0 + tile_bytes)
+// and leaves the bytes in q (LDS).  kPath: threads take groups of 4 bytes,
+// aligned float4 cells of one partition at a time, or single bytes,
+// interleaved so every load and store instruction is coalesced.  Ends with
+// a barrier.
+template <int kPath>
+__device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float* __restrict__ r,
+                                              uint64_t n, uint32_t m, const Scale& sc,
+                                              uint64_t q0, uint32_t tile_bytes, uint8_t* q) {
+  if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
+    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
+      *reinterpret_cast<uint32_t*>(q + g * 4u) =
+          quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+  } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
+    quantize_tile_shifted(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
+                          reinterpret_cast<uint32_t*>(q));
+  } else {  // 1 byte per thread: dword accesses, still contiguous per wave
+    for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
+      q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
+  }
+  __syncthreads();
+}
+
+// Encodes tile `lt` (kEncTile quartic bytes) of one tensor of a batch whose
+// scale is sc.  Phase 1: quantize_tile.  Phase 2: each thread takes
 // kEncTile/256 consecutive bytes and summarises them as a RunSum; the block
 // scans the summaries, the tile gets its prefix by decoupled look-back
 // (status slot floor + lt; slot floor is the tensor's first tile), and
@@ -199,18 +225,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
-    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
-      *reinterpret_cast<uint32_t*>(sh.q + g * 4u) =
-          quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
-  } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
-    quantize_tile_shifted(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
-                          reinterpret_cast<uint32_t*>(sh.q));
-  } else {  // 1 byte per thread: dword accesses, still contiguous per wave
-    for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
-      sh.q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
-  }
-  __syncthreads();
+  quantize_tile<kPath>(x, r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- phase 2: Section 3.3
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
@@ -302,23 +317,244 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   if (last_tile && threadIdx.x == 0) res->len = tile_end;
 }
 
+// ---------------------------------------------------------------- single tensor, three passes
+// A single tensor is encoded without any wait between tiles:
+//   pass A (tlc_quant_encode_kernel, one block per tile): quantize_tile, then
+//     zero-run encode the tile from its first non-121 byte on into its own
+//     slot.  That part does not depend on earlier tiles: the byte closes the
+//     run before it, so the encoder is at phase 0 there.  Each tile records
+//     its summary (RunSum), the length of its leading 121 run and the slot
+//     length.
+//   pass B (tlc_zre_chunk_kernel, tlc_zre_chunk_scan_kernel): every tile's
+//     prefix within its chunk of 64 tiles and the chunk summaries, then one
+//     block scans the chunk summaries.
+//   pass C (tlc_zre_compact_kernel, one block per tile): the tile's prefix
+//     (its output offset and incoming run phase) from its chunk's prefix
+//     and its own within the chunk, then the leading run's codes, which
+//     need the incoming phase (one 255 per 14th byte of the grown run, then
+//     its remainder code if the tile has a non-121 byte), and the slot; the
+//     last tile adds the remainder of a run that ends the stream.
+
+// Block-wide minimum; every thread gets the result (lds[kWaves], one
+// barrier; callers that reuse lds must barrier again first).
+__device__ __forceinline__ uint32_t block_min(uint32_t v, uint32_t* lds) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, d, 64));
+  if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = lds[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r = min(r, lds[w]);
+  return r;
+}
+
 template <int kPath>
-__global__ __launch_bounds__(kThreads) void tlc_quant_encode_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5)))
+void tlc_quant_encode_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
-    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
-    uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
-    Ctrl* __restrict__ ctrl) {
+    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ slots,
+    TileRec* __restrict__ recs, Ctrl* __restrict__ ctrl) {
+  constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
+  static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
   __shared__ EncShared sh;
-  __shared__ uint32_t s_tile;
-  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
-  const uint32_t tile = s_tile;
-  if (tile == 0 && threadIdx.x == 0) {
+  const uint32_t t = blockIdx.x;
+  if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
   if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
-  encode_tile<kPath>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+  const uint64_t q0 = (uint64_t)t * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  quantize_tile<kPath>(x, r, n, m, sc, q0, tile_bytes, sh.q);
+
+  // ---- Section 3.3 from the tile's first non-121 byte (index L) on
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
+  uint8_t b[kBytes];
+  bool zero = cnt == (uint32_t)kBytes;  // a full chunk of five-zero groups (byte 121)
+#pragma unroll
+  for (int h = 0; h < kBytes / 16; ++h) {
+    const uint4 w = *reinterpret_cast<const uint4*>(sh.q + lo + 16 * h);
+    zero = zero && w.x == 0x79797979u && w.y == 0x79797979u && w.z == 0x79797979u &&
+           w.w == 0x79797979u;
+    unpack16(w, b + 16 * h);
+  }
+  uint32_t first = tile_bytes;
+  if (!zero) {
+#pragma unroll
+    for (int i = kBytes - 1; i >= 0; --i)
+      if ((uint32_t)i < cnt && b[i] != kZeroGroup) first = lo + i;
+  }
+  const uint32_t L = block_min(first, sh.red);
+  const bool mine = lo + cnt > L;  // the thread holds bytes at index >= L
+  RunSum own = rs_identity();
+  if (mine) {
+    if (zero) {
+      own = rs_zero_run(kBytes);  // lo > L: a whole chunk of the run after L
+    } else {
+#pragma unroll
+      for (int i = 0; i < kBytes; ++i)
+        if ((uint32_t)i < cnt && lo + i >= L) own = rs_combine(own, rs_byte(b[i]));
+    }
+  }
+  RunSum incl = own;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    RunSum o = shfl_up_rs(incl, d);
+    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
+  }
+  RunSum excl_lane = shfl_up_rs(incl, 1);
+  if (lane == 0) excl_lane = rs_identity();
+  if (lane == 63) sh.wave[wid] = incl;
+  __syncthreads();
+  RunSum wpre = rs_identity();
+  RunSum agg = rs_identity();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    if ((uint32_t)w < wid) wpre = rs_combine(wpre, sh.wave[w]);
+    agg = rs_combine(agg, sh.wave[w]);
+  }
+  const RunSum P = rs_combine(wpre, excl_lane);
+  uint32_t o = rs_emitted(P);
+  uint32_t phi = rs_phase(P);
+  auto put = [&](uint32_t c) {
+    if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
+    ++o;
+  };
+  if (mine) {
+    if (zero) {
+      phi = rs_zero_walk(kBytes, phi, put);
+    } else {
+#pragma unroll
+      for (int i = 0; i < kBytes; ++i)
+        if ((uint32_t)i < cnt && lo + i >= L) phi = rs_step(b[i], phi, put);
+    }
+  }
+  // the slot holds at most the tile's own bytes; the clamp only keeps a
+  // logic error inside the slot
+  const uint32_t len = min<uint32_t>(rs_emitted(agg), tile_bytes);
+  __syncthreads();
+  for (uint32_t i = 16u * threadIdx.x; i < len; i += 16u * kThreads)
+    *reinterpret_cast<uint4*>(slots + q0 + i) = *reinterpret_cast<const uint4*>(sh.out + i);
+  if (threadIdx.x == 0) {
+    TileRec rec;
+    rec.agg = rs_combine(rs_zero_run(L), agg).v;
+    rec.lead = L;
+    rec.len = len;
+    recs[t] = rec;
+  }
+}
+
+// Pass B1: one wave per chunk of 64 tiles: every tile's prefix within its
+// chunk (an ordered wave scan) and the chunk's summary.
+constexpr uint32_t kChunkTiles = 64;
+constexpr uint32_t kChunkScanThreads = 1024;
+
+__global__ __launch_bounds__(kThreads) void tlc_zre_chunk_kernel(
+    const TileRec* __restrict__ recs, uint32_t ntiles, uint64_t* __restrict__ local_pre,
+    uint64_t* __restrict__ chunk_agg, const Ctrl* __restrict__ ctrl) {
+  if (ctrl->enc.err) return;  // pass A refused the tensor
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint32_t nchunks = (ntiles + kChunkTiles - 1) / kChunkTiles;
+  const uint32_t c = blockIdx.x * kWaves + wid;
+  if (c >= nchunks) return;  // whole waves only: no barrier follows
+  const uint32_t i = c * kChunkTiles + lane;
+  RunSum a = rs_identity();
+  if (i < ntiles) a.v = recs[i].agg;
+  RunSum incl = a;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    RunSum o = shfl_up_rs(incl, d);
+    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
+  }
+  RunSum ex = shfl_up_rs(incl, 1);
+  if (lane == 0) ex = rs_identity();
+  if (i < ntiles) local_pre[i] = ex.v;
+  if (lane == 63) chunk_agg[c] = incl.v;
+}
+
+// Pass B2: one block scans the chunk summaries in place (each entry becomes
+// the chunk's exclusive prefix); thread j takes a run of consecutive
+// chunks.
+__global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
+    uint32_t nchunks, uint64_t* __restrict__ chunk_agg, const Ctrl* __restrict__ ctrl) {
+  constexpr int kScanWaves = kChunkScanThreads / 64;
+  __shared__ RunSum s_wave[kScanWaves];
+  if (ctrl->enc.err) return;
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  const uint32_t per = (nchunks + kChunkScanThreads - 1) / kChunkScanThreads;
+  const uint32_t j0 = threadIdx.x * per, j1 = min(j0 + per, nchunks);
+  RunSum mine = rs_identity();
+  for (uint32_t j = j0; j < j1; ++j) {
+    RunSum a;
+    a.v = chunk_agg[j];
+    mine = rs_combine(mine, a);
+  }
+  RunSum incl = mine;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    RunSum o = shfl_up_rs(incl, d);
+    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
+  }
+  RunSum ex = shfl_up_rs(incl, 1);
+  if (lane == 0) ex = rs_identity();
+  if (lane == 63) s_wave[wid] = incl;
+  __syncthreads();
+  RunSum p = rs_identity();
+  for (uint32_t w = 0; w < wid; ++w) p = rs_combine(p, s_wave[w]);
+  p = rs_combine(p, ex);
+  for (uint32_t j = j0; j < j1; ++j) {  // every load of the run came before these stores
+    RunSum a;
+    a.v = chunk_agg[j];
+    chunk_agg[j] = p.v;
+    p = rs_combine(p, a);
+  }
+}
+
+// Pass C: one block per tile.  Prefix = the chunk's prefix combined with
+// the tile's prefix within its chunk; then the leading run's codes and the
+// slot; the last tile also writes the remainder of a run that ends the
+// stream and the stream length.  Every write is clamped to the m-byte
+// output (the stream never exceeds m bytes; the clamp only contains a logic
+// error).
+__global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
+    const TileRec* __restrict__ recs, const uint64_t* __restrict__ chunk_pre,
+    const uint64_t* __restrict__ local_pre, const uint8_t* __restrict__ slots, uint32_t m,
+    uint8_t* __restrict__ out, Ctrl* __restrict__ ctrl) {
+  if (ctrl->enc.err) return;
+  const uint32_t t = blockIdx.x;
+  RunSum cp, lp;
+  cp.v = chunk_pre[t / kChunkTiles];
+  lp.v = local_pre[t];
+  const RunSum P = rs_combine(cp, lp);
+  const TileRec rec = recs[t];
+  const uint64_t q0 = (uint64_t)t * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  const uint32_t off = rs_emitted(P);
+  const uint32_t grown = rs_phase(P) + rec.lead;  // the open run after the leading 121s
+  const uint32_t n255 = grown / kRunMax, rho = grown % kRunMax;
+  const bool rest = rec.lead < tile_bytes;
+  const uint32_t code = (rest && rho) ? 1u : 0u;
+  for (uint32_t i = threadIdx.x; i < n255; i += kThreads)
+    if (off + i < m) out[off + i] = (uint8_t)kFullChunk;
+  if (code && threadIdx.x == 0 && off + n255 < m) out[off + n255] = (uint8_t)rs_code(rho);
+  if (rest) {
+    const uint32_t at = off + n255 + code;
+    const uint32_t len = min<uint32_t>(rec.len, tile_bytes);
+    for (uint32_t i = threadIdx.x; i < len; i += kThreads)
+      if (at + i < m) out[at + i] = slots[q0 + i];
+  }
+  if (t + 1 == gridDim.x && threadIdx.x == 0) {  // a run that ends the stream; the length
+    RunSum a;
+    a.v = rec.agg;
+    const RunSum T = rs_combine(P, a);
+    const uint32_t total = rs_total(T);
+    if (rs_phase(T) && total >= 1u && total - 1u < m)
+      out[total - 1u] = (uint8_t)rs_code(rs_phase(T));
+    ctrl->enc.len = total;
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
@@ -449,19 +685,39 @@ hipError_t launch_absmax(const float* x, const float* r, uint64_t n, uint32_t* p
 }
 
 hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
-                               const uint32_t* partials, uint32_t npartials, uint8_t* out,
-                               uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                               uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+                               const uint32_t* partials, uint32_t npartials, uint8_t* slots,
+                               TileRec* recs, Ctrl* ctrl, hipStream_t st) {
+  const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(x) && aligned16(r);
   if (al && m % 4 == 0)
-    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(x, r, n, m, s, partials,
+                                                                   npartials, slots, recs, ctrl);
   else if (al)
     tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+        x, r, n, m, s, partials, npartials, slots, recs, ctrl);
   else
     tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+        x, r, n, m, s, partials, npartials, slots, recs, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
+                             uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st) {
+  const uint32_t nchunks = (ntiles + kChunkTiles - 1) / kChunkTiles;
+  tlc_zre_chunk_kernel<<<(nchunks + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+      recs, ntiles, local_pre, chunk_agg, ctrl);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  tlc_zre_chunk_scan_kernel<<<1, kChunkScanThreads, 0, st>>>(nchunks, chunk_agg, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
+                              const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
+                              uint8_t* out, Ctrl* ctrl, hipStream_t st) {
+  const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
+  tlc_zre_compact_kernel<<<ntiles, kThreads, 0, st>>>(recs, chunk_pre, local_pre, slots, m, out,
+                                                      ctrl);
   return hipGetLastError();
 }
 

@@ -52,7 +52,8 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_absmax_batch_kernel",     "tlc_quant_encode_batch_kernel",
     "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
     "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel",
-    "tlc_int8_quant_kernel",       "tlc_int8_dequant_kernel"};
+    "tlc_int8_quant_kernel",       "tlc_int8_dequant_kernel",
+    "tlc_zre_chunk_kernel",        "tlc_zre_compact_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -82,6 +83,11 @@ struct tlc_ctx {
   EncDesc* enc_descs = nullptr;
   DecDesc* dec_descs = nullptr;
   EncResult* enc_results = nullptr;
+  // single-tensor encoder: per-tile slots and records, chunk summaries
+  uint8_t* slots = nullptr;
+  TileRec* recs = nullptr;
+  uint64_t* chunk_agg = nullptr;  // chunk summaries, scanned in place into chunk prefixes
+  uint64_t* local_pre = nullptr;  // every tile's prefix within its chunk
   // pinned host memory: status readback, batch results, descriptor staging
   HostReadback* rb = nullptr;
   EncResult* host_results = nullptr;
@@ -267,8 +273,10 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->enc_status_words = mm / kEncTile + max_tensors + 2;
   c->dec_status_words = mm / kZreTile + max_tensors + 2;
   c->start_words = mm / kDecRange + max_tensors + 2;
+  const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
   // layout: ctrl | partials | enc status | dec status | start | enc descs |
-  //         dec descs | enc results
+  //         dec descs | enc results | tile records | chunk summaries |
+  //         tile prefixes in their chunks | slots
   size_t off = sizeof(Ctrl);
   const size_t off_partials = off;
   off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
@@ -283,7 +291,15 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   const size_t off_ddesc = off;
   off = round_up(off + max_tensors * sizeof(DecDesc), 256);
   const size_t off_res = off;
-  const size_t total = round_up(off + max_tensors * sizeof(EncResult), 256);
+  off = round_up(off + max_tensors * sizeof(EncResult), 256);
+  const size_t off_recs = off;
+  off = round_up(off + tiles1 * sizeof(TileRec), 256);
+  const size_t off_chunks = off;
+  off = round_up(off + (tiles1 / 64 + 1) * sizeof(uint64_t), 256);
+  const size_t off_local = off;
+  off = round_up(off + tiles1 * sizeof(uint64_t), 256);
+  const size_t off_slots = off;
+  const size_t total = round_up(off + tiles1 * (size_t)kEncTile, 256);
   e = hipMalloc(&c->ws, total);
   if (e != hipSuccess) {
     delete c;
@@ -298,6 +314,10 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->enc_descs = (EncDesc*)(base + off_edesc);
   c->dec_descs = (DecDesc*)(base + off_ddesc);
   c->enc_results = (EncResult*)(base + off_res);
+  c->recs = (TileRec*)(base + off_recs);
+  c->chunk_agg = (uint64_t*)(base + off_chunks);
+  c->local_pre = (uint64_t*)(base + off_local);
+  c->slots = base + off_slots;
   e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e == hipSuccess)
@@ -378,17 +398,21 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
-  uint32_t epoch = 0;
-  st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
-  if (st) return st;
-  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
-    return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, bytes,
-                               c->enc_status, ntiles, c->enc_ticket_base, epoch, c->ctrl,
-                               c->stream);
+    return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, c->slots,
+                               c->recs, c->ctrl, c->stream);
   });
   if (st) return st;
-  c->enc_ticket_base += ntiles;
+  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
+  st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
+    return launch_zre_chunks(c->recs, ntiles, c->local_pre, c->chunk_agg, c->ctrl, c->stream);
+  });
+  if (st) return st;
+  st = timed_launch(c, TLC_KERNEL_ZRE_COMPACT, [&] {
+    return launch_zre_compact(c->recs, c->chunk_agg, c->local_pre, c->slots, (uint32_t)m, bytes,
+                              c->ctrl, c->stream);
+  });
+  if (st) return st;
   st = sync_and_read(c);
   if (st) return st;
   if (c->rb->fault) {

@@ -60,6 +60,17 @@ struct EncDesc {
 };
 static_assert(sizeof(EncDesc) == 64, "EncDesc is 64 bytes");
 
+// Per-tile record of the single-tensor encoder's first pass: the zero-run
+// summary of the whole tile (RunSum bits), the length of its leading run of
+// 121 bytes, and how many bytes it wrote into its slot (its encoding from
+// the first non-121 byte on).
+struct TileRec {
+  uint64_t agg;
+  uint32_t lead;
+  uint32_t len;
+};
+static_assert(sizeof(TileRec) == 16, "TileRec is 16 bytes");
+
 // One stream of a batched decode or of a decode-sum.
 struct DecDesc {
   const uint8_t* C;
@@ -80,9 +91,13 @@ static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
 hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
                          uint32_t* partials, uint32_t* nblocks, hipStream_t st);
 hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
-                               const uint32_t* partials, uint32_t npartials, uint8_t* out,
-                               uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                               uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+                               const uint32_t* partials, uint32_t npartials, uint8_t* slots,
+                               TileRec* recs, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
+                             uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
+hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
+                              const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
+                              uint8_t* out, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, float s,
                              int stochastic, uint64_t seed, uint64_t step,
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,

@@ -67,26 +67,33 @@ TLC_HD RunSum rs_byte(uint32_t b) {
   return b == kZeroGroup ? rs_make(1u, 1u, 1u, 0u) : rs_make(0u, 0u, 0u, 1u);
 }
 
+// Run lengths are kept mod 14, so the sum s of two of them is at most 26:
+// s / 14 is (s >= 14), s mod 14 is s or s - 14, and ceil(s / 14) is
+// (s > 0) + (s > 14).
+TLC_HD uint32_t rs_div14(uint32_t s) { return s >= kRunMax ? 1u : 0u; }
+TLC_HD uint32_t rs_mod14(uint32_t s) { return s >= kRunMax ? s - kRunMax : s; }
+TLC_HD uint32_t rs_ceil14(uint32_t s) { return (s != 0u ? 1u : 0u) + (s > kRunMax ? 1u : 0u); }
+
 // Summary of segment a followed by segment b.
 TLC_HD RunSum rs_combine(RunSum a, RunSum b) {
   uint32_t aall = rs_all(a), ball = rs_all(b);
   uint32_t cnt = rs_cnt(a) + rs_cnt(b);
   if (aall & ball) {
     uint32_t s = rs_ld(a) + rs_ld(b);
-    return rs_make(1u, s % kRunMax, s % kRunMax, cnt + s / kRunMax);
+    return rs_make(1u, rs_mod14(s), rs_mod14(s), cnt + rs_div14(s));
   }
   if (aall) {  // the run at the end of a continues into b's leading run
     uint32_t s = rs_ld(a) + rs_ld(b);
-    return rs_make(0u, s % kRunMax, rs_tr(b), cnt + s / kRunMax);
+    return rs_make(0u, rs_mod14(s), rs_tr(b), cnt + rs_div14(s));
   }
   if (ball) {  // b extends a's trailing run
     uint32_t s = rs_tr(a) + rs_ld(b);
-    return rs_make(0u, rs_ld(a), s % kRunMax, cnt + s / kRunMax);
+    return rs_make(0u, rs_ld(a), rs_mod14(s), cnt + rs_div14(s));
   }
   // a's trailing run and b's leading run join into one run closed on both
   // sides: its remainder costs one more code if non-empty.
   uint32_t s = rs_tr(a) + rs_ld(b);
-  return rs_make(0u, rs_ld(a), rs_tr(b), cnt + (s + kRunMax - 1u) / kRunMax);
+  return rs_make(0u, rs_ld(a), rs_tr(b), cnt + rs_ceil14(s));
 }
 
 // Bytes already written by everything before a point whose prefix (from

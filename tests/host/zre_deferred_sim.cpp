@@ -1,0 +1,89 @@
+// Host-only simulation of the three-pass zero-run encoder:
+//   pass A, per tile of `tile` bytes cut into threads of `per` bytes: L =
+//     index of the tile's first non-121 byte (tile length if none); every
+//     thread summarises its bytes at index >= L, the tile scans those
+//     summaries, and each thread encodes its bytes from its own prefix
+//     into the tile's slot (phase 0 at the first non-121 byte, so nothing
+//     depends on earlier tiles); record = (summary of the whole tile, L,
+//     slot length);
+//   pass B: exclusive scan of the tile summaries in tile order;
+//   pass C, per tile: with phase phi and output offset from its prefix,
+//     write (phi + L) / 14 codes 255, then (if the tile has a non-121 byte)
+//     the remainder code of (phi + L) mod 14 and the slot; after the last
+//     tile, the remainder of a run that ends the stream.
+// Reads raw bytes on stdin, writes the encoded stream on stdout.
+// Usage: zre_deferred_sim TILE PER < in > out
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#include "../../paper_1802_07389_amd/csrc/zre_scan.hpp"
+
+using namespace tlc;
+
+struct Rec {
+  RunSum agg;
+  uint32_t lead, len;
+};
+
+int main(int argc, char** argv) {
+  if (argc != 3) return 2;
+  const size_t tile = std::strtoul(argv[1], nullptr, 10);
+  const size_t per = std::strtoul(argv[2], nullptr, 10);
+  if (!tile || !per || tile % per) return 2;
+  std::vector<uint8_t> q;
+  int ch;
+  while ((ch = std::getchar()) != EOF) q.push_back((uint8_t)ch);
+  const size_t m = q.size();
+  const size_t ntiles = (m + tile - 1) / tile;
+  std::vector<uint8_t> slots(ntiles * tile, 0xEE);
+  std::vector<Rec> rec(ntiles);
+  // pass A
+  for (size_t t = 0; t < ntiles; ++t) {
+    const size_t q0 = t * tile, tb = (q0 + tile <= m) ? tile : m - q0;
+    size_t L = tb;
+    for (size_t j = 0; j < tb; ++j)
+      if (q[q0 + j] != kZeroGroup) {
+        L = j;
+        break;
+      }
+    RunSum pre = rs_identity();  // exclusive prefix of the thread, bytes >= L only
+    for (size_t lo = 0; lo < tb; lo += per) {
+      const size_t hi = lo + per < tb ? lo + per : tb;
+      const size_t s0 = lo > L ? lo : L;
+      uint32_t o = rs_emitted(pre), phi = rs_phase(pre);
+      RunSum own = rs_identity();
+      for (size_t j = s0; j < hi; ++j) {
+        phi = rs_step(q[q0 + j], phi, [&](uint32_t b) { slots[t * tile + o++] = (uint8_t)b; });
+        own = rs_combine(own, rs_byte(q[q0 + j]));
+      }
+      pre = rs_combine(pre, own);
+    }
+    rec[t] = {rs_combine(rs_zero_run((uint32_t)L), pre), (uint32_t)L, rs_emitted(pre)};
+    if (rec[t].len > tb) return 3;
+  }
+  // pass B
+  std::vector<RunSum> excl(ntiles);
+  RunSum run = rs_identity();
+  for (size_t t = 0; t < ntiles; ++t) {
+    excl[t] = run;
+    run = rs_combine(run, rec[t].agg);
+  }
+  const uint32_t total = m ? rs_total(run) : 0;
+  // pass C
+  std::vector<uint8_t> out(total, 0xEE);
+  for (size_t t = 0; t < ntiles; ++t) {
+    const size_t q0 = t * tile, tb = (q0 + tile <= m) ? tile : m - q0;
+    const uint32_t phi = rs_phase(excl[t]);
+    uint32_t o = rs_emitted(excl[t]);
+    const uint32_t grown = phi + rec[t].lead;
+    for (uint32_t e = 0; e < grown / kRunMax; ++e) out.at(o++) = (uint8_t)kFullChunk;
+    if (rec[t].lead < tb) {
+      if (grown % kRunMax) out.at(o++) = (uint8_t)rs_code(grown % kRunMax);
+      for (uint32_t i = 0; i < rec[t].len; ++i) out.at(o++) = slots[t * tile + i];
+    }
+    if (t + 1 == ntiles && rs_phase(run)) out.at(total - 1) = (uint8_t)rs_code(rs_phase(run));
+  }
+  std::fwrite(out.data(), 1, out.size(), stdout);
+  return 0;
+}

@@ -55,7 +55,7 @@ def test_host_only_entry_points():
                      "tlc_quant_encode_batch_kernel", "tlc_zre_index_batch_kernel",
                      "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel",
                      "tlc_quant_pack_kernel", "tlc_int8_quant_kernel",
-                     "tlc_int8_dequant_kernel"]
+                     "tlc_int8_dequant_kernel", "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
     assert tlc.tlc_kernel_name(99) is None
 
 
@@ -90,6 +90,31 @@ def test_zre_tiling_matches_oracle(zsim, tile, per):
         p = rng.choice([0.0, 0.3, 0.9, 0.97, 0.999, 1.0])
         Q = np.where(rng.random(m) < p, 121, rng.integers(0, 243, m)).astype(np.uint8)
         r = subprocess.run([zsim, str(tile), str(per)], input=Q.tobytes(),
+                           capture_output=True, check=True)
+        assert np.array_equal(np.frombuffer(r.stdout, np.uint8), oracle.zre_encode(Q)), trial
+
+
+@pytest.fixture(scope="module")
+def zdef(tmp_path_factory):
+    exe = str(tmp_path_factory.mktemp("zdef") / "zre_deferred_sim")
+    subprocess.run(["g++", "-std=c++17", "-O2", "-Wall", "-Werror", "-o", exe,
+                    os.path.join(ROOT, "tests", "host", "zre_deferred_sim.cpp")], check=True)
+    return exe
+
+
+@pytest.mark.parametrize("tile,per", [(4096, 16), (64, 16), (16, 4), (14, 7), (5, 1), (28, 14),
+                                      (30, 2)])
+def test_zre_three_pass_matches_oracle(zdef, tile, per):
+    """The single-tensor encoder's three passes (each tile encoded from its
+    first non-121 byte into its own slot, a scan of tile summaries, then the
+    leading runs' codes written with the incoming phase) reproduce the
+    sequential zero-run encoding exactly."""
+    rng = np.random.default_rng(tile * 1000 + per)
+    for trial in range(60):
+        m = int(rng.integers(0, 9000))
+        p = rng.choice([0.0, 0.3, 0.9, 0.97, 0.999, 1.0])
+        Q = np.where(rng.random(m) < p, 121, rng.integers(0, 243, m)).astype(np.uint8)
+        r = subprocess.run([zdef, str(tile), str(per)], input=Q.tobytes(),
                            capture_output=True, check=True)
         assert np.array_equal(np.frombuffer(r.stdout, np.uint8), oracle.zre_encode(Q)), trial
 
