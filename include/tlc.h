@@ -220,7 +220,8 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_INT8_DEQUANT 11  /* 8-bit comparator: decode */
 #define TLC_KERNEL_ZRE_CHUNKS 12    /* zero-run encoding: summaries of tile chunks */
 #define TLC_KERNEL_ZRE_COMPACT 13   /* zero-run encoding: tiles compacted into the stream */
-#define TLC_KERNEL_COUNT 14
+#define TLC_KERNEL_QUANT_ENCODE_CHAINED 14 /* a small tensor's encode in one chained pass */
+#define TLC_KERNEL_COUNT 15
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context. */

@@ -7,8 +7,9 @@
 //       pack and each tile's own zero-run encoding; then a scan of the tile
 //       summaries and the compaction into one stream
 //                                             (Eq. 1-2, Sections 3.2-3.3)
-//   tlc_quant_encode_batch_kernel
-//       many tensors in one pass, tiles chained by decoupled look-back
+//   tlc_quant_encode_chained_kernel, tlc_quant_encode_batch_kernel
+//       a small tensor, or many tensors, in one pass: tiles chained by
+//       decoupled look-back
 //
 // The batch kernels run many tensors in one launch: every block maps its
 // index (absmax) or its ticket (encoder) to a tensor through the sorted
@@ -557,6 +558,28 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
   }
 }
 
+// A small tensor in one pass: tiles taken in order from the ticket and
+// chained by decoupled look-back (status slot = tile).  With few tiles the
+// look-back rarely waits, and this saves the two small passes' launches.
+template <int kPath>
+__global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
+    uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
+    Ctrl* __restrict__ ctrl) {
+  __shared__ EncShared sh;
+  __shared__ uint32_t s_tile;
+  if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
+  const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+  const uint32_t tile = s_tile;
+  if (tile == 0 && threadIdx.x == 0) {
+    ctrl->enc.err = sc.bad;
+    ctrl->enc.scale = sc.M;
+  }
+  if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
+  encode_tile<kPath>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+}
+
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
     const EncDesc* __restrict__ descs, uint32_t count, const uint32_t* __restrict__ partials,
     EncResult* __restrict__ results, uint64_t* __restrict__ status, uint32_t ticket_base,
@@ -698,6 +721,23 @@ hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m,
   else
     tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
         x, r, n, m, s, partials, npartials, slots, recs, ctrl);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                                       const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                                       uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                                       uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+  const bool al = aligned16(x) && aligned16(r);
+  if (al && m % 4 == 0)
+    tlc_quant_encode_chained_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+  else if (al)
+    tlc_quant_encode_chained_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+  else
+    tlc_quant_encode_chained_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
+        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
 

@@ -53,7 +53,8 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
     "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel",
     "tlc_int8_quant_kernel",       "tlc_int8_dequant_kernel",
-    "tlc_zre_chunk_kernel",        "tlc_zre_compact_kernel"};
+    "tlc_zre_chunk_kernel",        "tlc_zre_compact_kernel",
+    "tlc_quant_encode_chained_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -219,6 +220,21 @@ int sync_and_read(tlc_ctx* c) {
   e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   collect_timings(c);
+  return TLC_OK;
+}
+
+// Waits for an encode and reports its result (the stream length and M).
+int finish_compress(tlc_ctx* c, const char* fn, size_t* bytes_len, float* scale) {
+  int st = sync_and_read(c);
+  if (st) return st;
+  if (c->rb->fault) {
+    c->broken = true;
+    return fail(TLC_E_DEVICE, "%s: look-back wait timed out", fn);
+  }
+  if (c->rb->enc.err)
+    return fail(TLC_E_NONFINITE, "%s: NaN/Inf in tensor+residual or max*s overflow", fn);
+  *bytes_len = c->rb->enc.len;
+  *scale = c->rb->enc.scale;
   return TLC_OK;
 }
 
@@ -398,12 +414,25 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
+  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
+  if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
+    uint32_t epoch = 0;
+    st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
+    if (st) return st;
+    st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_CHAINED, [&] {
+      return launch_quant_encode_chained(tensor, residual, n, (uint32_t)m, s, c->partials, np,
+                                         bytes, c->enc_status, ntiles, c->enc_ticket_base, epoch,
+                                         c->ctrl, c->stream);
+    });
+    if (st) return st;
+    c->enc_ticket_base += ntiles;
+    return finish_compress(c, "tlc_compress", bytes_len, scale);
+  }
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, c->slots,
                                c->recs, c->ctrl, c->stream);
   });
   if (st) return st;
-  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
     return launch_zre_chunks(c->recs, ntiles, c->local_pre, c->chunk_agg, c->ctrl, c->stream);
   });
@@ -413,17 +442,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
                               c->ctrl, c->stream);
   });
   if (st) return st;
-  st = sync_and_read(c);
-  if (st) return st;
-  if (c->rb->fault) {
-    c->broken = true;
-    return fail(TLC_E_DEVICE, "tlc_compress: look-back wait timed out");
-  }
-  if (c->rb->enc.err)
-    return fail(TLC_E_NONFINITE, "tlc_compress: NaN/Inf in tensor+residual or max*s overflow");
-  *bytes_len = c->rb->enc.len;
-  *scale = c->rb->enc.scale;
-  return TLC_OK;
+  return finish_compress(c, "tlc_compress", bytes_len, scale);
 }
 
 namespace {

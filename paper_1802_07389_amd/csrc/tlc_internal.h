@@ -14,6 +14,9 @@ constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
 constexpr uint32_t kAbsmaxMaxBlocks = 256;  // partial maxima per encode (one block per CU)
+// Tensors of at least this many encoder tiles take the three-pass encoder
+// (no waits between tiles); smaller ones the single chained pass.
+constexpr uint32_t kThreePassMinTiles = 512;
 
 // Per-tensor encode result (device), written by the encoder's tiles.
 struct EncResult {
@@ -93,6 +96,10 @@ hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
 hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, Ctrl* ctrl, hipStream_t st);
+hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m, float s,
+                                       const uint32_t* partials, uint32_t npartials, uint8_t* out,
+                                       uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
+                                       uint32_t epoch, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
                              uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,

@@ -38,7 +38,8 @@ TLC_KERNEL_INT8_QUANT = 10
 TLC_KERNEL_INT8_DEQUANT = 11
 TLC_KERNEL_ZRE_CHUNKS = 12
 TLC_KERNEL_ZRE_COMPACT = 13
-TLC_KERNEL_COUNT = 14
+TLC_KERNEL_QUANT_ENCODE_CHAINED = 14
+TLC_KERNEL_COUNT = 15
 
 TLC_MODE_3LC = 0
 TLC_MODE_NO_ZRE = 1

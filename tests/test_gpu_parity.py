@@ -150,6 +150,38 @@ def test_partitions_off_float4_grid(ctx, n, offset):
     check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, offset=offset, tag=f"shift dense n={n}")
 
 
+# tensors of 520 encoder tiles and more take the three-pass encoder (each
+# tile encoded into its own slot, then the tile summaries scanned and the
+# stream compacted); the patterns below stress its tile boundaries
+THREE_PASS_N = [5 * 4096 * 520, 5 * 4096 * 520 + 13, 5 * (4096 * 531 + 2) - 1]
+
+
+@pytest.mark.parametrize("n", THREE_PASS_N)
+def test_three_pass_encoder_patterns(ctx, n):
+    m = (n + 4) // 5
+    g = G()
+    check_encode_decode(ctx, np.zeros(n, F32), np.zeros(n, F32), 1.0, tag=f"zeros n={n}")
+    # non-zero groups just before, at and after tile edges, and runs of every
+    # length mod 14 ending at a tile edge
+    rng = np.random.default_rng(n % 1000)
+    x = np.zeros(n, F32)
+    js = [4096 * t + d for t in range(1, m // 4096, 37) for d in (-15, -14, -13, -1, 0, 1)]
+    js += [4096 * 7 - 14 * k - r for k in range(3) for r in range(14)]
+    js += list(rng.integers(0, m, 300))
+    js = np.unique([j for j in js if 0 <= j < m])
+    x[js] = F32(1.0)
+    x[4 * m + (js[js < n - 4 * m] if n - 4 * m > 0 else js[:0])] = F32(-1.0)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"edge spikes n={n}")
+    x = workloads.runs_tensor([50, n], n)
+    r = workloads.normal([51, n], n, 1e-4)
+    check_encode_decode(ctx, x, r, 1.5, out0=workloads.normal([52, n], n), accumulate=True,
+                        tag=f"runs n={n}")
+    check_encode_decode(ctx, x, r, 1.5, offset=1, tag=f"runs unaligned n={n}")
+    x = workloads.normal([53, n], n, 1.0)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"dense n={n}")
+    g.log(f"three-pass patterns n={n} ok")
+
+
 @pytest.mark.parametrize("offset", [1, 2, 3])
 def test_unaligned_pointers(ctx, offset):
     """Tensors that are not 16-byte aligned take the scalar kernels."""
