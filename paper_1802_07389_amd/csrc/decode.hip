@@ -188,12 +188,35 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
 // sweep then beat the plain one and five-partition float4 groups, and its
 // stores leave no dirty lines for the next encode to write back.  Outputs
 // that fit the cache decode faster with plain accesses.
-template <int K, bool kAcc, bool kNT>
+constexpr int kSweepCells = (kDecRange + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
+
+// The kAcc loads of partition K's full cells (the cells the sweep below
+// adds to), issued before the range's zero-run expansion so that their
+// latency overlaps it.
+template <int K, bool kNT>
+__device__ __forceinline__ void sweep_preload(uint64_t q0, uint32_t qn, uint64_t n, uint64_t m,
+                                              const float* __restrict__ out,
+                                              float4 (&o)[kSweepCells]) {
+  const uint64_t base = (uint64_t)K * m + q0;
+  const uint32_t a = (uint32_t)(base & 3u);
+  const uint64_t e0 = base - a;
+  const uint32_t nf = (qn + a + 3u) >> 2;
+#pragma unroll
+  for (int i = 0; i < kSweepCells; ++i) {
+    const uint32_t f = threadIdx.x + kThreads * i;
+    if (f < nf && 4u * f >= a && 4u * f + 4u <= qn + a && e0 + 4ull * f + 4u <= n)
+      o[i] = kNT ? ld_stream(out + e0 + 4ull * f)
+                 : *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
+  }
+}
+
+template <int K, bool kAcc, bool kNT, bool kPre = false>
 __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, uint64_t q0,
                                                           uint32_t qn, uint64_t n, uint64_t m,
-                                                          float M, float* __restrict__ out) {
+                                                          float M, float* __restrict__ out,
+                                                          const float4* pre = nullptr) {
   constexpr uint32_t kPlace = K == 0 ? 81u : (K == 1 ? 27u : (K == 2 ? 9u : (K == 3 ? 3u : 1u)));
-  constexpr int kCells = (kDecRange + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
+  constexpr int kCells = kSweepCells;
   const uint32_t* qw = reinterpret_cast<const uint32_t*>(s_q);
   const uint64_t base = (uint64_t)K * m + q0;
   const uint32_t a = (uint32_t)(base & 3u);
@@ -205,9 +228,13 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
   for (int i = 0; i < kCells; ++i) {
     const uint32_t f = threadIdx.x + kThreads * i;
     full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= qn + a && e0 + 4ull * f + 4u <= n;
-    if (kAcc && full[i])
-      o[i] = kNT ? ld_stream(out + e0 + 4ull * f)
-                 : *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
+    if (kAcc && full[i]) {
+      if (kPre)
+        o[i] = pre[i];
+      else
+        o[i] = kNT ? ld_stream(out + e0 + 4ull * f)
+                   : *reinterpret_cast<const float4*>(out + e0 + 4ull * f);
+    }
   }
 #pragma unroll
   for (int i = 0; i < kCells; ++i) {
@@ -336,6 +363,21 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  if (kPath == kPathShift && kAcc && kNT) {
+    // large outputs: the first two partitions' loads overlap the expansion
+    // (on gfx950 15 us of 410 on a 2^28-value decode; outputs that fit the
+    // cache gained nothing)
+    float4 p0[kSweepCells], p1[kSweepCells];
+    sweep_preload<0, kNT>(q0, qn, n, m, out, p0);
+    sweep_preload<1, kNT>(q0, qn, n, m, out, p1);
+    expand_range(C, c, start, k, m, qn, s_q, red);
+    dequant_partition_shifted<0, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, p0);
+    dequant_partition_shifted<1, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, p1);
+    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    return;
+  }
   expand_range(C, c, start, k, m, qn, s_q, red);
   dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
 }
