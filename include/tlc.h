@@ -224,8 +224,15 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_COUNT 15
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
- * every kernel launch of the context. */
+ * every kernel launch of the context (of the kernels selected by
+ * tlc_profile_mask; all of them by default). */
 int tlc_profile_enable(tlc_ctx* ctx, int on);
+
+/* Select which kernels are timed while profiling is enabled: bit k of mask
+ * selects kernel id k (TLC_KERNEL_*).  Each timed launch adds an event pair
+ * to the stream, whose ordering costs some microseconds of device time, so
+ * a caller measuring throughput may time only the kernel it needs. */
+int tlc_profile_mask(tlc_ctx* ctx, uint32_t mask);
 
 /* Synchronize, then report the summed device time (ms) and the number of
  * timed launches of kernel `kernel` since the last reset. */

@@ -102,6 +102,7 @@ struct tlc_ctx {
   bool broken = false;
   // profiling
   bool profiling = false;
+  uint32_t profile_mask = 0xffffffffu;  // bit k: time kernel id k
   std::vector<hipEvent_t> free_events;
   std::vector<PendingTiming> pending;
   double total_ms[TLC_KERNEL_COUNT] = {};
@@ -150,7 +151,7 @@ void collect_timings(tlc_ctx* c) {
 template <class F>
 int timed_launch(tlc_ctx* c, int kernel, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (c->profiling) {
+  if (c->profiling && ((c->profile_mask >> kernel) & 1u)) {
     a = take_event(c);
     b = take_event(c);
     if (a && b && hipEventRecord(a, c->stream) != hipSuccess) {
@@ -881,6 +882,12 @@ TLC_API int tlc_sync(tlc_ctx* c) {
 TLC_API int tlc_profile_enable(tlc_ctx* c, int on) {
   if (!c) return fail(TLC_E_INVALID, "tlc_profile_enable: NULL context");
   c->profiling = on != 0;
+  return TLC_OK;
+}
+
+TLC_API int tlc_profile_mask(tlc_ctx* c, uint32_t mask) {
+  if (!c) return fail(TLC_E_INVALID, "tlc_profile_mask: NULL context");
+  c->profile_mask = mask;
   return TLC_OK;
 }
 

@@ -51,7 +51,7 @@ EXPORTS = (
     "tlc_ctx_destroy", "tlc_compress", "tlc_compress_ex", "tlc_compress_batch",
     "tlc_decompress", "tlc_decompress_ex",
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
-    "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_get",
+    "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_mask", "tlc_profile_get",
     "tlc_profile_reset", "tlc_kernel_name",
 )
 
@@ -101,6 +101,8 @@ def _load():
     L.tlc_last_error_string.restype = ctypes.c_char_p
     L.tlc_profile_enable.argtypes = [vp, i]
     L.tlc_profile_enable.restype = i
+    L.tlc_profile_mask.argtypes = [vp, ctypes.c_uint32]
+    L.tlc_profile_mask.restype = i
     L.tlc_profile_get.argtypes = [vp, i, ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(ctypes.c_uint64)]
     L.tlc_profile_get.restype = i
@@ -214,6 +216,10 @@ def tlc_sync(ctx):
 
 def tlc_profile_enable(ctx, on):
     return lib.tlc_profile_enable(ctx, int(bool(on)))
+
+
+def tlc_profile_mask(ctx, mask):
+    return lib.tlc_profile_mask(ctx, int(mask) & 0xffffffff)
 
 
 def tlc_profile_get(ctx, kernel):
@@ -351,7 +357,11 @@ class Context:
         _check(tlc_sync(self.handle))
 
     # per-kernel event timing
-    def profile(self, on=True):
+    def profile(self, on=True, kernels=None):
+        """Enable or disable per-kernel event timing; `kernels` (a list of
+        TLC_KERNEL_* ids) limits it to those kernels (default: all)."""
+        mask = 0xffffffff if kernels is None else sum(1 << k for k in kernels)
+        _check(tlc_profile_mask(self.handle, mask))
         _check(tlc_profile_enable(self.handle, on))
 
     def profile_reset(self):
