@@ -75,10 +75,11 @@ constexpr int kPathByte = 2;
 // 25 % faster with it, the 8-bit kernels (contiguous read/write streams,
 // both sides hinted) 10-15 % faster, and the decoder's partition-by-
 // partition sweep gains too (its hinted stores leave no dirty lines for the
-// next encode).  The 3LC encoder keeps plain accesses: its hinted stores
-// slowed the decode that follows by more than they saved.  The hint
-// changes neither values nor visibility: the next kernel on the stream
-// sees the stores.
+// next encode).  The 3LC encoder hints only its loads of the tensor, which
+// nothing reads again (a C4 round trip 1.5 % faster); hinting its residual
+// loads or stores slowed it or the decode that follows.  The hint changes
+// neither values nor visibility: the next kernel on the stream sees the
+// stores.
 typedef float tlc_f4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float4 ld_stream(const float* p) {
   const tlc_f4 v = __builtin_nontemporal_load(reinterpret_cast<const tlc_f4*>(p));
@@ -187,7 +188,7 @@ __device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
   uint32_t code[4] = {0u, 0u, 0u, 0u};
   float4 a[5], b[5];
 #pragma unroll
-  for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(x + k * m + j);
+  for (int k = 0; k < 5; ++k) a[k] = ld_stream(x + k * m + j);  // x is not read again
 #pragma unroll
   for (int k = 0; k < 5; ++k) b[k] = *reinterpret_cast<const float4*>(r + k * m + j);
 #pragma unroll
