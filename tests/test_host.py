@@ -33,6 +33,18 @@ def test_library_exports_every_declared_function():
         getattr(tlc.lib, name)
 
 
+@pytest.mark.parametrize("std", ["c99", "c11"])
+def test_header_is_plain_c(tmp_path, std):
+    """include/tlc.h is a C ABI: it compiles as strict C with every warning,
+    and a C caller can name every entry point."""
+    src = tmp_path / "use.c"
+    calls = "\n".join(f"  (void){name};" for name in header_functions())
+    src.write_text('#include "tlc.h"\nint main(void) {\n' + calls + "\n  return TLC_OK;\n}\n")
+    subprocess.run(["gcc", f"-std={std}", "-pedantic", "-Wall", "-Wextra", "-Werror", "-c",
+                    "-I", os.path.join(ROOT, "include"), str(src), "-o", str(tmp_path / "use.o")],
+                   check=True)
+
+
 def test_binding_constants_match_header():
     """Every TLC_* integer #define of the C header has the same value in the
     Python binding."""
