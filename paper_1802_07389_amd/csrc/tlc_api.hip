@@ -103,6 +103,11 @@ struct tlc_ctx {
   // profiling
   bool profiling = false;
   uint32_t profile_mask = 0xffffffffu;  // bit k: time kernel id k
+  // host-side descriptor tables of the batched calls (capacity max_tensors,
+  // reserved at creation, so the calls do not allocate)
+  std::vector<EncDesc> enc_host;
+  std::vector<DecDesc> dec_host;
+  std::vector<size_t> which;
   std::vector<hipEvent_t> free_events;
   std::vector<PendingTiming> pending;
   double total_ms[TLC_KERNEL_COUNT] = {};
@@ -111,16 +116,29 @@ struct tlc_ctx {
 
 namespace {
 
-int ensure_device(tlc_ctx* c) {
-  int cur = -1;
-  hipError_t e = hipGetDevice(&cur);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  if (cur != c->device) {
-    e = hipSetDevice(c->device);
-    if (e != hipSuccess) return hip_fail(e, "hipSetDevice");
+// Makes the context's device current for one entry point and restores the
+// caller's device when the entry point returns.
+class DeviceScope {
+ public:
+  explicit DeviceScope(int dev) {
+    err_ = hipGetDevice(&prev_);
+    if (err_ == hipSuccess && prev_ != dev) {
+      err_ = hipSetDevice(dev);
+      switched_ = err_ == hipSuccess;
+    }
   }
-  return TLC_OK;
-}
+  ~DeviceScope() {
+    if (switched_) (void)hipSetDevice(prev_);
+  }
+  DeviceScope(const DeviceScope&) = delete;
+  DeviceScope& operator=(const DeviceScope&) = delete;
+  int status() const { return err_ == hipSuccess ? TLC_OK : hip_fail(err_, "hipSetDevice"); }
+
+ private:
+  int prev_ = -1;
+  bool switched_ = false;
+  hipError_t err_ = hipSuccess;
+};
 
 hipEvent_t take_event(tlc_ctx* c) {
   if (!c->free_events.empty()) {
@@ -180,11 +198,16 @@ int timed_launch(tlc_ctx* c, int kernel, F&& launch) {
 
 // Next look-back epoch (never 0, the value of cleared status words); when
 // the counter wraps the status array is cleared on the stream first.
+// Next launch epoch (1 .. max_epoch).  When the counter wraps, the status
+// words are cleared, and so is `stale` (a device word that may hold an
+// epoch number of the old cycle: the decoder's bad-stream mark), so that no
+// old value can match a new launch.
 int next_epoch(tlc_ctx* c, uint32_t* epoch, uint32_t max_epoch, uint64_t* status,
-               size_t words, uint32_t* out) {
+               size_t words, uint32_t* stale, uint32_t* out) {
   if (*epoch >= max_epoch) {
     *epoch = 0;
     hipError_t e = hipMemsetAsync(status, 0, words * sizeof(uint64_t), c->stream);
+    if (e == hipSuccess && stale) e = hipMemsetAsync(stale, 0, sizeof(uint32_t), c->stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(status)");
   }
   *out = ++*epoch;
@@ -358,6 +381,14 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
     return hip_fail(e, "tlc_ctx_create: workspace init");
   }
   memset(c->rb, 0, sizeof(HostReadback));
+  try {
+    c->enc_host.reserve(max_tensors);
+    c->dec_host.reserve(max_tensors);
+    c->which.reserve(max_tensors);
+  } catch (...) {
+    tlc_ctx_destroy(c);
+    return fail(TLC_E_DEVICE, "tlc_ctx_create: out of host memory");
+  }
   *out = c;
   return TLC_OK;
 }
@@ -368,7 +399,7 @@ TLC_API int tlc_ctx_create(tlc_ctx** out, size_t max_n, void* hip_stream) {
 
 TLC_API int tlc_ctx_destroy(tlc_ctx* c) {
   if (!c) return TLC_OK;
-  ensure_device(c);
+  DeviceScope dev(c->device);
   (void)hipStreamSynchronize(c->stream);
   collect_timings(c);
   for (hipEvent_t ev : c->free_events) (void)hipEventDestroy(ev);
@@ -407,7 +438,8 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (overlap(tensor, n * 4, residual, n * 4) || overlap(tensor, n * 4, bytes, m) ||
       overlap(residual, n * 4, bytes, m))
     return fail(TLC_E_INVALID, "tlc_compress: tensor, residual and bytes overlap");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
 
   uint32_t np = 0;
@@ -418,7 +450,8 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
     uint32_t epoch = 0;
-    st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
+    st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, nullptr,
+                  &epoch);
     if (st) return st;
     st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_CHAINED, [&] {
       return launch_quant_encode_chained(tensor, residual, n, (uint32_t)m, s, c->partials, np,
@@ -467,7 +500,8 @@ int compress_int8(tlc_ctx* c, const float* tensor, float* residual, size_t n, fl
   if (overlap(tensor, n * 4, bytes, n) ||
       (residual && (overlap(tensor, n * 4, residual, n * 4) || overlap(residual, n * 4, bytes, n))))
     return fail(TLC_E_INVALID, "tlc_compress_ex: tensor, residual and bytes overlap");
-  int st = ensure_device(c);
+  DeviceScope dev(c->device);
+  int st = dev.status();
   if (st) return st;
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
@@ -521,7 +555,8 @@ TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* re
   if (overlap(tensor, n * 4, bytes, m) ||
       (!stoch && (overlap(tensor, n * 4, residual, n * 4) || overlap(residual, n * 4, bytes, m))))
     return fail(TLC_E_INVALID, "tlc_compress_ex: tensor, residual and bytes overlap");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   float* r = stoch ? nullptr : residual;  // the stochastic mode has no error feedback
   uint32_t np = 0;
@@ -584,9 +619,10 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   if (total_n > c->max_n)
     return fail(TLC_E_INVALID, "tlc_compress_batch: %zu values exceed the context's max_n %zu",
                 total_n, c->max_n);
-  std::vector<EncDesc> d;
-  std::vector<size_t> which;  // batch position of each launched tensor
-  d.reserve(count);
+  std::vector<EncDesc>& d = c->enc_host;
+  std::vector<size_t>& which = c->which;  // batch position of each launched tensor
+  d.clear();
+  which.clear();
   uint32_t blocks = 0, tiles = 0;
   for (size_t t = 0; t < count; ++t) {
     if (ns[t] == 0) continue;
@@ -610,7 +646,8 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   if (d.empty()) return TLC_OK;
   if (blocks > c->partials_cap || tiles > c->enc_status_words)
     return fail(TLC_E_INVALID, "tlc_compress_batch: batch exceeds the context's workspace");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
@@ -620,7 +657,8 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   });
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, &epoch);
+  st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, nullptr,
+                  &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_BATCH, [&] {
     return launch_quant_encode_batch(c->enc_descs, cnt, tiles, c->partials, c->enc_results,
@@ -689,10 +727,12 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
   st = check_stream("tlc_decompress", 0, bytes, bytes_len, scale, n, out, &skip);
   if (st || skip) return st;
   const size_t m = quartic_len(n);
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
+                  &c->ctrl->dec_bad_epoch, &epoch);
   if (st) return st;
   const uint32_t ntiles = (uint32_t)ceil_div(bytes_len, kZreTile);
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
@@ -726,7 +766,8 @@ TLC_API int tlc_decompress_ex(tlc_ctx* c, int mode, const uint8_t* bytes, size_t
                 bytes_len, n);
   if (n == 0) return TLC_OK;
   if (!bytes || !out) return fail(TLC_E_INVALID, "tlc_decompress_ex: NULL pointer");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   return timed_launch(c, TLC_KERNEL_INT8_DEQUANT, [&] {
     return launch_int8_dequant(bytes, n, scale, out, accumulate, c->stream);
@@ -745,8 +786,8 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
     return fail(TLC_E_INVALID, "tlc_decompress_batch: %zu streams exceed the context's %zu",
                 count, c->max_tensors);
   size_t total_n = 0;
-  std::vector<DecDesc> d;
-  d.reserve(count);
+  std::vector<DecDesc>& d = c->dec_host;
+  d.clear();
   uint32_t tiles = 0, ranges = 0;
   for (size_t t = 0; t < count; ++t) {
     if (ns[t] > c->max_n)
@@ -778,13 +819,15 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
   if (d.empty()) return TLC_OK;
   if (tiles > c->dec_status_words || ranges > c->start_words)
     return fail(TLC_E_INVALID, "tlc_decompress_batch: batch exceeds the context's workspace");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
+                  &c->ctrl->dec_bad_epoch, &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
@@ -815,8 +858,8 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
                 count, n, c->max_n);
   const size_t m = quartic_len(n);
   const uint32_t nranges = (uint32_t)ceil_div(m, kDecRange);
-  std::vector<DecDesc> d;
-  d.reserve(count);
+  std::vector<DecDesc>& d = c->dec_host;
+  d.clear();
   uint32_t tiles = 0;
   for (size_t t = 0; t < count; ++t) {
     bool skip = false;
@@ -838,13 +881,15 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
   if (d.empty()) return TLC_OK;
   if (tiles > c->dec_status_words || (size_t)count * nranges > c->start_words)
     return fail(TLC_E_INVALID, "tlc_decompress_sum: streams exceed the context's workspace");
-  st = ensure_device(c);
+  DeviceScope dev(c->device);
+  st = dev.status();
   if (st) return st;
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words, &epoch);
+  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
+                  &c->ctrl->dec_bad_epoch, &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
@@ -861,7 +906,8 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
 
 TLC_API int tlc_sync(tlc_ctx* c) {
   if (!c) return fail(TLC_E_INVALID, "tlc_sync: NULL context");
-  int st = ensure_device(c);
+  DeviceScope dev(c->device);
+  int st = dev.status();
   if (st) return st;
   st = sync_and_read(c);
   if (st) return st;
@@ -894,7 +940,8 @@ TLC_API int tlc_profile_mask(tlc_ctx* c, uint32_t mask) {
 TLC_API int tlc_profile_get(tlc_ctx* c, int kernel, double* total_ms, uint64_t* launches) {
   if (!c || !total_ms || !launches || kernel < 0 || kernel >= TLC_KERNEL_COUNT)
     return fail(TLC_E_INVALID, "tlc_profile_get: bad argument");
-  int st = ensure_device(c);
+  DeviceScope dev(c->device);
+  int st = dev.status();
   if (st) return st;
   hipError_t e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
@@ -906,7 +953,8 @@ TLC_API int tlc_profile_get(tlc_ctx* c, int kernel, double* total_ms, uint64_t* 
 
 TLC_API int tlc_profile_reset(tlc_ctx* c) {
   if (!c) return fail(TLC_E_INVALID, "tlc_profile_reset: NULL context");
-  int st = ensure_device(c);
+  DeviceScope dev(c->device);
+  int st = dev.status();
   if (st) return st;
   hipError_t e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
