@@ -174,6 +174,7 @@ int tlc_ref_compress(const float* x, float* r, size_t n, float s,
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M); /* Eq. 1 */
   if (st != TLC_REF_OK) {
+    memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
     free(acc);
     return st;
   }
@@ -266,6 +267,7 @@ int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t*
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M);
   if (st != TLC_REF_OK) {
+    memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
     free(acc);
     return st;
   }
@@ -361,6 +363,7 @@ int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* 
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M);
   if (st != TLC_REF_OK) {
+    if (r) memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
     free(acc);
     return st;
   }

@@ -75,7 +75,10 @@ int tlc_ref_zre_decode(const uint8_t* C, size_t c, uint8_t* Q, size_t m);
 
 /* Whole encoder.  x is read only, r is the error-accumulation buffer
  * (in/out), bytes receives *len bytes (cap must be >= ceil(n/5)), *scale
- * receives M.  On any error r and bytes are left unchanged and *len = 0. */
+ * receives M.  *len = 0 on any error.  Errors found before step 1 (bad
+ * arguments, capacity) leave r and bytes unchanged.  TLC_REF_E_NONFINITE
+ * comes after step 1, which accumulates x into the buffer itself (Section
+ * 3.1, Fig. 3): r then holds acc = x + r and the bytes are unchanged. */
 int tlc_ref_compress(const float* x, float* r, size_t n, float s,
                      uint8_t* bytes, size_t cap, size_t* len, float* scale);
 
@@ -116,7 +119,9 @@ float tlc_ref_int8_step(float M);
 void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float* resid);
 
 /* Encoder: acc = x + r when r != NULL (error feedback, r updated), else acc
- * = x.  bytes receives the n codes as two's-complement int8 (cap >= n). */
+ * = x.  bytes receives the n codes as two's-complement int8 (cap >= n).
+ * Errors as for tlc_ref_compress (on TLC_REF_E_NONFINITE a non-NULL r
+ * holds acc). */
 int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
                           size_t cap, size_t* len, float* scale);
 

@@ -88,7 +88,9 @@ def test_zero_empty_and_nonfinite():
     r = workloads.normal([963], 100, 1e-3)
     r0 = r.copy()
     st, C, M = oracle.compress_int8(x, r, 1.0)
-    assert st == oracle.E_NONFINITE and C.size == 0 and np.array_equal(r, r0)
+    # step 1 has added x into the buffer; no code is produced
+    assert st == oracle.E_NONFINITE and C.size == 0
+    assert np.array_equal(r.view(np.uint32), (x + r0).view(np.uint32))
     st, *_ = oracle.compress_int8(np.ones(4, F32), None, 2.0)
     assert st == oracle.E_INVALID
 

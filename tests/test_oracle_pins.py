@@ -324,19 +324,28 @@ def test_subnormal_inputs_and_scale():
     assert q.tolist() == [1, 0, -1, 0, 0]
 
 
-def test_nonfinite_is_rejected_and_leaves_state():
+def test_nonfinite_is_rejected_after_step_1():
+    """Step 1 (Section 3.1, Fig. 3) adds x into the buffer before Eq. 1 can
+    see the NaN/Inf: the buffer keeps that sum, no byte is produced."""
     for bad in (np.inf, -np.inf, np.nan):
-        x = workloads.normal([400], 100, 1.0)
-        x[37] = bad
-        r = workloads.normal([401], 100, 1.0)
-        r0 = r.copy()
-        st, C, M = oracle.compress(x, r, 1.0)
-        assert st == oracle.E_NONFINITE and C.size == 0
-        assert np.array_equal(bits(r), bits(r0))
-    # overflow of max * s
+        for enc in (oracle.compress, oracle.compress_nozre):
+            x = workloads.normal([400], 100, 1.0)
+            x[37] = bad
+            r = workloads.normal([401], 100, 1.0)
+            r0 = r.copy()
+            st, C, M = enc(x, r, 1.0)
+            assert st == oracle.E_NONFINITE and C.size == 0
+            assert np.array_equal(bits(r), bits(x + r0))
+    # overflow of max * s: every sum is finite and stays in the buffer
     x = np.array([3.0e38, 1.0], F32)
-    r = np.zeros(2, F32)
+    r = np.array([-0.0, 0.5], F32)
     assert oracle.compress(x, r, 1.5)[0] == oracle.E_NONFINITE
+    assert np.array_equal(bits(r), bits(np.array([3.0e38, 1.5], F32)))
+    # an error found before step 1 leaves the buffer alone
+    r = np.ones(2, F32)
+    assert oracle.compress(x, r, 2.0)[0] == oracle.E_INVALID
+    assert oracle.compress(x, r, 1.0, cap=0)[0] == oracle.E_CAPACITY
+    assert r.tolist() == [1.0, 1.0]
 
 
 def test_invalid_s_rejected():
