@@ -10,7 +10,7 @@ them, cycled), resident in HBM before timing starts.
 
 Prints ONE JSON line.  ``value`` is GB/s of fp32 input per step (4n bytes
 per round trip).  ``roofline`` is for the dominant kernel
-(tlc_quant_encode_kernel), timed with HIP events on the library's stream.
+(tlc_accum_absmax_kernel), timed with HIP events on the library's stream.
 """
 import argparse
 import hashlib
@@ -30,16 +30,19 @@ METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compress
 KERNEL_SRC = [os.path.join(ROOT, "paper_1802_07389_amd", "csrc", f)
               for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp",
                         "tlc_internal.h")]
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "tlc_quant_encode_kernel_c4_traffic.md")
+DOMINANT = "tlc_accum_absmax_kernel"  # the longest kernel of a step
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", DOMINANT + "_c4_traffic.md")
 
-# Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, all
-# fp32 tensors 4 B/value; the quartic bytes never leave LDS).
-def algorithmic_bytes(n, c):
+# Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, nnz =
+# values with q != 0, all fp32 tensors 4 B/value; the quartic bytes never
+# leave LDS).
+def algorithmic_bytes(n, c, nnz):
     tiles = -(-(-(-n // 5)) // 4096)  # 4096-byte quartic tiles
     return {
-        "tlc_absmax_kernel": 8 * n,                      # read x, r
-        # read x, r; write r, each tile's own stream bytes (c in all) and record
-        "tlc_quant_encode_kernel": 12 * n + c + 16 * tiles,
+        "tlc_accum_absmax_kernel": 12 * n,               # read x, r; write r = x + r
+        # read r; write r where q != 0, each tile's own stream bytes (c in all)
+        # and record
+        "tlc_quant_encode_kernel": 4 * n + 4 * nnz + c + 16 * tiles,
         # tile records in, tile prefixes and chunk summaries out
         "tlc_zre_chunk_kernel": 24 * tiles,
         # records, prefixes and slot bytes in, the stream out
@@ -59,7 +62,7 @@ def kernel_source_hash():
 
 
 def measured_traffic(n):
-    """HBM bytes per launch of tlc_quant_encode_kernel from the committed
+    """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 counter summary, if it was taken on the current kernel source."""
     if not os.path.exists(TRAFFIC_SUMMARY):
         return None
@@ -429,7 +432,7 @@ def main():
     stream = torch.cuda.current_stream(dev)
     ctx = tlc.Context(max_n=n, stream=stream, device=dev)
 
-    lens = []
+    lens, scales = [], []
 
     # One step: encode (synchronous: it returns the stream length), then the
     # asynchronous decode-accumulate.  Stream order makes step k's decode
@@ -439,6 +442,7 @@ def main():
         C, M = ctx.compress(xs[k % n_inputs], resid, s, out=payload)
         ctx.decompress(C, M, n, model, accumulate=True)
         lens.append(C.numel())
+        scales.append(M)
 
     for k in range(args.warmup):
         step(k)
@@ -447,8 +451,9 @@ def main():
 
     # Timed region: only the dominant kernel carries HIP events (each timed
     # launch adds an event pair to the stream, which costs device time).
-    dom = "tlc_quant_encode_kernel"
-    ctx.profile(True, kernels=[tlc.TLC_KERNEL_QUANT_ENCODE])
+    dom = DOMINANT
+    dom_id = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)].index(dom)
+    ctx.profile(True, kernels=[dom_id])
     ctx.profile_reset()
     lens.clear()
     torch.cuda.synchronize()
@@ -459,7 +464,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ctx.profile(False)
-    dom_ms_timed, dom_cnt = ctx.profile_get(tlc.TLC_KERNEL_QUANT_ENCODE)
+    dom_ms_timed, dom_cnt = ctx.profile_get(dom_id)
     dom_ms_timed /= max(dom_cnt, 1)
     timed_lens = list(lens)
 
@@ -476,17 +481,25 @@ def main():
         ms, cnt = ctx.profile_get(kid)
         kern[tlc.tlc_kernel_name(kid)] = (ms / cnt if cnt else 0.0, cnt)
 
+    # Values with q != 0 in the last step's stream: its decode into zeros is
+    # non-zero exactly there (M > 0).
+    probe = torch.zeros(n, dtype=torch.float32, device=dev)
+    ctx.decompress(payload[:lens[-1]], scales[-1], n, probe, accumulate=False)
+    ctx.sync()
+    nnz = int(torch.count_nonzero(probe).item())
+    del probe
+
     elapsed = t1 - t0
     ms_per_step = elapsed / args.steps * 1e3
     value = 4 * n * args.steps / elapsed / 1e9
     c_avg = float(np.mean(timed_lens))
-    algo = algorithmic_bytes(n, c_avg)
+    algo = algorithmic_bytes(n, c_avg, nnz)
 
     dom_ms = dom_ms_timed
     achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(n)
 
-    enc_k = ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_chunk_kernel",
+    enc_k = ["tlc_accum_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_chunk_kernel",
              "tlc_zre_compact_kernel"]
     dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
@@ -533,6 +546,7 @@ def main():
         "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
         "kernels_avg_ms_note": "every kernel timed over %d further steps after the timed "
                                "region; the roofline kernel is timed inside it" % kern_steps,
+        "nonzero_q_last_step": nnz,
         "compression_ratio": round(4 * n / (c_avg + 4), 2),
         "compression_ratio_payload_only": round(4 * n / c_avg, 2),
         "kernel_source_sha256_16": kernel_source_hash(),

@@ -112,6 +112,7 @@ int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
  *   n           value count of the encoded tensor, <= max_n.
  *   out         device fp32[n]: out = M*q (accumulate == 0) or
  *               out = out + M*q (accumulate != 0), every element written.
+ *               Must not overlap bytes (TLC_E_INVALID).
  * Asynchronous on the context's stream; returns only errors detectable on
  * the host.  If the stream does not expand to exactly ceil(n/5) bytes, out
  * is left unchanged and the next tlc_sync() returns TLC_E_CORRUPT. */

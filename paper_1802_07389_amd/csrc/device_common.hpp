@@ -151,11 +151,12 @@ __device__ __forceinline__ uint32_t quantize_one(float acc, float M, float U,
   return pos ? 2u : (neg ? 0u : 1u);
 }
 
-// Quartic byte j < m: quantizes the five elements j + k*m (contiguous
-// partitions, p0 most significant; elements past n are the zero padding of
-// Section 3.2, step 4), writes their residuals and returns the byte.
-__device__ __forceinline__ uint32_t quantize_byte(const float* __restrict__ x,
-                                                  float* __restrict__ r, uint64_t n,
+// Quartic byte j < m: quantizes the five accumulated values r[j + k*m]
+// (contiguous partitions, p0 most significant; elements past n are the zero
+// padding of Section 3.2, step 4) and returns the byte.  A value with q = 0
+// keeps acc as its residual, which the buffer already holds, so only q != 0
+// writes back.
+__device__ __forceinline__ uint32_t quantize_byte(float* __restrict__ r, uint64_t n,
                                                   uint64_t m, uint64_t j, float M, float U) {
   uint32_t code = 0u;
 #pragma unroll
@@ -164,41 +165,44 @@ __device__ __forceinline__ uint32_t quantize_byte(const float* __restrict__ x,
     uint32_t t = 0u;
     if (e < n) {
       float o;
-      t = quantize_one(x[e] + r[e], M, U, o);
-      r[e] = o;
+      t = quantize_one(r[e], M, U, o);
+      if (t != 1u) r[e] = o;
     }
     code = code * 3u + t;
   }
   return code;
 }
 
-// Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and 16-byte aligned x
-// and r, so every partition slice is one float4; returns the four bytes
-// packed little-endian.
-__device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
-                                                    float* __restrict__ r, uint64_t n,
+// Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and r 16-byte
+// aligned, so every partition slice is one float4; returns the four bytes
+// packed little-endian.  A slice is stored back only if one of its values
+// has q != 0.
+__device__ __forceinline__ uint32_t quantize_group4(float* __restrict__ r, uint64_t n,
                                                     uint64_t m, uint64_t j, float M,
                                                     float U) {
   if (4 * m + j + 4 > n) {  // the group that reaches into the padding of p4
     uint32_t w = 0u;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) w |= quantize_byte(x, r, n, m, j + c, M, U) << (8 * c);
+    for (int c = 0; c < 4; ++c) w |= quantize_byte(r, n, m, j + c, M, U) << (8 * c);
     return w;
   }
   uint32_t code[4] = {0u, 0u, 0u, 0u};
-  float4 a[5], b[5];
+  float4 a[5];
 #pragma unroll
-  for (int k = 0; k < 5; ++k) a[k] = ld_stream(x + k * m + j);  // x is not read again
-#pragma unroll
-  for (int k = 0; k < 5; ++k) b[k] = *reinterpret_cast<const float4*>(r + k * m + j);
+  for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(r + k * m + j);
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
     float4 o;
-    code[0] = code[0] * 3u + quantize_one(a[k].x + b[k].x, M, U, o.x);
-    code[1] = code[1] * 3u + quantize_one(a[k].y + b[k].y, M, U, o.y);
-    code[2] = code[2] * 3u + quantize_one(a[k].z + b[k].z, M, U, o.z);
-    code[3] = code[3] * 3u + quantize_one(a[k].w + b[k].w, M, U, o.w);
-    *reinterpret_cast<float4*>(r + k * m + j) = o;
+    const uint32_t t0 = quantize_one(a[k].x, M, U, o.x);
+    const uint32_t t1 = quantize_one(a[k].y, M, U, o.y);
+    const uint32_t t2 = quantize_one(a[k].z, M, U, o.z);
+    const uint32_t t3 = quantize_one(a[k].w, M, U, o.w);
+    code[0] = code[0] * 3u + t0;
+    code[1] = code[1] * 3u + t1;
+    code[2] = code[2] * 3u + t2;
+    code[3] = code[3] * 3u + t3;
+    if ((t0 ^ 1u) | (t1 ^ 1u) | (t2 ^ 1u) | (t3 ^ 1u))
+      *reinterpret_cast<float4*>(r + k * m + j) = o;
   }
   return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
 }

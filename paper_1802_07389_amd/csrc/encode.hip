@@ -1,12 +1,14 @@
 // encode.hip -- gfx950 encode kernels of the 3LC path.
 //
-//   tlc_absmax_kernel / _batch_kernel
-//       partial maxima of |tensor + residual|                          (Eq. 1)
+//   tlc_accum_absmax_kernel / _batch_kernel
+//       step 1 of error accumulation (the tensor is added into the buffer,
+//       in place) and partial maxima of the sums               (Section 3.1,
+//                                                               Fig. 3, Eq. 1)
 //   tlc_quant_encode_kernel, tlc_zre_chunk(_scan)_kernel, tlc_zre_compact_kernel
-//       one tensor: M, 3-value quantization, residual write-back, quartic
-//       pack and each tile's own zero-run encoding; then a scan of the tile
-//       summaries and the compaction into one stream
-//                                             (Eq. 1-2, Sections 3.2-3.3)
+//       one tensor: M, 3-value quantization of the buffer, residual
+//       write-back where q != 0, quartic pack and each tile's own zero-run
+//       encoding; then a scan of the tile summaries and the compaction into
+//       one stream                             (Eq. 1-2, Sections 3.2-3.3)
 //   tlc_quant_encode_chained_kernel, tlc_quant_encode_batch_kernel
 //       a small tensor, or many tensors, in one pass: tiles chained by
 //       decoupled look-back
@@ -22,13 +24,17 @@
 namespace tlc {
 
 // ---------------------------------------------------------------- Eq. 1
-// max |x + r| is taken on the bit patterns with the sign cleared: for
-// non-negative IEEE values integer order equals numeric order, so the u32
-// max is exact and independent of reduction order, and any NaN/Inf makes
-// the result >= 0x7f800000.  Block `blk` of `nblk` strides over [0, n).
+// Step 1 and Eq. 1 in one read of the tensor: with kResid the buffer
+// becomes acc = x + r (the quantizer then reads only the buffer and writes
+// back just the values with q != 0, whose residual differs from acc);
+// without, acc = x and nothing is written.  max |acc| is taken on the bit
+// patterns with the sign cleared: for non-negative IEEE values integer
+// order equals numeric order, so the u32 max is exact and independent of
+// reduction order, and any NaN/Inf makes the result >= 0x7f800000.  Block
+// `blk` of `nblk` strides over [0, n).
 template <bool kVec, bool kResid = true>
 __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
-                                                const float* __restrict__ r, uint64_t n,
+                                                float* __restrict__ r, uint64_t n,
                                                 uint32_t blk, uint32_t nblk) {
   uint32_t mx = 0;
   const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
@@ -42,34 +48,51 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       for (int u = 0; u < 4; ++u) a[u] = ld_stream(x + 4 * (i + u * stride));
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        b[u] = kResid ? ld_stream(r + 4 * (i + u * stride)) : make_float4(0, 0, 0, 0);
+        b[u] = kResid ? *reinterpret_cast<const float4*>(r + 4 * (i + u * stride))
+                      : make_float4(0, 0, 0, 0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        mx = max(mx, abs_bits(a[u].x + b[u].x));
-        mx = max(mx, abs_bits(a[u].y + b[u].y));
-        mx = max(mx, abs_bits(a[u].z + b[u].z));
-        mx = max(mx, abs_bits(a[u].w + b[u].w));
+        const float4 v = kResid ? make_float4(a[u].x + b[u].x, a[u].y + b[u].y,
+                                              a[u].z + b[u].z, a[u].w + b[u].w)
+                                : a[u];
+        if (kResid) *reinterpret_cast<float4*>(r + 4 * (i + u * stride)) = v;
+        mx = max(mx, abs_bits(v.x));
+        mx = max(mx, abs_bits(v.y));
+        mx = max(mx, abs_bits(v.z));
+        mx = max(mx, abs_bits(v.w));
       }
     }
     for (; i < nv; i += stride) {
-      float4 a = ld_stream(x + 4 * i), b = kResid ? ld_stream(r + 4 * i) : make_float4(0, 0, 0, 0);
-      mx = max(mx, abs_bits(a.x + b.x));
-      mx = max(mx, abs_bits(a.y + b.y));
-      mx = max(mx, abs_bits(a.z + b.z));
-      mx = max(mx, abs_bits(a.w + b.w));
+      const float4 a = ld_stream(x + 4 * i);
+      float4 v = a;
+      if (kResid) {
+        const float4 b = *reinterpret_cast<const float4*>(r + 4 * i);
+        v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+        *reinterpret_cast<float4*>(r + 4 * i) = v;
+      }
+      mx = max(mx, abs_bits(v.x));
+      mx = max(mx, abs_bits(v.y));
+      mx = max(mx, abs_bits(v.z));
+      mx = max(mx, abs_bits(v.w));
     }
-    for (uint64_t e = (nv << 2) + tid; e < n; e += stride)
-      mx = max(mx, abs_bits(kResid ? x[e] + r[e] : x[e]));
+    for (uint64_t e = (nv << 2) + tid; e < n; e += stride) {
+      const float v = kResid ? x[e] + r[e] : x[e];
+      if (kResid) r[e] = v;
+      mx = max(mx, abs_bits(v));
+    }
   } else {
-    for (uint64_t e = tid; e < n; e += stride)
-      mx = max(mx, abs_bits(kResid ? x[e] + r[e] : x[e]));
+    for (uint64_t e = tid; e < n; e += stride) {
+      const float v = kResid ? x[e] + r[e] : x[e];
+      if (kResid) r[e] = v;
+      mx = max(mx, abs_bits(v));
+    }
   }
   return mx;
 }
 
 template <bool kVec, bool kResid>
-__global__ __launch_bounds__(kThreads) void tlc_absmax_kernel(
-    const float* __restrict__ x, const float* __restrict__ r, uint64_t n,
+__global__ __launch_bounds__(kThreads) void tlc_accum_absmax_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n,
     uint32_t* __restrict__ partials) {
   __shared__ uint32_t lds[kWaves];
   const uint32_t mx =
@@ -77,14 +100,14 @@ __global__ __launch_bounds__(kThreads) void tlc_absmax_kernel(
   if (threadIdx.x == 0) partials[blockIdx.x] = mx;
 }
 
-__global__ __launch_bounds__(kThreads) void tlc_absmax_batch_kernel(
+__global__ __launch_bounds__(kThreads) void tlc_accum_absmax_batch_kernel(
     const EncDesc* __restrict__ descs, uint32_t count, uint32_t* __restrict__ partials) {
   __shared__ uint32_t lds[kWaves];
   const uint32_t t =
       find_desc(descs, count, blockIdx.x, [](const EncDesc& d) { return d.blk0; });
   const EncDesc& d = descs[t];
   const uint32_t blk = blockIdx.x - d.blk0;
-  const uint32_t mx = (d.vec & 2u) ? absmax_part<true>(d.x, d.r, d.n, blk, d.nblk)
+  const uint32_t mx = (d.vec & 4u) ? absmax_part<true>(d.x, d.r, d.n, blk, d.nblk)
                                    : absmax_part<false>(d.x, d.r, d.n, blk, d.nblk);
   const uint32_t bm = block_max(mx, lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = bm;
@@ -92,17 +115,17 @@ __global__ __launch_bounds__(kThreads) void tlc_absmax_batch_kernel(
 
 // ---------------------------------------------------------------- Eq. 2, 3.2
 // Phase 1 of a tile (quartic bytes [q0, q0 + T), T <= kEncTile) when
-// m % 4 != 0 but x and r are 16-byte aligned.  Partition k of the tile
+// m % 4 != 0 but the buffer r is 16-byte aligned.  Partition k of the tile
 // starts a = (k*m + q0) mod 4 values past a float4 boundary, so the block
 // sweeps it in aligned float4 cells: cell f holds the values of tile bytes
 // 4f - a .. 4f + 3 - a.  A cell shared with a neighbouring tile or
 // partition, or reaching past n, is read and written value by value, so
-// every value's residual has one writer.  Partition 0 (a = 0, as q0 is a
+// every value's residual has one writer (and only values with q != 0 are
+// written).  Partition 0 (a = 0, as q0 is a
 // multiple of 4) stores the bytes; partitions 1-4 add their weighted trits
 // with LDS atomics on the two words a cell straddles: a byte's total stays
 // below 243, so no carry crosses into the next byte.
-__device__ __forceinline__ void quantize_tile_shifted(const float* __restrict__ x,
-                                                      float* __restrict__ r, uint64_t n,
+__device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uint64_t n,
                                                       uint64_t m, uint64_t q0, uint32_t T,
                                                       float M, float U, uint32_t* qw) {
   constexpr int kCells = (kEncTile + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
@@ -113,17 +136,14 @@ __device__ __forceinline__ void quantize_tile_shifted(const float* __restrict__ 
     const uint64_t e0 = base - a;  // first value of cell 0
     const uint32_t nf = (T + a + 3u) >> 2;
     const uint32_t w = trit_weight(k);
-    float4 xa[kCells], ra[kCells];
+    float4 ra[kCells];
     bool full[kCells];
 #pragma unroll
     for (int i = 0; i < kCells; ++i) {
       const uint32_t f = threadIdx.x + kThreads * i;
       const uint64_t e = e0 + 4ull * f;
       full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= T + a && e + 4u <= n;
-      if (full[i]) {
-        xa[i] = *reinterpret_cast<const float4*>(x + e);
-        ra[i] = *reinterpret_cast<const float4*>(r + e);
-      }
+      if (full[i]) ra[i] = *reinterpret_cast<const float4*>(r + e);
     }
 #pragma unroll
     for (int i = 0; i < kCells; ++i) {
@@ -133,19 +153,20 @@ __device__ __forceinline__ void quantize_tile_shifted(const float* __restrict__ 
       uint32_t t[4] = {0u, 0u, 0u, 0u};  // padding and other tiles' values add nothing
       if (full[i]) {
         float4 o;
-        t[0] = quantize_one(xa[i].x + ra[i].x, M, U, o.x);
-        t[1] = quantize_one(xa[i].y + ra[i].y, M, U, o.y);
-        t[2] = quantize_one(xa[i].z + ra[i].z, M, U, o.z);
-        t[3] = quantize_one(xa[i].w + ra[i].w, M, U, o.w);
-        *reinterpret_cast<float4*>(r + e) = o;
+        t[0] = quantize_one(ra[i].x, M, U, o.x);
+        t[1] = quantize_one(ra[i].y, M, U, o.y);
+        t[2] = quantize_one(ra[i].z, M, U, o.z);
+        t[3] = quantize_one(ra[i].w, M, U, o.w);
+        if ((t[0] ^ 1u) | (t[1] ^ 1u) | (t[2] ^ 1u) | (t[3] ^ 1u))
+          *reinterpret_cast<float4*>(r + e) = o;
       } else {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const uint32_t p = 4u * f + c;  // position in the partition's cell grid
           if (p >= a && p - a < T && e + c < n) {
             float o;
-            t[c] = quantize_one(x[e + c] + r[e + c], M, U, o);
-            r[e + c] = o;
+            t[c] = quantize_one(r[e + c], M, U, o);
+            if (t[c] != 1u) r[e + c] = o;
           }
         }
       }
@@ -180,26 +201,26 @@ struct EncShared {
   __align__(16) uint8_t out[kEncTile + 16];
 };
 
-// Phase 1 of a tile (Eq. 1-2, residual write-back, quartic pack): the block
-// quantizes the 5 * tile_bytes values of quartic bytes [q0, q0 + tile_bytes)
-// and leaves the bytes in q (LDS).  kPath: threads take groups of 4 bytes,
+// Phase 1 of a tile (Eq. 2, residual write-back, quartic pack): the block
+// quantizes the 5 * tile_bytes accumulated values of quartic bytes
+// [q0, q0 + tile_bytes), held in the buffer r, and leaves the bytes in q
+// (LDS).  kPath: threads take groups of 4 bytes,
 // aligned float4 cells of one partition at a time, or single bytes,
 // interleaved so every load and store instruction is coalesced.  Ends with
 // a barrier.
 template <int kPath>
-__device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float* __restrict__ r,
-                                              uint64_t n, uint32_t m, const Scale& sc,
-                                              uint64_t q0, uint32_t tile_bytes, uint8_t* q) {
+__device__ __forceinline__ void quantize_tile(float* __restrict__ r, uint64_t n, uint32_t m,
+                                              const Scale& sc, uint64_t q0,
+                                              uint32_t tile_bytes, uint8_t* q) {
   if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
     for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
       *reinterpret_cast<uint32_t*>(q + g * 4u) =
-          quantize_group4(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+          quantize_group4(r, n, m, q0 + g * 4u, sc.M, sc.U);
   } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
-    quantize_tile_shifted(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
-                          reinterpret_cast<uint32_t*>(q));
+    quantize_tile_shifted(r, n, m, q0, tile_bytes, sc.M, sc.U, reinterpret_cast<uint32_t*>(q));
   } else {  // 1 byte per thread: dword accesses, still contiguous per wave
     for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
-      q[lj] = (uint8_t)quantize_byte(x, r, n, m, q0 + lj, sc.M, sc.U);
+      q[lj] = (uint8_t)quantize_byte(r, n, m, q0 + lj, sc.M, sc.U);
   }
   __syncthreads();
 }
@@ -213,8 +234,7 @@ __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float
 // block then copies the tile's output into the stream.  The last tile
 // stores the stream length in res->len.
 template <int kPath>
-__device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* __restrict__ r,
-                                            uint64_t n, uint32_t m, const Scale& sc,
+__device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, uint32_t m, const Scale& sc,
                                             uint32_t lt, uint32_t floor,
                                             uint8_t* __restrict__ out,
                                             uint64_t* __restrict__ status, uint32_t epoch,
@@ -226,7 +246,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  quantize_tile<kPath>(x, r, n, m, sc, q0, tile_bytes, sh.q);
+  quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- phase 2: Section 3.3
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
@@ -352,7 +372,7 @@ __device__ __forceinline__ uint32_t block_min(uint32_t v, uint32_t* lds) {
 template <int kPath>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5)))
 void tlc_quant_encode_kernel(
-    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ slots,
     TileRec* __restrict__ recs, Ctrl* __restrict__ ctrl) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
@@ -364,10 +384,10 @@ void tlc_quant_encode_kernel(
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
-  if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
+  if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  quantize_tile<kPath>(x, r, n, m, sc, q0, tile_bytes, sh.q);
+  quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- Section 3.3 from the tile's first non-121 byte (index L) on
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
@@ -563,7 +583,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
 // look-back rarely waits, and this saves the two small passes' launches.
 template <int kPath>
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
-    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
     Ctrl* __restrict__ ctrl) {
@@ -576,8 +596,8 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
-  if (sc.bad) return;  // NaN/Inf or overflow: residual and stream untouched
-  encode_tile<kPath>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+  if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
+  encode_tile<kPath>(r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
@@ -600,22 +620,23 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
   }
   if (sc.bad) return;  // this tensor is refused; the others go on
   if (d.vec & 1u)
-    encode_tile<kPathVec>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+    encode_tile<kPathVec>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
                           &results[t], sh);
   else if (d.vec & 2u)
-    encode_tile<kPathShift>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+    encode_tile<kPathShift>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
                             &results[t], sh);
   else
-    encode_tile<kPathByte>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+    encode_tile<kPathByte>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
                            &results[t], sh);
 }
 
 // ---------------------------------------------------------------- comparison modes
 // Quantization + quartic pack without zero-run encoding: the quartic bytes
 // are the payload (m bytes), so tiles are independent and need no
-// look-back.  kStoch selects stochastic 3-value quantization with Philox
-// random words (no error feedback: r is not read or written); otherwise
-// Eq. 2 with the residual write-back, exactly as in tlc_quant_encode_kernel.
+// look-back.  kStoch selects stochastic 3-value quantization of x with
+// Philox random words (no error feedback: r is not read or written);
+// otherwise Eq. 2 on the accumulated buffer r with the residual write-back,
+// exactly as in tlc_quant_encode_kernel (x is not read).
 template <bool kVec, bool kStoch>
 __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
@@ -636,7 +657,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
       const uint64_t j = q0 + g * 4u;
       uint32_t w;
       if (!kStoch) {
-        w = quantize_group4(x, r, n, m, j, sc.M, sc.U);
+        w = quantize_group4(r, n, m, j, sc.M, sc.U);
       } else {
         uint32_t code[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -666,7 +687,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
       const uint64_t j = q0 + lj;
       uint32_t code;
       if (!kStoch) {
-        code = quantize_byte(x, r, n, m, j, sc.M, sc.U);
+        code = quantize_byte(r, n, m, j, sc.M, sc.U);
       } else {
         code = 0u;
 #pragma unroll
@@ -687,8 +708,8 @@ static inline bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
 }
 
-hipError_t launch_absmax(const float* x, const float* r, uint64_t n, uint32_t* partials,
-                         uint32_t* nblocks, hipStream_t st) {
+hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* partials,
+                               uint32_t* nblocks, hipStream_t st) {
   const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
   const uint64_t items = vec ? (n >> 2) : n;
   uint64_t blocks = (items + kThreads * 4 - 1) / (kThreads * 4);
@@ -696,48 +717,51 @@ hipError_t launch_absmax(const float* x, const float* r, uint64_t n, uint32_t* p
   *nblocks = (uint32_t)blocks;
   if (r == nullptr) {  // no error buffer: max |x|
     if (aligned16(x))
-      tlc_absmax_kernel<true, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+      tlc_accum_absmax_kernel<true, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
+                                                                                  partials);
     else
-      tlc_absmax_kernel<false, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+      tlc_accum_absmax_kernel<false, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
+                                                                                   partials);
   } else if (vec) {
-    tlc_absmax_kernel<true, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+    tlc_accum_absmax_kernel<true, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
   } else {
-    tlc_absmax_kernel<false, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+    tlc_accum_absmax_kernel<false, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
+                                                                                partials);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
+hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, Ctrl* ctrl, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
-  const bool al = aligned16(x) && aligned16(r);
+  const bool al = aligned16(r);
   if (al && m % 4 == 0)
-    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(x, r, n, m, s, partials,
+    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(r, n, m, s, partials,
                                                                    npartials, slots, recs, ctrl);
   else if (al)
     tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, slots, recs, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, ctrl);
   else
     tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, slots, recs, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, ctrl);
   return hipGetLastError();
 }
 
-hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m, float s,
+hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
                                        const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                        uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                                        uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  const bool al = aligned16(x) && aligned16(r);
+  const bool al = aligned16(r);
   if (al && m % 4 == 0)
     tlc_quant_encode_chained_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   else if (al)
     tlc_quant_encode_chained_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   else
     tlc_quant_encode_chained_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
 
@@ -761,9 +785,9 @@ hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
   return hipGetLastError();
 }
 
-hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
-                               uint32_t* partials, hipStream_t st) {
-  tlc_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
+hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_blocks, uint32_t* partials, hipStream_t st) {
+  tlc_accum_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
   return hipGetLastError();
 }
 
@@ -786,8 +810,7 @@ hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, f
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
                              Ctrl* ctrl, hipStream_t st) {
   const uint32_t blocks = (uint32_t)((m + kEncTile - 1) / kEncTile);
-  const bool al = aligned16(x) && (stochastic || aligned16(r));
-  const bool vec = (m % 4 == 0) && al;
+  const bool vec = (m % 4 == 0) && aligned16(stochastic ? x : r);
 #define TLC_LAUNCH(V, S)                                                                      \
   tlc_quant_pack_kernel<V, S><<<blocks, kThreads, 0, st>>>(x, r, n, m, s, seed, step, partials, \
                                                            npartials, out, ctrl)

@@ -4,7 +4,9 @@
 //
 //   tlc_int8_quant_kernel    code = rint(acc / D) clamped to [-127, 127]
 //                            (0 when D == 0), residual acc - code * D,
-//                            one int8 byte per value
+//                            one int8 byte per value; acc is the buffer
+//                            that tlc_accum_absmax_kernel has accumulated
+//                            (error feedback) or the tensor itself
 //   tlc_int8_dequant_kernel  out = code * D, or out + code * D
 //
 // Both are elementwise streams: a block covers kI8Rows rows of 1024 values;
@@ -42,15 +44,15 @@ __device__ __forceinline__ float int8_value(uint32_t byte, float D) {
 
 // One value: code byte and (kResid) residual acc - fl(code * D).
 template <bool kResid>
-__device__ __forceinline__ uint32_t int8_one(float x, float r, float D, float& res) {
-  const float acc = kResid ? __fadd_rn(x, r) : x;
+__device__ __forceinline__ uint32_t int8_one(float acc, float D, float& res) {
   const float code = int8_code(acc, D);
   if (kResid) res = __fsub_rn(acc, __fmul_rn(code, D));
   return int8_byte(code);
 }
 
-// kVec: x (and r) 16-byte aligned, out 4-byte aligned.  kResid: error
-// feedback (acc = x + r, r rewritten); otherwise acc = x and r is unused.
+// kVec: the values read (r or x) 16-byte aligned, out 4-byte aligned.
+// kResid: error feedback, acc = r (already x + r) and r is rewritten, x is
+// unused; otherwise acc = x and r is unused.
 template <bool kVec, bool kResid>
 __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n, float s,
@@ -63,33 +65,30 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
     ctrl->enc.scale = sc.M;
     ctrl->enc.len = sc.bad ? 0u : (uint32_t)n;
   }
-  if (sc.bad) return;  // NaN/Inf or overflow: residual and bytes untouched
+  if (sc.bad) return;  // NaN/Inf or overflow: no bytes, the buffer keeps acc
   const float D = int8_step(sc.M);
   const uint64_t base = (uint64_t)blockIdx.x * kI8Row * kI8Rows;
+  const float* __restrict__ src = kResid ? r : x;
   if (kVec) {
 #pragma unroll 1
     for (int h = 0; h < kI8Rows; h += kI8Batch) {
-      float4 xa[kI8Batch], ra[kI8Batch];
+      float4 a[kI8Batch];
       bool full[kI8Batch];
 #pragma unroll
       for (int i = 0; i < kI8Batch; ++i) {
         const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
         full[i] = e + 4u <= n;
-        if (full[i]) {
-          xa[i] = ld_stream(x + e);
-          if (kResid) ra[i] = ld_stream(r + e);
-        }
+        if (full[i]) a[i] = ld_stream(src + e);
       }
 #pragma unroll
       for (int i = 0; i < kI8Batch; ++i) {
         const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
         if (full[i]) {
           float4 o;
-          const float4 rr = kResid ? ra[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-          const uint32_t w = int8_one<kResid>(xa[i].x, rr.x, D, o.x) |
-                             int8_one<kResid>(xa[i].y, rr.y, D, o.y) << 8 |
-                             int8_one<kResid>(xa[i].z, rr.z, D, o.z) << 16 |
-                             int8_one<kResid>(xa[i].w, rr.w, D, o.w) << 24;
+          const uint32_t w = int8_one<kResid>(a[i].x, D, o.x) |
+                             int8_one<kResid>(a[i].y, D, o.y) << 8 |
+                             int8_one<kResid>(a[i].z, D, o.z) << 16 |
+                             int8_one<kResid>(a[i].w, D, o.w) << 24;
           if (kResid) st_stream(r + e, o);
           *reinterpret_cast<uint32_t*>(out + e) = w;
         } else {
@@ -97,7 +96,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
           for (int c = 0; c < 4; ++c) {
             if (e + c < n) {
               float o = 0.0f;
-              out[e + c] = (uint8_t)int8_one<kResid>(x[e + c], kResid ? r[e + c] : 0.0f, D, o);
+              out[e + c] = (uint8_t)int8_one<kResid>(src[e + c], D, o);
               if (kResid) r[e + c] = o;
             }
           }
@@ -109,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_quant_kernel(
       const uint64_t e = base + k;
       if (e >= n) break;
       float o = 0.0f;
-      out[e] = (uint8_t)int8_one<kResid>(x[e], kResid ? r[e] : 0.0f, D, o);
+      out[e] = (uint8_t)int8_one<kResid>(src[e], D, o);
       if (kResid) r[e] = o;
     }
   }
@@ -186,7 +185,8 @@ hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
                              Ctrl* ctrl, hipStream_t st) {
   const uint32_t blocks = int8_blocks(n);
-  const bool vec = aligned(x, 16) && (r == nullptr || aligned(r, 16)) && aligned(out, 4);
+  const bool vec = aligned(r ? r : x, 16) && aligned(out, 4);
+  if (r) x = nullptr;  // the buffer already holds x + r
 #define TLC_LAUNCH(V, R)                                                                 \
   tlc_int8_quant_kernel<V, R><<<blocks, kThreads, 0, st>>>(x, r, n, s, partials, npartials, \
                                                            out, ctrl)

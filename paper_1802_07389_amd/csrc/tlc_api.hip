@@ -47,13 +47,13 @@ bool overlap(const void* a, size_t an, const void* b, size_t bn) {
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0u; }
 
 const char* const kKernelNames[TLC_KERNEL_COUNT] = {
-    "tlc_absmax_kernel",           "tlc_quant_encode_kernel",
-    "tlc_zre_index_kernel",        "tlc_expand_dequant_kernel",
-    "tlc_absmax_batch_kernel",     "tlc_quant_encode_batch_kernel",
-    "tlc_zre_index_batch_kernel",  "tlc_expand_dequant_batch_kernel",
-    "tlc_expand_sum_kernel",       "tlc_quant_pack_kernel",
-    "tlc_int8_quant_kernel",       "tlc_int8_dequant_kernel",
-    "tlc_zre_chunk_kernel",        "tlc_zre_compact_kernel",
+    "tlc_accum_absmax_kernel",       "tlc_quant_encode_kernel",
+    "tlc_zre_index_kernel",          "tlc_expand_dequant_kernel",
+    "tlc_accum_absmax_batch_kernel", "tlc_quant_encode_batch_kernel",
+    "tlc_zre_index_batch_kernel",    "tlc_expand_dequant_batch_kernel",
+    "tlc_expand_sum_kernel",         "tlc_quant_pack_kernel",
+    "tlc_int8_quant_kernel",         "tlc_int8_dequant_kernel",
+    "tlc_zre_chunk_kernel",          "tlc_zre_compact_kernel",
     "tlc_quant_encode_chained_kernel"};
 
 struct PendingTiming {
@@ -444,7 +444,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
 
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
   const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
@@ -454,8 +454,8 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
                   &epoch);
     if (st) return st;
     st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_CHAINED, [&] {
-      return launch_quant_encode_chained(tensor, residual, n, (uint32_t)m, s, c->partials, np,
-                                         bytes, c->enc_status, ntiles, c->enc_ticket_base, epoch,
+      return launch_quant_encode_chained(residual, n, (uint32_t)m, s, c->partials, np, bytes,
+                                         c->enc_status, ntiles, c->enc_ticket_base, epoch,
                                          c->ctrl, c->stream);
     });
     if (st) return st;
@@ -463,8 +463,8 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     return finish_compress(c, "tlc_compress", bytes_len, scale);
   }
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
-    return launch_quant_encode(tensor, residual, n, (uint32_t)m, s, c->partials, np, c->slots,
-                               c->recs, c->ctrl, c->stream);
+    return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
+                               c->ctrl, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
@@ -505,7 +505,7 @@ int compress_int8(tlc_ctx* c, const float* tensor, float* residual, size_t n, fl
   if (st) return st;
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_absmax(tensor, residual, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, residual, n, c->partials, &np, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_INT8_QUANT, [&] {
@@ -561,7 +561,7 @@ TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* re
   float* r = stoch ? nullptr : residual;  // the stochastic mode has no error feedback
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_absmax(tensor, r, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, r, n, c->partials, &np, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_PACK, [&] {
@@ -635,9 +635,10 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
     e.s = s[t];
     e.tile0 = tiles;
     e.blk0 = blocks;
-    const bool al = aligned16(tensors[t]) && aligned16(residuals[t]);
+    const bool ral = aligned16(residuals[t]);
+    const bool al = ral && aligned16(tensors[t]);
     e.nblk = batch_absmax_blocks(al ? ns[t] / 4 : ns[t]);
-    e.vec = ((e.m % 4 == 0 && al) ? 1u : 0u) | (al ? 2u : 0u);
+    e.vec = ((e.m % 4 == 0 && ral) ? 1u : 0u) | (ral ? 2u : 0u) | (al ? 4u : 0u);
     blocks += e.nblk;
     tiles += (uint32_t)ceil_div(e.m, kEncTile);
     d.push_back(e);
@@ -653,7 +654,7 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ABSMAX_BATCH, [&] {
-    return launch_absmax_batch(c->enc_descs, cnt, blocks, c->partials, c->stream);
+    return launch_accum_absmax_batch(c->enc_descs, cnt, blocks, c->partials, c->stream);
   });
   if (st) return st;
   uint32_t epoch = 0;
@@ -711,6 +712,8 @@ int check_stream(const char* fn, size_t t, const uint8_t* bytes, size_t len, flo
   if (len == 0 || len > quartic_len(n))
     return fail(TLC_E_CORRUPT, "%s: stream %zu: length %zu impossible for n = %zu", fn, t, len,
                 n);
+  if (overlap(bytes, len, out, n * 4))
+    return fail(TLC_E_INVALID, "%s: stream %zu: bytes overlap the output", fn, t);
   return TLC_OK;
 }
 
@@ -766,6 +769,8 @@ TLC_API int tlc_decompress_ex(tlc_ctx* c, int mode, const uint8_t* bytes, size_t
                 bytes_len, n);
   if (n == 0) return TLC_OK;
   if (!bytes || !out) return fail(TLC_E_INVALID, "tlc_decompress_ex: NULL pointer");
+  if (overlap(bytes, n, out, n * 4))
+    return fail(TLC_E_INVALID, "tlc_decompress_ex: bytes overlap the output");
   DeviceScope dev(c->device);
   st = dev.status();
   if (st) return st;

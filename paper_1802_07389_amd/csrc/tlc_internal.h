@@ -58,7 +58,8 @@ struct EncDesc {
   uint32_t tile0;  // first encoder tile (global tile numbering of the launch)
   uint32_t blk0;   // first absmax block / partial maximum of this tensor
   uint32_t nblk;   // absmax blocks of this tensor
-  uint32_t vec;    // bit 0: m % 4 == 0 and x, r 16-byte aligned; bit 1: x, r aligned
+  uint32_t vec;    // bit 0: m % 4 == 0 and r 16-byte aligned; bit 1: r aligned;
+                   // bit 2: x and r aligned (float4 accumulation)
   uint32_t pad[2];
 };
 static_assert(sizeof(EncDesc) == 64, "EncDesc is 64 bytes");
@@ -91,12 +92,12 @@ static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
 
 // Launchers (encode.hip, decode.hip, int8.hip).  All return the hipError_t of the
 // launch.
-hipError_t launch_absmax(const float* x, const float* r, uint64_t n,
-                         uint32_t* partials, uint32_t* nblocks, hipStream_t st);
-hipError_t launch_quant_encode(const float* x, float* r, uint64_t n, uint32_t m, float s,
+hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
+                               uint32_t* partials, uint32_t* nblocks, hipStream_t st);
+hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, Ctrl* ctrl, hipStream_t st);
-hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m, float s,
+hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
                                        const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                        uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                                        uint32_t epoch, Ctrl* ctrl, hipStream_t st);
@@ -114,8 +115,8 @@ hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
                              Ctrl* ctrl, hipStream_t st);
 hipError_t launch_int8_dequant(const uint8_t* C, uint64_t n, float M, float* out,
                                int accumulate, hipStream_t st);
-hipError_t launch_absmax_batch(const EncDesc* descs, uint32_t count, uint32_t total_blocks,
-                               uint32_t* partials, hipStream_t st);
+hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_blocks, uint32_t* partials, hipStream_t st);
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
                                      EncResult* results, uint64_t* status,

@@ -33,11 +33,12 @@ def to_dev(a, offset=0):
     return view
 
 
-def gpu_compress(ctx, x, r, s, offset=0):
-    """Return (status, bytes np.uint8, scale, residual np.float32)."""
+def gpu_compress(ctx, x, r, s, offset=0, r_offset=None):
+    """Return (status, bytes np.uint8, scale, residual np.float32).  The
+    residual sits r_offset elements into its buffer (default: offset)."""
     n = x.size
     xd = to_dev(x, offset)
-    rd = to_dev(r, offset)
+    rd = to_dev(r, offset if r_offset is None else r_offset)
     cap = max(tlc.tlc_max_compressed_bytes(n), 1)
     out = torch.full((cap,), 0xAB, dtype=torch.uint8, device="cuda")
     st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr() if n else None,

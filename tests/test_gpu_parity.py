@@ -192,6 +192,23 @@ def test_unaligned_pointers(ctx, offset):
                         offset=offset, tag=f"offset {offset}")
 
 
+@pytest.mark.parametrize("n", [5 * 4096 * 3 + 20, 5 * 4096 * 3 + 7, THREE_PASS_N[0],
+                               THREE_PASS_N[2]])
+@pytest.mark.parametrize("x_off,r_off", [(1, 0), (0, 3)])
+def test_mixed_alignment(ctx, n, x_off, r_off):
+    """Only one of tensor and residual 16-byte aligned: the accumulation
+    takes its scalar loop, the quantizer the path the buffer allows."""
+    g = G()
+    x = workloads.normal([43, n, x_off], n)
+    r = workloads.normal([44, n, r_off], n, 1e-4)
+    r_ref = r.copy()
+    st_ref, C_ref, M_ref = oracle.compress(x, r_ref, 1.5)
+    st, C, M, r_gpu = g.gpu_compress(ctx, x, r, 1.5, offset=x_off, r_offset=r_off)
+    assert st == st_ref == 0 and M == M_ref
+    assert np.array_equal(C, C_ref)
+    assert np.array_equal(g.bits(r_gpu), g.bits(r_ref))
+
+
 def test_threshold_boundaries(ctx):
     """Values on both sides of the q = +-1 decision (M/2 and its rounding)."""
     for M_target in [1.0, 3.0, 1.2345678, 7.1e-39, 3 * 2.0 ** -140, 1.0e30]:
@@ -225,25 +242,34 @@ def test_negative_zero_accumulate(ctx):
 
 
 # ------------------------------------------------------------------ error paths
-def test_nonfinite_leaves_residual_and_bytes(ctx):
+def test_nonfinite_keeps_sum_and_no_bytes(ctx):
+    """NaN/Inf: no byte is written and the buffer holds the step-1 sum x + r,
+    as in the oracle.  Both the chained (small) and three-pass (large)
+    encoders."""
     import torch
     from paper_1802_07389_amd import tlc
-    n = 100_000
-    for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
-        x = workloads.normal([70, pos], n)
-        x[pos] = bad
-        r = workloads.normal([71, pos], n)
-        xd, rd = torch.from_numpy(x).cuda(), torch.from_numpy(r).cuda()
-        out = torch.full((n // 5 + 1,), 7, dtype=torch.uint8, device="cuda")
-        st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, 1.0,
-                                      out.data_ptr(), out.numel())
-        assert st == tlc.TLC_E_NONFINITE and ln == 0
-        assert np.array_equal(G().bits(rd.cpu().numpy()), G().bits(r))
-        assert bool((out == 7).all())
-    # overflow of max * s
+    for n in (100_000, THREE_PASS_N[0]):
+        for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
+            x = workloads.normal([70, pos], n)
+            x[pos] = bad
+            r = workloads.normal([71, pos], n)
+            r_ref = r.copy()
+            st_ref, _, _ = oracle.compress(x, r_ref, 1.0)
+            xd, rd = torch.from_numpy(x).cuda(), torch.from_numpy(r).cuda()
+            out = torch.full((n // 5 + 1,), 7, dtype=torch.uint8, device="cuda")
+            st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, 1.0,
+                                          out.data_ptr(), out.numel())
+            assert st == st_ref == tlc.TLC_E_NONFINITE and ln == 0
+            assert np.array_equal(G().bits(rd.cpu().numpy()), G().bits(r_ref))
+            assert bool((out == 7).all())
+    # overflow of max * s: the finite sums stay in the buffer
     x = np.array([3.0e38, 1.0, 2.0, 3.0, 4.0], F32)
-    st, *_ = G().gpu_compress(ctx, x, np.zeros(5, F32), 1.5)
+    r0 = np.array([-0.0, 0.5, 0.0, -1.0, 2.0], F32)
+    r_ref = r0.copy()
+    assert oracle.compress(x, r_ref, 1.5)[0] == oracle.E_NONFINITE
+    st, _, _, r_gpu = G().gpu_compress(ctx, x, r0.copy(), 1.5)
     assert st == tlc.TLC_E_NONFINITE
+    assert np.array_equal(G().bits(r_gpu), G().bits(r_ref))
     # the context still works afterwards
     check_encode_decode(ctx, workloads.normal([72], 1000), np.zeros(1000, F32), 1.0)
 
@@ -272,6 +298,16 @@ def test_invalid_arguments(ctx):
                               xd.data_ptr(), 0) == tlc.TLC_E_CORRUPT
     assert tlc.tlc_decompress(ctx.handle, out.data_ptr(), 0, 1.0, n,
                               xd.data_ptr(), 0) == tlc.TLC_E_CORRUPT
+    # a stream that lies inside its own output is refused before any launch
+    inside = xd.data_ptr() + 4 * (n - 10)
+    assert tlc.tlc_decompress(ctx.handle, inside, 40, 1.0, n,
+                              xd.data_ptr(), 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress_ex(ctx.handle, tlc.TLC_MODE_INT8, xd.data_ptr(), n, 1.0, n,
+                                 xd.data_ptr(), 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress_batch(ctx.handle, [inside], [40], [1.0], [n],
+                                    [xd.data_ptr()], 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_decompress_sum(ctx.handle, [out.data_ptr(), inside], [40, 40],
+                                  [1.0, 1.0], n, xd.data_ptr(), 0) == tlc.TLC_E_INVALID
     assert tlc.tlc_sync(ctx.handle) == tlc.TLC_OK
 
 

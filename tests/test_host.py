@@ -62,8 +62,8 @@ def test_host_only_entry_points():
     for n in list(range(0, 50)) + [2 ** 20, 2 ** 28, 25_600_000, 4294967295]:
         assert tlc.tlc_max_compressed_bytes(n) == -(-n // 5)
     names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
-    assert names == ["tlc_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
-                     "tlc_expand_dequant_kernel", "tlc_absmax_batch_kernel",
+    assert names == ["tlc_accum_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_index_kernel",
+                     "tlc_expand_dequant_kernel", "tlc_accum_absmax_batch_kernel",
                      "tlc_quant_encode_batch_kernel", "tlc_zre_index_batch_kernel",
                      "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel",
                      "tlc_quant_pack_kernel", "tlc_int8_quant_kernel",
