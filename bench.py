@@ -40,13 +40,14 @@ def algorithmic_bytes(n, c, nnz):
     tiles = -(-(-(-n // 5)) // 4096)  # 4096-byte quartic tiles
     return {
         "tlc_accum_absmax_kernel": 12 * n,               # read x, r; write r = x + r
-        # read r; write r where q != 0, each tile's own stream bytes (c in all)
-        # and record
-        "tlc_quant_encode_kernel": 4 * n + 4 * nnz + c + 16 * tiles,
+        # read r; write each tile's own stream bytes (c in all) and record
+        "tlc_quant_encode_kernel": 4 * n + c + 16 * tiles,
         # tile records in, tile prefixes and chunk summaries out
         "tlc_zre_chunk_kernel": 24 * tiles,
-        # records, prefixes and slot bytes in, the stream out
-        "tlc_zre_compact_kernel": 2 * c + 32 * tiles,
+        # records, prefixes and slot bytes in, the stream out, and the
+        # residuals of the nnz values with q != 0 into r (the first pass
+        # hands them over in its per-tile lists)
+        "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 4 * nnz,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
         "tlc_expand_dequant_kernel": c + 8 * n,          # read C; read+write out
     }

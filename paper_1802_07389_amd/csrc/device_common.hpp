@@ -174,22 +174,26 @@ __device__ __forceinline__ uint32_t quantize_byte(float* __restrict__ r, uint64_
 }
 
 // Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and r 16-byte
-// aligned, so every partition slice is one float4; returns the four bytes
-// packed little-endian.  A slice is stored back only if one of its values
-// has q != 0.
-__device__ __forceinline__ uint32_t quantize_group4(float* __restrict__ r, uint64_t n,
-                                                    uint64_t m, uint64_t j, float M,
-                                                    float U) {
-  if (4 * m + j + 4 > n) {  // the group that reaches into the padding of p4
-    uint32_t w = 0u;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) w |= quantize_byte(r, n, m, j + c, M, U) << (8 * c);
-    return w;
-  }
-  uint32_t code[4] = {0u, 0u, 0u, 0u};
-  float4 a[5];
+// aligned: every partition slice is one float4.  group4_full says whether
+// all twenty values exist (only the last groups reach into the padding of
+// p4); load_group4 fetches the five slices and quantize_group4_loaded
+// quantizes them, stores back a slice only if one of its values has q != 0,
+// and returns the four bytes packed little-endian.  Split so a caller can
+// keep the loads of several groups in flight at once.
+__device__ __forceinline__ bool group4_full(uint64_t n, uint64_t m, uint64_t j) {
+  return 4 * m + j + 4 <= n;
+}
+
+__device__ __forceinline__ void load_group4(const float* __restrict__ r, uint64_t m,
+                                            uint64_t j, float4 (&a)[5]) {
 #pragma unroll
   for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(r + k * m + j);
+}
+
+__device__ __forceinline__ uint32_t quantize_group4_loaded(float* __restrict__ r, uint64_t m,
+                                                           uint64_t j, const float4 (&a)[5],
+                                                           float M, float U) {
+  uint32_t code[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
     float4 o;
@@ -205,6 +209,25 @@ __device__ __forceinline__ uint32_t quantize_group4(float* __restrict__ r, uint6
       *reinterpret_cast<float4*>(r + k * m + j) = o;
   }
   return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+}
+
+// The group by single bytes (any group, including those in the padding).
+__device__ __forceinline__ uint32_t quantize_group4_bytes(float* __restrict__ r, uint64_t n,
+                                                          uint64_t m, uint64_t j, float M,
+                                                          float U) {
+  uint32_t w = 0u;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) w |= quantize_byte(r, n, m, j + c, M, U) << (8 * c);
+  return w;
+}
+
+__device__ __forceinline__ uint32_t quantize_group4(float* __restrict__ r, uint64_t n,
+                                                    uint64_t m, uint64_t j, float M,
+                                                    float U) {
+  if (!group4_full(n, m, j)) return quantize_group4_bytes(r, n, m, j, M, U);
+  float4 a[5];
+  load_group4(r, m, j, a);
+  return quantize_group4_loaded(r, m, j, a, M, U);
 }
 
 // ---------------------------------------------------------------- stochastic mode

@@ -31,7 +31,10 @@ namespace tlc {
 // patterns with the sign cleared: for non-negative IEEE values integer
 // order equals numeric order, so the u32 max is exact and independent of
 // reduction order, and any NaN/Inf makes the result >= 0x7f800000.  Block
-// `blk` of `nblk` strides over [0, n).
+// `blk` of `nblk` strides over [0, n).  The float4 path marks its loads and
+// stores nontemporal: nothing here is read again before the whole tensor
+// has streamed through, and the hint measured faster for this kernel and
+// for the quantizer that follows.
 template <bool kVec, bool kResid = true>
 __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
                                                 float* __restrict__ r, uint64_t n,
@@ -48,14 +51,13 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       for (int u = 0; u < 4; ++u) a[u] = ld_stream(x + 4 * (i + u * stride));
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        b[u] = kResid ? *reinterpret_cast<const float4*>(r + 4 * (i + u * stride))
-                      : make_float4(0, 0, 0, 0);
+        b[u] = kResid ? ld_stream(r + 4 * (i + u * stride)) : make_float4(0, 0, 0, 0);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const float4 v = kResid ? make_float4(a[u].x + b[u].x, a[u].y + b[u].y,
                                               a[u].z + b[u].z, a[u].w + b[u].w)
                                 : a[u];
-        if (kResid) *reinterpret_cast<float4*>(r + 4 * (i + u * stride)) = v;
+        if (kResid) st_stream(r + 4 * (i + u * stride), v);
         mx = max(mx, abs_bits(v.x));
         mx = max(mx, abs_bits(v.y));
         mx = max(mx, abs_bits(v.z));
@@ -66,9 +68,9 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       const float4 a = ld_stream(x + 4 * i);
       float4 v = a;
       if (kResid) {
-        const float4 b = *reinterpret_cast<const float4*>(r + 4 * i);
+        const float4 b = ld_stream(r + 4 * i);
         v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-        *reinterpret_cast<float4*>(r + 4 * i) = v;
+        st_stream(r + 4 * i, v);
       }
       mx = max(mx, abs_bits(v.x));
       mx = max(mx, abs_bits(v.y));
@@ -195,6 +197,7 @@ __device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uin
 struct EncShared {
   uint32_t red[kWaves];
   uint32_t fault;
+  uint32_t nfix;  // entries taken in the tile's fix list (may pass kFixCap)
   RunSum wave[kWaves];
   RunSum excl;
   __align__(16) uint8_t q[kEncTile];
@@ -369,15 +372,81 @@ __device__ __forceinline__ uint32_t block_min(uint32_t v, uint32_t* lds) {
   return r;
 }
 
+// Residual v of the tile's value `local` (k * kEncTile + position) when
+// `has`: the wave takes consecutive entries of the fix list with one LDS
+// atomic; a value whose entry falls past kFixCap is stored at dst at once.
+__device__ __forceinline__ void fix_put(bool has, uint32_t local, float v, float* dst,
+                                        uint32_t* nfix, uint2* __restrict__ fix) {
+  const uint64_t bal = __ballot(has);
+  if (bal == 0u) return;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t leader = (uint32_t)__ffsll((unsigned long long)bal) - 1u;
+  const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+      (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  uint32_t base = 0u;
+  if (lane == leader) base = atomicAdd(nfix, (uint32_t)__popcll(bal));
+  base = (uint32_t)__shfl((int)base, (int)leader, 64);
+  if (has) {
+    const uint32_t slot = base + rank;
+    if (slot < kFixCap)
+      fix[slot] = make_uint2(local, __float_as_uint(v));
+    else
+      *dst = v;
+  }
+}
+
+// Phase 1 of a first-pass tile on the float4 path: quantize_tile<kPathVec>
+// with the residuals of q != 0 put into the tile's fix list.  The groups
+// that reach into the padding store theirs directly.  Ends with a barrier.
+__device__ __forceinline__ void quantize_tile_vec_deferred(float* __restrict__ r, uint64_t n,
+                                                           uint32_t m, const Scale& sc,
+                                                           uint64_t q0, uint32_t tile_bytes,
+                                                           uint8_t* q, uint2* __restrict__ fix,
+                                                           uint32_t* nfix) {
+  static_assert(kEncTile == 4096, "fix entries hold k * 4096 + position");
+  uint32_t* qw = reinterpret_cast<uint32_t*>(q);
+  for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads) {
+    const uint64_t j = q0 + g * 4u;
+    if (!group4_full(n, m, j)) {
+      qw[g] = quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
+      continue;
+    }
+    float4 a[5];
+    load_group4(r, m, j, a);
+    uint32_t code[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      float4 o;
+      const uint32_t t0 = quantize_one(a[k].x, sc.M, sc.U, o.x);
+      const uint32_t t1 = quantize_one(a[k].y, sc.M, sc.U, o.y);
+      const uint32_t t2 = quantize_one(a[k].z, sc.M, sc.U, o.z);
+      const uint32_t t3 = quantize_one(a[k].w, sc.M, sc.U, o.w);
+      code[0] = code[0] * 3u + t0;
+      code[1] = code[1] * 3u + t1;
+      code[2] = code[2] * 3u + t2;
+      code[3] = code[3] * 3u + t3;
+      float* e = r + k * m + j;
+      const uint32_t local = (uint32_t)k * kEncTile + g * 4u;
+      fix_put(t0 != 1u, local, o.x, e, nfix, fix);
+      fix_put(t1 != 1u, local + 1u, o.y, e + 1, nfix, fix);
+      fix_put(t2 != 1u, local + 2u, o.z, e + 2, nfix, fix);
+      fix_put(t3 != 1u, local + 3u, o.w, e + 3, nfix, fix);
+    }
+    qw[g] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+  }
+  __syncthreads();
+}
+
 template <int kPath>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5)))
 void tlc_quant_encode_kernel(
     float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ slots,
-    TileRec* __restrict__ recs, Ctrl* __restrict__ ctrl) {
+    TileRec* __restrict__ recs, uint2* __restrict__ fix, Ctrl* __restrict__ ctrl) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
   __shared__ EncShared sh;
+  if (threadIdx.x == 0) sh.nfix = 0u;
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   const uint32_t t = blockIdx.x;
   if (t == 0 && threadIdx.x == 0) {
@@ -387,7 +456,11 @@ void tlc_quant_encode_kernel(
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
+  if (kPath == kPathVec)
+    quantize_tile_vec_deferred(r, n, m, sc, q0, tile_bytes, sh.q, fix + (uint64_t)t * kFixCap,
+                               &sh.nfix);
+  else
+    quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- Section 3.3 from the tile's first non-121 byte (index L) on
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
@@ -462,8 +535,9 @@ void tlc_quant_encode_kernel(
   if (threadIdx.x == 0) {
     TileRec rec;
     rec.agg = rs_combine(rs_zero_run(L), agg).v;
-    rec.lead = L;
-    rec.len = len;
+    rec.lead = (uint16_t)L;
+    rec.len = (uint16_t)len;
+    rec.nfix = min<uint32_t>(sh.nfix, kFixCap);
     recs[t] = rec;
   }
 }
@@ -543,7 +617,8 @@ __global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
 __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
     const TileRec* __restrict__ recs, const uint64_t* __restrict__ chunk_pre,
     const uint64_t* __restrict__ local_pre, const uint8_t* __restrict__ slots, uint32_t m,
-    uint8_t* __restrict__ out, Ctrl* __restrict__ ctrl) {
+    uint8_t* __restrict__ out, const uint2* __restrict__ fix, float* __restrict__ r, uint64_t n,
+    Ctrl* __restrict__ ctrl) {
   if (ctrl->enc.err) return;
   const uint32_t t = blockIdx.x;
   RunSum cp, lp;
@@ -566,6 +641,15 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
     const uint32_t len = min<uint32_t>(rec.len, tile_bytes);
     for (uint32_t i = threadIdx.x; i < len; i += kThreads)
       if (at + i < m) out[at + i] = slots[q0 + i];
+  }
+  // the residuals the first pass left in the tile's fix list
+  const uint2* tf = fix + (uint64_t)t * kFixCap;
+  const uint32_t nf = min<uint32_t>(rec.nfix, kFixCap);
+  for (uint32_t i = threadIdx.x; i < nf; i += kThreads) {
+    const uint2 f = tf[i];
+    const uint32_t k = f.x / (uint32_t)kEncTile, p = f.x % (uint32_t)kEncTile;
+    const uint64_t e = (uint64_t)k * m + q0 + p;
+    if (k < 5u && p < tile_bytes && e < n) r[e] = __uint_as_float(f.y);
   }
   if (t + 1 == gridDim.x && threadIdx.x == 0) {  // a run that ends the stream; the length
     RunSum a;
@@ -733,18 +817,18 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* p
 
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, Ctrl* ctrl, hipStream_t st) {
+                               TileRec* recs, uint2* fix, Ctrl* ctrl, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
   if (al && m % 4 == 0)
-    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(r, n, m, s, partials,
-                                                                   npartials, slots, recs, ctrl);
+    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
+        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
   else if (al)
     tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
   else
     tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
   return hipGetLastError();
 }
 
@@ -778,10 +862,11 @@ hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* loc
 
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
-                              uint8_t* out, Ctrl* ctrl, hipStream_t st) {
+                              uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
+                              hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   tlc_zre_compact_kernel<<<ntiles, kThreads, 0, st>>>(recs, chunk_pre, local_pre, slots, m, out,
-                                                      ctrl);
+                                                      fix, r, n, ctrl);
   return hipGetLastError();
 }
 

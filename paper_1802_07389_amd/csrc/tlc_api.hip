@@ -89,6 +89,7 @@ struct tlc_ctx {
   TileRec* recs = nullptr;
   uint64_t* chunk_agg = nullptr;  // chunk summaries, scanned in place into chunk prefixes
   uint64_t* local_pre = nullptr;  // every tile's prefix within its chunk
+  uint2* fix = nullptr;           // per tile kFixCap deferred residuals
   // pinned host memory: status readback, batch results, descriptor staging
   HostReadback* rb = nullptr;
   EncResult* host_results = nullptr;
@@ -316,7 +317,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
   // layout: ctrl | partials | enc status | dec status | start | enc descs |
   //         dec descs | enc results | tile records | chunk summaries |
-  //         tile prefixes in their chunks | slots
+  //         tile prefixes in their chunks | fix lists | slots
   size_t off = sizeof(Ctrl);
   const size_t off_partials = off;
   off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
@@ -338,6 +339,8 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   off = round_up(off + (tiles1 / 64 + 1) * sizeof(uint64_t), 256);
   const size_t off_local = off;
   off = round_up(off + tiles1 * sizeof(uint64_t), 256);
+  const size_t off_fix = off;
+  off = round_up(off + tiles1 * (size_t)kFixCap * sizeof(uint2), 256);
   const size_t off_slots = off;
   const size_t total = round_up(off + tiles1 * (size_t)kEncTile, 256);
   e = hipMalloc(&c->ws, total);
@@ -357,6 +360,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->recs = (TileRec*)(base + off_recs);
   c->chunk_agg = (uint64_t*)(base + off_chunks);
   c->local_pre = (uint64_t*)(base + off_local);
+  c->fix = (uint2*)(base + off_fix);
   c->slots = base + off_slots;
   e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -464,7 +468,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   }
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
-                               c->ctrl, c->stream);
+                               c->fix, c->ctrl, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
@@ -473,7 +477,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_COMPACT, [&] {
     return launch_zre_compact(c->recs, c->chunk_agg, c->local_pre, c->slots, (uint32_t)m, bytes,
-                              c->ctrl, c->stream);
+                              c->fix, residual, n, c->ctrl, c->stream);
   });
   if (st) return st;
   return finish_compress(c, "tlc_compress", bytes_len, scale);

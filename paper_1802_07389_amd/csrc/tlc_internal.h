@@ -66,13 +66,21 @@ static_assert(sizeof(EncDesc) == 64, "EncDesc is 64 bytes");
 
 // Per-tile record of the single-tensor encoder's first pass: the zero-run
 // summary of the whole tile (RunSum bits), the length of its leading run of
-// 121 bytes, and how many bytes it wrote into its slot (its encoding from
-// the first non-121 byte on).
+// 121 bytes, how many bytes it wrote into its slot (its encoding from the
+// first non-121 byte on), and how many residuals it left in its fix list.
 struct TileRec {
   uint64_t agg;
-  uint32_t lead;
-  uint32_t len;
+  uint16_t lead;  // <= kEncTile
+  uint16_t len;   // <= kEncTile
+  uint32_t nfix;  // <= kFixCap
 };
+static_assert(sizeof(TileRec) == 16, "TileRec is 16 bytes");
+
+// Residuals with q != 0 that a first-pass tile of the float4 path leaves to
+// the compaction pass, as (k * kEncTile + position in the tile, value
+// bits): a few scattered stores cost far less in a pass of their own than
+// mixed into the first pass's read stream.  Further ones are stored at once.
+constexpr uint32_t kFixCap = 256;
 static_assert(sizeof(TileRec) == 16, "TileRec is 16 bytes");
 
 // One stream of a batched decode or of a decode-sum.
@@ -96,7 +104,7 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
                                uint32_t* partials, uint32_t* nblocks, hipStream_t st);
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, Ctrl* ctrl, hipStream_t st);
+                               TileRec* recs, uint2* fix, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
                                        const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                        uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
@@ -105,7 +113,8 @@ hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* loc
                              uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
-                              uint8_t* out, Ctrl* ctrl, hipStream_t st);
+                              uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
+                              hipStream_t st);
 hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, float s,
                              int stochastic, uint64_t seed, uint64_t step,
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
