@@ -373,10 +373,11 @@ __device__ __forceinline__ uint32_t block_min(uint32_t v, uint32_t* lds) {
 }
 
 // Residual v of the tile's value `local` (k * kEncTile + position) when
-// `has`: the wave takes consecutive entries of the fix list with one LDS
-// atomic; a value whose entry falls past kFixCap is stored at dst at once.
+// `has`: the wave takes consecutive entries of the tile's fix list (in LDS)
+// with one LDS atomic; a value whose entry falls past kFixCap is stored at
+// dst at once.
 __device__ __forceinline__ void fix_put(bool has, uint32_t local, float v, float* dst,
-                                        uint32_t* nfix, uint2* __restrict__ fix) {
+                                        uint32_t* nfix, uint2* fix) {
   const uint64_t bal = __ballot(has);
   if (bal == 0u) return;
   const uint32_t lane = threadIdx.x & 63u;
@@ -396,13 +397,16 @@ __device__ __forceinline__ void fix_put(bool has, uint32_t local, float v, float
 }
 
 // Phase 1 of a first-pass tile on the float4 path: quantize_tile<kPathVec>
-// with the residuals of q != 0 put into the tile's fix list.  The groups
-// that reach into the padding store theirs directly.  Ends with a barrier.
+// with the residuals of q != 0 put into the tile's fix list, which is built
+// in LDS (s_fix) and then copied out whole, so HBM sees a few full lines
+// per tile rather than one partial line per value.  The groups that reach
+// into the padding store theirs directly.  Ends with a barrier.
 __device__ __forceinline__ void quantize_tile_vec_deferred(float* __restrict__ r, uint64_t n,
                                                            uint32_t m, const Scale& sc,
                                                            uint64_t q0, uint32_t tile_bytes,
-                                                           uint8_t* q, uint2* __restrict__ fix,
-                                                           uint32_t* nfix) {
+                                                           uint8_t* q, uint2* s_fix,
+                                                           uint32_t* nfix,
+                                                           uint2* __restrict__ fix) {
   static_assert(kEncTile == 4096, "fix entries hold k * 4096 + position");
   uint32_t* qw = reinterpret_cast<uint32_t*>(q);
   for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads) {
@@ -427,14 +431,16 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(float* __restrict__ r
       code[3] = code[3] * 3u + t3;
       float* e = r + k * m + j;
       const uint32_t local = (uint32_t)k * kEncTile + g * 4u;
-      fix_put(t0 != 1u, local, o.x, e, nfix, fix);
-      fix_put(t1 != 1u, local + 1u, o.y, e + 1, nfix, fix);
-      fix_put(t2 != 1u, local + 2u, o.z, e + 2, nfix, fix);
-      fix_put(t3 != 1u, local + 3u, o.w, e + 3, nfix, fix);
+      fix_put(t0 != 1u, local, o.x, e, nfix, s_fix);
+      fix_put(t1 != 1u, local + 1u, o.y, e + 1, nfix, s_fix);
+      fix_put(t2 != 1u, local + 2u, o.z, e + 2, nfix, s_fix);
+      fix_put(t3 != 1u, local + 3u, o.w, e + 3, nfix, s_fix);
     }
     qw[g] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
   }
   __syncthreads();
+  const uint32_t nf = min<uint32_t>(*nfix, kFixCap);
+  for (uint32_t i = threadIdx.x; i < nf; i += kThreads) fix[i] = s_fix[i];
 }
 
 template <int kPath>
@@ -446,6 +452,7 @@ void tlc_quant_encode_kernel(
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
   __shared__ EncShared sh;
+  __shared__ uint2 s_fix[kPath == kPathVec ? kFixCap : 1];
   if (threadIdx.x == 0) sh.nfix = 0u;
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   const uint32_t t = blockIdx.x;
@@ -457,8 +464,8 @@ void tlc_quant_encode_kernel(
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
   if (kPath == kPathVec)
-    quantize_tile_vec_deferred(r, n, m, sc, q0, tile_bytes, sh.q, fix + (uint64_t)t * kFixCap,
-                               &sh.nfix);
+    quantize_tile_vec_deferred(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
+                               fix + (uint64_t)t * kFixCap);
   else
     quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
 
