@@ -35,10 +35,18 @@ namespace tlc {
 // stores nontemporal: nothing here is read again before the whole tensor
 // has streamed through, and the hint measured faster for this kernel and
 // for the quantizer that follows.
-template <bool kVec, bool kResid = true>
+//
+// kSum (float4 path with a buffer): also store, for float4 number i of the
+// buffer, the top 16 bits of the bit pattern of its largest |acc|.  That
+// half-word h bounds the four values from above (|acc| < (h + 1) * 2^16 as
+// bit patterns), so the quantizer can skip every float4 whose h lies below
+// the top half of its threshold U: all four have q = 0 and keep acc.
+template <bool kVec, bool kResid = true, bool kSum = false>
 __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
                                                 float* __restrict__ r, uint64_t n,
-                                                uint32_t blk, uint32_t nblk) {
+                                                uint32_t blk, uint32_t nblk,
+                                                uint16_t* __restrict__ summ = nullptr) {
+  static_assert(!kSum || (kVec && kResid), "summaries come from the float4 buffer path");
   uint32_t mx = 0;
   const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
   const uint64_t stride = (uint64_t)nblk * kThreads;
@@ -58,10 +66,10 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
                                               a[u].z + b[u].z, a[u].w + b[u].w)
                                 : a[u];
         if (kResid) st_stream(r + 4 * (i + u * stride), v);
-        mx = max(mx, abs_bits(v.x));
-        mx = max(mx, abs_bits(v.y));
-        mx = max(mx, abs_bits(v.z));
-        mx = max(mx, abs_bits(v.w));
+        const uint32_t m4 =
+            max(max(abs_bits(v.x), abs_bits(v.y)), max(abs_bits(v.z), abs_bits(v.w)));
+        if (kSum) summ[i + u * stride] = (uint16_t)(m4 >> 16);
+        mx = max(mx, m4);
       }
     }
     for (; i < nv; i += stride) {
@@ -72,10 +80,10 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
         v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
         st_stream(r + 4 * i, v);
       }
-      mx = max(mx, abs_bits(v.x));
-      mx = max(mx, abs_bits(v.y));
-      mx = max(mx, abs_bits(v.z));
-      mx = max(mx, abs_bits(v.w));
+      const uint32_t m4 =
+          max(max(abs_bits(v.x), abs_bits(v.y)), max(abs_bits(v.z), abs_bits(v.w)));
+      if (kSum) summ[i] = (uint16_t)(m4 >> 16);
+      mx = max(mx, m4);
     }
     for (uint64_t e = (nv << 2) + tid; e < n; e += stride) {
       const float v = kResid ? x[e] + r[e] : x[e];
@@ -92,13 +100,13 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
   return mx;
 }
 
-template <bool kVec, bool kResid>
+template <bool kVec, bool kResid, bool kSum>
 __global__ __launch_bounds__(kThreads) void tlc_accum_absmax_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n,
-    uint32_t* __restrict__ partials) {
+    uint32_t* __restrict__ partials, uint16_t* __restrict__ summ) {
   __shared__ uint32_t lds[kWaves];
   const uint32_t mx =
-      block_max(absmax_part<kVec, kResid>(x, r, n, blockIdx.x, gridDim.x), lds);
+      block_max(absmax_part<kVec, kResid, kSum>(x, r, n, blockIdx.x, gridDim.x, summ), lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = mx;
 }
 
@@ -197,12 +205,27 @@ __device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uin
 struct EncShared {
   uint32_t red[kWaves];
   uint32_t fault;
-  uint32_t nfix;  // entries taken in the tile's fix list (may pass kFixCap)
+  uint32_t nfix;   // entries taken in the tile's fix list (may pass kFixCap)
+  uint32_t nneed;  // float4 slices the tile has to load (summaries)
   RunSum wave[kWaves];
   RunSum excl;
   __align__(16) uint8_t q[kEncTile];
   __align__(16) uint8_t out[kEncTile + 16];
 };
+
+// Mask of the non-121 bytes among the kEncTile / kThreads = 16 quartic
+// bytes q[lo .. lo + cnt) of one thread (bit i: byte lo + i).
+__device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
+                                                       uint32_t cnt) {
+  static_assert(kEncTile / kThreads == 16, "one uint4 of quartic bytes per thread");
+  const uint4 w = *reinterpret_cast<const uint4*>(q + lo);
+  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+  uint32_t nz = 0u;
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    nz |= (((wd[i / 4] >> (8 * (i % 4))) & 0xffu) != kZeroGroup ? 1u : 0u) << i;
+  return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
+}
 
 // Phase 1 of a tile (Eq. 2, residual write-back, quartic pack): the block
 // quantizes the 5 * tile_bytes accumulated values of quartic bytes
@@ -255,22 +278,8 @@ __device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, u
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t lo = threadIdx.x * kBytes;
   const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
-  uint8_t b[kBytes];
-  bool zero = cnt == (uint32_t)kBytes;  // a full chunk of five-zero groups (byte 121)
-#pragma unroll
-  for (int h = 0; h < kBytes / 16; ++h) {
-    const uint4 w = *reinterpret_cast<const uint4*>(sh.q + lo + 16 * h);
-    zero = zero && w.x == 0x79797979u && w.y == 0x79797979u && w.z == 0x79797979u &&
-           w.w == 0x79797979u;
-    unpack16(w, b + 16 * h);
-  }
-  RunSum sum = rs_zero_run(kBytes);
-  if (!zero) {
-    sum = rs_identity();
-#pragma unroll
-    for (int i = 0; i < kBytes; ++i)
-      if ((uint32_t)i < cnt) sum = rs_combine(sum, rs_byte(b[i]));
-  }
+  const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
+  const RunSum sum = rs_mask_summary(nz, cnt);
 
   RunSum incl = sum;
 #pragma unroll
@@ -319,13 +328,7 @@ __device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, u
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
-  if (zero) {
-    phi = rs_zero_walk(kBytes, phi, put);
-  } else {
-#pragma unroll
-    for (int i = 0; i < kBytes; ++i)
-      if ((uint32_t)i < cnt) phi = rs_step(b[i], phi, put);
-  }
+  phi = rs_mask_walk(nz, cnt, phi, [&](uint32_t i) { return (uint32_t)sh.q[lo + i]; }, put);
   if (cnt && q0 + lo + cnt == m && phi) put(rs_code(phi));  // stream ends in a run
 
   const bool last_tile = q0 + kEncTile >= m;
@@ -396,47 +399,165 @@ __device__ __forceinline__ void fix_put(bool has, uint32_t local, float v, float
   }
 }
 
+// Slice k of group g (values j..j+3 of partition k, loaded as a) of a
+// first-pass tile: the four trits, and the residuals of q != 0 put into the
+// tile's fix list.
+__device__ __forceinline__ void quantize_slice(const float4& a, uint32_t k, uint32_t g,
+                                               float* e, const Scale& sc, uint32_t (&t)[4],
+                                               uint32_t* nfix, uint2* s_fix) {
+  float4 o;
+  t[0] = quantize_one(a.x, sc.M, sc.U, o.x);
+  t[1] = quantize_one(a.y, sc.M, sc.U, o.y);
+  t[2] = quantize_one(a.z, sc.M, sc.U, o.z);
+  t[3] = quantize_one(a.w, sc.M, sc.U, o.w);
+  const uint32_t local = k * kEncTile + g * 4u;
+  fix_put(t[0] != 1u, local, o.x, e, nfix, s_fix);
+  fix_put(t[1] != 1u, local + 1u, o.y, e + 1, nfix, s_fix);
+  fix_put(t[2] != 1u, local + 2u, o.z, e + 2, nfix, s_fix);
+  fix_put(t[3] != 1u, local + 3u, o.w, e + 3, nfix, s_fix);
+}
+
+// A tile with at most this many float4 slices to load (of 5 * 1024) takes
+// the sparse form below.
+constexpr uint32_t kSparseSlices = 512;
+constexpr int kGroupsPerThread = kEncTile / 4 / kThreads;  // groups of 4 bytes per thread
+// Slices a thread of a sparse tile loads together (more go one at a time).
+constexpr int kSparseBatch = 4;
+
+// The max pass's bounds of this thread's slices (group it = threadIdx.x +
+// kThreads * it, partition k); 0 for groups that are missing or reach into
+// the padding.  They do not depend on M, so the loads are issued before the
+// block reduces it.
+__device__ __forceinline__ void load_bounds(const uint16_t* __restrict__ summ, uint64_t n,
+                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
+                                            uint32_t (&h)[kGroupsPerThread][5]) {
+#pragma unroll
+  for (int it = 0; it < kGroupsPerThread; ++it) {
+    const uint32_t g = threadIdx.x + kThreads * it;
+    const uint64_t j = q0 + g * 4u;
+    const bool full = g * 4u < tile_bytes && group4_full(n, m, j);
+#pragma unroll
+    for (int k = 0; k < 5; ++k) h[it][k] = full ? summ[(k * (uint64_t)m + j) >> 2] : 0u;
+  }
+}
+
 // Phase 1 of a first-pass tile on the float4 path: quantize_tile<kPathVec>
 // with the residuals of q != 0 put into the tile's fix list, which is built
 // in LDS (s_fix) and then copied out whole, so HBM sees a few full lines
-// per tile rather than one partial line per value.  The groups that reach
-// into the padding store theirs directly.  Ends with a barrier.
-__device__ __forceinline__ void quantize_tile_vec_deferred(float* __restrict__ r, uint64_t n,
-                                                           uint32_t m, const Scale& sc,
-                                                           uint64_t q0, uint32_t tile_bytes,
-                                                           uint8_t* q, uint2* s_fix,
-                                                           uint32_t* nfix,
-                                                           uint2* __restrict__ fix) {
+// per tile rather than one partial line per value.
+//
+// With the max pass's bounds (kSum; h from load_bounds) a slice is needed
+// only if its bound reaches the top half of U; the others hold four values
+// with q = 0, contribute trit 1 and are neither read nor written.  If the
+// block needs few slices (typical: most groups of five values quantize to
+// zero), every group starts from the all-zero byte 121 and its owner loads
+// its first kSparseBatch needed slices together, moving each byte by
+// (t - 1) * 3^(4-k); otherwise the groups are quantized in turn with their
+// needed slices loaded together.  The groups that reach into the padding
+// store theirs directly.  Ends with a barrier.
+template <bool kSum>
+__device__ __forceinline__ void quantize_tile_vec_deferred(
+    float* __restrict__ r, uint64_t n, uint32_t m, const Scale& sc, uint64_t q0,
+    uint32_t tile_bytes, uint8_t* q, uint2* s_fix, uint32_t* nfix, uint32_t* nneed,
+    uint2* __restrict__ fix, const uint32_t (&h)[kGroupsPerThread][5]) {
   static_assert(kEncTile == 4096, "fix entries hold k * 4096 + position");
+  static_assert(kGroupsPerThread * 5 <= 32, "a thread's slices fit one mask");
   uint32_t* qw = reinterpret_cast<uint32_t*>(q);
-  for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads) {
-    const uint64_t j = q0 + g * 4u;
-    if (!group4_full(n, m, j)) {
-      qw[g] = quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
-      continue;
-    }
-    float4 a[5];
-    load_group4(r, m, j, a);
-    uint32_t code[4] = {0u, 0u, 0u, 0u};
+  uint32_t need = 0u;  // bit 5 * it + k: slice k of group it is loaded
+  bool sparse = false;
+  if (kSum) {
+    const uint32_t hU = __float_as_uint(sc.U) >> 16;
 #pragma unroll
-    for (int k = 0; k < 5; ++k) {
-      float4 o;
-      const uint32_t t0 = quantize_one(a[k].x, sc.M, sc.U, o.x);
-      const uint32_t t1 = quantize_one(a[k].y, sc.M, sc.U, o.y);
-      const uint32_t t2 = quantize_one(a[k].z, sc.M, sc.U, o.z);
-      const uint32_t t3 = quantize_one(a[k].w, sc.M, sc.U, o.w);
-      code[0] = code[0] * 3u + t0;
-      code[1] = code[1] * 3u + t1;
-      code[2] = code[2] * 3u + t2;
-      code[3] = code[3] * 3u + t3;
-      float* e = r + k * m + j;
-      const uint32_t local = (uint32_t)k * kEncTile + g * 4u;
-      fix_put(t0 != 1u, local, o.x, e, nfix, s_fix);
-      fix_put(t1 != 1u, local + 1u, o.y, e + 1, nfix, s_fix);
-      fix_put(t2 != 1u, local + 2u, o.z, e + 2, nfix, s_fix);
-      fix_put(t3 != 1u, local + 3u, o.w, e + 3, nfix, s_fix);
+    for (int it = 0; it < kGroupsPerThread; ++it)
+#pragma unroll
+      for (int k = 0; k < 5; ++k) need |= (h[it][k] >= hU ? 1u : 0u) << (5 * it + k);
+    if (need) atomicAdd(nneed, (uint32_t)__popc(need));
+    __syncthreads();
+    sparse = *nneed <= kSparseSlices;
+  }
+  if (sparse) {
+    int code[kGroupsPerThread][4];
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) code[it][c] = 121;  // five zero values per byte
+    // the first kSparseBatch needed slices: loads issued together
+    float4 a[kSparseBatch];
+    uint32_t sel[kSparseBatch];
+    uint32_t rest = need;
+#pragma unroll
+    for (int b = 0; b < kSparseBatch; ++b) {
+      sel[b] = rest ? (uint32_t)__ffs(rest) - 1u : 32u;
+      rest &= rest - 1u;
+      if (sel[b] < 32u) {
+        const uint32_t it = sel[b] / 5u, k = sel[b] % 5u;
+        a[b] = *reinterpret_cast<const float4*>(r + (uint64_t)k * m + q0 +
+                                                (threadIdx.x + kThreads * it) * 4u);
+      }
     }
-    qw[g] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+    auto apply = [&](uint32_t bit, const float4& v) {
+      const uint32_t it = bit / 5u, k = bit % 5u;
+      const uint32_t g = threadIdx.x + kThreads * it;
+      float* e = r + (uint64_t)k * m + q0 + g * 4u;
+      uint32_t t[4];
+      quantize_slice(v, k, g, e, sc, t, nfix, s_fix);
+      const int w = (int)trit_weight((int)k);
+#pragma unroll
+      for (int gi = 0; gi < kGroupsPerThread; ++gi)
+        if ((uint32_t)gi == it) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) code[gi][c] += ((int)t[c] - 1) * w;
+        }
+    };
+#pragma unroll
+    for (int b = 0; b < kSparseBatch; ++b)
+      if (sel[b] < 32u) apply(sel[b], a[b]);
+    while (rest) {  // rare: more needed slices than one batch
+      const uint32_t bit = (uint32_t)__ffs(rest) - 1u;
+      rest &= rest - 1u;
+      const uint32_t it = bit / 5u, k = bit % 5u;
+      apply(bit, *reinterpret_cast<const float4*>(r + (uint64_t)k * m + q0 +
+                                                  (threadIdx.x + kThreads * it) * 4u));
+    }
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it) {
+      const uint32_t g = threadIdx.x + kThreads * it;
+      if (g * 4u >= tile_bytes) break;
+      const uint64_t j = q0 + g * 4u;
+      qw[g] = group4_full(n, m, j)
+                  ? (uint32_t)code[it][0] | ((uint32_t)code[it][1] << 8) |
+                        ((uint32_t)code[it][2] << 16) | ((uint32_t)code[it][3] << 24)
+                  : quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it) {
+      const uint32_t g = threadIdx.x + kThreads * it;
+      if (g * 4u >= tile_bytes) break;
+      const uint64_t j = q0 + g * 4u;
+      if (!group4_full(n, m, j)) {
+        qw[g] = quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
+        continue;
+      }
+      float4 a[5];
+      if (kSum) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k)
+          a[k] = (need >> (5 * it + k)) & 1u ? *reinterpret_cast<const float4*>(r + (uint64_t)k * m + j)
+                                             : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        load_group4(r, m, j, a);
+      }
+      uint32_t code[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int k = 0; k < 5; ++k) {
+        uint32_t t[4];
+        quantize_slice(a[k], (uint32_t)k, g, r + (uint64_t)k * m + j, sc, t, nfix, s_fix);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) code[c] = code[c] * 3u + t[c];
+      }
+      qw[g] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+    }
   }
   __syncthreads();
   const uint32_t nf = min<uint32_t>(*nfix, kFixCap);
@@ -448,58 +569,51 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5)))
 void tlc_quant_encode_kernel(
     float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ slots,
-    TileRec* __restrict__ recs, uint2* __restrict__ fix, Ctrl* __restrict__ ctrl) {
+    TileRec* __restrict__ recs, uint2* __restrict__ fix, const uint16_t* __restrict__ summ,
+    Ctrl* __restrict__ ctrl) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
   __shared__ EncShared sh;
   __shared__ uint2 s_fix[kPath == kPathVec ? kFixCap : 1];
-  if (threadIdx.x == 0) sh.nfix = 0u;
-  const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+  if (threadIdx.x == 0) {
+    sh.nfix = 0u;
+    sh.nneed = 0u;
+  }
   const uint32_t t = blockIdx.x;
+  const uint64_t q0 = (uint64_t)t * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  uint32_t h[kGroupsPerThread][5];
+  if (kPath == kPathVec && summ) load_bounds(summ, n, m, q0, tile_bytes, h);
+  const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
-  const uint64_t q0 = (uint64_t)t * kEncTile;
-  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  if (kPath == kPathVec)
-    quantize_tile_vec_deferred(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
-                               fix + (uint64_t)t * kFixCap);
-  else
+  if (kPath == kPathVec) {
+    if (summ)
+      quantize_tile_vec_deferred<true>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
+                                       &sh.nneed, fix + (uint64_t)t * kFixCap, h);
+    else
+      quantize_tile_vec_deferred<false>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
+                                        &sh.nneed, fix + (uint64_t)t * kFixCap, h);
+  } else {
     quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
+  }
 
   // ---- Section 3.3 from the tile's first non-121 byte (index L) on
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t lo = threadIdx.x * kBytes;
   const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
-  uint8_t b[kBytes];
-  bool zero = cnt == (uint32_t)kBytes;  // a full chunk of five-zero groups (byte 121)
-#pragma unroll
-  for (int h = 0; h < kBytes / 16; ++h) {
-    const uint4 w = *reinterpret_cast<const uint4*>(sh.q + lo + 16 * h);
-    zero = zero && w.x == 0x79797979u && w.y == 0x79797979u && w.z == 0x79797979u &&
-           w.w == 0x79797979u;
-    unpack16(w, b + 16 * h);
-  }
-  uint32_t first = tile_bytes;
-  if (!zero) {
-#pragma unroll
-    for (int i = kBytes - 1; i >= 0; --i)
-      if ((uint32_t)i < cnt && b[i] != kZeroGroup) first = lo + i;
-  }
+  const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
+  const uint32_t first = nz ? lo + (uint32_t)__builtin_ctz(nz) : tile_bytes;
   const uint32_t L = block_min(first, sh.red);
   const bool mine = lo + cnt > L;  // the thread holds bytes at index >= L
-  RunSum own = rs_identity();
-  if (mine) {
-    if (zero) {
-      own = rs_zero_run(kBytes);  // lo > L: a whole chunk of the run after L
-    } else {
-#pragma unroll
-      for (int i = 0; i < kBytes; ++i)
-        if ((uint32_t)i < cnt && lo + i >= L) own = rs_combine(own, rs_byte(b[i]));
-    }
-  }
+  // the thread's segment: its bytes at index >= L
+  const uint32_t s0 = mine && L > lo ? L - lo : 0u;
+  const uint32_t seg = mine ? cnt - s0 : 0u;
+  const uint32_t seg_nz = mine ? nz >> s0 : 0u;
+  const RunSum own = rs_mask_summary(seg_nz, seg);
   RunSum incl = own;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
@@ -524,15 +638,9 @@ void tlc_quant_encode_kernel(
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
-  if (mine) {
-    if (zero) {
-      phi = rs_zero_walk(kBytes, phi, put);
-    } else {
-#pragma unroll
-      for (int i = 0; i < kBytes; ++i)
-        if ((uint32_t)i < cnt && lo + i >= L) phi = rs_step(b[i], phi, put);
-    }
-  }
+  if (mine)
+    phi = rs_mask_walk(seg_nz, seg, phi,
+                       [&](uint32_t i) { return (uint32_t)sh.q[lo + s0 + i]; }, put);
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
   const uint32_t len = min<uint32_t>(rs_emitted(agg), tile_bytes);
@@ -800,42 +908,41 @@ static inline bool aligned16(const void* p) {
 }
 
 hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* partials,
-                               uint32_t* nblocks, hipStream_t st) {
+                               uint32_t* nblocks, uint16_t* summ, hipStream_t st) {
   const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
+  if (summ && !(vec && r)) return hipErrorInvalidValue;  // summaries need the float4 path
   const uint64_t items = vec ? (n >> 2) : n;
   uint64_t blocks = (items + kThreads * 4 - 1) / (kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > kAbsmaxMaxBlocks ? kAbsmaxMaxBlocks : blocks);
   *nblocks = (uint32_t)blocks;
+#define TLC_LAUNCH(V, R, S) \
+  tlc_accum_absmax_kernel<V, R, S><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials, summ)
   if (r == nullptr) {  // no error buffer: max |x|
-    if (aligned16(x))
-      tlc_accum_absmax_kernel<true, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
-                                                                                  partials);
-    else
-      tlc_accum_absmax_kernel<false, false><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
-                                                                                   partials);
+    if (aligned16(x)) TLC_LAUNCH(true, false, false); else TLC_LAUNCH(false, false, false);
   } else if (vec) {
-    tlc_accum_absmax_kernel<true, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials);
+    if (summ) TLC_LAUNCH(true, true, true); else TLC_LAUNCH(true, true, false);
   } else {
-    tlc_accum_absmax_kernel<false, true><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n,
-                                                                                partials);
+    TLC_LAUNCH(false, true, false);
   }
+#undef TLC_LAUNCH
   return hipGetLastError();
 }
 
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, uint2* fix, Ctrl* ctrl, hipStream_t st) {
+                               TileRec* recs, uint2* fix, const uint16_t* summ, Ctrl* ctrl,
+                               hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
   if (al && m % 4 == 0)
     tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
   else if (al)
     tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, fix, nullptr, ctrl);
   else
     tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, ctrl);
+        r, n, m, s, partials, npartials, slots, recs, fix, nullptr, ctrl);
   return hipGetLastError();
 }
 

@@ -90,6 +90,7 @@ struct tlc_ctx {
   uint64_t* chunk_agg = nullptr;  // chunk summaries, scanned in place into chunk prefixes
   uint64_t* local_pre = nullptr;  // every tile's prefix within its chunk
   uint2* fix = nullptr;           // per tile kFixCap deferred residuals
+  uint16_t* summ = nullptr;       // per float4 of the buffer: top half of max |acc|
   // pinned host memory: status readback, batch results, descriptor staging
   HostReadback* rb = nullptr;
   EncResult* host_results = nullptr;
@@ -317,7 +318,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
   // layout: ctrl | partials | enc status | dec status | start | enc descs |
   //         dec descs | enc results | tile records | chunk summaries |
-  //         tile prefixes in their chunks | fix lists | slots
+  //         tile prefixes in their chunks | fix lists | float4 summaries | slots
   size_t off = sizeof(Ctrl);
   const size_t off_partials = off;
   off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
@@ -341,6 +342,8 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   off = round_up(off + tiles1 * sizeof(uint64_t), 256);
   const size_t off_fix = off;
   off = round_up(off + tiles1 * (size_t)kFixCap * sizeof(uint2), 256);
+  const size_t off_summ = off;
+  off = round_up(off + (max_n / 4) * sizeof(uint16_t), 256);
   const size_t off_slots = off;
   const size_t total = round_up(off + tiles1 * (size_t)kEncTile, 256);
   e = hipMalloc(&c->ws, total);
@@ -361,6 +364,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->chunk_agg = (uint64_t*)(base + off_chunks);
   c->local_pre = (uint64_t*)(base + off_local);
   c->fix = (uint2*)(base + off_fix);
+  c->summ = (uint16_t*)(base + off_summ);
   c->slots = base + off_slots;
   e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -446,12 +450,18 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   st = dev.status();
   if (st) return st;
 
+  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
+  // The three passes' float4 path skips float4s of the buffer whose bound
+  // from the max pass (which writes them on its own float4 path) is below U.
+  uint16_t* summ = (ntiles >= kThreePassMinTiles && aligned16(tensor) && aligned16(residual) &&
+                    m % 4 == 0)
+                       ? c->summ
+                       : nullptr;
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, residual, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, residual, n, c->partials, &np, summ, c->stream);
   });
   if (st) return st;
-  const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
     uint32_t epoch = 0;
     st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, nullptr,
@@ -468,7 +478,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   }
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
-                               c->fix, c->ctrl, c->stream);
+                               c->fix, summ, c->ctrl, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
@@ -509,7 +519,7 @@ int compress_int8(tlc_ctx* c, const float* tensor, float* residual, size_t n, fl
   if (st) return st;
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, residual, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, residual, n, c->partials, &np, nullptr, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_INT8_QUANT, [&] {
@@ -565,7 +575,7 @@ TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* re
   float* r = stoch ? nullptr : residual;  // the stochastic mode has no error feedback
   uint32_t np = 0;
   st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, r, n, c->partials, &np, c->stream);
+    return launch_accum_absmax(tensor, r, n, c->partials, &np, nullptr, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_PACK, [&] {

@@ -100,11 +100,15 @@ static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
 
 // Launchers (encode.hip, decode.hip, int8.hip).  All return the hipError_t of the
 // launch.
+// summ (may be NULL): per float4 of r, the top half of its largest |acc|;
+// only written on the float4 path (x and r 16-byte aligned).
 hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
-                               uint32_t* partials, uint32_t* nblocks, hipStream_t st);
+                               uint32_t* partials, uint32_t* nblocks, uint16_t* summ,
+                               hipStream_t st);
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, uint2* fix, Ctrl* ctrl, hipStream_t st);
+                               TileRec* recs, uint2* fix, const uint16_t* summ, Ctrl* ctrl,
+                               hipStream_t st);
 hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
                                        const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                        uint64_t* status, uint32_t ntiles, uint32_t ticket_base,

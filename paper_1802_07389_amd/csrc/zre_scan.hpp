@@ -153,6 +153,39 @@ TLC_HD uint32_t rs_zero_walk(uint32_t len, uint32_t phi, Put&& put) {
   return t % kRunMax;
 }
 
+// Closed forms for a short segment of len <= 16 bytes given by the mask nz
+// of its non-121 bytes (bit i: byte i; no bits at or above len).  A run
+// between two non-121 bytes is then at most 14 bytes long and costs
+// exactly one code, so the summary needs only the leading and trailing run
+// lengths, the count of non-121 bytes and the count of gaps between them
+// (maximal runs of set bits, less one).  rs_mask_walk encodes the segment
+// after phase phi, visiting only the non-121 bytes (byte(i) returns byte
+// i), and returns the new phase.
+TLC_HD RunSum rs_mask_summary(uint32_t nz, uint32_t len) {
+  if (nz == 0u) return rs_zero_run(len);
+  const uint32_t lead = (uint32_t)__builtin_ctz(nz);
+  const uint32_t trail = len - 1u - (31u - (uint32_t)__builtin_clz(nz));
+  const uint32_t runs = (uint32_t)__builtin_popcount(nz & ~(nz << 1));
+  const uint32_t cnt =
+      lead / kRunMax + (uint32_t)__builtin_popcount(nz) + (runs - 1u) + trail / kRunMax;
+  return rs_make(0u, lead % kRunMax, trail % kRunMax, cnt);
+}
+
+template <class Byte, class Put>
+TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byte, Put&& put) {
+  uint32_t pos = 0u;
+  while (nz) {
+    const uint32_t p = (uint32_t)__builtin_ctz(nz);
+    nz &= nz - 1u;
+    phi = rs_zero_walk(p - pos, phi, put);
+    if (phi != 0u) put(rs_code(phi));
+    phi = 0u;
+    put(byte(p));
+    pos = p + 1u;
+  }
+  return rs_zero_walk(len - pos, phi, put);
+}
+
 // rs_step over `count` bytes.  The caller writes the final remainder code
 // (rs_code) if the stream ends with a non-zero phase.
 template <class Put>

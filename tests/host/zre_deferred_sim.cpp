@@ -11,6 +11,9 @@
 //     write (phi + L) / 14 codes 255, then (if the tile has a non-121 byte)
 //     the remainder code of (phi + L) mod 14 and the slot; after the last
 //     tile, the remainder of a run that ends the stream.
+// For PER <= 16 every thread's segment is also summarised and encoded from
+// the mask of its non-121 bytes (rs_mask_summary, rs_mask_walk), which must
+// agree with the byte-by-byte forms (exit 4, 5, 6 otherwise).
 // Reads raw bytes on stdin, writes the encoded stream on stdout.
 // Usage: zre_deferred_sim TILE PER < in > out
 #include <cstdio>
@@ -51,11 +54,29 @@ int main(int argc, char** argv) {
     for (size_t lo = 0; lo < tb; lo += per) {
       const size_t hi = lo + per < tb ? lo + per : tb;
       const size_t s0 = lo > L ? lo : L;
-      uint32_t o = rs_emitted(pre), phi = rs_phase(pre);
+      const uint32_t o0 = rs_emitted(pre), phi0 = rs_phase(pre);
+      uint32_t o = o0, phi = phi0;
       RunSum own = rs_identity();
       for (size_t j = s0; j < hi; ++j) {
         phi = rs_step(q[q0 + j], phi, [&](uint32_t b) { slots[t * tile + o++] = (uint8_t)b; });
         own = rs_combine(own, rs_byte(q[q0 + j]));
+      }
+      // the same segment from the mask of its non-121 bytes (segments of
+      // at most 16 bytes): summary and bytes must agree
+      if (per <= 16) {
+        const uint32_t len = s0 < hi ? (uint32_t)(hi - s0) : 0u;
+        uint32_t nz = 0u;
+        for (uint32_t i = 0; i < len; ++i)
+          if (q[q0 + s0 + i] != kZeroGroup) nz |= 1u << i;
+        if (rs_mask_summary(nz, len).v != own.v) return 4;
+        uint32_t o2 = o0;
+        const uint32_t phi2 = rs_mask_walk(
+            nz, len, phi0, [&](uint32_t i) { return (uint32_t)q[q0 + s0 + i]; },
+            [&](uint32_t b) {
+              if (o2 >= o || slots[t * tile + o2] != (uint8_t)b) std::exit(5);
+              ++o2;
+            });
+        if (phi2 != phi || o2 != o) return 6;
       }
       pre = rs_combine(pre, own);
     }

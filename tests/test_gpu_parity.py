@@ -227,6 +227,54 @@ def test_threshold_boundaries(ctx):
         check_encode_decode(ctx, x, np.zeros_like(x), 1.0, tag=f"M={M_target}")
 
 
+@pytest.mark.parametrize("M_target", [1.0, 1.2345678, 3 * 2.0 ** -140])
+def test_float4_skip_bound_edges(ctx, M_target):
+    """Large tensors on the float4 path skip float4s whose bound from the
+    max pass (top 16 bits of the largest |acc|) is below U's top 16 bits.
+    Plant values at U, one ulp either side, and at both ends of U's top-half
+    bucket among small values, in every partition and at tile edges."""
+    g = G()
+    n = THREE_PASS_N[0]
+    m = -(-n // 5)
+    assert m % 4 == 0
+    M = F32(M_target)
+    half = np.float64(M) * (0.5 + 2.0 ** -25)
+    U = F32(half)
+    if np.float64(U) <= half:
+        U = np.nextafter(U, F32(np.inf))
+    ub = int(np.array([U], F32).view(np.uint32)[0])
+    edges = [ub, ub - 1, ub + 1, ub & ~0xFFFF, (ub & ~0xFFFF) - 1, ub | 0xFFFF,
+             ((ub >> 16) + 1) << 16, ((ub >> 16) - 1) << 16 | 0xFFFF]
+    # (for a subnormal U the top half is 0 and nothing may be skipped)
+    mb = int(np.array([M], F32).view(np.uint32)[0])
+    vals = np.array([e for e in edges if 0 < e < mb], np.uint32).view(F32)
+    assert vals.size >= 3 and (vals < M).all()
+    x = (workloads.normal([45], n, 1.0) * (M * F32(1e-3))).astype(F32)
+    rng = np.random.default_rng(46)
+    pos = set(int(p) for p in rng.integers(0, n, 400))
+    for k in range(5):
+        for t in (0, 1, 37, m // 4096 - 1):
+            for d in (0, 1, 3, 4, 4095):
+                pos.add(k * m + t * 4096 + d)
+    pos = sorted(p for p in pos if 0 <= p < n)
+    for i, p in enumerate(pos):
+        x[p] = vals[i % len(vals)] * (1 if i % 3 else -1)
+    x[n // 2 + 1] = M  # the largest |acc|: s = 1 gives exactly M
+    r = np.zeros(n, F32)
+    r_ref = r.copy()
+    st_ref, C_ref, M_ref = oracle.compress(x, r_ref, 1.0)
+    assert st_ref == 0 and M_ref == M
+    st, C, Mg, r_gpu = g.gpu_compress(ctx, x, r, 1.0)
+    assert st == 0 and Mg == M_ref
+    assert np.array_equal(C, C_ref)
+    assert np.array_equal(g.bits(r_gpu), g.bits(r_ref))
+    # a second step on the returned residual (acc = x + r)
+    st_ref, C_ref, M_ref = oracle.compress(x, r_ref, 1.0)
+    st, C, Mg, r_gpu2 = g.gpu_compress(ctx, x, r_gpu, 1.0)
+    assert st == st_ref == 0 and Mg == M_ref and np.array_equal(C, C_ref)
+    assert np.array_equal(g.bits(r_gpu2), g.bits(r_ref))
+
+
 def test_subnormals(ctx):
     x = (workloads.normal([50], 50000, 1.0) * F32(2.0 ** -130)).astype(F32)
     check_encode_decode(ctx, x, np.zeros_like(x), 1.0, tag="subnormal")
