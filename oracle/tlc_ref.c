@@ -75,7 +75,10 @@ void tlc_ref_dequantize(const int8_t* q, size_t n, float M, float* out,
                         int accumulate) {
   for (size_t i = 0; i < n; ++i) {
     float t = M * (float)q[i];
-    out[i] = accumulate ? out[i] + t : t;
+    if (!accumulate)
+      out[i] = t;
+    else if (q[i] != 0) /* a zero update leaves the aggregate as it is */
+      out[i] = out[i] + t;
   }
 }
 
@@ -389,7 +392,10 @@ int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_
   const float D = tlc_ref_int8_step(scale);
   for (size_t i = 0; i < n; ++i) {
     const float v = (float)(int8_t)bytes[i] * D;
-    out[i] = accumulate ? out[i] + v : v;
+    if (!accumulate)
+      out[i] = v;
+    else if (bytes[i] != 0) /* a zero code leaves the aggregate as it is */
+      out[i] = out[i] + v;
   }
   return TLC_REF_OK;
 }

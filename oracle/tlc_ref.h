@@ -54,7 +54,10 @@ int tlc_ref_absmax_scale(const float* acc, size_t n, float s, float* scale);
 void tlc_ref_quantize(const float* acc, size_t n, float M, int8_t* q,
                       float* resid);
 
-/* Eq. 3: out[i] = M*q[i], or out[i] = out[i] + M*q[i] when accumulate. */
+/* Eq. 3: out[i] = M*q[i], or, when accumulate, out[i] = out[i] + M*q[i]
+ * for q[i] != 0.  A value with q[i] = 0 adds nothing to the aggregate and
+ * keeps its bits (IEEE would turn -0 + 0 into +0 and quiet a signalling
+ * NaN; the decoder leaves both alone). */
 void tlc_ref_dequantize(const int8_t* q, size_t n, float M, float* out,
                         int accumulate);
 
@@ -125,9 +128,10 @@ void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float
 int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
                           size_t cap, size_t* len, float* scale);
 
-/* Decoder: out_i = fl(q_i * D) or fl(out_i + fl(q_i * D)), D = fl(scale /
- * 127), every int8 code accepted; len != n is TLC_REF_E_CORRUPT with out
- * unchanged. */
+/* Decoder: out_i = fl(q_i * D) or, accumulating, fl(out_i + fl(q_i * D))
+ * for q_i != 0 (out_i kept for q_i = 0, as in tlc_ref_dequantize), D =
+ * fl(scale / 127), every int8 code accepted; len != n is
+ * TLC_REF_E_CORRUPT with out unchanged. */
 int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_t n,
                             float* out, int accumulate);
 

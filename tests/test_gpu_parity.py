@@ -282,7 +282,8 @@ def test_subnormals(ctx):
 
 
 def test_negative_zero_accumulate(ctx):
-    """Dense Eq. 3: -0.0 + M*0 = +0.0 on both sides."""
+    """Accumulating keeps -0.0 where q = 0 and adds M*q elsewhere, as in the
+    oracle."""
     n = 4096
     x = workloads.normal([60], n, 1.0)
     out0 = np.full(n, -0.0, F32)

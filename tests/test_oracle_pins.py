@@ -363,13 +363,33 @@ def test_empty_tensor():
 
 # ------------------------------------------------------------------ Eq. 3
 def test_dequantize_and_signed_zero_accumulate():
-    """Eq. 3 applied densely: -0.0 + M*0 gives +0.0 (every element written)."""
+    """Eq. 3; accumulating adds M*q only where q != 0, so -0.0 with q = 0
+    stays -0.0 (IEEE -0 + 0 would give +0); without accumulation every
+    element is M*q."""
     q = np.array([1, 0, -1, 0], np.int8)
     out = np.array([-0.0, -0.0, 2.0, 5.0], F32)
     oracle.dequantize(q, F32(0.25), out, accumulate=True)
-    assert np.array_equal(bits(out), bits(np.array([0.25, 0.0, 1.75, 5.0], F32)))
+    assert np.array_equal(bits(out), bits(np.array([0.25, -0.0, 1.75, 5.0], F32)))
     out = oracle.dequantize(q, F32(0.25))
     assert np.array_equal(bits(out), bits(np.array([0.25, 0.0, -0.25, 0.0], F32)))
+
+
+def test_zero_update_leaves_aggregate_bits():
+    """A stream of all-zero groups (the encoding of an all-zero change)
+    accumulated into any aggregate leaves every bit as it was: -0.0, +-Inf
+    and NaNs with payloads included."""
+    n = 1003
+    special = np.array([0x80000000, 0x7F800000, 0xFF800000, 0x7FC00001, 0x7F800001,
+                        0xFFFFFFFF, 0x00000001, 0x80000001], np.uint32)
+    out0 = workloads.normal([502], n, 1.0)
+    out0.view(np.uint32)[::7][:special.size] = special
+    st, C, M = oracle.compress(np.zeros(n, F32), np.zeros(n, F32), 1.0)
+    assert st == oracle.OK and M == 0.0
+    for scale in (0.0, 1.0):  # any scale: q = 0 everywhere
+        st, out = oracle.decompress(C, scale, n, out0.copy(), accumulate=True)
+        assert st == oracle.OK and np.array_equal(bits(out), bits(out0))
+    st, out = oracle.decompress_int8(np.zeros(n, np.uint8), 1.0, n, out0.copy(), True)
+    assert st == oracle.OK and np.array_equal(bits(out), bits(out0))
 
 
 def test_decompress_corrupt_leaves_out_unchanged():
