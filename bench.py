@@ -49,7 +49,9 @@ def algorithmic_bytes(n, c, nnz):
         # hands them over in its per-tile lists)
         "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 4 * nnz,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
-        "tlc_expand_dequant_kernel": c + 8 * n,          # read C; read+write out
+        # read C; accumulating, out changes only where q != 0 (read + write
+        # of those nnz values; ranges with many non-zero bytes sweep densely)
+        "tlc_expand_dequant_kernel": c + 8 * nnz,
     }
 
 

@@ -245,17 +245,18 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
     const uint32_t lo = (a != 0u && f >= 1u) ? qw[f - 1] : 0u;
     const uint32_t hi = 4u * f < qn ? qw[f] : 0u;
     const uint32_t w4 = a ? (uint32_t)((((uint64_t)hi << 32) | lo) >> (8u * (4u - a))) : hi;
-    float v[4];
+    uint32_t d[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = trit_value((((w4 >> (8 * c)) & 0xffu) / kPlace) % 3u, M);
+    for (int c = 0; c < 4; ++c) d[c] = (((w4 >> (8 * c)) & 0xffu) / kPlace) % 3u;
     if (full[i]) {
       if (kAcc) {
-        o[i].x = o[i].x + v[0];
-        o[i].y = o[i].y + v[1];
-        o[i].z = o[i].z + v[2];
-        o[i].w = o[i].w + v[3];
+        o[i].x = acc_trit(o[i].x, d[0], M);
+        o[i].y = acc_trit(o[i].y, d[1], M);
+        o[i].z = acc_trit(o[i].z, d[2], M);
+        o[i].w = acc_trit(o[i].w, d[3], M);
       } else {
-        o[i] = make_float4(v[0], v[1], v[2], v[3]);
+        o[i] = make_float4(trit_value(d[0], M), trit_value(d[1], M), trit_value(d[2], M),
+                           trit_value(d[3], M));
       }
       if (kNT)
         st_stream(out + e, o[i]);
@@ -265,7 +266,8 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const uint32_t p = 4u * f + c;
-        if (p >= a && p - a < qn && e + c < n) out[e + c] = kAcc ? out[e + c] + v[c] : v[c];
+        if (p >= a && p - a < qn && e + c < n)
+          out[e + c] = kAcc ? acc_trit(out[e + c], d[c], M) : trit_value(d[c], M);
       }
     }
   }
@@ -308,10 +310,10 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 #pragma unroll
         for (int k = 0; k < 5; ++k) {
           if (kAcc) {
-            o[k].x = o[k].x + trit_value(t[0][k], M);
-            o[k].y = o[k].y + trit_value(t[1][k], M);
-            o[k].z = o[k].z + trit_value(t[2][k], M);
-            o[k].w = o[k].w + trit_value(t[3][k], M);
+            o[k].x = acc_trit(o[k].x, t[0][k], M);
+            o[k].y = acc_trit(o[k].y, t[1][k], M);
+            o[k].z = acc_trit(o[k].z, t[2][k], M);
+            o[k].w = acc_trit(o[k].w, t[3][k], M);
           } else {
             o[k].x = trit_value(t[0][k], M);
             o[k].y = trit_value(t[1][k], M);
@@ -326,10 +328,7 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
             const uint64_t e = k * m + j + cc;
-            if (e < n) {
-              const float v = trit_value(t[cc][k], M);
-              out[e] = kAcc ? out[e] + v : v;
-            }
+            if (e < n) out[e] = kAcc ? acc_trit(out[e], t[cc][k], M) : trit_value(t[cc][k], M);
           }
         }
       }
@@ -342,13 +341,47 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 #pragma unroll
       for (int k = 0; k < 5; ++k) {
         const uint64_t e = k * m + j;
-        if (e < n) {
-          const float v = trit_value(t[k], M);
-          out[e] = kAcc ? out[e] + v : v;
-        }
+        if (e < n) out[e] = kAcc ? acc_trit(out[e], t[k], M) : trit_value(t[k], M);
       }
     }
   }
+}
+
+// ---------------------------------------------------------------- sparse Eq. 3
+// Accumulating, a value with q = 0 is left alone (it adds nothing), so a
+// range whose quartic bytes are mostly 121 only has to touch the values
+// of its other bytes: each thread takes the non-121 bytes among its 16 and
+// adds M*q into out for their non-zero digits (one read and one write per
+// value, instead of the whole range's five partition slices).  A range
+// with a stream segment of at most kSparseStream bytes is tried this way;
+// if it holds more than kSparseBytes non-121 bytes it takes the dense
+// sweep after all.
+constexpr uint32_t kSparseStream = 1024;
+constexpr uint32_t kSparseBytes = 256;
+
+// Returns false, having written nothing, when the range is too dense.
+// s_q holds the range's qn quartic bytes (expand_range); red is reused.
+__device__ __forceinline__ bool sparse_accumulate(const uint8_t* s_q, uint64_t q0, uint32_t qn,
+                                                  uint64_t n, uint64_t m, float M,
+                                                  float* __restrict__ out, uint32_t* red) {
+  static_assert(kDecRange / kThreads == 16, "16 quartic bytes per thread");
+  const uint32_t lo = threadIdx.x * 16u;
+  const uint32_t cnt = lo < qn ? min<uint32_t>(16u, qn - lo) : 0u;
+  uint32_t nz = cnt ? nonzero_group_mask(s_q, lo, cnt) : 0u;
+  if (block_scan_u32((uint32_t)__popc(nz), red).total > kSparseBytes) return false;
+  while (nz) {
+    const uint32_t i = (uint32_t)__builtin_ctz(nz);
+    nz &= nz - 1u;
+    const uint64_t j = q0 + lo + i;
+    uint32_t t[5];
+    digits5(s_q[lo + i], t);
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const uint64_t e = (uint64_t)k * m + j;
+      if (t[k] != 1u && e < n) out[e] = out[e] + trit_value(t[k], M);
+    }
+  }
+  return true;
 }
 
 // One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
@@ -363,6 +396,12 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  if (kAcc && range_end(start, k, m, c) - (uint32_t)(start[k] >> 8) <= kSparseStream) {
+    expand_range(C, c, start, k, m, qn, s_q, red);
+    if (!sparse_accumulate(s_q, q0, qn, n, m, M, out, red))
+      dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    return;
+  }
   if (kPath == kPathShift && kAcc && kNT) {
     // large outputs: the first two partitions' loads overlap the expansion
     // (on gfx950 15 us of 410 on a 2^28-value decode; outputs that fit the
@@ -467,10 +506,9 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
         uint32_t t[5];
         digits5((w >> (8 * cc)) & 0xffu, t);
 #pragma unroll
-        for (int kk = 0; kk < 5; ++kk) {
-          const float v = trit_value(t[kk], d.scale);
-          acc[g][kk][cc] = (!kAcc && p == 0) ? v : acc[g][kk][cc] + v;
-        }
+        for (int kk = 0; kk < 5; ++kk)
+          acc[g][kk][cc] = (!kAcc && p == 0) ? trit_value(t[kk], d.scale)
+                                             : acc_trit(acc[g][kk][cc], t[kk], d.scale);
       }
     }
     __syncthreads();  // s_q is rewritten by the next stream

@@ -335,6 +335,27 @@ __device__ __forceinline__ float trit_value(uint32_t t, float M) {
   return t == 0u ? -M : (t == 1u ? 0.0f : M);
 }
 
+// Eq. 3 accumulated into out: out + M*q for q != 0; a zero trit (t = 1)
+// adds nothing and leaves out's bits as they are (-0.0 and NaN payloads
+// included).
+__device__ __forceinline__ float acc_trit(float out, uint32_t t, float M) {
+  return t == 1u ? out : out + trit_value(t, M);
+}
+
+// Mask of the non-121 bytes among the 16 quartic bytes q[lo .. lo + cnt)
+// (cnt <= 16; q + lo 16-byte aligned) that one thread holds: bit i for
+// byte lo + i.
+__device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
+                                                       uint32_t cnt) {
+  const uint4 w = *reinterpret_cast<const uint4*>(q + lo);
+  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+  uint32_t nz = 0u;
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    nz |= (((wd[i / 4] >> (8 * (i % 4))) & 0xffu) != kZeroGroup ? 1u : 0u) << i;
+  return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
+}
+
 // Base-3 digits of a quartic byte, most significant first (weights 81, 27,
 // 9, 3, 1): Section 3.2, decoding step 1.
 __device__ __forceinline__ void digits5(uint32_t byte, uint32_t (&t)[5]) {

@@ -213,19 +213,7 @@ struct EncShared {
   __align__(16) uint8_t out[kEncTile + 16];
 };
 
-// Mask of the non-121 bytes among the kEncTile / kThreads = 16 quartic
-// bytes q[lo .. lo + cnt) of one thread (bit i: byte lo + i).
-__device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
-                                                       uint32_t cnt) {
-  static_assert(kEncTile / kThreads == 16, "one uint4 of quartic bytes per thread");
-  const uint4 w = *reinterpret_cast<const uint4*>(q + lo);
-  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
-  uint32_t nz = 0u;
-#pragma unroll
-  for (int i = 0; i < 16; ++i)
-    nz |= (((wd[i / 4] >> (8 * (i % 4))) & 0xffu) != kZeroGroup ? 1u : 0u) << i;
-  return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
-}
+static_assert(kEncTile / kThreads == 16, "one uint4 of quartic bytes per thread");
 
 // Phase 1 of a tile (Eq. 2, residual write-back, quartic pack): the block
 // quantizes the 5 * tile_bytes accumulated values of quartic bytes

@@ -7,7 +7,7 @@
 //                            one int8 byte per value; acc is the buffer
 //                            that tlc_accum_absmax_kernel has accumulated
 //                            (error feedback) or the tensor itself
-//   tlc_int8_dequant_kernel  out = code * D, or out + code * D
+//   tlc_int8_dequant_kernel  out = code * D, or out + code * D for code != 0
 //
 // Both are elementwise streams: a block covers kI8Rows rows of 1024 values;
 // in a row lane t owns values 4t .. 4t + 3 (one float4 per tensor and one
@@ -40,6 +40,11 @@ __device__ __forceinline__ uint32_t int8_byte(float code) {
 // Value of one byte: fl(code * D) (code 0 gives +0).
 __device__ __forceinline__ float int8_value(uint32_t byte, float D) {
   return __fmul_rn((float)(int32_t)(int8_t)(uint8_t)byte, D);
+}
+
+// out + fl(code * D) for a non-zero code; code 0 leaves out's bits alone.
+__device__ __forceinline__ float int8_acc(float out, uint32_t byte, float D) {
+  return (byte & 0xffu) == 0u ? out : __fadd_rn(out, int8_value(byte, D));
 }
 
 // One value: code byte and (kResid) residual acc - fl(code * D).
@@ -139,23 +144,20 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_dequant_kernel(
       for (int i = 0; i < kI8Batch; ++i) {
         const uint64_t e = base + (uint64_t)(h + i) * kI8Row + 4u * threadIdx.x;
         if (full[i]) {
-          const float v0 = int8_value(w[i], D), v1 = int8_value(w[i] >> 8, D);
-          const float v2 = int8_value(w[i] >> 16, D), v3 = int8_value(w[i] >> 24, D);
           float4 res;
           if (kAcc) {
-            res = make_float4(__fadd_rn(o[i].x, v0), __fadd_rn(o[i].y, v1),
-                              __fadd_rn(o[i].z, v2), __fadd_rn(o[i].w, v3));
+            res = make_float4(int8_acc(o[i].x, w[i], D), int8_acc(o[i].y, w[i] >> 8, D),
+                              int8_acc(o[i].z, w[i] >> 16, D), int8_acc(o[i].w, w[i] >> 24, D));
           } else {
-            res = make_float4(v0, v1, v2, v3);
+            res = make_float4(int8_value(w[i], D), int8_value(w[i] >> 8, D),
+                              int8_value(w[i] >> 16, D), int8_value(w[i] >> 24, D));
           }
           st_stream(out + e, res);
         } else {
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
-            if (e + c < n) {
-              const float v = int8_value(C[e + c], D);
-              out[e + c] = kAcc ? __fadd_rn(out[e + c], v) : v;
-            }
+            if (e + c < n)
+              out[e + c] = kAcc ? int8_acc(out[e + c], C[e + c], D) : int8_value(C[e + c], D);
           }
         }
       }
@@ -164,8 +166,7 @@ __global__ __launch_bounds__(kThreads) void tlc_int8_dequant_kernel(
     for (uint32_t k = threadIdx.x; k < kI8Row * kI8Rows; k += kThreads) {
       const uint64_t e = base + k;
       if (e >= n) break;
-      const float v = int8_value(C[e], D);
-      out[e] = kAcc ? __fadd_rn(out[e], v) : v;
+      out[e] = kAcc ? int8_acc(out[e], C[e], D) : int8_value(C[e], D);
     }
   }
 }
