@@ -39,15 +39,18 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", DOMINANT + "_c4_traffic.md")
 def algorithmic_bytes(n, c, nnz):
     tiles = -(-(-(-n // 5)) // 4096)  # 4096-byte quartic tiles
     return {
-        "tlc_accum_absmax_kernel": 12 * n,               # read x, r; write r = x + r
-        # read r; write each tile's own stream bytes (c in all) and record
-        "tlc_quant_encode_kernel": 4 * n + c + 16 * tiles,
+        # read x, r; write r = x + r (the 2-byte bound per float4 it also
+        # writes, n/2 bytes, is not counted)
+        "tlc_accum_absmax_kernel": 12 * n,
+        # read the bounds (n/2) and at most one float4 per value with q != 0;
+        # write each tile's own stream bytes (c in all), record and the
+        # (index, residual) list of its values with q != 0
+        "tlc_quant_encode_kernel": n // 2 + 16 * nnz + c + 16 * tiles + 8 * nnz,
         # tile records in, tile prefixes and chunk summaries out
         "tlc_zre_chunk_kernel": 24 * tiles,
-        # records, prefixes and slot bytes in, the stream out, and the
-        # residuals of the nnz values with q != 0 into r (the first pass
-        # hands them over in its per-tile lists)
-        "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 4 * nnz,
+        # records, prefixes and slot bytes in, the stream out, and the lists'
+        # residuals into r
+        "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 12 * nnz,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
         # read C; accumulating, out changes only where q != 0 (read + write
         # of those nnz values; ranges with many non-zero bytes sweep densely)
