@@ -350,35 +350,57 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 // ---------------------------------------------------------------- sparse Eq. 3
 // Accumulating, a value with q = 0 is left alone (it adds nothing), so a
 // range whose quartic bytes are mostly 121 only has to touch the values
-// of its other bytes: each thread takes the non-121 bytes among its 16 and
-// adds M*q into out for their non-zero digits (one read and one write per
-// value, instead of the whole range's five partition slices).  A range
-// with a stream segment of at most kSparseStream bytes is tried this way;
-// if it holds more than kSparseBytes non-121 bytes it takes the dense
-// sweep after all.
+// of its other bytes.  Those are the stream's literal bytes other than 121
+// (a run code, or 121 itself, expands to zero groups only).  One block
+// scan over the range's stream bytes gives both each byte's position and
+// the count of such literals (packed as length + (literals << 16): a
+// range expands to fewer than 4096 + 28 bytes and a thread's 16 stream
+// bytes to at most 224, so no carry crosses); if there are at most
+// kSparseBytes, each thread adds M*q into out for the non-zero digits of
+// its literals, one read and one write per value.  Ranges with a stream
+// slice longer than kSparseStream bytes are not tried.
 constexpr uint32_t kSparseStream = 1024;
 constexpr uint32_t kSparseBytes = 256;
 
 // Returns false, having written nothing, when the range is too dense.
-// s_q holds the range's qn quartic bytes (expand_range); red is reused.
-__device__ __forceinline__ bool sparse_accumulate(const uint8_t* s_q, uint64_t q0, uint32_t qn,
-                                                  uint64_t n, uint64_t m, float M,
-                                                  float* __restrict__ out, uint32_t* red) {
-  static_assert(kDecRange / kThreads == 16, "16 quartic bytes per thread");
-  const uint32_t lo = threadIdx.x * 16u;
-  const uint32_t cnt = lo < qn ? min<uint32_t>(16u, qn - lo) : 0u;
-  uint32_t nz = cnt ? nonzero_group_mask(s_q, lo, cnt) : 0u;
-  if (block_scan_u32((uint32_t)__popc(nz), red).total > kSparseBytes) return false;
-  while (nz) {
-    const uint32_t i = (uint32_t)__builtin_ctz(nz);
-    nz &= nz - 1u;
-    const uint64_t j = q0 + lo + i;
-    uint32_t t[5];
-    digits5(s_q[lo + i], t);
+__device__ __forceinline__ bool sparse_expand_accumulate(
+    const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ starts, uint32_t k,
+    uint64_t n, uint64_t m, uint64_t q0, uint32_t qn, float M, float* __restrict__ out,
+    uint32_t* red) {
+  constexpr int kBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
+  const uint64_t s0 = starts[k];
+  const uint32_t i0 = (uint32_t)(s0 >> 8);
+  const uint32_t skip = (uint32_t)(s0 & 255u);
+  const uint32_t i1 = range_end(starts, k, m, c);
+  const uint32_t count = i1 > i0 ? min<uint32_t>(i1 - i0, kDecRange) : 0u;
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < count ? min<uint32_t>(kBytes, count - lo) : 0u;
+  uint8_t b[kBytes];
 #pragma unroll
-    for (int k = 0; k < 5; ++k) {
-      const uint64_t e = (uint64_t)k * m + j;
-      if (t[k] != 1u && e < n) out[e] = out[e] + trit_value(t[k], M);
+  for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[i0 + lo + i] : (uint8_t)0;
+  uint32_t packed = 0u;
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i)
+    if ((uint32_t)i < cnt)
+      packed += expanded_len(b[i]) + (b[i] < kRunBase && b[i] != kZeroGroup ? 1u << 16 : 0u);
+  const ScanU32 sc = block_scan_u32(packed, red);
+  if ((sc.total >> 16) > kSparseBytes) return false;
+  int pos = (int)(sc.excl & 0xffffu) - (int)skip;  // range-relative position of b[0]
+#pragma unroll
+  for (int i = 0; i < kBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t x = b[i];
+      if (x < kRunBase && x != kZeroGroup && pos >= 0 && (uint32_t)pos < qn) {
+        const uint64_t j = q0 + (uint32_t)pos;
+        uint32_t t[5];
+        digits5(x, t);
+#pragma unroll
+        for (int kk = 0; kk < 5; ++kk) {
+          const uint64_t e = (uint64_t)kk * m + j;
+          if (t[kk] != 1u && e < n) out[e] = out[e] + trit_value(t[kk], M);
+        }
+      }
+      pos += (int)expanded_len(x);
     }
   }
   return true;
@@ -397,9 +419,10 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
   if (kAcc && range_end(start, k, m, c) - (uint32_t)(start[k] >> 8) <= kSparseStream) {
+    if (sparse_expand_accumulate(C, c, start, k, n, m, q0, qn, M, out, red)) return;
+    __syncthreads();  // red is reused by the expansion
     expand_range(C, c, start, k, m, qn, s_q, red);
-    if (!sparse_accumulate(s_q, q0, qn, n, m, M, out, red))
-      dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
     return;
   }
   if (kPath == kPathShift && kAcc && kNT) {

@@ -67,6 +67,29 @@ def test_single_stream(ctx, n, offset):
     assert np.array_equal(g.bits(out), g.bits(ref)), (n, offset)
 
 
+@pytest.mark.parametrize("every", [10, 17, 60])
+def test_single_stream_literal_density(ctx, every):
+    """Non-zero quartic bytes at two offsets every `every` bytes.  10: a
+    range's stream slice passes 1024 bytes (dense sweep from the start);
+    17: about 960 stream bytes but about 480 non-121 bytes, over the 256 at
+    which the sparse attempt goes back to the dense sweep; 60: about 140,
+    the sparse update."""
+    g = G()
+    n = 5 * 4096 * 3 + 20
+    m = -(-n // 5)
+    x, out0 = sparse_case(940 + every, n, spikes=0)
+    x[:m:every] = 1.0  # partition 0: q = 1 (s = 1: M = 1)
+    x[3 * m + 5:4 * m:every] = -1.0
+    zero = x == 0
+    out0[~zero] = workloads.normal([941, every], int((~zero).sum()), 1.0)
+    out0[np.flatnonzero(~zero)[::5]] = -0.0
+    C, M = encode(x)
+    st_ref, ref = oracle.decompress(C, M, n, out0.copy(), accumulate=True)
+    st, out = g.gpu_decompress(ctx, C, M, n, out0.copy(), accumulate=True)
+    assert st == st_ref == 0
+    assert np.array_equal(g.bits(out), g.bits(ref)), every
+
+
 def test_single_stream_large(ctx):
     """2^27 values: the decode of outputs of 512 MiB and more (nontemporal
     sweep)."""
