@@ -61,6 +61,31 @@ __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
   return r;
 }
 
+// Exclusive max-scan over the block (0 for thread 0) and the block's max
+// (all threads; ends with a barrier-protected read of lds).
+__device__ __forceinline__ ScanU32 block_scan_max_u32(uint32_t v, uint32_t* lds) {
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t o = __shfl_up(incl, d, 64);
+    if (lane >= (uint32_t)d) incl = max(incl, o);
+  }
+  uint32_t excl = __shfl_up(incl, 1, 64);
+  if (lane == 0) excl = 0u;
+  if (lane == 63) lds[wid] = incl;
+  __syncthreads();
+  ScanU32 r;
+  r.excl = excl;
+  r.total = 0u;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    if ((uint32_t)w < wid) r.excl = max(r.excl, lds[w]);
+    r.total = max(r.total, lds[w]);
+  }
+  return r;
+}
+
 // How a kernel reaches the five partitions of a tile: one float4 per
 // partition slice (m % 4 == 0, 16-byte aligned tensors), aligned float4
 // cells off the slice grid (aligned tensors, m % 4 != 0), or one quartic

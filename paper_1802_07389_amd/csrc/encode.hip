@@ -207,6 +207,8 @@ struct EncShared {
   uint32_t fault;
   uint32_t nfix;   // entries taken in the tile's fix list (may pass kFixCap)
   uint32_t nneed;  // float4 slices the tile has to load (summaries)
+  uint32_t red2[kWaves];
+  uint32_t lead;   // the tile's first non-121 byte (first pass)
   RunSum wave[kWaves];
   RunSum excl;
   __align__(16) uint8_t q[kEncTile];
@@ -349,19 +351,6 @@ __device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, u
 //     need the incoming phase (one 255 per 14th byte of the grown run, then
 //     its remainder code if the tile has a non-121 byte), and the slot; the
 //     last tile adds the remainder of a run that ends the stream.
-
-// Block-wide minimum; every thread gets the result (lds[kWaves], one
-// barrier; callers that reuse lds must barrier again first).
-__device__ __forceinline__ uint32_t block_min(uint32_t v, uint32_t* lds) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, d, 64));
-  if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = v;
-  __syncthreads();
-  uint32_t r = lds[0];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) r = min(r, lds[w]);
-  return r;
-}
 
 // Residual v of the tile's value `local` (k * kEncTile + position) when
 // `has`: the wave takes consecutive entries of the tile's fix list (in LDS)
@@ -589,57 +578,47 @@ void tlc_quant_encode_kernel(
     quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
   }
 
-  // ---- Section 3.3 from the tile's first non-121 byte (index L) on
-  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
+  // ---- Section 3.3 from the tile's first non-121 byte on, from the gaps
+  // between non-121 bytes: a max-scan over the threads' last non-121
+  // positions gives each thread the previous one, a sum-scan of what each
+  // thread emits gives its output offset (zre_scan.hpp: rs_gaps_len,
+  // rs_gaps_emit); the thread with the tile's last non-121 byte adds the
+  // trailing run's codes 255.
   const uint32_t lo = threadIdx.x * kBytes;
   const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
   const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
-  const uint32_t first = nz ? lo + (uint32_t)__builtin_ctz(nz) : tile_bytes;
-  const uint32_t L = block_min(first, sh.red);
-  const bool mine = lo + cnt > L;  // the thread holds bytes at index >= L
-  // the thread's segment: its bytes at index >= L
-  const uint32_t s0 = mine && L > lo ? L - lo : 0u;
-  const uint32_t seg = mine ? cnt - s0 : 0u;
-  const uint32_t seg_nz = mine ? nz >> s0 : 0u;
-  const RunSum own = rs_mask_summary(seg_nz, seg);
-  RunSum incl = own;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    RunSum o = shfl_up_rs(incl, d);
-    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
-  }
-  RunSum excl_lane = shfl_up_rs(incl, 1);
-  if (lane == 0) excl_lane = rs_identity();
-  if (lane == 63) sh.wave[wid] = incl;
-  __syncthreads();
-  RunSum wpre = rs_identity();
-  RunSum agg = rs_identity();
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    if ((uint32_t)w < wid) wpre = rs_combine(wpre, sh.wave[w]);
-    agg = rs_combine(agg, sh.wave[w]);
-  }
-  const RunSum P = rs_combine(wpre, excl_lane);
-  uint32_t o = rs_emitted(P);
-  uint32_t phi = rs_phase(P);
+  const uint32_t last = nz ? lo + 31u - (uint32_t)__builtin_clz(nz) : 0u;
+  const ScanU32 pm = block_scan_max_u32(nz ? last + 1u : 0u, sh.red);
+  const int prev = (int)pm.excl - 1;  // the previous non-121 byte, -1 if none
+  const bool tail = nz != 0u && last + 1u == pm.total;
+  if (nz != 0u && prev < 0) sh.lead = lo + (uint32_t)__builtin_ctz(nz);
+  const uint32_t trail = tile_bytes - pm.total;  // 121s after the last non-121 byte
+  const uint32_t mine = rs_gaps_len(nz, lo, prev) + (tail ? trail / kRunMax : 0u);
+  const ScanU32 off = block_scan_u32(mine, sh.red2);
+  uint32_t o = off.excl;
   auto put = [&](uint32_t c) {
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
-  if (mine)
-    phi = rs_mask_walk(seg_nz, seg, phi,
-                       [&](uint32_t i) { return (uint32_t)sh.q[lo + s0 + i]; }, put);
+  rs_gaps_emit(nz, lo, prev, [&](uint32_t i) { return (uint32_t)sh.q[lo + i]; }, put);
+  if (tail) rs_zero_walk(trail, 0u, put);
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
-  const uint32_t len = min<uint32_t>(rs_emitted(agg), tile_bytes);
+  const uint32_t len = min<uint32_t>(off.total, tile_bytes);
   __syncthreads();
   for (uint32_t i = 16u * threadIdx.x; i < len; i += 16u * kThreads)
     *reinterpret_cast<uint4*>(slots + q0 + i) = *reinterpret_cast<const uint4*>(sh.out + i);
   if (threadIdx.x == 0) {
     TileRec rec;
-    rec.agg = rs_combine(rs_zero_run(L), agg).v;
-    rec.lead = (uint16_t)L;
-    rec.len = (uint16_t)len;
+    if (pm.total == 0u) {  // all 121: one run
+      rec.agg = rs_zero_run(tile_bytes).v;
+      rec.lead = (uint16_t)tile_bytes;
+      rec.len = 0u;
+    } else {
+      rec.agg = rs_combine(rs_zero_run(sh.lead), rs_make(0u, 0u, trail % kRunMax, off.total)).v;
+      rec.lead = (uint16_t)sh.lead;
+      rec.len = (uint16_t)len;
+    }
     rec.nfix = min<uint32_t>(sh.nfix, kFixCap);
     recs[t] = rec;
   }

@@ -186,6 +186,45 @@ TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byt
   return rs_zero_walk(len - pos, phi, put);
 }
 
+// A segment that starts at a non-121 byte (phase 0) in terms of the gaps
+// between its non-121 bytes: a gap of g bytes of 121 costs floor(g/14)
+// codes 255 and, if g mod 14 != 0, one remainder code; each non-121 byte
+// costs itself.  For the non-121 bytes of one thread (mask nz, bit i at
+// position lo + i) after the segment's previous non-121 byte at prev
+// (prev < 0: none; the thread's first byte then opens the segment),
+// rs_gaps_len counts the bytes they emit with their gaps and rs_gaps_emit
+// emits them; the trailing run after the segment's last non-121 byte emits
+// its floor(g/14) codes 255 separately (rs_zero_walk from phase 0).
+TLC_HD uint32_t rs_gap_len(uint32_t g) { return g / kRunMax + (g % kRunMax != 0u ? 1u : 0u); }
+
+TLC_HD uint32_t rs_gaps_len(uint32_t nz, uint32_t lo, int prev) {
+  uint32_t len = 0u;
+  while (nz) {
+    const uint32_t p = lo + (uint32_t)__builtin_ctz(nz);
+    nz &= nz - 1u;
+    if (prev >= 0) len += rs_gap_len(p - (uint32_t)prev - 1u);
+    len += 1u;
+    prev = (int)p;
+  }
+  return len;
+}
+
+template <class Byte, class Put>
+TLC_HD void rs_gaps_emit(uint32_t nz, uint32_t lo, int prev, Byte&& byte, Put&& put) {
+  while (nz) {
+    const uint32_t i = (uint32_t)__builtin_ctz(nz);
+    const uint32_t p = lo + i;
+    nz &= nz - 1u;
+    if (prev >= 0) {
+      const uint32_t g = p - (uint32_t)prev - 1u;
+      for (uint32_t e = 0; e < g / kRunMax; ++e) put(kFullChunk);
+      if (g % kRunMax != 0u) put(rs_code(g % kRunMax));
+    }
+    put(byte(i));
+    prev = (int)p;
+  }
+}
+
 // rs_step over `count` bytes.  The caller writes the final remainder code
 // (rs_code) if the stream ends with a non-zero phase.
 template <class Put>

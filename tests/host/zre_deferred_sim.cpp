@@ -13,7 +13,10 @@
 //     tile, the remainder of a run that ends the stream.
 // For PER <= 16 every thread's segment is also summarised and encoded from
 // the mask of its non-121 bytes (rs_mask_summary, rs_mask_walk), which must
-// agree with the byte-by-byte forms (exit 4, 5, 6 otherwise).
+// agree with the byte-by-byte forms (exit 4, 5, 6 otherwise), and every
+// tile is also encoded in the gap form (rs_gaps_len, rs_gaps_emit: output
+// offsets from a sum over threads, the previous non-121 byte from a max),
+// which must give the same slot and record (exit 7-10 otherwise).
 // Reads raw bytes on stdin, writes the encoded stream on stdout.
 // Usage: zre_deferred_sim TILE PER < in > out
 #include <cstdio>
@@ -82,6 +85,47 @@ int main(int argc, char** argv) {
     }
     rec[t] = {rs_combine(rs_zero_run((uint32_t)L), pre), (uint32_t)L, rs_emitted(pre)};
     if (rec[t].len > tb) return 3;
+    // the gap form (threads of `per` <= 16 bytes): previous non-121 byte by
+    // an exclusive max over the threads' last ones, output offsets by an
+    // exclusive sum of the threads' lengths; the thread with the tile's last
+    // non-121 byte adds the trailing run's codes 255
+    if (per <= 16) {
+      std::vector<uint32_t> nzs, lens;
+      int last_all = -1;
+      for (size_t lo = 0; lo < tb; lo += per) {
+        const size_t hi = lo + per < tb ? lo + per : tb;
+        uint32_t nz = 0u;
+        for (size_t j = lo; j < hi; ++j)
+          if (q[q0 + j] != kZeroGroup) nz |= 1u << (j - lo);
+        nzs.push_back(nz);
+        if (nz) last_all = (int)(lo + 31 - __builtin_clz(nz));
+      }
+      std::vector<uint8_t> gslot;
+      int prev = -1;
+      uint32_t total = 0u;
+      for (size_t ti = 0; ti < nzs.size(); ++ti) {
+        const uint32_t lo = (uint32_t)(ti * per), nz = nzs[ti];
+        const int last = nz ? (int)(lo + 31 - __builtin_clz(nz)) : -1;
+        uint32_t len = rs_gaps_len(nz, lo, prev);
+        if (nz && last == last_all) len += (uint32_t)(tb - 1 - last) / kRunMax;
+        const size_t before = gslot.size();
+        rs_gaps_emit(
+            nz, lo, prev, [&](uint32_t i) { return (uint32_t)q[q0 + lo + i]; },
+            [&](uint32_t b) { gslot.push_back((uint8_t)b); });
+        if (nz && last == last_all)
+          rs_zero_walk((uint32_t)(tb - 1 - last), 0u, [&](uint32_t b) { gslot.push_back((uint8_t)b); });
+        if (gslot.size() - before != len) return 7;
+        total += len;
+        if (nz) prev = last;
+      }
+      if (total != rec[t].len) return 8;
+      for (uint32_t i = 0; i < total; ++i)
+        if (gslot[i] != slots[t * tile + i]) return 9;
+      const RunSum agg = last_all < 0 ? rs_zero_run((uint32_t)tb)
+                                      : rs_combine(rs_zero_run((uint32_t)L),
+                                                   rs_make(0u, 0u, (uint32_t)(tb - 1 - last_all) % kRunMax, total));
+      if (agg.v != rec[t].agg.v) return 10;
+    }
   }
   // pass B
   std::vector<RunSum> excl(ntiles);
