@@ -583,7 +583,7 @@ void tlc_quant_encode_kernel(
   // positions gives each thread the previous one, a sum-scan of what each
   // thread emits gives its output offset (zre_scan.hpp: rs_gaps_len,
   // rs_gaps_emit); the thread with the tile's last non-121 byte adds the
-  // trailing run's codes 255.
+  // trailing run's codes 255 to its length.
   const uint32_t lo = threadIdx.x * kBytes;
   const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
   const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
@@ -594,14 +594,20 @@ void tlc_quant_encode_kernel(
   if (nz != 0u && prev < 0) sh.lead = lo + (uint32_t)__builtin_ctz(nz);
   const uint32_t trail = tile_bytes - pm.total;  // 121s after the last non-121 byte
   const uint32_t mine = rs_gaps_len(nz, lo, prev) + (tail ? trail / kRunMax : 0u);
+  // every output byte that is not a remainder code or a non-121 byte is a
+  // 255: fill the whole output with 255 first (the scan's barrier orders
+  // it before the writes below), so runs only advance the offset
+  static_assert(sizeof(sh.out) == 16 * (kThreads + 1), "one uint4 of output per thread, +1");
+  reinterpret_cast<uint4*>(sh.out)[threadIdx.x] = make_uint4(~0u, ~0u, ~0u, ~0u);
+  if (threadIdx.x == 0) reinterpret_cast<uint4*>(sh.out)[kThreads] = make_uint4(~0u, ~0u, ~0u, ~0u);
   const ScanU32 off = block_scan_u32(mine, sh.red2);
   uint32_t o = off.excl;
   auto put = [&](uint32_t c) {
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
-  rs_gaps_emit(nz, lo, prev, [&](uint32_t i) { return (uint32_t)sh.q[lo + i]; }, put);
-  if (tail) rs_zero_walk(trail, 0u, put);
+  rs_gaps_emit(nz, lo, prev, [&](uint32_t i) { return (uint32_t)sh.q[lo + i]; }, put,
+               [&](uint32_t k) { o += k; });
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
   const uint32_t len = min<uint32_t>(off.total, tile_bytes);

@@ -193,8 +193,10 @@ TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byt
 // position lo + i) after the segment's previous non-121 byte at prev
 // (prev < 0: none; the thread's first byte then opens the segment),
 // rs_gaps_len counts the bytes they emit with their gaps and rs_gaps_emit
-// emits them; the trailing run after the segment's last non-121 byte emits
-// its floor(g/14) codes 255 separately (rs_zero_walk from phase 0).
+// emits them, handing each gap's k codes 255 to fill(k) and every other
+// byte to put (a caller whose output already holds 255 everywhere only
+// advances its offset in fill); the trailing run after the segment's last
+// non-121 byte emits its floor(g/14) codes 255 separately.
 TLC_HD uint32_t rs_gap_len(uint32_t g) { return g / kRunMax + (g % kRunMax != 0u ? 1u : 0u); }
 
 TLC_HD uint32_t rs_gaps_len(uint32_t nz, uint32_t lo, int prev) {
@@ -209,15 +211,16 @@ TLC_HD uint32_t rs_gaps_len(uint32_t nz, uint32_t lo, int prev) {
   return len;
 }
 
-template <class Byte, class Put>
-TLC_HD void rs_gaps_emit(uint32_t nz, uint32_t lo, int prev, Byte&& byte, Put&& put) {
+template <class Byte, class Put, class Fill>
+TLC_HD void rs_gaps_emit(uint32_t nz, uint32_t lo, int prev, Byte&& byte, Put&& put,
+                         Fill&& fill) {
   while (nz) {
     const uint32_t i = (uint32_t)__builtin_ctz(nz);
     const uint32_t p = lo + i;
     nz &= nz - 1u;
     if (prev >= 0) {
       const uint32_t g = p - (uint32_t)prev - 1u;
-      for (uint32_t e = 0; e < g / kRunMax; ++e) put(kFullChunk);
+      fill(g / kRunMax);
       if (g % kRunMax != 0u) put(rs_code(g % kRunMax));
     }
     put(byte(i));

@@ -109,11 +109,13 @@ int main(int argc, char** argv) {
         uint32_t len = rs_gaps_len(nz, lo, prev);
         if (nz && last == last_all) len += (uint32_t)(tb - 1 - last) / kRunMax;
         const size_t before = gslot.size();
+        auto fill = [&](uint32_t k) {
+          for (uint32_t e = 0; e < k; ++e) gslot.push_back((uint8_t)kFullChunk);
+        };
         rs_gaps_emit(
             nz, lo, prev, [&](uint32_t i) { return (uint32_t)q[q0 + lo + i]; },
-            [&](uint32_t b) { gslot.push_back((uint8_t)b); });
-        if (nz && last == last_all)
-          rs_zero_walk((uint32_t)(tb - 1 - last), 0u, [&](uint32_t b) { gslot.push_back((uint8_t)b); });
+            [&](uint32_t b) { gslot.push_back((uint8_t)b); }, fill);
+        if (nz && last == last_all) fill((uint32_t)(tb - 1 - last) / kRunMax);
         if (gslot.size() - before != len) return 7;
         total += len;
         if (nz) prev = last;
