@@ -57,12 +57,15 @@ def lib():
     L.tlc_ref_compress.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
                                    ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
     L.tlc_ref_compress.restype = c_i
+    L.tlc_ref_compress_in_place.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
+                                            ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+    L.tlc_ref_compress_in_place.restype = c_i
     L.tlc_ref_decompress.argtypes = [vp, c_sz, c_f, c_sz, vp, c_i]
     L.tlc_ref_decompress.restype = c_i
     L.tlc_ref_philox4x32_10.argtypes = [vp, vp, vp]
     L.tlc_ref_philox4x32_10.restype = None
     L.tlc_ref_compress_nozre.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
-                                         ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+                                         ctypes.POINTER(c_sz), ctypes.POINTER(c_f), c_i]
     L.tlc_ref_compress_nozre.restype = c_i
     u64 = ctypes.c_uint64
     L.tlc_ref_compress_stochastic.argtypes = [vp, c_sz, c_f, u64, u64, vp, c_sz,
@@ -73,7 +76,7 @@ def lib():
     L.tlc_ref_int8_quantize.argtypes = [vp, c_sz, c_f, vp, vp]
     L.tlc_ref_int8_quantize.restype = None
     L.tlc_ref_compress_int8.argtypes = [vp, vp, c_sz, c_f, vp, c_sz,
-                                        ctypes.POINTER(c_sz), ctypes.POINTER(c_f)]
+                                        ctypes.POINTER(c_sz), ctypes.POINTER(c_f), c_i]
     L.tlc_ref_compress_int8.restype = c_i
     L.tlc_ref_decompress_int8.argtypes = [vp, c_sz, c_f, c_sz, vp, c_i]
     L.tlc_ref_decompress_int8.restype = c_i
@@ -156,8 +159,9 @@ def zre_decode(C, m):
     return st, Q
 
 
-def compress(x, r, s, cap=None):
+def compress(x, r, s, cap=None, in_place=False):
     """Encode x with error buffer r (updated in place, float32 contiguous).
+    in_place: tlc_ref_compress_in_place (on NaN/Inf r keeps x + r).
 
     Return (status, bytes uint8[len], M).
     """
@@ -170,8 +174,8 @@ def compress(x, r, s, cap=None):
     out = np.zeros(max(cap, 1), dtype=np.uint8)
     ln = ctypes.c_size_t(0)
     M = ctypes.c_float(0.0)
-    st = lib().tlc_ref_compress(_ptr(x), _ptr(r), n, s, out.ctypes.data, cap,
-                                ctypes.byref(ln), ctypes.byref(M))
+    fn = lib().tlc_ref_compress_in_place if in_place else lib().tlc_ref_compress
+    st = fn(_ptr(x), _ptr(r), n, s, out.ctypes.data, cap, ctypes.byref(ln), ctypes.byref(M))
     return st, out[:ln.value].copy(), M.value
 
 
@@ -195,7 +199,7 @@ def philox4x32_10(ctr, key):
     return [int(v) for v in out]
 
 
-def compress_nozre(x, r, s):
+def compress_nozre(x, r, s, in_place=False):
     """Quantize + quartic encode without zero-run encoding; r updated in place.
     Return (status, bytes, M)."""
     x = _f32(x)
@@ -205,7 +209,7 @@ def compress_nozre(x, r, s):
     ln = ctypes.c_size_t(0)
     M = ctypes.c_float(0.0)
     st = lib().tlc_ref_compress_nozre(_ptr(x), _ptr(r), x.size, s, out.ctypes.data, m,
-                                      ctypes.byref(ln), ctypes.byref(M))
+                                      ctypes.byref(ln), ctypes.byref(M), int(in_place))
     return st, out[:ln.value].copy(), M.value
 
 
@@ -237,7 +241,7 @@ def int8_quantize(acc, M, residual=True):
     return q, res
 
 
-def compress_int8(x, r, s):
+def compress_int8(x, r, s, in_place=False):
     """8-bit encode; r (float32, updated in place) or None for no error
     feedback.  Return (status, bytes, M)."""
     x = _f32(x)
@@ -247,7 +251,8 @@ def compress_int8(x, r, s):
     ln = ctypes.c_size_t(0)
     M = ctypes.c_float(0.0)
     st = lib().tlc_ref_compress_int8(_ptr(x), _ptr(r) if r is not None else None, x.size, s,
-                                     out.ctypes.data, x.size, ctypes.byref(ln), ctypes.byref(M))
+                                     out.ctypes.data, x.size, ctypes.byref(ln), ctypes.byref(M),
+                                     int(in_place))
     return st, out[:ln.value].copy(), M.value
 
 

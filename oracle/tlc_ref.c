@@ -75,10 +75,7 @@ void tlc_ref_dequantize(const int8_t* q, size_t n, float M, float* out,
                         int accumulate) {
   for (size_t i = 0; i < n; ++i) {
     float t = M * (float)q[i];
-    if (!accumulate)
-      out[i] = t;
-    else if (q[i] != 0) /* a zero update leaves the aggregate as it is */
-      out[i] = out[i] + t;
+    out[i] = accumulate ? out[i] + t : t; /* dense, every element */
   }
 }
 
@@ -159,8 +156,8 @@ int tlc_ref_zre_decode(const uint8_t* C, size_t c, uint8_t* Q, size_t m) {
   return pos == m ? TLC_REF_OK : TLC_REF_E_CORRUPT;
 }
 
-int tlc_ref_compress(const float* x, float* r, size_t n, float s,
-                     uint8_t* bytes, size_t cap, size_t* len, float* scale) {
+static int ref_compress(const float* x, float* r, size_t n, float s, uint8_t* bytes,
+                        size_t cap, size_t* len, float* scale, int in_place) {
   if (len) *len = 0;
   if (!len || !scale) return TLC_REF_E_INVALID;
   if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
@@ -177,7 +174,7 @@ int tlc_ref_compress(const float* x, float* r, size_t n, float s,
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M); /* Eq. 1 */
   if (st != TLC_REF_OK) {
-    memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
+    if (in_place) memcpy(r, acc, n * sizeof(float)); /* step 1 already done in the buffer */
     free(acc);
     return st;
   }
@@ -199,6 +196,16 @@ int tlc_ref_compress(const float* x, float* r, size_t n, float s,
   free(q);
   free(acc);
   return TLC_REF_OK;
+}
+
+int tlc_ref_compress(const float* x, float* r, size_t n, float s,
+                     uint8_t* bytes, size_t cap, size_t* len, float* scale) {
+  return ref_compress(x, r, n, s, bytes, cap, len, scale, 0);
+}
+
+int tlc_ref_compress_in_place(const float* x, float* r, size_t n, float s,
+                              uint8_t* bytes, size_t cap, size_t* len, float* scale) {
+  return ref_compress(x, r, n, s, bytes, cap, len, scale, 1);
 }
 
 int tlc_ref_decompress(const uint8_t* bytes, size_t len, float scale,
@@ -254,7 +261,7 @@ void tlc_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_
 }
 
 int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t* bytes,
-                           size_t cap, size_t* len, float* scale) {
+                           size_t cap, size_t* len, float* scale, int in_place) {
   if (len) *len = 0;
   if (!len || !scale) return TLC_REF_E_INVALID;
   if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
@@ -270,7 +277,7 @@ int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t*
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M);
   if (st != TLC_REF_OK) {
-    memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
+    if (in_place) memcpy(r, acc, n * sizeof(float)); /* step 1 already done in the buffer */
     free(acc);
     return st;
   }
@@ -348,7 +355,7 @@ void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float
 }
 
 int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
-                          size_t cap, size_t* len, float* scale) {
+                          size_t cap, size_t* len, float* scale, int in_place) {
   if (len) *len = 0;
   if (!len || !scale) return TLC_REF_E_INVALID;
   if (!(s >= 1.0f && s < 2.0f)) return TLC_REF_E_INVALID;
@@ -366,7 +373,7 @@ int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* 
   float M = 0.0f;
   int st = tlc_ref_absmax_scale(acc, n, s, &M);
   if (st != TLC_REF_OK) {
-    if (r) memcpy(r, acc, n * sizeof(float)); /* step 1 accumulates into the buffer itself */
+    if (r && in_place) memcpy(r, acc, n * sizeof(float)); /* step 1 already done */
     free(acc);
     return st;
   }
@@ -392,10 +399,7 @@ int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_
   const float D = tlc_ref_int8_step(scale);
   for (size_t i = 0; i < n; ++i) {
     const float v = (float)(int8_t)bytes[i] * D;
-    if (!accumulate)
-      out[i] = v;
-    else if (bytes[i] != 0) /* a zero code leaves the aggregate as it is */
-      out[i] = out[i] + v;
+    out[i] = accumulate ? out[i] + v : v; /* dense, every element */
   }
   return TLC_REF_OK;
 }

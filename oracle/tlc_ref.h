@@ -54,10 +54,8 @@ int tlc_ref_absmax_scale(const float* acc, size_t n, float s, float* scale);
 void tlc_ref_quantize(const float* acc, size_t n, float M, int8_t* q,
                       float* resid);
 
-/* Eq. 3: out[i] = M*q[i], or, when accumulate, out[i] = out[i] + M*q[i]
- * for q[i] != 0.  A value with q[i] = 0 adds nothing to the aggregate and
- * keeps its bits (IEEE would turn -0 + 0 into +0 and quiet a signalling
- * NaN; the decoder leaves both alone). */
+/* Eq. 3: out[i] = M*q[i], or out[i] = out[i] + M*q[i] when accumulate,
+ * densely for every i (so -0.0 + M*0 gives +0.0). */
 void tlc_ref_dequantize(const int8_t* q, size_t n, float M, float* out,
                         int accumulate);
 
@@ -78,12 +76,17 @@ int tlc_ref_zre_decode(const uint8_t* C, size_t c, uint8_t* Q, size_t m);
 
 /* Whole encoder.  x is read only, r is the error-accumulation buffer
  * (in/out), bytes receives *len bytes (cap must be >= ceil(n/5)), *scale
- * receives M.  *len = 0 on any error.  Errors found before step 1 (bad
- * arguments, capacity) leave r and bytes unchanged.  TLC_REF_E_NONFINITE
- * comes after step 1, which accumulates x into the buffer itself (Section
- * 3.1, Fig. 3): r then holds acc = x + r and the bytes are unchanged. */
+ * receives M.  On any error r and bytes are left unchanged and *len = 0
+ * (NaN/Inf: no meaningful quantization exists). */
 int tlc_ref_compress(const float* x, float* r, size_t n, float s,
                      uint8_t* bytes, size_t cap, size_t* len, float* scale);
+
+/* As tlc_ref_compress, except that step 1 (Section 3.1, Fig. 3) is taken as
+ * accumulating x into the buffer itself before Eq. 1 is known: on
+ * TLC_REF_E_NONFINITE r holds acc = x + r (argument errors still leave it
+ * unchanged).  Every other result is identical. */
+int tlc_ref_compress_in_place(const float* x, float* r, size_t n, float s,
+                              uint8_t* bytes, size_t cap, size_t* len, float* scale);
 
 /* Whole decoder.  On any error out is left unchanged. */
 int tlc_ref_decompress(const uint8_t* bytes, size_t len, float scale,
@@ -99,9 +102,9 @@ void tlc_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_
 
 /* Quantization + quartic encoding without zero-run encoding (Table 2, row
  * "No ZRE"): bytes receives the ceil(n/5) quartic bytes, error feedback as in
- * tlc_ref_compress. */
+ * tlc_ref_compress (in_place != 0: as in tlc_ref_compress_in_place). */
 int tlc_ref_compress_nozre(const float* x, float* r, size_t n, float s, uint8_t* bytes,
-                           size_t cap, size_t* len, float* scale);
+                           size_t cap, size_t* len, float* scale, int in_place);
 
 /* Stochastic 3-value quantization + quartic encoding, no error feedback
  * (the "Stoch 3-value + QE" comparator of Section 5.1, described in Section
@@ -123,13 +126,12 @@ void tlc_ref_int8_quantize(const float* acc, size_t n, float M, int8_t* q, float
 
 /* Encoder: acc = x + r when r != NULL (error feedback, r updated), else acc
  * = x.  bytes receives the n codes as two's-complement int8 (cap >= n).
- * Errors as for tlc_ref_compress (on TLC_REF_E_NONFINITE a non-NULL r
- * holds acc). */
+ * Errors as for tlc_ref_compress (in_place != 0: on TLC_REF_E_NONFINITE a
+ * non-NULL r holds acc). */
 int tlc_ref_compress_int8(const float* x, float* r, size_t n, float s, uint8_t* bytes,
-                          size_t cap, size_t* len, float* scale);
+                          size_t cap, size_t* len, float* scale, int in_place);
 
-/* Decoder: out_i = fl(q_i * D) or, accumulating, fl(out_i + fl(q_i * D))
- * for q_i != 0 (out_i kept for q_i = 0, as in tlc_ref_dequantize), D =
+/* Decoder: out_i = fl(q_i * D) or fl(out_i + fl(q_i * D)), densely, D =
  * fl(scale / 127), every int8 code accepted; len != n is
  * TLC_REF_E_CORRUPT with out unchanged. */
 int tlc_ref_decompress_int8(const uint8_t* bytes, size_t len, float scale, size_t n,

@@ -324,9 +324,11 @@ def test_subnormal_inputs_and_scale():
     assert q.tolist() == [1, 0, -1, 0, 0]
 
 
-def test_nonfinite_is_rejected_after_step_1():
-    """Step 1 (Section 3.1, Fig. 3) adds x into the buffer before Eq. 1 can
-    see the NaN/Inf: the buffer keeps that sum, no byte is produced."""
+def test_nonfinite_is_rejected_and_leaves_state():
+    """NaN/Inf, or max*s overflowing: no quantization exists, so the buffer
+    and the bytes are left alone (reading A4); the in-place variant has
+    done step 1 (Section 3.1, Fig. 3) in the buffer already, so it keeps
+    x + r there."""
     for bad in (np.inf, -np.inf, np.nan):
         for enc in (oracle.compress, oracle.compress_nozre):
             x = workloads.normal([400], 100, 1.0)
@@ -335,17 +337,34 @@ def test_nonfinite_is_rejected_after_step_1():
             r0 = r.copy()
             st, C, M = enc(x, r, 1.0)
             assert st == oracle.E_NONFINITE and C.size == 0
+            assert np.array_equal(bits(r), bits(r0))
+            r = r0.copy()
+            st, C, M = enc(x, r, 1.0, in_place=True)
+            assert st == oracle.E_NONFINITE and C.size == 0
             assert np.array_equal(bits(r), bits(x + r0))
-    # overflow of max * s: every sum is finite and stays in the buffer
+    # overflow of max * s: every sum is finite
     x = np.array([3.0e38, 1.0], F32)
     r = np.array([-0.0, 0.5], F32)
     assert oracle.compress(x, r, 1.5)[0] == oracle.E_NONFINITE
+    assert np.array_equal(bits(r), bits(np.array([-0.0, 0.5], F32)))
+    assert oracle.compress(x, r, 1.5, in_place=True)[0] == oracle.E_NONFINITE
     assert np.array_equal(bits(r), bits(np.array([3.0e38, 1.5], F32)))
-    # an error found before step 1 leaves the buffer alone
+    # argument errors leave the buffer alone in both forms
     r = np.ones(2, F32)
-    assert oracle.compress(x, r, 2.0)[0] == oracle.E_INVALID
-    assert oracle.compress(x, r, 1.0, cap=0)[0] == oracle.E_CAPACITY
+    for ip in (False, True):
+        assert oracle.compress(x, r, 2.0, in_place=ip)[0] == oracle.E_INVALID
+        assert oracle.compress(x, r, 1.0, cap=0, in_place=ip)[0] == oracle.E_CAPACITY
     assert r.tolist() == [1.0, 1.0]
+
+
+def test_in_place_variant_matches_on_finite_input():
+    x = workloads.normal([402], 5003, 1.0)
+    r0 = workloads.normal([403], 5003, 1e-2)
+    r1, r2 = r0.copy(), r0.copy()
+    a = oracle.compress(x, r1, 1.5)
+    b = oracle.compress(x, r2, 1.5, in_place=True)
+    assert a[0] == b[0] == 0 and a[2] == b[2] and np.array_equal(a[1], b[1])
+    assert np.array_equal(bits(r1), bits(r2))
 
 
 def test_invalid_s_rejected():
@@ -363,33 +382,36 @@ def test_empty_tensor():
 
 # ------------------------------------------------------------------ Eq. 3
 def test_dequantize_and_signed_zero_accumulate():
-    """Eq. 3; accumulating adds M*q only where q != 0, so -0.0 with q = 0
-    stays -0.0 (IEEE -0 + 0 would give +0); without accumulation every
-    element is M*q."""
+    """Eq. 3 applied densely (reading A13): every element is written, so
+    -0.0 + M*0 gives +0.0."""
     q = np.array([1, 0, -1, 0], np.int8)
     out = np.array([-0.0, -0.0, 2.0, 5.0], F32)
     oracle.dequantize(q, F32(0.25), out, accumulate=True)
-    assert np.array_equal(bits(out), bits(np.array([0.25, -0.0, 1.75, 5.0], F32)))
+    assert np.array_equal(bits(out), bits(np.array([0.25, 0.0, 1.75, 5.0], F32)))
     out = oracle.dequantize(q, F32(0.25))
     assert np.array_equal(bits(out), bits(np.array([0.25, 0.0, -0.25, 0.0], F32)))
 
 
-def test_zero_update_leaves_aggregate_bits():
-    """A stream of all-zero groups (the encoding of an all-zero change)
-    accumulated into any aggregate leaves every bit as it was: -0.0, +-Inf
-    and NaNs with payloads included."""
+def test_zero_update_accumulates_densely():
+    """The encoding of an all-zero change accumulated into an aggregate adds
+    +0.0 to every element: -0.0 becomes +0.0, every other finite value and
+    the infinities keep their bits, NaNs stay NaN."""
     n = 1003
-    special = np.array([0x80000000, 0x7F800000, 0xFF800000, 0x7FC00001, 0x7F800001,
-                        0xFFFFFFFF, 0x00000001, 0x80000001], np.uint32)
+    special = np.array([0x80000000, 0x7F800000, 0xFF800000, 0x7FC00001, 0x00000001,
+                        0x80000001], np.uint32)
     out0 = workloads.normal([502], n, 1.0)
     out0.view(np.uint32)[::7][:special.size] = special
     st, C, M = oracle.compress(np.zeros(n, F32), np.zeros(n, F32), 1.0)
     assert st == oracle.OK and M == 0.0
+    expect = out0.copy()
+    expect[(expect == 0) & np.signbit(expect)] = 0.0
     for scale in (0.0, 1.0):  # any scale: q = 0 everywhere
         st, out = oracle.decompress(C, scale, n, out0.copy(), accumulate=True)
-        assert st == oracle.OK and np.array_equal(bits(out), bits(out0))
-    st, out = oracle.decompress_int8(np.zeros(n, np.uint8), 1.0, n, out0.copy(), True)
-    assert st == oracle.OK and np.array_equal(bits(out), bits(out0))
+        assert st == oracle.OK
+        nan = np.isnan(expect)
+        assert np.array_equal(np.isnan(out), nan)
+        assert np.array_equal(bits(out[~nan]), bits(expect[~nan]))
+        assert not (np.signbit(out) & (out == 0)).any()
 
 
 def test_decompress_corrupt_leaves_out_unchanged():
