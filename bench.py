@@ -39,6 +39,8 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", DOMINANT + "_c4_traffic.md")
 def algorithmic_bytes(n, c, nnz):
     tiles = -(-(-(-n // 5)) // 4096)  # 4096-byte quartic tiles
     return {
+        # the check pass of the default error policy: read x, r
+        "tlc_absmax_check_kernel": 8 * n,
         # read x, r; write r = x + r (the 2-byte bound per float4 it also
         # writes, n/2 bytes, is not counted)
         "tlc_accum_absmax_kernel": 12 * n,
@@ -52,9 +54,9 @@ def algorithmic_bytes(n, c, nnz):
         # residuals into r
         "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 12 * nnz,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
-        # read C; accumulating, out changes only where q != 0 (read + write
-        # of those nnz values; ranges with many non-zero bytes sweep densely)
-        "tlc_expand_dequant_kernel": c + 8 * nnz,
+        # read C; accumulating densely, read every value of out and store the
+        # sums that change it (the nnz values with q != 0 here)
+        "tlc_expand_dequant_kernel": c + 4 * n + 4 * nnz,
     }
 
 
@@ -487,6 +489,23 @@ def main():
         ms, cnt = ctx.profile_get(kid)
         kern[tlc.tlc_kernel_name(kid)] = (ms / cnt if cnt else 0.0, cnt)
 
+    # The same steps with TLC_OPT_IN_PLACE_FEEDBACK (no check pass before the
+    # in-place max pass; only the residual after NaN/Inf differs), timed the
+    # same way without any events.
+    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
+    base = args.warmup + args.steps + kern_steps
+    for k in range(2):
+        step(base + k)
+    ctx.sync()
+    torch.cuda.synchronize()
+    t0_ip = time.perf_counter()
+    for k in range(args.steps):
+        step(base + 2 + k)
+    ctx.sync()
+    torch.cuda.synchronize()
+    t1_ip = time.perf_counter()
+    ctx.set_options(0)
+
     # Values with q != 0 in the last step's stream: its decode into zeros is
     # non-zero exactly there (M > 0).
     probe = torch.zeros(n, dtype=torch.float32, device=dev)
@@ -505,8 +524,8 @@ def main():
     achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(n)
 
-    enc_k = ["tlc_accum_absmax_kernel", "tlc_quant_encode_kernel", "tlc_zre_chunk_kernel",
-             "tlc_zre_compact_kernel"]
+    enc_k = ["tlc_absmax_check_kernel", "tlc_accum_absmax_kernel", "tlc_quant_encode_kernel",
+             "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
     dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
     dec_kernel_ms = sum(kern[k][0] for k in dec_k)
@@ -552,6 +571,13 @@ def main():
         "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
         "kernels_avg_ms_note": "every kernel timed over %d further steps after the timed "
                                "region; the roofline kernel is timed inside it" % kern_steps,
+        "in_place_feedback": {
+            "value": round(4 * n * args.steps / (t1_ip - t0_ip) / 1e9, 2),
+            "ms_per_step": round((t1_ip - t0_ip) / args.steps * 1e3, 4),
+            "note": "the same steps with TLC_OPT_IN_PLACE_FEEDBACK: no check pass before the "
+                    "in-place max pass (every output identical; only the residual after "
+                    "NaN/Inf differs)",
+        },
         "nonzero_q_last_step": nnz,
         "compression_ratio": round(4 * n / (c_avg + 4), 2),
         "compression_ratio_payload_only": round(4 * n / c_avg, 2),

@@ -92,9 +92,9 @@ int tlc_ctx_destroy(tlc_ctx* ctx);
 
 /* Encode one tensor (Sections 3.1-3.3).
  *   tensor    device fp32[n], read only (the new state change).
- *   residual  device fp32[n], in/out: the error-accumulation buffer.  Step
- *             1 (Section 3.1, Fig. 3) adds the tensor into it (acc); on
- *             success it holds acc - M*q.  Must not overlap tensor.
+ *   residual  device fp32[n], in/out: the error-accumulation buffer
+ *             (Section 3.1, Fig. 3); on success it holds acc - M*q with
+ *             acc = tensor + residual.  Must not overlap tensor.
  *   n         value count, 0 <= n <= max_n of the context.
  *   s         sparsity multiplier, 1 <= s < 2.
  *   bytes     device uint8[bytes_cap] receiving the zero-run encoded stream.
@@ -102,9 +102,8 @@ int tlc_ctx_destroy(tlc_ctx* ctx);
  *   bytes_len host out: stream length (0 on error).
  *   scale     host out: M (0 when n == 0).
  * Synchronous: returns after the stream length is known.  On
- * TLC_E_NONFINITE (found after step 1) the bytes are left unchanged and
- * the residual holds acc = tensor + residual; argument errors leave both
- * unchanged. */
+ * TLC_E_NONFINITE the residual and the bytes are left unchanged (with
+ * TLC_OPT_IN_PLACE_FEEDBACK the residual holds acc instead). */
 int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
                  float s, uint8_t* bytes, size_t bytes_cap, size_t* bytes_len,
                  float* scale);
@@ -113,11 +112,11 @@ int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,
  *   bytes       device uint8[bytes_len] from tlc_compress.
  *   scale       M from tlc_compress: finite and >= 0.
  *   n           value count of the encoded tensor, <= max_n.
- *   out         device fp32[n]: out = M*q, every element written
- *               (accumulate == 0), or out = out + M*q for q != 0
- *               (accumulate != 0; a value with q = 0 keeps its bits,
- *               -0.0 and NaN payloads included).  Must not overlap bytes
- *               (TLC_E_INVALID).
+ *   out         device fp32[n]: out = M*q (accumulate == 0) or
+ *               out = out + M*q (accumulate != 0), for every element
+ *               (-0.0 + M*0 gives +0.0; a value whose sum has the bits it
+ *               already holds is not stored again).  Must not overlap
+ *               bytes (TLC_E_INVALID).
  * Asynchronous on the context's stream; returns only errors detectable on
  * the host.  If the stream does not expand to exactly ceil(n/5) bytes, out
  * is left unchanged and the next tlc_sync() returns TLC_E_CORRUPT. */
@@ -152,8 +151,9 @@ int tlc_decompress(tlc_ctx* ctx, const uint8_t* bytes, size_t bytes_len,
  * (Eq. 1), step D = fl(M / 127); byte i is the two's-complement int8 code
  * rint(fl(acc_i / D)) clamped to [-127, 127] (0 when D == 0) and the
  * residual becomes fl(acc_i - fl(code * D)).  bytes_cap >= n; *bytes_len =
- * n.  Synchronous; on TLC_E_NONFINITE the bytes are unchanged and a
- * non-NULL residual holds acc (step 1 done), as for tlc_compress. */
+ * n.  Synchronous; on TLC_E_NONFINITE the residual and bytes are unchanged
+ * (with TLC_OPT_IN_PLACE_FEEDBACK a non-NULL residual holds acc), as for
+ * tlc_compress; the same holds for TLC_MODE_NO_ZRE. */
 int tlc_compress_ex(tlc_ctx* ctx, int mode, const float* tensor, float* residual, size_t n,
                     float s, uint64_t seed, uint64_t step, uint8_t* bytes, size_t bytes_cap,
                     size_t* bytes_len, float* scale);
@@ -161,8 +161,7 @@ int tlc_compress_ex(tlc_ctx* ctx, int mode, const float* tensor, float* residual
 /* Decode a stream of any mode.  TLC_MODE_3LC, TLC_MODE_NO_ZRE and
  * TLC_MODE_STOCHASTIC forward to tlc_decompress.  TLC_MODE_INT8: bytes is
  * device uint8[n] of int8 codes (every code accepted), out = fl(code * D)
- * or, accumulating, out + fl(code * D) for code != 0 (code 0 keeps out's
- * bits) with D = fl(scale / 127); bytes_len != n returns
+ * or out + fl(code * D) with D = fl(scale / 127); bytes_len != n returns
  * TLC_E_CORRUPT at once with out unchanged.  Asynchronous on the context's
  * stream. */
 int tlc_decompress_ex(tlc_ctx* ctx, int mode, const uint8_t* bytes, size_t bytes_len,
@@ -174,9 +173,9 @@ int tlc_decompress_ex(tlc_ctx* ctx, int mode, const uint8_t* bytes, size_t bytes
  * arrays of `count` entries; the pointers in them are device pointers, and
  * buffers of different tensors must not overlap.  Argument errors reject the
  * whole call before any work.  status[t] receives TLC_OK or
- * TLC_E_NONFINITE (that tensor's bytes unchanged and its residual holding
- * acc, bytes_len[t] = 0); the call returns TLC_E_NONFINITE if any tensor
- * was refused. */
+ * TLC_E_NONFINITE (that tensor's residual and bytes unchanged, or its
+ * residual holding acc with TLC_OPT_IN_PLACE_FEEDBACK; bytes_len[t] = 0);
+ * the call returns TLC_E_NONFINITE if any tensor was refused. */
 int tlc_compress_batch(tlc_ctx* ctx, size_t count, const float* const* tensors,
                        float* const* residuals, const size_t* ns, const float* s,
                        uint8_t* const* bytes, const size_t* caps, size_t* bytes_len,
@@ -195,8 +194,7 @@ int tlc_decompress_batch(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes
  * `count` streams of the same n-value tensor and add them into one fp32
  * output in stream order, element by element:
  *   out = (((accumulate ? out : 0) + v_0) + v_1) + ... + v_{count-1}
- * (with accumulate == 0 the first term is v_0 itself; a zero v_t is not
- * added, as in tlc_decompress), bit-identical to
+ * (with accumulate == 0 the first term is v_0 itself), bit-identical to
  * tlc_decompress(stream 0, accumulate) followed by tlc_decompress(stream
  * t, accumulate = 1) for t = 1 .. count-1, but reading and writing out only
  * once.  Asynchronous; if any stream is corrupt out is left unchanged and
@@ -205,6 +203,22 @@ int tlc_decompress_batch(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes
 int tlc_decompress_sum(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes,
                        const size_t* bytes_len, const float* scales, size_t n, float* out,
                        int accumulate);
+
+/* ---- options ------------------------------------------------------------ */
+
+/* TLC_OPT_IN_PLACE_FEEDBACK: take step 1 of error accumulation (Section
+ * 3.1, Fig. 3: the tensor is added into the buffer) as done in the
+ * residual itself before Eq. 1 is known.  The encoders then read tensor and
+ * residual once instead of twice (12 instead of 20 bytes per value for the
+ * 3-value modes); every result is the same, except that after
+ * TLC_E_NONFINITE the residual holds tensor + residual instead of being
+ * left unchanged.  For callers that check their tensors for NaN/Inf
+ * themselves, or reset the residual after such an error. */
+#define TLC_OPT_IN_PLACE_FEEDBACK 1u
+
+/* Set the context's options (a combination of TLC_OPT_*; 0, the default,
+ * is the behaviour documented above).  Takes effect from the next call. */
+int tlc_ctx_set_options(tlc_ctx* ctx, uint32_t options);
 
 /* Wait for all work of the context and return (then clear) the sticky
  * status of asynchronous decodes: TLC_OK or TLC_E_CORRUPT. */
@@ -215,7 +229,7 @@ const char* tlc_last_error_string(void);
 
 /* ---- per-kernel timing (HIP events on the context's stream) ----------- */
 
-#define TLC_KERNEL_ABSMAX 0         /* partial max of |tensor + residual| (Eq. 1) */
+#define TLC_KERNEL_ABSMAX 0         /* step 1 into the residual, partial max (Eq. 1) */
 #define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, each tile's own
                                        zero-run encoding */
 #define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts */
@@ -231,7 +245,9 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_ZRE_CHUNKS 12    /* zero-run encoding: summaries of tile chunks */
 #define TLC_KERNEL_ZRE_COMPACT 13   /* zero-run encoding: tiles compacted into the stream */
 #define TLC_KERNEL_QUANT_ENCODE_CHAINED 14 /* a small tensor's encode in one chained pass */
-#define TLC_KERNEL_COUNT 15
+#define TLC_KERNEL_ABSMAX_CHECK 15  /* partial max of |tensor + residual|, nothing written */
+#define TLC_KERNEL_ABSMAX_CHECK_BATCH 16
+#define TLC_KERNEL_COUNT 17
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context (of the kernels selected by

@@ -249,25 +249,29 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
 #pragma unroll
     for (int c = 0; c < 4; ++c) d[c] = (((w4 >> (8 * c)) & 0xffu) / kPlace) % 3u;
     if (full[i]) {
+      bool store = true;
       if (kAcc) {
-        o[i].x = acc_trit(o[i].x, d[0], M);
-        o[i].y = acc_trit(o[i].y, d[1], M);
-        o[i].z = acc_trit(o[i].z, d[2], M);
-        o[i].w = acc_trit(o[i].w, d[3], M);
+        store = acc_trit4(o[i], d, M);
       } else {
         o[i] = make_float4(trit_value(d[0], M), trit_value(d[1], M), trit_value(d[2], M),
                            trit_value(d[3], M));
       }
-      if (kNT)
-        st_stream(out + e, o[i]);
-      else
-        *reinterpret_cast<float4*>(out + e) = o[i];
+      if (store) {
+        if (kNT)
+          st_stream(out + e, o[i]);
+        else
+          *reinterpret_cast<float4*>(out + e) = o[i];
+      }
     } else {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const uint32_t p = 4u * f + c;
-        if (p >= a && p - a < qn && e + c < n)
-          out[e + c] = kAcc ? acc_trit(out[e + c], d[c], M) : trit_value(d[c], M);
+        if (p >= a && p - a < qn && e + c < n) {
+          if (kAcc)
+            acc_trit_at(out, e + c, d[c], M);
+          else
+            out[e + c] = trit_value(d[c], M);
+        }
       }
     }
   }
@@ -309,18 +313,17 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
         }
 #pragma unroll
         for (int k = 0; k < 5; ++k) {
+          bool store = true;
           if (kAcc) {
-            o[k].x = acc_trit(o[k].x, t[0][k], M);
-            o[k].y = acc_trit(o[k].y, t[1][k], M);
-            o[k].z = acc_trit(o[k].z, t[2][k], M);
-            o[k].w = acc_trit(o[k].w, t[3][k], M);
+            const uint32_t dk[4] = {t[0][k], t[1][k], t[2][k], t[3][k]};
+            store = acc_trit4(o[k], dk, M);
           } else {
             o[k].x = trit_value(t[0][k], M);
             o[k].y = trit_value(t[1][k], M);
             o[k].z = trit_value(t[2][k], M);
             o[k].w = trit_value(t[3][k], M);
           }
-          *reinterpret_cast<float4*>(out + k * m + j) = o[k];
+          if (store) *reinterpret_cast<float4*>(out + k * m + j) = o[k];
         }
       } else {  // the group whose p4 slice reaches into the padding
 #pragma unroll
@@ -328,7 +331,12 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
             const uint64_t e = k * m + j + cc;
-            if (e < n) out[e] = kAcc ? acc_trit(out[e], t[cc][k], M) : trit_value(t[cc][k], M);
+            if (e < n) {
+              if (kAcc)
+                acc_trit_at(out, e, t[cc][k], M);
+              else
+                out[e] = trit_value(t[cc][k], M);
+            }
           }
         }
       }
@@ -341,69 +349,15 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
 #pragma unroll
       for (int k = 0; k < 5; ++k) {
         const uint64_t e = k * m + j;
-        if (e < n) out[e] = kAcc ? acc_trit(out[e], t[k], M) : trit_value(t[k], M);
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------- sparse Eq. 3
-// Accumulating, a value with q = 0 is left alone (it adds nothing), so a
-// range whose quartic bytes are mostly 121 only has to touch the values
-// of its other bytes.  Those are the stream's literal bytes other than 121
-// (a run code, or 121 itself, expands to zero groups only).  One block
-// scan over the range's stream bytes gives both each byte's position and
-// the count of such literals (packed as length + (literals << 16): a
-// range expands to fewer than 4096 + 28 bytes and a thread's 16 stream
-// bytes to at most 224, so no carry crosses); if there are at most
-// kSparseBytes, each thread adds M*q into out for the non-zero digits of
-// its literals, one read and one write per value.  Ranges with a stream
-// slice longer than kSparseStream bytes are not tried.
-constexpr uint32_t kSparseStream = 1024;
-constexpr uint32_t kSparseBytes = 256;
-
-// Returns false, having written nothing, when the range is too dense.
-__device__ __forceinline__ bool sparse_expand_accumulate(
-    const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ starts, uint32_t k,
-    uint64_t n, uint64_t m, uint64_t q0, uint32_t qn, float M, float* __restrict__ out,
-    uint32_t* red) {
-  constexpr int kBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
-  const uint64_t s0 = starts[k];
-  const uint32_t i0 = (uint32_t)(s0 >> 8);
-  const uint32_t skip = (uint32_t)(s0 & 255u);
-  const uint32_t i1 = range_end(starts, k, m, c);
-  const uint32_t count = i1 > i0 ? min<uint32_t>(i1 - i0, kDecRange) : 0u;
-  const uint32_t lo = threadIdx.x * kBytes;
-  const uint32_t cnt = lo < count ? min<uint32_t>(kBytes, count - lo) : 0u;
-  uint8_t b[kBytes];
-#pragma unroll
-  for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[i0 + lo + i] : (uint8_t)0;
-  uint32_t packed = 0u;
-#pragma unroll
-  for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt)
-      packed += expanded_len(b[i]) + (b[i] < kRunBase && b[i] != kZeroGroup ? 1u << 16 : 0u);
-  const ScanU32 sc = block_scan_u32(packed, red);
-  if ((sc.total >> 16) > kSparseBytes) return false;
-  int pos = (int)(sc.excl & 0xffffu) - (int)skip;  // range-relative position of b[0]
-#pragma unroll
-  for (int i = 0; i < kBytes; ++i) {
-    if ((uint32_t)i < cnt) {
-      const uint32_t x = b[i];
-      if (x < kRunBase && x != kZeroGroup && pos >= 0 && (uint32_t)pos < qn) {
-        const uint64_t j = q0 + (uint32_t)pos;
-        uint32_t t[5];
-        digits5(x, t);
-#pragma unroll
-        for (int kk = 0; kk < 5; ++kk) {
-          const uint64_t e = (uint64_t)kk * m + j;
-          if (t[kk] != 1u && e < n) out[e] = out[e] + trit_value(t[kk], M);
+        if (e < n) {
+          if (kAcc)
+            acc_trit_at(out, e, t[k], M);
+          else
+            out[e] = trit_value(t[k], M);
         }
       }
-      pos += (int)expanded_len(x);
     }
   }
-  return true;
 }
 
 // One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
@@ -418,13 +372,6 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
-  if (kAcc && range_end(start, k, m, c) - (uint32_t)(start[k] >> 8) <= kSparseStream) {
-    if (sparse_expand_accumulate(C, c, start, k, n, m, q0, qn, M, out, red)) return;
-    __syncthreads();  // red is reused by the expansion
-    expand_range(C, c, start, k, m, qn, s_q, red);
-    dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    return;
-  }
   if (kPath == kPathShift && kAcc && kNT) {
     // large outputs: the first two partitions' loads overlap the expansion
     // (on gfx950 15 us of 410 on a 2^28-value decode; outputs that fit the

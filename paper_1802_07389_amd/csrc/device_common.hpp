@@ -360,11 +360,31 @@ __device__ __forceinline__ float trit_value(uint32_t t, float M) {
   return t == 0u ? -M : (t == 1u ? 0.0f : M);
 }
 
-// Eq. 3 accumulated into out: out + M*q for q != 0; a zero trit (t = 1)
-// adds nothing and leaves out's bits as they are (-0.0 and NaN payloads
-// included).
+// Eq. 3 accumulated densely into out (every value: out + M*q, so -0.0 + 0
+// gives +0.0).  acc_trit4 returns whether any of the four sums has other
+// bits than its input: a store of identical bits can be skipped without
+// changing any result, and with few values q != 0 most stores are.
 __device__ __forceinline__ float acc_trit(float out, uint32_t t, float M) {
-  return t == 1u ? out : out + trit_value(t, M);
+  return out + trit_value(t, M);
+}
+
+__device__ __forceinline__ bool acc_trit4(float4& o, const uint32_t (&d)[4], float M) {
+  const float4 r = make_float4(o.x + trit_value(d[0], M), o.y + trit_value(d[1], M),
+                               o.z + trit_value(d[2], M), o.w + trit_value(d[3], M));
+  const bool changed = ((__float_as_uint(r.x) ^ __float_as_uint(o.x)) |
+                        (__float_as_uint(r.y) ^ __float_as_uint(o.y)) |
+                        (__float_as_uint(r.z) ^ __float_as_uint(o.z)) |
+                        (__float_as_uint(r.w) ^ __float_as_uint(o.w))) != 0u;
+  o = r;
+  return changed;
+}
+
+// out[e] += M*q, stored only if the bits change.
+__device__ __forceinline__ void acc_trit_at(float* __restrict__ out, uint64_t e, uint32_t t,
+                                            float M) {
+  const float o = out[e];
+  const float r = o + trit_value(t, M);
+  if (__float_as_uint(r) != __float_as_uint(o)) out[e] = r;
 }
 
 // Mask of the non-121 bytes among the 16 quartic bytes q[lo .. lo + cnt)

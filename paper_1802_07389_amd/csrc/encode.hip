@@ -1,5 +1,8 @@
 // encode.hip -- gfx950 encode kernels of the 3LC path.
 //
+//   tlc_absmax_check_kernel / _batch_kernel
+//       partial maxima of |tensor + buffer|, nothing written: lets the
+//       default error policy refuse NaN/Inf before the buffer changes
 //   tlc_accum_absmax_kernel / _batch_kernel
 //       step 1 of error accumulation (the tensor is added into the buffer,
 //       in place) and partial maxima of the sums               (Section 3.1,
@@ -41,12 +44,16 @@ namespace tlc {
 // half-word h bounds the four values from above (|acc| < (h + 1) * 2^16 as
 // bit patterns), so the quantizer can skip every float4 whose h lies below
 // the top half of its threshold U: all four have q = 0 and keep acc.
-template <bool kVec, bool kResid = true, bool kSum = false>
+//
+// kStore false (with kResid): the check pass of the default error policy,
+// which only reduces max|x + r| and writes nothing.
+template <bool kVec, bool kResid = true, bool kSum = false, bool kStore = kResid>
 __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
                                                 float* __restrict__ r, uint64_t n,
                                                 uint32_t blk, uint32_t nblk,
                                                 uint16_t* __restrict__ summ = nullptr) {
-  static_assert(!kSum || (kVec && kResid), "summaries come from the float4 buffer path");
+  static_assert(!kSum || (kVec && kStore), "summaries come from the float4 buffer path");
+  static_assert(!kStore || kResid, "only a buffer is stored");
   uint32_t mx = 0;
   const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
   const uint64_t stride = (uint64_t)nblk * kThreads;
@@ -65,7 +72,7 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
         const float4 v = kResid ? make_float4(a[u].x + b[u].x, a[u].y + b[u].y,
                                               a[u].z + b[u].z, a[u].w + b[u].w)
                                 : a[u];
-        if (kResid) st_stream(r + 4 * (i + u * stride), v);
+        if (kStore) st_stream(r + 4 * (i + u * stride), v);
         const uint32_t m4 =
             max(max(abs_bits(v.x), abs_bits(v.y)), max(abs_bits(v.z), abs_bits(v.w)));
         if (kSum) summ[i + u * stride] = (uint16_t)(m4 >> 16);
@@ -78,7 +85,7 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
       if (kResid) {
         const float4 b = ld_stream(r + 4 * i);
         v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-        st_stream(r + 4 * i, v);
+        if (kStore) st_stream(r + 4 * i, v);
       }
       const uint32_t m4 =
           max(max(abs_bits(v.x), abs_bits(v.y)), max(abs_bits(v.z), abs_bits(v.w)));
@@ -87,40 +94,93 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
     }
     for (uint64_t e = (nv << 2) + tid; e < n; e += stride) {
       const float v = kResid ? x[e] + r[e] : x[e];
-      if (kResid) r[e] = v;
+      if (kStore) r[e] = v;
       mx = max(mx, abs_bits(v));
     }
   } else {
     for (uint64_t e = tid; e < n; e += stride) {
       const float v = kResid ? x[e] + r[e] : x[e];
-      if (kResid) r[e] = v;
+      if (kStore) r[e] = v;
       mx = max(mx, abs_bits(v));
     }
   }
   return mx;
 }
 
+// Partial maxima of |x + r| that write nothing: the check pass that lets
+// the default error policy refuse NaN/Inf before the buffer is touched.
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void tlc_absmax_check_kernel(
+    const float* __restrict__ x, const float* __restrict__ r, uint64_t n,
+    uint32_t* __restrict__ partials) {
+  __shared__ uint32_t lds[kWaves];
+  const uint32_t mx = block_max(
+      absmax_part<kVec, true, false, false>(x, const_cast<float*>(r), n, blockIdx.x, gridDim.x),
+      lds);
+  if (threadIdx.x == 0) partials[blockIdx.x] = mx;
+}
+
+// The guard of a writing pass: with the check pass's partial maxima (guard
+// != nullptr), a tensor whose scale would be NaN/Inf or overflow is left
+// untouched, and the pass posts a partial that makes every later kernel
+// refuse it as well.  Returns true when the block must stop.  Ends with a
+// barrier when it reads the guard.
+__device__ __forceinline__ bool refused_by_guard(const uint32_t* __restrict__ guard,
+                                                 uint32_t guard_np, float s, uint32_t* lds,
+                                                 uint32_t* __restrict__ partial) {
+  if (guard == nullptr) return false;
+  const Scale g = finish_scale(guard, guard_np, s, lds);
+  __syncthreads();  // lds is reused by the caller
+  if (!g.bad) return false;
+  if (threadIdx.x == 0) *partial = 0xffffffffu;
+  return true;
+}
+
 template <bool kVec, bool kResid, bool kSum>
 __global__ __launch_bounds__(kThreads) void tlc_accum_absmax_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n,
-    uint32_t* __restrict__ partials, uint16_t* __restrict__ summ) {
+    uint32_t* __restrict__ partials, uint16_t* __restrict__ summ,
+    const uint32_t* __restrict__ guard, uint32_t guard_np, float s) {
   __shared__ uint32_t lds[kWaves];
+  if (refused_by_guard(guard, guard_np, s, lds, &partials[blockIdx.x])) return;
   const uint32_t mx =
       block_max(absmax_part<kVec, kResid, kSum>(x, r, n, blockIdx.x, gridDim.x, summ), lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = mx;
 }
 
-__global__ __launch_bounds__(kThreads) void tlc_accum_absmax_batch_kernel(
-    const EncDesc* __restrict__ descs, uint32_t count, uint32_t* __restrict__ partials) {
-  __shared__ uint32_t lds[kWaves];
+// One block of the batch's max passes.  kStore false: the check pass.
+// guard (kStore): the check pass's partial maxima, same block numbering.
+template <bool kStore>
+__device__ __forceinline__ void accum_absmax_batch_block(const EncDesc* __restrict__ descs,
+                                                         uint32_t count,
+                                                         uint32_t* __restrict__ partials,
+                                                         const uint32_t* __restrict__ guard,
+                                                         uint32_t* lds) {
   const uint32_t t =
       find_desc(descs, count, blockIdx.x, [](const EncDesc& d) { return d.blk0; });
   const EncDesc& d = descs[t];
   const uint32_t blk = blockIdx.x - d.blk0;
-  const uint32_t mx = (d.vec & 4u) ? absmax_part<true>(d.x, d.r, d.n, blk, d.nblk)
-                                   : absmax_part<false>(d.x, d.r, d.n, blk, d.nblk);
+  if (kStore && refused_by_guard(guard ? guard + d.blk0 : nullptr, d.nblk, d.s, lds,
+                                 &partials[blockIdx.x]))
+    return;
+  const uint32_t mx = (d.vec & 4u)
+                          ? absmax_part<true, true, false, kStore>(d.x, d.r, d.n, blk, d.nblk)
+                          : absmax_part<false, true, false, kStore>(d.x, d.r, d.n, blk, d.nblk);
   const uint32_t bm = block_max(mx, lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = bm;
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_absmax_check_batch_kernel(
+    const EncDesc* __restrict__ descs, uint32_t count, uint32_t* __restrict__ partials) {
+  __shared__ uint32_t lds[kWaves];
+  accum_absmax_batch_block<false>(descs, count, partials, nullptr, lds);
+}
+
+__global__ __launch_bounds__(kThreads) void tlc_accum_absmax_batch_kernel(
+    const EncDesc* __restrict__ descs, uint32_t count, uint32_t* __restrict__ partials,
+    const uint32_t* __restrict__ guard) {
+  __shared__ uint32_t lds[kWaves];
+  accum_absmax_batch_block<true>(descs, count, partials, guard, lds);
 }
 
 // ---------------------------------------------------------------- Eq. 2, 3.2
@@ -880,16 +940,37 @@ static inline bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0u;
 }
 
-hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* partials,
-                               uint32_t* nblocks, uint16_t* summ, hipStream_t st) {
-  const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
-  if (summ && !(vec && r)) return hipErrorInvalidValue;  // summaries need the float4 path
+namespace {
+uint32_t absmax_blocks(uint64_t n, bool vec) {
   const uint64_t items = vec ? (n >> 2) : n;
   uint64_t blocks = (items + kThreads * 4 - 1) / (kThreads * 4);
-  blocks = blocks < 1 ? 1 : (blocks > kAbsmaxMaxBlocks ? kAbsmaxMaxBlocks : blocks);
-  *nblocks = (uint32_t)blocks;
-#define TLC_LAUNCH(V, R, S) \
-  tlc_accum_absmax_kernel<V, R, S><<<(uint32_t)blocks, kThreads, 0, st>>>(x, r, n, partials, summ)
+  return (uint32_t)(blocks < 1 ? 1 : (blocks > kAbsmaxMaxBlocks ? kAbsmaxMaxBlocks : blocks));
+}
+}  // namespace
+
+hipError_t launch_absmax_check(const float* x, const float* r, uint64_t n, uint32_t* partials,
+                               uint32_t* nblocks, hipStream_t st) {
+  const bool vec = aligned16(x) && aligned16(r);
+  const uint32_t blocks = absmax_blocks(n, vec);
+  *nblocks = blocks;
+  if (vec)
+    tlc_absmax_check_kernel<true><<<blocks, kThreads, 0, st>>>(x, r, n, partials);
+  else
+    tlc_absmax_check_kernel<false><<<blocks, kThreads, 0, st>>>(x, r, n, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* partials,
+                               uint32_t* nblocks, uint16_t* summ, const uint32_t* guard,
+                               uint32_t guard_np, float s, hipStream_t st) {
+  const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
+  if (summ && !(vec && r)) return hipErrorInvalidValue;  // summaries need the float4 path
+  const uint32_t blocks = absmax_blocks(n, vec);
+  if (guard && guard_np != blocks) return hipErrorInvalidValue;  // same launch as the check
+  *nblocks = blocks;
+#define TLC_LAUNCH(V, R, S)                                                                 \
+  tlc_accum_absmax_kernel<V, R, S><<<blocks, kThreads, 0, st>>>(x, r, n, partials, summ, guard, \
+                                                                guard_np, s)
   if (r == nullptr) {  // no error buffer: max |x|
     if (aligned16(x)) TLC_LAUNCH(true, false, false); else TLC_LAUNCH(false, false, false);
   } else if (vec) {
@@ -957,9 +1038,17 @@ hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
   return hipGetLastError();
 }
 
-hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+hipError_t launch_absmax_check_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_blocks, uint32_t* partials, hipStream_t st) {
-  tlc_accum_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
+  tlc_absmax_check_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_blocks, uint32_t* partials,
+                                     const uint32_t* guard, hipStream_t st) {
+  tlc_accum_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials,
+                                                                   guard);
   return hipGetLastError();
 }
 

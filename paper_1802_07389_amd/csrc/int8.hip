@@ -7,7 +7,7 @@
 //                            one int8 byte per value; acc is the buffer
 //                            that tlc_accum_absmax_kernel has accumulated
 //                            (error feedback) or the tensor itself
-//   tlc_int8_dequant_kernel  out = code * D, or out + code * D for code != 0
+//   tlc_int8_dequant_kernel  out = code * D, or out + code * D
 //
 // Both are elementwise streams: a block covers kI8Rows rows of 1024 values;
 // in a row lane t owns values 4t .. 4t + 3 (one float4 per tensor and one
@@ -42,9 +42,9 @@ __device__ __forceinline__ float int8_value(uint32_t byte, float D) {
   return __fmul_rn((float)(int32_t)(int8_t)(uint8_t)byte, D);
 }
 
-// out + fl(code * D) for a non-zero code; code 0 leaves out's bits alone.
+// out + fl(code * D), densely (code 0 adds +0).
 __device__ __forceinline__ float int8_acc(float out, uint32_t byte, float D) {
-  return (byte & 0xffu) == 0u ? out : __fadd_rn(out, int8_value(byte, D));
+  return __fadd_rn(out, int8_value(byte, D));
 }
 
 // One value: code byte and (kResid) residual acc - fl(code * D).

@@ -54,7 +54,8 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_expand_sum_kernel",         "tlc_quant_pack_kernel",
     "tlc_int8_quant_kernel",         "tlc_int8_dequant_kernel",
     "tlc_zre_chunk_kernel",          "tlc_zre_compact_kernel",
-    "tlc_quant_encode_chained_kernel"};
+    "tlc_quant_encode_chained_kernel", "tlc_absmax_check_kernel",
+    "tlc_absmax_check_batch_kernel"};
 
 struct PendingTiming {
   int kernel;
@@ -74,6 +75,7 @@ struct tlc_ctx {
   void* ws = nullptr;
   Ctrl* ctrl = nullptr;
   uint32_t* partials = nullptr;
+  uint32_t* partials_chk = nullptr;  // the check pass's partial maxima
   size_t partials_cap = 0;
   uint64_t* enc_status = nullptr;
   size_t enc_status_words = 0;
@@ -102,6 +104,7 @@ struct tlc_ctx {
   uint32_t enc_ticket_base = 0, dec_ticket_base = 0;
   uint32_t enc_epoch = 0, dec_epoch = 0;
   bool broken = false;
+  uint32_t options = 0;  // TLC_OPT_*
   // profiling
   bool profiling = false;
   uint32_t profile_mask = 0xffffffffu;  // bit k: time kernel id k
@@ -316,11 +319,13 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->dec_status_words = mm / kZreTile + max_tensors + 2;
   c->start_words = mm / kDecRange + max_tensors + 2;
   const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
-  // layout: ctrl | partials | enc status | dec status | start | enc descs |
+  // layout: ctrl | partials | check partials | enc status | dec status | start | enc descs |
   //         dec descs | enc results | tile records | chunk summaries |
   //         tile prefixes in their chunks | fix lists | float4 summaries | slots
   size_t off = sizeof(Ctrl);
   const size_t off_partials = off;
+  off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
+  const size_t off_partials_chk = off;
   off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
   const size_t off_enc = off;
   off = round_up(off + c->enc_status_words * sizeof(uint64_t), 256);
@@ -354,6 +359,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   uint8_t* base = (uint8_t*)c->ws;
   c->ctrl = (Ctrl*)base;
   c->partials = (uint32_t*)(base + off_partials);
+  c->partials_chk = (uint32_t*)(base + off_partials_chk);
   c->enc_status = (uint64_t*)(base + off_enc);
   c->dec_status = (uint64_t*)(base + off_dec);
   c->start = (uint64_t*)(base + off_start);
@@ -422,6 +428,39 @@ TLC_API int tlc_ctx_destroy(tlc_ctx* c) {
 }
 
 // ---------------------------------------------------------------- encode
+namespace {
+
+// Step 1 and Eq. 1 for one tensor (r may be NULL: no error buffer).  With
+// the default error policy a check pass first reduces max|x + r| without
+// writing, and the writing pass leaves a tensor whose scale is bad
+// untouched, so the buffer keeps its values on TLC_E_NONFINITE;
+// TLC_OPT_IN_PLACE_FEEDBACK drops the check pass.
+int launch_max_passes(tlc_ctx* c, const float* x, float* r, size_t n, float s, uint16_t* summ,
+                      uint32_t* np) {
+  const uint32_t* guard = nullptr;
+  uint32_t guard_np = 0;
+  if (r && !(c->options & TLC_OPT_IN_PLACE_FEEDBACK)) {
+    int st = timed_launch(c, TLC_KERNEL_ABSMAX_CHECK, [&] {
+      return launch_absmax_check(x, r, n, c->partials_chk, &guard_np, c->stream);
+    });
+    if (st) return st;
+    guard = c->partials_chk;
+  }
+  return timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
+    return launch_accum_absmax(x, r, n, c->partials, np, summ, guard, guard_np, s, c->stream);
+  });
+}
+
+}  // namespace
+
+TLC_API int tlc_ctx_set_options(tlc_ctx* c, uint32_t options) {
+  if (!c) return fail(TLC_E_INVALID, "tlc_ctx_set_options: NULL context");
+  if (options & ~TLC_OPT_IN_PLACE_FEEDBACK)
+    return fail(TLC_E_INVALID, "tlc_ctx_set_options: unknown option bits 0x%x", options);
+  c->options = options;
+  return TLC_OK;
+}
+
 TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_t n,
                          float s, uint8_t* bytes, size_t bytes_cap, size_t* bytes_len,
                          float* scale) {
@@ -458,9 +497,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
                        ? c->summ
                        : nullptr;
   uint32_t np = 0;
-  st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, residual, n, c->partials, &np, summ, c->stream);
-  });
+  st = launch_max_passes(c, tensor, residual, n, s, summ, &np);
   if (st) return st;
   if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
     uint32_t epoch = 0;
@@ -518,9 +555,7 @@ int compress_int8(tlc_ctx* c, const float* tensor, float* residual, size_t n, fl
   int st = dev.status();
   if (st) return st;
   uint32_t np = 0;
-  st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, residual, n, c->partials, &np, nullptr, c->stream);
-  });
+  st = launch_max_passes(c, tensor, residual, n, s, nullptr, &np);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_INT8_QUANT, [&] {
     return launch_int8_quant(tensor, residual, n, s, c->partials, np, bytes, c->ctrl,
@@ -574,9 +609,7 @@ TLC_API int tlc_compress_ex(tlc_ctx* c, int mode, const float* tensor, float* re
   if (st) return st;
   float* r = stoch ? nullptr : residual;  // the stochastic mode has no error feedback
   uint32_t np = 0;
-  st = timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(tensor, r, n, c->partials, &np, nullptr, c->stream);
-  });
+  st = launch_max_passes(c, tensor, r, n, s, nullptr, &np);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_PACK, [&] {
     return launch_quant_pack(tensor, r, n, (uint32_t)m, s, stoch ? 1 : 0, seed, step,
@@ -667,8 +700,16 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
   if (st) return st;
+  const bool check = !(c->options & TLC_OPT_IN_PLACE_FEEDBACK);
+  if (check) {  // the default error policy: see launch_max_passes
+    st = timed_launch(c, TLC_KERNEL_ABSMAX_CHECK_BATCH, [&] {
+      return launch_absmax_check_batch(c->enc_descs, cnt, blocks, c->partials_chk, c->stream);
+    });
+    if (st) return st;
+  }
   st = timed_launch(c, TLC_KERNEL_ABSMAX_BATCH, [&] {
-    return launch_accum_absmax_batch(c->enc_descs, cnt, blocks, c->partials, c->stream);
+    return launch_accum_absmax_batch(c->enc_descs, cnt, blocks, c->partials,
+                                     check ? c->partials_chk : nullptr, c->stream);
   });
   if (st) return st;
   uint32_t epoch = 0;

@@ -100,10 +100,16 @@ static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
 
 // Launchers (encode.hip, decode.hip, int8.hip).  All return the hipError_t of the
 // launch.
+// The check pass: partial maxima of |x + r|, nothing written.
+hipError_t launch_absmax_check(const float* x, const float* r, uint64_t n, uint32_t* partials,
+                               uint32_t* nblocks, hipStream_t st);
 // summ (may be NULL): per float4 of r, the top half of its largest |acc|;
-// only written on the float4 path (x and r 16-byte aligned).
+// only written on the float4 path (x and r 16-byte aligned).  guard (may
+// be NULL): the check pass's guard_np partial maxima; if they give a bad
+// scale (with s), nothing is written and the partials mark the tensor bad.
 hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
                                uint32_t* partials, uint32_t* nblocks, uint16_t* summ,
+                               const uint32_t* guard, uint32_t guard_np, float s,
                                hipStream_t st);
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
@@ -128,8 +134,11 @@ hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
                              Ctrl* ctrl, hipStream_t st);
 hipError_t launch_int8_dequant(const uint8_t* C, uint64_t n, float M, float* out,
                                int accumulate, hipStream_t st);
-hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+hipError_t launch_absmax_check_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_blocks, uint32_t* partials, hipStream_t st);
+hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
+                                     uint32_t total_blocks, uint32_t* partials,
+                                     const uint32_t* guard, hipStream_t st);
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
                                      EncResult* results, uint64_t* status,

@@ -39,7 +39,11 @@ TLC_KERNEL_INT8_DEQUANT = 11
 TLC_KERNEL_ZRE_CHUNKS = 12
 TLC_KERNEL_ZRE_COMPACT = 13
 TLC_KERNEL_QUANT_ENCODE_CHAINED = 14
-TLC_KERNEL_COUNT = 15
+TLC_KERNEL_ABSMAX_CHECK = 15
+TLC_KERNEL_ABSMAX_CHECK_BATCH = 16
+TLC_KERNEL_COUNT = 17
+
+TLC_OPT_IN_PLACE_FEEDBACK = 1
 
 TLC_MODE_3LC = 0
 TLC_MODE_NO_ZRE = 1
@@ -52,7 +56,7 @@ EXPORTS = (
     "tlc_decompress", "tlc_decompress_ex",
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
     "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_mask", "tlc_profile_get",
-    "tlc_profile_reset", "tlc_kernel_name",
+    "tlc_profile_reset", "tlc_kernel_name", "tlc_ctx_set_options",
 )
 
 
@@ -108,6 +112,8 @@ def _load():
     L.tlc_profile_get.restype = i
     L.tlc_profile_reset.argtypes = [vp]
     L.tlc_profile_reset.restype = i
+    L.tlc_ctx_set_options.argtypes = [vp, ctypes.c_uint32]
+    L.tlc_ctx_set_options.restype = i
     L.tlc_kernel_name.argtypes = [i]
     L.tlc_kernel_name.restype = ctypes.c_char_p
     return L
@@ -234,6 +240,10 @@ def tlc_profile_reset(ctx):
     return lib.tlc_profile_reset(ctx)
 
 
+def tlc_ctx_set_options(ctx, options):
+    return lib.tlc_ctx_set_options(ctx, int(options) & 0xffffffff)
+
+
 def tlc_kernel_name(kernel):
     r = lib.tlc_kernel_name(kernel)
     return r.decode() if r is not None else None
@@ -255,7 +265,7 @@ def _dev_u8(t, name):
 class Context:
     """One compression context (one tensor, one direction) on one stream."""
 
-    def __init__(self, max_n, stream=None, device=None, max_tensors=1):
+    def __init__(self, max_n, stream=None, device=None, max_tensors=1, options=0):
         self.device = torch.device(device) if device is not None else torch.device(
             "cuda", torch.cuda.current_device())
         with torch.cuda.device(self.device):
@@ -264,6 +274,12 @@ class Context:
             self.max_tensors = int(max_tensors)
             self.handle = tlc_ctx_create_batch(self.max_n, self.max_tensors,
                                                self.stream.cuda_stream)
+        if options:
+            self.set_options(options)
+
+    def set_options(self, options):
+        """TLC_OPT_* flags (0: the default error policy)."""
+        _check(tlc_ctx_set_options(self.handle, options))
 
     def close(self):
         if getattr(self, "handle", None):

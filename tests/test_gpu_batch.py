@@ -86,9 +86,7 @@ def test_batch_nonfinite_tensor_is_refused_alone(bctx):
     assert stat == [0, 0, tlc.TLC_E_NONFINITE, 0]
     C, M, r_gpu, raw = res[2]
     assert C.size == 0
-    r_ref = rs[2].copy()
-    assert oracle.compress(xs[2], r_ref, 1.0)[0] == oracle.E_NONFINITE
-    assert np.array_equal(g.bits(r_gpu), g.bits(r_ref))  # the step-1 sum x + r
+    assert np.array_equal(g.bits(r_gpu), g.bits(rs[2]))  # residual untouched
     assert bool((raw == 0xAB).all())  # bytes untouched
     keep = [0, 1, 3]
     check_against_oracle([xs[i] for i in keep], [rs[i] for i in keep], [ss[i] for i in keep],

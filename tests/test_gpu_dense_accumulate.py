@@ -1,9 +1,9 @@
-"""Accumulating decodes leave an aggregate value's bits alone where q = 0
-(Eq. 3: M*0 adds nothing) and add M*q elsewhere, on every decode path,
-bit for bit as in the oracle.  The aggregates hold -0.0, infinities and
-NaNs with payloads where the update is zero, and -0.0 or ordinary values
-where it is not (an add need not keep a NaN's payload, so no NaN meets a
-non-zero update)."""
+"""Accumulating decodes add M*q into every aggregate value, on every
+decode path, bit for bit as in the oracle (reading A13: -0.0 + M*0 gives
++0.0).  The decoder stores only the sums whose bits differ from what is
+there, so the aggregates here hold -0.0 (which must turn into +0.0),
+infinities, subnormals and ordinary values both where q = 0 and where
+q != 0.  (No NaNs: an add need not keep a NaN's payload.)"""
 import numpy as np
 import pytest
 
@@ -13,8 +13,8 @@ from paper_1802_07389_amd import workloads
 pytestmark = pytest.mark.gpu
 
 F32 = np.float32
-SPECIAL = np.array([0x80000000, 0x7F800000, 0xFF800000, 0x7FC00001, 0x7F800001, 0xFFFFFFFF,
-                    0x00000001, 0x80000001], np.uint32)
+SPECIAL = np.array([0x80000000, 0x7F800000, 0xFF800000, 0x00000001, 0x80000001, 0x00800000,
+                    0x80000000, 0x80000000], np.uint32)
 
 
 def G():
@@ -23,7 +23,8 @@ def G():
 
 
 def sparse_case(seed, n, spikes=300):
-    """x: zeros with spikes (q != 0 only there); out0: specials where x = 0."""
+    """x: zeros with spikes (q != 0 only there); out0: specials where x = 0,
+    -0.0 at half the spikes."""
     rng = np.random.default_rng(seed)
     P = np.unique(rng.integers(0, n, spikes))
     x = np.zeros(n, F32)
@@ -69,11 +70,8 @@ def test_single_stream(ctx, n, offset):
 
 @pytest.mark.parametrize("every", [10, 17, 60])
 def test_single_stream_literal_density(ctx, every):
-    """Non-zero quartic bytes at two offsets every `every` bytes.  10: a
-    range's stream slice passes 1024 bytes (dense sweep from the start);
-    17: about 960 stream bytes but about 480 non-121 bytes, over the 256 at
-    which the sparse attempt goes back to the dense sweep; 60: about 140,
-    the sparse update."""
+    """Non-zero quartic bytes at two offsets every `every` bytes: ranges
+    from many to few stored float4s."""
     g = G()
     n = 5 * 4096 * 3 + 20
     m = -(-n // 5)
@@ -92,7 +90,7 @@ def test_single_stream_literal_density(ctx, every):
 
 def test_single_stream_large(ctx):
     """2^27 values: the decode of outputs of 512 MiB and more (nontemporal
-    sweep)."""
+    sweep, with the stores of unchanged float4s skipped)."""
     g = G()
     n = 1 << 27
     x, out0 = sparse_case(910, n, spikes=20000)
@@ -134,7 +132,7 @@ def test_batch_and_sum(ctx):
         assert np.array_equal(g.bits(od.cpu().numpy()), g.bits(ref)), acc
 
 
-def test_int8_zero_codes(ctx):
+def test_int8_dense(ctx):
     import torch
     from paper_1802_07389_amd import tlc
     g = G()

@@ -129,11 +129,18 @@ def test_int8_errors(ctx):
     x = workloads.normal([973], 1000)
     x[10] = np.nan
     r = workloads.normal([974], 1000, 1e-3)
-    r_ref = r.copy()
-    assert oracle.compress_int8(x, r_ref, 1.0)[0] == oracle.E_NONFINITE
     st, C, M, r_gpu = gpu_int8(ctx, x, r, 1.0)
     assert st == tlc.TLC_E_NONFINITE and C.size == 0
-    assert np.array_equal(G().bits(r_gpu), G().bits(r_ref))  # the step-1 sum
+    assert np.array_equal(G().bits(r_gpu), G().bits(r))  # untouched
+    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
+    try:
+        r_ref = r.copy()
+        assert oracle.compress_int8(x, r_ref, 1.0, in_place=True)[0] == oracle.E_NONFINITE
+        st, C, M, r_gpu = gpu_int8(ctx, x, r, 1.0)
+        assert st == tlc.TLC_E_NONFINITE and C.size == 0
+        assert np.array_equal(G().bits(r_gpu), G().bits(r_ref))  # x + r
+    finally:
+        ctx.set_options(0)
     xd = torch.zeros(100, device="cuda")
     o = torch.zeros(100, dtype=torch.uint8, device="cuda")
     st, ln, sc = tlc.tlc_compress_ex(ctx.handle, tlc.TLC_MODE_INT8, xd.data_ptr(), None, 100,

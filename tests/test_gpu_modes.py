@@ -99,8 +99,17 @@ def test_modes_reject_bad_input(ctx):
     r = workloads.normal([922], 1000, 1e-3)
     r_ref = r.copy()
     assert oracle.compress_nozre(x, r_ref, 1.0)[0] == oracle.E_NONFINITE
-    st, Q, M, r_gpu = gpu_mode(ctx, tlc.TLC_MODE_NO_ZRE, x, r, 1.0)
+    st, Q, M, r_gpu = gpu_mode(ctx, tlc.TLC_MODE_NO_ZRE, x, r.copy(), 1.0)
     assert st == tlc.TLC_E_NONFINITE and Q.size == 0
-    assert np.array_equal(r_gpu.view(np.uint32), r_ref.view(np.uint32))
+    assert np.array_equal(r_gpu.view(np.uint32), r_ref.view(np.uint32))  # untouched
+    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
+    try:
+        r_ref = r.copy()
+        assert oracle.compress_nozre(x, r_ref, 1.0, in_place=True)[0] == oracle.E_NONFINITE
+        st, Q, M, r_gpu = gpu_mode(ctx, tlc.TLC_MODE_NO_ZRE, x, r.copy(), 1.0)
+        assert st == tlc.TLC_E_NONFINITE and Q.size == 0
+        assert np.array_equal(r_gpu.view(np.uint32), r_ref.view(np.uint32))  # x + r
+    finally:
+        ctx.set_options(0)
     st, *_ = gpu_mode(ctx, 7, workloads.normal([921], 10), np.zeros(10, F32), 1.0)
     assert st == tlc.TLC_E_INVALID

@@ -282,8 +282,7 @@ def test_subnormals(ctx):
 
 
 def test_negative_zero_accumulate(ctx):
-    """Accumulating keeps -0.0 where q = 0 and adds M*q elsewhere, as in the
-    oracle."""
+    """Dense Eq. 3: -0.0 + M*0 = +0.0 on both sides."""
     n = 4096
     x = workloads.normal([60], n, 1.0)
     out0 = np.full(n, -0.0, F32)
@@ -291,36 +290,56 @@ def test_negative_zero_accumulate(ctx):
 
 
 # ------------------------------------------------------------------ error paths
-def test_nonfinite_keeps_sum_and_no_bytes(ctx):
-    """NaN/Inf: no byte is written and the buffer holds the step-1 sum x + r,
-    as in the oracle.  Both the chained (small) and three-pass (large)
-    encoders."""
+def test_nonfinite_leaves_residual_and_bytes(ctx):
+    """NaN/Inf: no byte is written and the residual is left as it was
+    (reading A4), on the chained (small) and three-pass (large) encoders;
+    with TLC_OPT_IN_PLACE_FEEDBACK it holds the step-1 sum x + r, as in
+    the oracle's in-place variant."""
     import torch
     from paper_1802_07389_amd import tlc
-    for n in (100_000, THREE_PASS_N[0]):
-        for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
-            x = workloads.normal([70, pos], n)
-            x[pos] = bad
-            r = workloads.normal([71, pos], n)
-            r_ref = r.copy()
-            st_ref, _, _ = oracle.compress(x, r_ref, 1.0)
-            xd, rd = torch.from_numpy(x).cuda(), torch.from_numpy(r).cuda()
-            out = torch.full((n // 5 + 1,), 7, dtype=torch.uint8, device="cuda")
-            st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n, 1.0,
-                                          out.data_ptr(), out.numel())
-            assert st == st_ref == tlc.TLC_E_NONFINITE and ln == 0
-            assert np.array_equal(G().bits(rd.cpu().numpy()), G().bits(r_ref))
-            assert bool((out == 7).all())
-    # overflow of max * s: the finite sums stay in the buffer
-    x = np.array([3.0e38, 1.0, 2.0, 3.0, 4.0], F32)
-    r0 = np.array([-0.0, 0.5, 0.0, -1.0, 2.0], F32)
-    r_ref = r0.copy()
-    assert oracle.compress(x, r_ref, 1.5)[0] == oracle.E_NONFINITE
-    st, _, _, r_gpu = G().gpu_compress(ctx, x, r0.copy(), 1.5)
-    assert st == tlc.TLC_E_NONFINITE
-    assert np.array_equal(G().bits(r_gpu), G().bits(r_ref))
+    for opts in (0, tlc.TLC_OPT_IN_PLACE_FEEDBACK):
+        ctx.set_options(opts)
+        try:
+            for n in (100_000, THREE_PASS_N[0]):
+                for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
+                    x = workloads.normal([70, pos], n)
+                    x[pos] = bad
+                    r = workloads.normal([71, pos], n)
+                    r_ref = r.copy()
+                    st_ref, _, _ = oracle.compress(x, r_ref, 1.0, in_place=bool(opts))
+                    xd, rd = torch.from_numpy(x).cuda(), torch.from_numpy(r).cuda()
+                    out = torch.full((n // 5 + 1,), 7, dtype=torch.uint8, device="cuda")
+                    st, ln, sc = tlc.tlc_compress(ctx.handle, xd.data_ptr(), rd.data_ptr(), n,
+                                                  1.0, out.data_ptr(), out.numel())
+                    assert st == st_ref == tlc.TLC_E_NONFINITE and ln == 0
+                    assert np.array_equal(G().bits(rd.cpu().numpy()), G().bits(r_ref)), opts
+                    assert bool((out == 7).all())
+            # overflow of max * s: every sum is finite
+            x = np.array([3.0e38, 1.0, 2.0, 3.0, 4.0], F32)
+            r0 = np.array([-0.0, 0.5, 0.0, -1.0, 2.0], F32)
+            r_ref = r0.copy()
+            assert oracle.compress(x, r_ref, 1.5, in_place=bool(opts))[0] == oracle.E_NONFINITE
+            st, _, _, r_gpu = G().gpu_compress(ctx, x, r0.copy(), 1.5)
+            assert st == tlc.TLC_E_NONFINITE
+            assert np.array_equal(G().bits(r_gpu), G().bits(r_ref)), opts
+        finally:
+            ctx.set_options(0)
     # the context still works afterwards
     check_encode_decode(ctx, workloads.normal([72], 1000), np.zeros(1000, F32), 1.0)
+
+
+@pytest.mark.parametrize("n", [100_003, THREE_PASS_N[0], THREE_PASS_N[1]])
+def test_in_place_option_same_results(ctx, n):
+    """On finite input the in-place option changes no byte or residual."""
+    from paper_1802_07389_amd import tlc
+    x = workloads.normal([73, n], n, 1.0)
+    r = workloads.normal([74, n], n, 1e-2)
+    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
+    try:
+        check_encode_decode(ctx, x, r, 1.5, out0=workloads.normal([75], n), accumulate=True,
+                            tag=f"in place n={n}")
+    finally:
+        ctx.set_options(0)
 
 
 def test_invalid_arguments(ctx):

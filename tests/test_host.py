@@ -68,7 +68,8 @@ def test_host_only_entry_points():
                      "tlc_expand_dequant_batch_kernel", "tlc_expand_sum_kernel",
                      "tlc_quant_pack_kernel", "tlc_int8_quant_kernel",
                      "tlc_int8_dequant_kernel", "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel",
-                     "tlc_quant_encode_chained_kernel"]
+                     "tlc_quant_encode_chained_kernel", "tlc_absmax_check_kernel",
+                     "tlc_absmax_check_batch_kernel"]
     assert tlc.tlc_kernel_name(99) is None
 
 
