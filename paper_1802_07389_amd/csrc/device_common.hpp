@@ -354,10 +354,11 @@ __device__ __forceinline__ void fill_zero_groups(uint8_t* lds, uint32_t lo, uint
 }
 
 // ---------------------------------------------------------------- Eq. 3
-// The dequantized value M*q for trit t = q + 1 is -M, +0 or M (M*(-1) is
-// the exact negation and M*0 is +0 for finite M >= 0).
+// The dequantized value M*q for trit t = q + 1 is -M, M*0 or M (M*(-1) is
+// the exact negation; M*0 is +0, or -0 for a scale of -0.0, which the
+// decoder accepts as >= 0).
 __device__ __forceinline__ float trit_value(uint32_t t, float M) {
-  return t == 0u ? -M : (t == 1u ? 0.0f : M);
+  return t == 0u ? -M : (t == 1u ? M * 0.0f : M);
 }
 
 // Eq. 3 accumulated densely into out (every value: out + M*q, so -0.0 + 0

@@ -289,6 +289,36 @@ def test_negative_zero_accumulate(ctx):
     check_encode_decode(ctx, x, np.zeros(n, F32), 1.9, out0=out0, accumulate=True, tag="-0")
 
 
+@pytest.mark.parametrize("scale", [-0.0, 0.0, 3.5])
+def test_decode_signed_zero_scales(ctx, scale):
+    """Eq. 3 takes M*q literally: a scale of -0.0 (accepted, as -0.0 >= 0)
+    gives M*0 = -0.0, so -0.0 + M*0 stays -0.0, and +0.0 + M*0 is +0.0.
+    Streams of random quartic bytes (q = -1, 0, 1 mixed, zero runs
+    included) decoded into outputs that mix -0.0, +0.0 and other values,
+    on the float4 path (m % 4 = 0, the last group in the padding), the
+    shifted path (m % 4 = 2) and unaligned outputs."""
+    g = G()
+    rng = np.random.default_rng([61, int(np.signbit(scale)), int(scale)])
+    for n, offset in [(5 * 4096 * 4, 0), (5 * 4096 * 4 - 3, 0), (61447, 0), (61447, 1)]:
+        m = oracle.quartic_len(n)
+        Q = rng.integers(0, 243, m, dtype=np.uint8)
+        Q[rng.random(m) < 0.6] = 121
+        C = oracle.zre_encode(Q)
+        out0 = rng.standard_normal(n).astype(F32)
+        pick = rng.random(n)
+        out0[pick < 0.3] = -0.0
+        out0[(pick >= 0.3) & (pick < 0.5)] = 0.0
+        for acc in (False, True):
+            tag = f"scale={scale!r} n={n} offset={offset} acc={acc}"
+            g.log(tag)
+            st_ref, out_ref = oracle.decompress(C, scale, n, out0.copy(), acc)
+            st, out = g.gpu_decompress(ctx, C, scale, n, out0.copy(), acc, offset=offset)
+            assert st == st_ref == 0, (tag, st, st_ref)
+            if not np.array_equal(g.bits(out), g.bits(out_ref)):
+                i = int(np.flatnonzero(g.bits(out) != g.bits(out_ref))[0])
+                raise AssertionError(f"{tag}: decoded {i} differs: {out[i]!r} vs {out_ref[i]!r}")
+
+
 # ------------------------------------------------------------------ error paths
 def test_nonfinite_leaves_residual_and_bytes(ctx):
     """NaN/Inf: no byte is written and the residual is left as it was
@@ -453,6 +483,45 @@ def test_c3_runs_sweep_s(ctx):
     for s in workloads.C3_S:
         check_encode_decode(ctx, x, np.zeros_like(x), s, tag=f"C3 s={s}")
         G().log(f"C3 s={s} ok")
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n", [(1 << 27) + 3, 134_217_738])
+def test_large_accumulate_nontemporal(ctx, n):
+    """Outputs of 512 MiB and more decode with the nontemporal partition
+    sweep.  Streams of synthetic quartic bytes: sparse ranges (~1.5 %
+    non-121 bytes) and 10 % dense ranges (half the bytes random), decoded
+    with accumulate into an output of -0.0, +0.0 and normal values (dense
+    Eq. 3: -0.0 + M*0 = +0.0); m % 4 = 3 (shifted cells) and m % 4 = 0, both
+    with values in the padding's partition.  A truncated and an extended
+    stream must leave the output untouched."""
+    from paper_1802_07389_amd import tlc
+    g = G()
+    rng = np.random.default_rng([62, n])
+    m = oracle.quartic_len(n)
+    Q = np.full(m, 121, np.uint8)
+    hit = rng.random(m) < 0.015
+    dense_ranges = rng.random(-(-m // 4096)) < 0.1
+    hit |= np.repeat(dense_ranges, 4096)[:m] & (rng.random(m) < 0.5)
+    Q[hit] = rng.integers(0, 243, int(hit.sum()), dtype=np.uint8)
+    C = oracle.zre_encode(Q)
+    out0 = rng.standard_normal(n).astype(F32)
+    pick = rng.random(n)
+    out0[pick < 0.2] = -0.0
+    out0[(pick >= 0.2) & (pick < 0.3)] = 0.0
+    M = np.float32(2.5e-3)
+    g.log(f"nontemporal accumulate n={n} m%4={m % 4} len={C.size}")
+    st_ref, out_ref = oracle.decompress(C, M, n, out0.copy(), True)
+    st, out = g.gpu_decompress(ctx, C, M, n, out0.copy(), True)
+    assert st == st_ref == 0, (st, st_ref)
+    if not np.array_equal(g.bits(out), g.bits(out_ref)):
+        i = int(np.flatnonzero(g.bits(out) != g.bits(out_ref))[0])
+        raise AssertionError(f"decoded {i} differs: {out[i]!r} vs {out_ref[i]!r}")
+    del out, out_ref
+    for bad in (C[:-1], np.append(C, C[-1:])):
+        st, out = g.gpu_decompress(ctx, bad, M, n, out0.copy(), True)
+        assert st == tlc.TLC_E_CORRUPT
+        assert np.array_equal(g.bits(out), g.bits(out0))
 
 
 @pytest.mark.timeout(900)
