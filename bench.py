@@ -41,18 +41,16 @@ def algorithmic_bytes(n, c, nnz):
     return {
         # the check pass of the default error policy: read x, r
         "tlc_absmax_check_kernel": 8 * n,
-        # read x, r; write r = x + r (the 2-byte bound per float4 it also
-        # writes, n/2 bytes, is not counted)
-        "tlc_accum_absmax_kernel": 12 * n,
-        # read the bounds (n/2) and at most one float4 per value with q != 0;
-        # write each tile's own stream bytes (c in all), record and the
-        # (index, residual) list of its values with q != 0
-        "tlc_quant_encode_kernel": n // 2 + 16 * nnz + c + 16 * tiles + 8 * nnz,
+        # read x, r; write the residual r = acc - M*q and one byte of 2-bit
+        # trits (q + 1) per float4 for the quartic pack
+        "tlc_accum_absmax_kernel": 12 * n + n // 4,
+        # read the trits; write each tile's own stream bytes (c in all) and
+        # its 16-byte record
+        "tlc_quant_encode_kernel": n // 4 + c + 16 * tiles,
         # tile records in, tile prefixes and chunk summaries out
         "tlc_zre_chunk_kernel": 24 * tiles,
-        # records, prefixes and slot bytes in, the stream out, and the lists'
-        # residuals into r
-        "tlc_zre_compact_kernel": 2 * c + 32 * tiles + 12 * nnz,
+        # records, prefixes and slot bytes in, the stream out
+        "tlc_zre_compact_kernel": 2 * c + 32 * tiles,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
         # read C; accumulating densely, read every value of out and store the
         # sums that change it (the nnz values with q != 0 here)

@@ -107,6 +107,51 @@ __device__ __forceinline__ uint32_t absmax_part(const float* __restrict__ x,
   return mx;
 }
 
+// The writing pass of the default error policy on the float4 path, once the
+// check pass has given M (Eq. 1): acc = x + r, q = round(acc / M) and the
+// residual acc - M*q (Eq. 2, Fig. 3 steps a-b) for every value; the
+// residual is stored in place and q + 1 kept as a 2-bit trit, one byte per
+// float4 of the buffer (value 4i + c in bits 2c, 2c + 1), from which the
+// quantizer packs the quartic bytes without reading the buffer again.  The
+// last n % 4 values are taken by one thread, which writes their byte.
+__device__ __forceinline__ void accum_quantize_part(const float* __restrict__ x,
+                                                    float* __restrict__ r, uint64_t n,
+                                                    uint32_t blk, uint32_t nblk, float M,
+                                                    float U, uint8_t* __restrict__ trits) {
+  const uint64_t tid = (uint64_t)blk * kThreads + threadIdx.x;
+  const uint64_t stride = (uint64_t)nblk * kThreads;
+  const uint64_t nv = n >> 2;
+  auto put4 = [&](uint64_t i, const float4& a, const float4& b) {
+    float4 o;
+    const uint32_t t0 = quantize_one(a.x + b.x, M, U, o.x);
+    const uint32_t t1 = quantize_one(a.y + b.y, M, U, o.y);
+    const uint32_t t2 = quantize_one(a.z + b.z, M, U, o.z);
+    const uint32_t t3 = quantize_one(a.w + b.w, M, U, o.w);
+    st_stream(r + 4 * i, o);
+    trits[i] = (uint8_t)(t0 | (t1 << 2) | (t2 << 4) | (t3 << 6));
+  };
+  uint64_t i = tid;
+  for (; i + 3 * stride < nv; i += 4 * stride) {
+    float4 a[4], b[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] = ld_stream(x + 4 * (i + u * stride));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) b[u] = ld_stream(r + 4 * (i + u * stride));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) put4(i + u * stride, a[u], b[u]);
+  }
+  for (; i < nv; i += stride) put4(i, ld_stream(x + 4 * i), ld_stream(r + 4 * i));
+  if (tid == 0 && (n & 3u)) {
+    uint32_t tb = 0u;
+    for (uint64_t e = nv << 2; e < n; ++e) {
+      float o;
+      tb |= quantize_one(x[e] + r[e], M, U, o) << (2u * (uint32_t)(e & 3u));
+      r[e] = o;
+    }
+    trits[nv] = (uint8_t)tb;
+  }
+}
+
 // Partial maxima of |x + r| that write nothing: the check pass that lets
 // the default error policy refuse NaN/Inf before the buffer is touched.
 template <bool kVec>
@@ -136,12 +181,27 @@ __device__ __forceinline__ bool refused_by_guard(const uint32_t* __restrict__ gu
   return true;
 }
 
-template <bool kVec, bool kResid, bool kSum>
+// kTrit (float4 path, after the check pass): the check pass's maxima give
+// M, the buffer receives the final residuals and `summ` the trits
+// (accum_quantize_part); the block's partial is the check pass's own.
+template <bool kVec, bool kResid, bool kSum, bool kTrit = false>
 __global__ __launch_bounds__(kThreads) void tlc_accum_absmax_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n,
     uint32_t* __restrict__ partials, uint16_t* __restrict__ summ,
     const uint32_t* __restrict__ guard, uint32_t guard_np, float s) {
   __shared__ uint32_t lds[kWaves];
+  if (kTrit) {
+    static_assert(!kTrit || (kVec && kResid && !kSum), "trits come from the float4 buffer path");
+    const Scale g = finish_scale(guard, guard_np, s, lds);
+    if (g.bad) {  // NaN/Inf or overflow: nothing written, later kernels refuse too
+      if (threadIdx.x == 0) partials[blockIdx.x] = 0xffffffffu;
+      return;
+    }
+    accum_quantize_part(x, r, n, blockIdx.x, gridDim.x, g.M, g.U,
+                        reinterpret_cast<uint8_t*>(summ));
+    if (threadIdx.x == 0) partials[blockIdx.x] = guard[blockIdx.x];
+    return;
+  }
   if (refused_by_guard(guard, guard_np, s, lds, &partials[blockIdx.x])) return;
   const uint32_t mx =
       block_max(absmax_part<kVec, kResid, kSum>(x, r, n, blockIdx.x, gridDim.x, summ), lds);
@@ -601,7 +661,49 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
   for (uint32_t i = threadIdx.x; i < nf; i += kThreads) fix[i] = s_fix[i];
 }
 
-template <int kPath>
+// Phase 1 of a first-pass tile when the max pass has quantized every value
+// (kTrit; m % 4 == 0, so the values j..j+3 of partition k are float4
+// (k*m + j)/4 of the buffer and their trits one byte): the quartic bytes
+// (Section 3.2), with the values past n as the zero padding (trit 0).
+// Group g = threadIdx.x + kThreads * it, as in the float4 path.  Ends with
+// a barrier.
+__device__ __forceinline__ void quartic_from_trits(const uint8_t* __restrict__ trits,
+                                                   uint64_t n, uint32_t m, uint64_t q0,
+                                                   uint32_t tile_bytes, uint8_t* q) {
+  uint32_t tb[kGroupsPerThread][5];
+#pragma unroll
+  for (int it = 0; it < kGroupsPerThread; ++it) {
+    const uint32_t g = threadIdx.x + kThreads * it;
+    const uint64_t j = q0 + g * 4u;
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const uint64_t e = (uint64_t)k * m + j;
+      tb[it][k] = (g * 4u < tile_bytes && e < n) ? (uint32_t)trits[e >> 2] : 0u;
+    }
+  }
+  uint32_t* qw = reinterpret_cast<uint32_t*>(q);
+#pragma unroll
+  for (int it = 0; it < kGroupsPerThread; ++it) {
+    const uint32_t g = threadIdx.x + kThreads * it;
+    if (g * 4u >= tile_bytes) break;
+    const uint64_t j = q0 + g * 4u;
+    uint32_t code[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const uint64_t e = (uint64_t)k * m + j;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        code[c] = code[c] * 3u + (e + c < n ? (tb[it][k] >> (2 * c)) & 3u : 0u);
+    }
+    qw[g] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+  }
+  __syncthreads();
+}
+
+// kTrit (kPathVec only): the buffer already holds the residuals and `summ`
+// the trits of every value (the max pass after the check pass); phase 1
+// only packs them, and the tile's residual list stays empty.
+template <int kPath, bool kTrit = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5)))
 void tlc_quant_encode_kernel(
     float* __restrict__ r, uint64_t n, uint32_t m, float s,
@@ -610,8 +712,9 @@ void tlc_quant_encode_kernel(
     Ctrl* __restrict__ ctrl) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
+  static_assert(!kTrit || kPath == kPathVec, "trits are kept on the float4 path");
   __shared__ EncShared sh;
-  __shared__ uint2 s_fix[kPath == kPathVec ? kFixCap : 1];
+  __shared__ uint2 s_fix[(kPath == kPathVec && !kTrit) ? kFixCap : 1];
   if (threadIdx.x == 0) {
     sh.nfix = 0u;
     sh.nneed = 0u;
@@ -620,14 +723,16 @@ void tlc_quant_encode_kernel(
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
   uint32_t h[kGroupsPerThread][5];
-  if (kPath == kPathVec && summ) load_bounds(summ, n, m, q0, tile_bytes, h);
+  if (kPath == kPathVec && !kTrit && summ) load_bounds(summ, n, m, q0, tile_bytes, h);
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
-  if (kPath == kPathVec) {
+  if (kTrit) {
+    quartic_from_trits(reinterpret_cast<const uint8_t*>(summ), n, m, q0, tile_bytes, sh.q);
+  } else if (kPath == kPathVec) {
     if (summ)
       quantize_tile_vec_deferred<true>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
                                        &sh.nneed, fix + (uint64_t)t * kFixCap, h);
@@ -962,12 +1067,18 @@ hipError_t launch_absmax_check(const float* x, const float* r, uint64_t n, uint3
 
 hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* partials,
                                uint32_t* nblocks, uint16_t* summ, const uint32_t* guard,
-                               uint32_t guard_np, float s, hipStream_t st) {
+                               uint32_t guard_np, float s, bool trit, hipStream_t st) {
   const bool vec = aligned16(x) && (r == nullptr || aligned16(r));
   if (summ && !(vec && r)) return hipErrorInvalidValue;  // summaries need the float4 path
+  if (trit && !(summ && guard)) return hipErrorInvalidValue;  // trits need M from the check
   const uint32_t blocks = absmax_blocks(n, vec);
   if (guard && guard_np != blocks) return hipErrorInvalidValue;  // same launch as the check
   *nblocks = blocks;
+  if (trit) {
+    tlc_accum_absmax_kernel<true, true, false, true><<<blocks, kThreads, 0, st>>>(
+        x, r, n, partials, summ, guard, guard_np, s);
+    return hipGetLastError();
+  }
 #define TLC_LAUNCH(V, R, S)                                                                 \
   tlc_accum_absmax_kernel<V, R, S><<<blocks, kThreads, 0, st>>>(x, r, n, partials, summ, guard, \
                                                                 guard_np, s)
@@ -984,11 +1095,15 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* p
 
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, uint2* fix, const uint16_t* summ, Ctrl* ctrl,
-                               hipStream_t st) {
+                               TileRec* recs, uint2* fix, const uint16_t* summ, bool trit,
+                               Ctrl* ctrl, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
-  if (al && m % 4 == 0)
+  if (trit) {
+    if (!(al && m % 4 == 0 && summ)) return hipErrorInvalidValue;
+    tlc_quant_encode_kernel<kPathVec, true><<<ntiles, kThreads, 0, st>>>(
+        r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
+  } else if (al && m % 4 == 0)
     tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
         r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
   else if (al)

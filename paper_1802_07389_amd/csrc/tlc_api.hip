@@ -435,8 +435,12 @@ namespace {
 // writing, and the writing pass leaves a tensor whose scale is bad
 // untouched, so the buffer keeps its values on TLC_E_NONFINITE;
 // TLC_OPT_IN_PLACE_FEEDBACK drops the check pass.
+// With summ (the three-pass float4 path) after a check pass, the writing
+// pass quantizes every value and leaves trits in summ (*trit set); in place
+// it leaves acc and bounds.
 int launch_max_passes(tlc_ctx* c, const float* x, float* r, size_t n, float s, uint16_t* summ,
-                      uint32_t* np) {
+                      uint32_t* np, bool* trit = nullptr) {
+  if (trit) *trit = false;
   const uint32_t* guard = nullptr;
   uint32_t guard_np = 0;
   if (r && !(c->options & TLC_OPT_IN_PLACE_FEEDBACK)) {
@@ -446,8 +450,11 @@ int launch_max_passes(tlc_ctx* c, const float* x, float* r, size_t n, float s, u
     if (st) return st;
     guard = c->partials_chk;
   }
+  const bool quantize = summ != nullptr && guard != nullptr;
+  if (trit) *trit = quantize;
   return timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
-    return launch_accum_absmax(x, r, n, c->partials, np, summ, guard, guard_np, s, c->stream);
+    return launch_accum_absmax(x, r, n, c->partials, np, summ, guard, guard_np, s, quantize,
+                               c->stream);
   });
 }
 
@@ -490,14 +497,17 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (st) return st;
 
   const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
-  // The three passes' float4 path skips float4s of the buffer whose bound
-  // from the max pass (which writes them on its own float4 path) is below U.
+  // The three passes' float4 path: after the check pass the max pass
+  // quantizes every value and keeps 2-bit trits per value in summ; in place
+  // it keeps a bound per float4 there, and the quantizer skips float4s of
+  // the buffer whose bound is below U.
   uint16_t* summ = (ntiles >= kThreePassMinTiles && aligned16(tensor) && aligned16(residual) &&
                     m % 4 == 0)
                        ? c->summ
                        : nullptr;
   uint32_t np = 0;
-  st = launch_max_passes(c, tensor, residual, n, s, summ, &np);
+  bool trit = false;
+  st = launch_max_passes(c, tensor, residual, n, s, summ, &np, &trit);
   if (st) return st;
   if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
     uint32_t epoch = 0;
@@ -515,7 +525,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   }
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
-                               c->fix, summ, c->ctrl, c->stream);
+                               c->fix, summ, trit, c->ctrl, c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {

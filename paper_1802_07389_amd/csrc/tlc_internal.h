@@ -107,14 +107,17 @@ hipError_t launch_absmax_check(const float* x, const float* r, uint64_t n, uint3
 // only written on the float4 path (x and r 16-byte aligned).  guard (may
 // be NULL): the check pass's guard_np partial maxima; if they give a bad
 // scale (with s), nothing is written and the partials mark the tensor bad.
+// trit: after the check pass (guard) on the float4 path, the pass quantizes
+// every value (final residuals in r, 2-bit trits in summ, one byte per
+// float4) and launch_quant_encode(trit) only packs the trits.
 hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
                                uint32_t* partials, uint32_t* nblocks, uint16_t* summ,
-                               const uint32_t* guard, uint32_t guard_np, float s,
+                               const uint32_t* guard, uint32_t guard_np, float s, bool trit,
                                hipStream_t st);
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
-                               TileRec* recs, uint2* fix, const uint16_t* summ, Ctrl* ctrl,
-                               hipStream_t st);
+                               TileRec* recs, uint2* fix, const uint16_t* summ, bool trit,
+                               Ctrl* ctrl, hipStream_t st);
 hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
                                        const uint32_t* partials, uint32_t npartials, uint8_t* out,
                                        uint64_t* status, uint32_t ntiles, uint32_t ticket_base,

@@ -152,8 +152,11 @@ def test_partitions_off_float4_grid(ctx, n, offset):
 
 # tensors of 520 encoder tiles and more take the three-pass encoder (each
 # tile encoded into its own slot, then the tile summaries scanned and the
-# stream compacted); the patterns below stress its tile boundaries
-THREE_PASS_N = [5 * 4096 * 520, 5 * 4096 * 520 + 13, 5 * (4096 * 531 + 2) - 1]
+# stream compacted); the patterns below stress its tile boundaries.  The
+# last two have m % 4 = 0 and n % 4 = 3 or 1: the float4 path with a
+# partial last float4, whose values the max pass quantizes one by one.
+THREE_PASS_N = [5 * 4096 * 520, 5 * 4096 * 520 + 13, 5 * (4096 * 531 + 2) - 1,
+                5 * 4096 * 520 - 1, 5 * 4096 * 520 - 3]
 
 
 @pytest.mark.parametrize("n", THREE_PASS_N)
@@ -229,10 +232,23 @@ def test_threshold_boundaries(ctx):
 
 @pytest.mark.parametrize("M_target", [1.0, 1.2345678, 3 * 2.0 ** -140])
 def test_float4_skip_bound_edges(ctx, M_target):
-    """Large tensors on the float4 path skip float4s whose bound from the
-    max pass (top 16 bits of the largest |acc|) is below U's top 16 bits.
-    Plant values at U, one ulp either side, and at both ends of U's top-half
-    bucket among small values, in every partition and at tile edges."""
+    """Large tensors on the float4 path: by default the max pass decides
+    every q against U itself (after the check pass has given M); with the
+    in-place option it leaves a bound per float4 (top 16 bits of the
+    largest |acc|) and the quantizer skips float4s whose bound is below U's
+    top 16 bits.  Plant values at U, one ulp either side, and at both ends
+    of U's top-half bucket among small values, in every partition and at
+    tile edges; both policies, two steps each."""
+    from paper_1802_07389_amd import tlc
+    for opts in (0, tlc.TLC_OPT_IN_PLACE_FEEDBACK):
+        ctx.set_options(opts)
+        try:
+            _skip_bound_edges(ctx, M_target)
+        finally:
+            ctx.set_options(0)
+
+
+def _skip_bound_edges(ctx, M_target):
     g = G()
     n = THREE_PASS_N[0]
     m = -(-n // 5)
@@ -358,7 +374,7 @@ def test_nonfinite_leaves_residual_and_bytes(ctx):
     check_encode_decode(ctx, workloads.normal([72], 1000), np.zeros(1000, F32), 1.0)
 
 
-@pytest.mark.parametrize("n", [100_003, THREE_PASS_N[0], THREE_PASS_N[1]])
+@pytest.mark.parametrize("n", [100_003, THREE_PASS_N[0], THREE_PASS_N[1], THREE_PASS_N[3]])
 def test_in_place_option_same_results(ctx, n):
     """On finite input the in-place option changes no byte or residual."""
     from paper_1802_07389_amd import tlc
