@@ -135,8 +135,11 @@ __device__ __forceinline__ uint32_t range_end(const uint64_t* __restrict__ start
 // s_q.  The stream bytes covering the range (found through the start
 // entries) are spread over the threads; a block scan of their expansion
 // lengths gives each one its position and each thread writes its own
-// expansions.  Ends with a barrier.
-__device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint32_t c,
+// expansions.  The same scan counts the slice's data bytes other than 121
+// (packed as length + (count << 16): a slice expands to fewer than
+// kDecRange + 28 bytes and holds at most kDecRange bytes, so no carry
+// crosses), which is returned.  Ends with a barrier.
+__device__ __forceinline__ uint32_t expand_range(const uint8_t* __restrict__ C, uint32_t c,
                                              const uint64_t* __restrict__ starts, uint32_t k,
                                              uint64_t m, uint32_t qn, uint8_t* s_q,
                                              uint32_t* red) {
@@ -154,9 +157,10 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
   uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+    if ((uint32_t)i < cnt)
+      sum += expanded_len(b[i]) + (b[i] < kRunBase && b[i] != kZeroGroup ? 1u << 16 : 0u);
   const ScanU32 sc = block_scan_u32(sum, red);
-  int pos = (int)sc.excl - (int)skip;  // range-relative start of b[0]
+  int pos = (int)(sc.excl & 0xffffu) - (int)skip;  // range-relative start of b[0]
 #pragma unroll
   for (int i = 0; i < kBytes; ++i) {
     if ((uint32_t)i < cnt) {
@@ -174,6 +178,7 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
     }
   }
   __syncthreads();
+  return sc.total >> 16;
 }
 
 // ---------------------------------------------------------------- Eq. 3
@@ -189,6 +194,13 @@ __device__ __forceinline__ void expand_range(const uint8_t* __restrict__ C, uint
 // stores leave no dirty lines for the next encode to write back.  Outputs
 // that fit the cache decode faster with plain accesses.
 constexpr int kSweepCells = (kDecRange + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
+
+// Accumulating, a sweep stores only the float4s whose sums change bits,
+// unless its range's stream slice has more than this many data bytes other
+// than 121: then most float4s change, and storing every one keeps the
+// writes a contiguous stream (scattered stores inside the read stream cost
+// far more than their bytes).  Either way every value gets out + M*q.
+constexpr uint32_t kDenseLiterals = kDecRange / 4;
 
 // The kAcc loads of partition K's full cells (the cells the sweep below
 // adds to), issued before the range's zero-run expansion so that their
@@ -214,6 +226,7 @@ template <int K, bool kAcc, bool kNT, bool kPre = false>
 __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, uint64_t q0,
                                                           uint32_t qn, uint64_t n, uint64_t m,
                                                           float M, float* __restrict__ out,
+                                                          bool dense,
                                                           const float4* pre = nullptr) {
   constexpr uint32_t kPlace = K == 0 ? 81u : (K == 1 ? 27u : (K == 2 ? 9u : (K == 3 ? 3u : 1u)));
   constexpr int kCells = kSweepCells;
@@ -251,7 +264,7 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
     if (full[i]) {
       bool store = true;
       if (kAcc) {
-        store = acc_trit4(o[i], d, M);
+        store = acc_trit4(o[i], d, M) || dense;
       } else {
         o[i] = make_float4(trit_value(d[0], M), trit_value(d[1], M), trit_value(d[2], M),
                            trit_value(d[3], M));
@@ -288,13 +301,13 @@ __device__ __forceinline__ void dequant_partition_shifted(const uint8_t* s_q, ui
 template <int kPath, bool kAcc, bool kNT = false>
 __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, uint32_t qn,
                                               uint64_t n, uint64_t m, float M,
-                                              float* __restrict__ out) {
+                                              float* __restrict__ out, bool dense) {
   if (kPath == kPathShift) {
-    dequant_partition_shifted<0, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<1, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    dequant_partition_shifted<0, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<1, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
   } else if (kPath == kPathVec) {
 #pragma unroll
     for (int g = 0; g < kDecRange / (4 * kThreads); ++g) {
@@ -316,7 +329,7 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
           bool store = true;
           if (kAcc) {
             const uint32_t dk[4] = {t[0][k], t[1][k], t[2][k], t[3][k]};
-            store = acc_trit4(o[k], dk, M);
+            store = acc_trit4(o[k], dk, M) || dense;
           } else {
             o[k].x = trit_value(t[0][k], M);
             o[k].y = trit_value(t[1][k], M);
@@ -379,16 +392,16 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
     float4 p0[kSweepCells], p1[kSweepCells];
     sweep_preload<0, kNT>(q0, qn, n, m, out, p0);
     sweep_preload<1, kNT>(q0, qn, n, m, out, p1);
-    expand_range(C, c, start, k, m, qn, s_q, red);
-    dequant_partition_shifted<0, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, p0);
-    dequant_partition_shifted<1, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, p1);
-    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
-    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+    const bool dense = expand_range(C, c, start, k, m, qn, s_q, red) > kDenseLiterals;
+    dequant_partition_shifted<0, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, dense, p0);
+    dequant_partition_shifted<1, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, dense, p1);
+    dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
+    dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
     return;
   }
-  expand_range(C, c, start, k, m, qn, s_q, red);
-  dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out);
+  const bool dense = expand_range(C, c, start, k, m, qn, s_q, red) > kDenseLiterals;
+  dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
 }
 
 template <bool kAcc>
@@ -404,13 +417,14 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
   const uint32_t k = blockIdx.x - d.range0;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, (uint64_t)d.m - q0);
-  expand_range(d.C, d.c, start + d.range0, k, d.m, qn, s_q, red);
+  const bool dense =
+      expand_range(d.C, d.c, start + d.range0, k, d.m, qn, s_q, red) > kDenseLiterals;
   if (d.vec & 1u)
-    dequant_range<kPathVec, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+    dequant_range<kPathVec, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out, dense);
   else if (d.vec & 2u)
-    dequant_range<kPathShift, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+    dequant_range<kPathShift, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out, dense);
   else
-    dequant_range<kPathByte, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out);
+    dequant_range<kPathByte, kAcc>(s_q, q0, qn, d.n, d.m, d.scale, d.out, dense);
 }
 
 // ---------------------------------------------------------------- aggregation
