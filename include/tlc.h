@@ -72,8 +72,11 @@ size_t tlc_max_compressed_bytes(size_t n);
 
 /* Create a context for tensors of up to max_n values (1 <= max_n <=
  * TLC_MAX_N) whose work is issued on `hip_stream` (a hipStream_t, or NULL).
- * Allocates about max_n/800 bytes of device workspace (partial maxima,
- * look-back status words and a start index for the decoder).  On success
+ * Allocates one device workspace of about 0.81 * max_n bytes (218 MB for
+ * max_n = 2^28): partial maxima, look-back status words, the decoder's
+ * start index, and for the single-tensor encoder per-tile slots, records
+ * and residual lists and two bytes per four values (bounds or trits of the
+ * max pass).  No later call allocates device memory.  On success
  * *ctx receives the context; on failure *ctx is NULL.  Same as
  * tlc_ctx_create_batch(ctx, max_n, 1, hip_stream). */
 int tlc_ctx_create(tlc_ctx** ctx, size_t max_n, void* hip_stream);
