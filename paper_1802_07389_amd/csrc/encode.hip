@@ -663,14 +663,15 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
 
 // Phase 1 of a first-pass tile when the max pass has quantized every value
 // (kTrit; m % 4 == 0, so the values j..j+3 of partition k are float4
-// (k*m + j)/4 of the buffer and their trits one byte): the quartic bytes
-// (Section 3.2), with the values past n as the zero padding (trit 0).
-// Group g = threadIdx.x + kThreads * it, as in the float4 path.  Ends with
-// a barrier.
-__device__ __forceinline__ void quartic_from_trits(const uint8_t* __restrict__ trits,
-                                                   uint64_t n, uint32_t m, uint64_t q0,
-                                                   uint32_t tile_bytes, uint8_t* q) {
-  uint32_t tb[kGroupsPerThread][5];
+// (k*m + j)/4 of the buffer and their trits one byte).  load_trits fetches
+// this thread's trit bytes (group g = threadIdx.x + kThreads * it, as in the
+// float4 path); they do not depend on M, so the loads are issued before the
+// block reduces it.  pack_trits then forms the quartic bytes (Section 3.2),
+// with the values past n as the zero padding (trit 0), and ends with a
+// barrier.
+__device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, uint64_t n,
+                                           uint32_t m, uint64_t q0, uint32_t tile_bytes,
+                                           uint32_t (&tb)[kGroupsPerThread][5]) {
 #pragma unroll
   for (int it = 0; it < kGroupsPerThread; ++it) {
     const uint32_t g = threadIdx.x + kThreads * it;
@@ -681,6 +682,11 @@ __device__ __forceinline__ void quartic_from_trits(const uint8_t* __restrict__ t
       tb[it][k] = (g * 4u < tile_bytes && e < n) ? (uint32_t)trits[e >> 2] : 0u;
     }
   }
+}
+
+__device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread][5], uint64_t n,
+                                           uint32_t m, uint64_t q0, uint32_t tile_bytes,
+                                           uint8_t* q) {
   uint32_t* qw = reinterpret_cast<uint32_t*>(q);
 #pragma unroll
   for (int it = 0; it < kGroupsPerThread; ++it) {
@@ -722,8 +728,11 @@ void tlc_quant_encode_kernel(
   const uint32_t t = blockIdx.x;
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  uint32_t h[kGroupsPerThread][5];
-  if (kPath == kPathVec && !kTrit && summ) load_bounds(summ, n, m, q0, tile_bytes, h);
+  uint32_t h[kGroupsPerThread][5];  // bounds, or with kTrit the trit bytes
+  if (kTrit)
+    load_trits(reinterpret_cast<const uint8_t*>(summ), n, m, q0, tile_bytes, h);
+  else if (kPath == kPathVec && summ)
+    load_bounds(summ, n, m, q0, tile_bytes, h);
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
@@ -731,7 +740,7 @@ void tlc_quant_encode_kernel(
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
   if (kTrit) {
-    quartic_from_trits(reinterpret_cast<const uint8_t*>(summ), n, m, q0, tile_bytes, sh.q);
+    pack_trits(h, n, m, q0, tile_bytes, sh.q);
   } else if (kPath == kPathVec) {
     if (summ)
       quantize_tile_vec_deferred<true>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
