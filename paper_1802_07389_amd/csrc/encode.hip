@@ -684,6 +684,12 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
   }
 }
 
+__device__ __forceinline__ uint32_t spread_trits(uint32_t tb) {
+  // the four 2-bit trits of one byte into the low bits of four bytes
+  tb = (tb | (tb << 12)) & 0x000f000fu;
+  return (tb | (tb << 6)) & 0x03030303u;
+}
+
 __device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread][5], uint64_t n,
                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
                                            uint8_t* q) {
@@ -693,6 +699,14 @@ __device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread
     const uint32_t g = threadIdx.x + kThreads * it;
     if (g * 4u >= tile_bytes) break;
     const uint64_t j = q0 + g * 4u;
+    if (4ull * m + j + 4u <= n) {
+      // all 20 values exist: the four bytes at once, 81*t0 + 27*t1 + 9*t2 +
+      // 3*t3 + t4 per byte lane (at most 242, so no carry crosses a lane)
+      qw[g] = 81u * spread_trits(tb[it][0]) + 27u * spread_trits(tb[it][1]) +
+              9u * spread_trits(tb[it][2]) + 3u * spread_trits(tb[it][3]) +
+              spread_trits(tb[it][4]);
+      continue;
+    }
     uint32_t code[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int k = 0; k < 5; ++k) {
