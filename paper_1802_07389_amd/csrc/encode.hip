@@ -662,24 +662,34 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
 }
 
 // Phase 1 of a first-pass tile when the max pass has quantized every value
-// (kTrit; m % 4 == 0, so the values j..j+3 of partition k are float4
-// (k*m + j)/4 of the buffer and their trits one byte).  load_trits fetches
-// this thread's trit bytes (group g = threadIdx.x + kThreads * it, as in the
-// float4 path); they do not depend on M, so the loads are issued before the
-// block reduces it.  pack_trits then forms the quartic bytes (Section 3.2),
-// with the values past n as the zero padding (trit 0), and ends with a
-// barrier.
+// (kTrit).  load_trits fetches, for each of this thread's groups (quartic
+// bytes j..j+3, g = threadIdx.x + kThreads * it, as in the float4 path) and
+// each partition k, the trits of values e = k*m + j .. e + 3 as one byte:
+// they start at bit 2*(e mod 4) of trit byte e/4 and run into the next one
+// when e mod 4 != 0 (m % 4 != 0).  They do not depend on M, so the loads
+// are issued before the block reduces it.  pack_trits then forms the
+// quartic bytes (Section 3.2), with the values past n as the zero padding
+// (trit 0), and ends with a barrier.
 __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, uint64_t n,
                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
                                            uint32_t (&tb)[kGroupsPerThread][5]) {
 #pragma unroll
-  for (int it = 0; it < kGroupsPerThread; ++it) {
-    const uint32_t g = threadIdx.x + kThreads * it;
-    const uint64_t j = q0 + g * 4u;
+  for (int k = 0; k < 5; ++k) {
+    // q0 and j are multiples of 4, so e mod 4 is the same for the whole block
+    const uint32_t a = (uint32_t)(((uint64_t)k * m) & 3u);
 #pragma unroll
-    for (int k = 0; k < 5; ++k) {
-      const uint64_t e = (uint64_t)k * m + j;
-      tb[it][k] = (g * 4u < tile_bytes && e < n) ? (uint32_t)trits[e >> 2] : 0u;
+    for (int it = 0; it < kGroupsPerThread; ++it) {
+      const uint32_t g = threadIdx.x + kThreads * it;
+      const uint64_t e = (uint64_t)k * m + q0 + g * 4u;
+      uint32_t v = 0u;
+      if (g * 4u < tile_bytes && e < n) {
+        v = trits[e >> 2];
+        if (a != 0u) {
+          if (((e >> 2) + 1u) * 4u < n) v |= (uint32_t)trits[(e >> 2) + 1u] << 8;
+          v = (v >> (2u * a)) & 0xffu;
+        }
+      }
+      tb[it][k] = v;
     }
   }
 }
@@ -1123,7 +1133,7 @@ hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
   if (trit) {
-    if (!(al && m % 4 == 0 && summ)) return hipErrorInvalidValue;
+    if (!summ) return hipErrorInvalidValue;
     tlc_quant_encode_kernel<kPathVec, true><<<ntiles, kThreads, 0, st>>>(
         r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
   } else if (al && m % 4 == 0)

@@ -501,8 +501,11 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   // quantizes every value and keeps 2-bit trits per value in summ; in place
   // it keeps a bound per float4 there, and the quantizer skips float4s of
   // the buffer whose bound is below U.
+  // (The bounds take the float4 slices of the partitions, so m % 4 == 0;
+  // the trits are kept per float4 of the buffer and serve any m.)
+  const bool in_place = (c->options & TLC_OPT_IN_PLACE_FEEDBACK) != 0u;
   uint16_t* summ = (ntiles >= kThreePassMinTiles && aligned16(tensor) && aligned16(residual) &&
-                    m % 4 == 0)
+                    (m % 4 == 0 || !in_place))
                        ? c->summ
                        : nullptr;
   uint32_t np = 0;

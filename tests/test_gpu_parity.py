@@ -346,7 +346,7 @@ def test_nonfinite_leaves_residual_and_bytes(ctx):
     for opts in (0, tlc.TLC_OPT_IN_PLACE_FEEDBACK):
         ctx.set_options(opts)
         try:
-            for n in (100_000, THREE_PASS_N[0]):
+            for n in (100_000, THREE_PASS_N[0], THREE_PASS_N[1]):
                 for pos, bad in [(0, np.nan), (n - 1, np.inf), (4321, -np.inf)]:
                     x = workloads.normal([70, pos], n)
                     x[pos] = bad
