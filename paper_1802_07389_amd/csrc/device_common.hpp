@@ -391,14 +391,23 @@ __device__ __forceinline__ void acc_trit_at(float* __restrict__ out, uint64_t e,
 // Mask of the non-121 bytes among the 16 quartic bytes q[lo .. lo + cnt)
 // (cnt <= 16; q + lo 16-byte aligned) that one thread holds: bit i for
 // byte lo + i.
+// Four bits: byte i of w differs from 121.  x = w ^ 0x79797979 has a zero
+// byte exactly where w holds 121; bit 7 of ((x & 0x7f..) + 0x7f..) | x is
+// set in every other byte (no carry leaves a byte); the multiply gathers
+// the four bit-7 flags, shifted to bits 0, 8, 16, 24, into bits 21..24
+// (the partial products occupy distinct bits, so nothing carries).
+__device__ __forceinline__ uint32_t nonzero_byte_mask4(uint32_t w) {
+  const uint32_t x = w ^ 0x79797979u;
+  const uint32_t y = (x | ((x & 0x7f7f7f7fu) + 0x7f7f7f7fu)) & 0x80808080u;
+  return ((y >> 7) * 0x00204081u) >> 21 & 0xfu;
+}
+
 __device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
                                                        uint32_t cnt) {
+  static_assert(kZeroGroup == 0x79u, "the mask compares against bytes of 121");
   const uint4 w = *reinterpret_cast<const uint4*>(q + lo);
-  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
-  uint32_t nz = 0u;
-#pragma unroll
-  for (int i = 0; i < 16; ++i)
-    nz |= (((wd[i / 4] >> (8 * (i % 4))) & 0xffu) != kZeroGroup ? 1u : 0u) << i;
+  const uint32_t nz = nonzero_byte_mask4(w.x) | (nonzero_byte_mask4(w.y) << 4) |
+                      (nonzero_byte_mask4(w.z) << 8) | (nonzero_byte_mask4(w.w) << 12);
   return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
 }
 

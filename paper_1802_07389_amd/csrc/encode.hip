@@ -675,17 +675,25 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
                                            uint32_t (&tb)[kGroupsPerThread][5]) {
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
-    // q0 and j are multiples of 4, so e mod 4 is the same for the whole block
-    const uint32_t a = (uint32_t)(((uint64_t)k * m) & 3u);
+    // group g's first value is e = base + 4g; q0 is a multiple of 4, so
+    // e mod 4 = base mod 4 = a for the whole block, e / 4 = base / 4 + g,
+    // and the values before n are those with 4g < n - base
+    const uint64_t base = (uint64_t)k * m + q0;
+    const uint32_t a = (uint32_t)(base & 3u);
+    const uint8_t* tp = trits + (base >> 2);
+    const uint64_t left = n > base ? n - base : 0u;  // values of the partition from base on
+    const uint32_t lim = (uint32_t)min<uint64_t>(left, tile_bytes);
+    const uint32_t cap = (uint32_t)min<uint64_t>(left + a, 2u * kEncTile);
 #pragma unroll
     for (int it = 0; it < kGroupsPerThread; ++it) {
       const uint32_t g = threadIdx.x + kThreads * it;
-      const uint64_t e = (uint64_t)k * m + q0 + g * 4u;
       uint32_t v = 0u;
-      if (g * 4u < tile_bytes && e < n) {
-        v = trits[e >> 2];
+      if (g * 4u < lim) {
+        v = tp[g];
         if (a != 0u) {
-          if (((e >> 2) + 1u) * 4u < n) v |= (uint32_t)trits[(e >> 2) + 1u] << 8;
+          // trit byte e/4 + 1 holds values from e + 4 - a on: it exists when
+          // 4g + 4 - a < left (4g + 4 <= tile_bytes + 3 < 2 * kEncTile)
+          if (g * 4u + 4u < cap) v |= (uint32_t)tp[g + 1u] << 8;
           v = (v >> (2u * a)) & 0xffu;
         }
       }
