@@ -566,6 +566,9 @@ def main():
         "decode_kernels_hbm_frac": round(dec_bytes / (dec_kernel_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "encode_kernel_ms": round(enc_kernel_ms, 5),
         "decode_kernel_ms": round(dec_kernel_ms, 5),
+        # a decoder that stores every sum moves c + 8n bytes; this is its time at
+        # the 8 TB/s peak, for comparison with the store-what-changes decoder above
+        "decode_dense_form_ms_at_peak": round((c_avg + 8 * n) / (PEAK_HBM_GBPS * 1e9) * 1e3, 5),
         "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
         "kernels_avg_ms_note": "every kernel timed over %d further steps after the timed "
                                "region; the roofline kernel is timed inside it" % kern_steps,
