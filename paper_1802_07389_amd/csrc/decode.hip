@@ -41,19 +41,31 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
   const uint64_t j0 = (uint64_t)lt * kZreTile + threadIdx.x * kBytes;
   const uint32_t cnt = j0 < c ? (uint32_t)min<uint64_t>(kBytes, c - j0) : 0u;
 
-  uint8_t b[kBytes];
+  // the thread's bytes stay packed four to a word; byte i is bits 8*(i%4) of w[i/4]
+  uint32_t w[kBytes / 4];
   if (cnt == (uint32_t)kBytes && ((reinterpret_cast<uintptr_t>(C + j0) & 15u) == 0u)) {
 #pragma unroll
-    for (int h = 0; h < kBytes / 16; ++h)
-      unpack16(*reinterpret_cast<const uint4*>(C + j0 + 16 * h), b + 16 * h);
+    for (int h = 0; h < kBytes / 16; ++h) {
+      const uint4 v = *reinterpret_cast<const uint4*>(C + j0 + 16 * h);
+      w[4 * h] = v.x;
+      w[4 * h + 1] = v.y;
+      w[4 * h + 2] = v.z;
+      w[4 * h + 3] = v.w;
+    }
   } else {
 #pragma unroll
-    for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[j0 + i] : (uint8_t)0;
+    for (int q = 0; q < kBytes / 4; ++q) {
+      uint32_t x = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if ((uint32_t)(4 * q + i) < cnt) x |= (uint32_t)C[j0 + 4 * q + i] << (8 * i);
+      w[q] = x;
+    }
   }
   uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt) sum += expanded_len(b[i]);
+    if ((uint32_t)i < cnt) sum += expanded_len((w[i >> 2] >> (8 * (i & 3))) & 255u);
   const ScanU32 sc = block_scan_u32(sum, sh.red);
   const uint32_t agg = sc.total;
 
@@ -81,16 +93,30 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
   __syncthreads();
   if (sh.fault) return;
 
-  uint64_t o = sh.excl + sc.excl;  // where this thread's first byte expands
+  // The thread's bytes expand to at most 14 * kBytes < kDecRange quartic
+  // bytes, so at most one range start falls among them: the first one at or
+  // after the thread's first position o.
+  static_assert(14 * kBytes < kDecRange, "one range start per thread at most");
+  const uint64_t o = sh.excl + sc.excl;
+  const uint64_t k = (o + kDecRange - 1) / kDecRange;
+  const uint64_t at = k * kDecRange;
+  if (at < m && at < o + sum) {
+    const uint32_t d = (uint32_t)(at - o);  // the start's distance into the thread's expansion
+    uint32_t rel = 0, hit = 0, into = 0;
+    bool found = false;
 #pragma unroll
-  for (int i = 0; i < kBytes; ++i) {
-    if ((uint32_t)i < cnt) {
-      const uint32_t len = expanded_len(b[i]);
-      const uint64_t k = (o + kDecRange - 1) / kDecRange;  // first range start >= o
-      const uint64_t at = k * kDecRange;
-      if (at < o + len && at < m) start[k] = ((j0 + i) << 8) | (at - o);
-      o += len;
+    for (int i = 0; i < kBytes; ++i) {
+      if ((uint32_t)i < cnt) {
+        const uint32_t len = expanded_len((w[i >> 2] >> (8 * (i & 3))) & 255u);
+        if (!found && d < rel + len) {
+          hit = (uint32_t)i;
+          into = d - rel;
+          found = true;
+        }
+        rel += len;
+      }
     }
+    start[k] = ((j0 + hit) << 8) | into;
   }
 }
 

@@ -9,8 +9,8 @@
 namespace tlc {
 
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
-constexpr int kZreBytesPerThread = 32;    // zero-run scans: two uint4 per thread
-constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 8192 bytes per tile
+constexpr int kZreBytesPerThread = 64;    // zero-run index scan: four uint4 per thread
+constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 16384 stream bytes per tile
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
 constexpr uint32_t kAbsmaxMaxBlocks = 256;  // partial maxima per encode (one block per CU)

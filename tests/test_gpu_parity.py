@@ -116,6 +116,27 @@ def test_all_zero_tensors(ctx, n):
         assert 4 * n / C.size == 280
 
 
+@pytest.mark.parametrize("m", [16383, 16384, 16385, 2 * 16384 - 1, 2 * 16384 + 1, 3 * 16384 + 5])
+def test_index_scan_tile_edges(ctx, m):
+    """Streams ending at and around the 16384-byte tiles of the zero-run
+    index scan.  All-ones tensors quantize to q = 1 everywhere (M = 1 at
+    s = 1), so every quartic byte is 242 and the stream is exactly m bytes,
+    with range starts on tile edges; then zero groups turn random spans of
+    bytes into 121, whose run codes land across the edges."""
+    n = 5 * m
+    x = np.ones(n, F32)
+    res = check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"ones m={m}")
+    assert res[0].size == m
+    rng = np.random.default_rng([31, m])
+    for trial in range(3):
+        x = np.ones(n, F32)
+        for j0 in rng.integers(0, m, size=60):
+            span = np.arange(j0, min(m, j0 + int(rng.integers(1, 60))))
+            for k in range(5):
+                x[k * m + span] = F32(0.0)
+        check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"ones+runs m={m} {trial}")
+
+
 def test_long_runs_with_sparse_spikes(ctx):
     """Runs of every length mod 14 ending exactly at and across tile edges."""
     rng = np.random.default_rng(30)
