@@ -23,7 +23,7 @@ struct IdxShared {
   uint64_t excl;
 };
 
-// Tile `lt` (kZreTile stream bytes) of one stream: expansion lengths are
+// Tile `lt` (kThreads * kBytes stream bytes) of one stream: expansion lengths are
 // scanned in the block and across tiles (decoupled look-back, status slot
 // floor + lt), which places every stream byte's expansion in the quartic
 // byte string.  The byte whose expansion contains position k * kDecRange
@@ -31,14 +31,15 @@ struct IdxShared {
 // start[k], so each expanding block finds its part of the stream with one
 // load.  The stream's last tile flags the launch's epoch as corrupt when
 // the expansion total is not exactly m.
+template <int kBytes>
 __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32_t c, uint32_t m,
                                            uint64_t* __restrict__ start,
                                            uint64_t* __restrict__ status, uint32_t floor,
                                            uint32_t lt, uint32_t epoch, Ctrl* __restrict__ ctrl,
                                            IdxShared& sh) {
-  constexpr int kBytes = kZreBytesPerThread;
+  constexpr uint32_t kTile = kThreads * kBytes;
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  const uint64_t j0 = (uint64_t)lt * kZreTile + threadIdx.x * kBytes;
+  const uint64_t j0 = (uint64_t)lt * kTile + threadIdx.x * kBytes;
   const uint32_t cnt = j0 < c ? (uint32_t)min<uint64_t>(kBytes, c - j0) : 0u;
 
   // the thread's bytes stay packed four to a word; byte i is bits 8*(i%4) of w[i/4]
@@ -82,7 +83,7 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
       sh.fault = fault ? 1u : 0u;
       if (fault)
         __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const bool last_tile = (uint64_t)(lt + 1) * kZreTile >= c;
+      const bool last_tile = (uint64_t)(lt + 1) * kTile >= c;
       if (last_tile && (fault || ex + agg != m)) {
         __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_kernel(
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
   __syncthreads();
-  index_tile(C, c, m, start, status, 0, s_tile, epoch, ctrl, sh);
+  index_tile<kZreBytesPerThread>(C, c, m, start, status, 0, s_tile, epoch, ctrl, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
@@ -142,7 +143,8 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
   const uint32_t T = s_tile;
   const uint32_t t = find_desc(descs, count, T, [](const DecDesc& d) { return d.tile0; });
   const DecDesc d = descs[t];
-  index_tile(d.C, d.c, d.m, start + d.range0, status, d.tile0, T - d.tile0, epoch, ctrl, sh);
+  index_tile<kZreBatchBytesPerThread>(d.C, d.c, d.m, start + d.range0, status, d.tile0,
+                                      T - d.tile0, epoch, ctrl, sh);
 }
 
 // ---------------------------------------------------------------- expansion

@@ -242,9 +242,12 @@ int upload(tlc_ctx* c, void* dst, const void* src, size_t bytes) {
   return TLC_OK;
 }
 
-int sync_and_read(tlc_ctx* c) {
-  hipError_t e = hipMemcpyAsync(c->rb, c->ctrl, sizeof(HostReadback),
-                                hipMemcpyDeviceToHost, c->stream);
+// Copies the control block's readback fields (and with `results` > 0 the
+// first `results` batch results after it) to the pinned block, then waits.
+int sync_and_read(tlc_ctx* c, size_t results = 0) {
+  const size_t bytes =
+      results ? sizeof(Ctrl) + results * sizeof(EncResult) : sizeof(HostReadback);
+  hipError_t e = hipMemcpyAsync(c->rb, c->ctrl, bytes, hipMemcpyDeviceToHost, c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(readback)");
   e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
@@ -316,13 +319,16 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->partials_cap =
       std::max<size_t>(kAbsmaxMaxBlocks, max_n / ((size_t)kThreads * 4) + max_tensors + 1);
   c->enc_status_words = mm / kEncTile + max_tensors + 2;
-  c->dec_status_words = mm / kZreTile + max_tensors + 2;
+  c->dec_status_words = mm / kZreBatchTile + max_tensors + 2;  // the smaller tile
   c->start_words = mm / kDecRange + max_tensors + 2;
   const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
-  // layout: ctrl | partials | check partials | enc status | dec status | start | enc descs |
-  //         dec descs | enc results | tile records | chunk summaries |
+  // layout: ctrl | enc results | partials | check partials | enc status | dec status |
+  //         start | enc descs | dec descs | tile records | chunk summaries |
   //         tile prefixes in their chunks | fix lists | float4 summaries | slots
-  size_t off = sizeof(Ctrl);
+  // (the batch results follow the control block, so that one copy reads both)
+  static_assert(sizeof(Ctrl) % alignof(EncResult) == 0, "results follow the control block");
+  const size_t off_res = sizeof(Ctrl);
+  size_t off = round_up(off_res + max_tensors * sizeof(EncResult), 256);
   const size_t off_partials = off;
   off = round_up(off + c->partials_cap * sizeof(uint32_t), 256);
   const size_t off_partials_chk = off;
@@ -337,8 +343,6 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   off = round_up(off + max_tensors * sizeof(EncDesc), 256);
   const size_t off_ddesc = off;
   off = round_up(off + max_tensors * sizeof(DecDesc), 256);
-  const size_t off_res = off;
-  off = round_up(off + max_tensors * sizeof(EncResult), 256);
   const size_t off_recs = off;
   off = round_up(off + tiles1 * sizeof(TileRec), 256);
   const size_t off_chunks = off;
@@ -374,11 +378,14 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   c->slots = base + off_slots;
   e = hipMemset(c->ws, 0, total);
   if (e == hipSuccess) e = hipDeviceSynchronize();
+  // pinned readback block, laid out as the workspace's head: the control
+  // block's slot, then the batch results
   if (e == hipSuccess)
-    e = hipHostMalloc((void**)&c->rb, sizeof(HostReadback), hipHostMallocDefault);
-  if (e == hipSuccess)
-    e = hipHostMalloc((void**)&c->host_results, max_tensors * sizeof(EncResult),
+    e = hipHostMalloc((void**)&c->rb, sizeof(Ctrl) + max_tensors * sizeof(EncResult),
                       hipHostMallocDefault);
+  if (e == hipSuccess)
+    c->host_results =
+        reinterpret_cast<EncResult*>(reinterpret_cast<uint8_t*>(c->rb) + sizeof(Ctrl));
   if (e == hipSuccess)
     e = hipHostMalloc((void**)&c->staging, kStagingSlots * max_tensors * 64,
                       hipHostMallocDefault);
@@ -388,7 +395,6 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
     for (int i = 0; i < kStagingSlots; ++i)
       if (c->staging_done[i]) (void)hipEventDestroy(c->staging_done[i]);
     if (c->staging) (void)hipHostFree(c->staging);
-    if (c->host_results) (void)hipHostFree(c->host_results);
     if (c->rb) (void)hipHostFree(c->rb);
     (void)hipFree(c->ws);
     delete c;
@@ -420,8 +426,7 @@ TLC_API int tlc_ctx_destroy(tlc_ctx* c) {
   for (int i = 0; i < kStagingSlots; ++i)
     if (c->staging_done[i]) (void)hipEventDestroy(c->staging_done[i]);
   if (c->staging) (void)hipHostFree(c->staging);
-  if (c->host_results) (void)hipHostFree(c->host_results);
-  if (c->rb) (void)hipHostFree(c->rb);
+  if (c->rb) (void)hipHostFree(c->rb);  // holds host_results too
   if (c->ws) (void)hipFree(c->ws);
   delete c;
   return TLC_OK;
@@ -736,10 +741,7 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   });
   if (st) return st;
   c->enc_ticket_base += tiles;
-  hipError_t e = hipMemcpyAsync(c->host_results, c->enc_results, cnt * sizeof(EncResult),
-                                hipMemcpyDeviceToHost, c->stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(results)");
-  st = sync_and_read(c);
+  st = sync_and_read(c, cnt);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -882,7 +884,7 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
     e.tile0 = tiles;
     e.range0 = ranges;
     e.vec = aligned16(outs[t]) ? (e.m % 4 == 0 ? 1u : 2u) : 0u;
-    tiles += (uint32_t)ceil_div(e.c, kZreTile);
+    tiles += (uint32_t)ceil_div(e.c, kZreBatchTile);
     ranges += (uint32_t)ceil_div(e.m, kDecRange);
     d.push_back(e);
   }
@@ -948,7 +950,7 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
     e.scale = scales[t];
     e.tile0 = tiles;
     e.range0 = (uint32_t)t * nranges;
-    tiles += (uint32_t)ceil_div(e.c, kZreTile);
+    tiles += (uint32_t)ceil_div(e.c, kZreBatchTile);
     d.push_back(e);
   }
   if (d.empty()) return TLC_OK;

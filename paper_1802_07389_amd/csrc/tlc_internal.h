@@ -11,6 +11,10 @@ namespace tlc {
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
 constexpr int kZreBytesPerThread = 64;    // zero-run index scan: four uint4 per thread
 constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 16384 stream bytes per tile
+// the batched scans, over many streams that mostly fit one tile, take half
+// as many bytes per thread (shorter per-thread loops on short streams)
+constexpr int kZreBatchBytesPerThread = 32;
+constexpr int kZreBatchTile = kThreads * kZreBatchBytesPerThread;  // 8192
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
 constexpr int kDecRange = 4096;           // quartic bytes per expand/dequantize block
 constexpr uint32_t kAbsmaxMaxBlocks = 256;  // partial maxima per encode (one block per CU)
