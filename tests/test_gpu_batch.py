@@ -93,6 +93,38 @@ def test_batch_nonfinite_tensor_is_refused_alone(bctx):
                          [res[i] for i in keep], "nonfinite-others")
 
 
+def test_batch_fills_the_context(bctx):
+    """A batch of exactly max_tensors tensors: the per-tensor results come
+    back with the control block in one copy, up to the last slot of the
+    context's readback block; then a smaller batch on the same context,
+    whose results must not be stale ones from the first."""
+    from paper_1802_07389_amd import tlc
+    T = 40
+    ctx = tlc.Context(max_n=T * 30000, max_tensors=T)
+    try:
+        sizes = [int(v) for v in np.random.default_rng(720).integers(1, 30000, size=T)]
+        sizes[5] = 0
+        xs = [workloads.normal([721, t], n, 1.0) for t, n in enumerate(sizes)]
+        rs = [workloads.normal([722, t], n, 1e-3) for t, n in enumerate(sizes)]
+        xs[T - 1][0] = np.inf  # the last slot reports its own error
+        ss = [[1.0, 1.25, 1.5, 1.99][t % 4] for t in range(T)]
+        st, stat, res = batch_encode(ctx, xs, rs, ss)
+        assert st == tlc.TLC_E_NONFINITE
+        assert stat == [0] * (T - 1) + [tlc.TLC_E_NONFINITE]
+        assert res[T - 1][0].size == 0
+        keep = [t for t in range(T - 1) if sizes[t]]
+        check_against_oracle([xs[i] for i in keep], [rs[i] for i in keep], [ss[i] for i in keep],
+                             [res[i] for i in keep], "full")
+        k = 7
+        xs2 = [workloads.normal([723, t], n, 1.0) for t, n in enumerate(sizes[:k])]
+        rs2 = [np.zeros(n, F32) for n in sizes[:k]]
+        st, stat, res = batch_encode(ctx, xs2, rs2, ss[:k])
+        assert st == 0 and stat == [0] * k
+        check_against_oracle(xs2, rs2, ss[:k], res, "smaller after full")
+    finally:
+        ctx.close()
+
+
 def test_batch_argument_errors(bctx):
     import torch
     from paper_1802_07389_amd import tlc
