@@ -10,7 +10,7 @@ them, cycled), resident in HBM before timing starts.
 
 Prints ONE JSON line.  ``value`` is GB/s of fp32 input per step (4n bytes
 per round trip).  ``roofline`` is for the dominant kernel
-(tlc_accum_absmax_kernel), timed with HIP events on the library's stream.
+(tlc_accum_quantize_kernel), timed with HIP events on the library's stream.
 """
 import argparse
 import hashlib
@@ -30,7 +30,7 @@ METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compress
 KERNEL_SRC = [os.path.join(ROOT, "paper_1802_07389_amd", "csrc", f)
               for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp",
                         "tlc_internal.h")]
-DOMINANT = "tlc_accum_absmax_kernel"  # the longest kernel of a step
+DOMINANT = "tlc_accum_quantize_kernel"  # the longest kernel of a step
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", DOMINANT + "_c4_traffic.md")
 
 # Algorithmic HBM bytes of each kernel per launch (c = compressed bytes, nnz =
@@ -43,7 +43,7 @@ def algorithmic_bytes(n, c, nnz):
         "tlc_absmax_check_kernel": 8 * n,
         # read x, r; write the residual r = acc - M*q and one byte of 2-bit
         # trits (q + 1) per float4 for the quartic pack
-        "tlc_accum_absmax_kernel": 12 * n + n // 4,
+        "tlc_accum_quantize_kernel": 12 * n + n // 4,
         # read the trits; write each tile's own stream bytes (c in all) and
         # its 16-byte record
         "tlc_quant_encode_kernel": n // 4 + c + 16 * tiles,
@@ -171,11 +171,12 @@ def _row(name, values, s, te, td, nbytes, ote=None, otd=None, ovalues=None, **ex
     return row
 
 
-def report(torch, tlc, workloads, dev):
-    """One JSON line per config (C1-C5): GPU and oracle GB/s of fp32 input
-    and the compression ratio 4n / (payload + 4-byte scale).  GPU encode
-    times include the host synchronisation of tlc_compress (it returns the
-    stream length)."""
+def config_rows(torch, tlc, workloads, dev, with_c4=True):
+    """One row per config (C1-C5, and the comparison encodings of Section
+    5.1 on the C4 step-0 tensor): GPU and oracle GB/s of fp32 input and the
+    compression ratio 4n / (payload + 4-byte scale).  GPU encode times
+    include the host synchronisation of tlc_compress (it returns the stream
+    length).  The oracle runs on one pinned host core."""
     try:
         os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
     except (AttributeError, OSError):
@@ -200,31 +201,35 @@ def report(torch, tlc, workloads, dev):
         rows.append(_row(f"C3 s={s3}", v, s3, te, td, nb, ote, otd, x3.size))
 
     # C4: 5 steps of 2^28 values, residual carried, decode-accumulate
-    x4 = [workloads.c4_tensor(k) for k in range(workloads.C4_STEPS)]
-    _gpu_round_trips(torch, ctx, x4[:1], workloads.C4_S, dev)
-    te, td, nb, v = _gpu_round_trips(torch, ctx, x4, workloads.C4_S, dev)
-    ote, otd = _oracle_round_trips(x4, workloads.C4_S)
-    rows.append(_row("C4 (5 steps)", v, workloads.C4_S, te, td, nb, ote, otd, v))
-    del x4
+    if with_c4:
+        x4 = [workloads.c4_tensor(k) for k in range(workloads.C4_STEPS)]
+        _gpu_round_trips(torch, ctx, x4[:1], workloads.C4_S, dev)
+        te, td, nb, v = _gpu_round_trips(torch, ctx, x4, workloads.C4_S, dev)
+        ote, otd = _oracle_round_trips(x4, workloads.C4_S)
+        rows.append(_row("C4 (5 steps)", v, workloads.C4_S, te, td, nb, ote, otd, v))
+        del x4
 
     # The comparison encodings of Section 5.1 on the C4 step-0 tensor: one
     # encode + decode-accumulate per rep, kernel averages from the library's
-    # timers, and the oracle on the same tensor
+    # timers, and the oracle on the same tensor.  The two designs of Section
+    # 5.1 run at s = 1 (TernGrad-like stochastic quantization with the plain
+    # max as its scale; 8-bit codes spanning all 255 levels); "No ZRE" is 3LC
+    # itself without the zero-run stage, at C4's s.
     import oracle
     xh = workloads.c4_tensor(0)
     x = torch.from_numpy(xh).to(dev)
     r = torch.zeros_like(x)
     out = torch.zeros_like(x)
     buf = torch.empty(x.numel(), dtype=torch.uint8, device=dev)
-    modes = [("No ZRE", tlc.TLC_MODE_NO_ZRE, (tlc.TLC_KERNEL_QUANT_PACK,
-                                              tlc.TLC_KERNEL_EXPAND_DEQUANT)),
-             ("Stoch 3-value + QE", tlc.TLC_MODE_STOCHASTIC, (tlc.TLC_KERNEL_QUANT_PACK,
-                                                              tlc.TLC_KERNEL_EXPAND_DEQUANT)),
-             ("8-bit int", tlc.TLC_MODE_INT8, (tlc.TLC_KERNEL_INT8_QUANT,
-                                               tlc.TLC_KERNEL_INT8_DEQUANT))]
-    for name, mode, kids in modes:
+    modes = [("No ZRE", tlc.TLC_MODE_NO_ZRE, workloads.C4_S,
+              (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+             ("Stoch 3-value + QE", tlc.TLC_MODE_STOCHASTIC, 1.0,
+              (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+             ("8-bit int", tlc.TLC_MODE_INT8, 1.0,
+              (tlc.TLC_KERNEL_INT8_QUANT, tlc.TLC_KERNEL_INT8_DEQUANT))]
+    for name, mode, sm, kids in modes:
         rr = None if mode == tlc.TLC_MODE_STOCHASTIC else r
-        C, M = ctx.compress_mode(mode, x, rr, workloads.C4_S, seed=7, step=0, out=buf)
+        C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=0, out=buf)
         ctx.decompress_mode(mode, C, M, out, accumulate=True)
         ctx.sync()
         ctx.profile(True)
@@ -234,7 +239,7 @@ def report(torch, tlc, workloads, dev):
         for k in range(reps):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            C, M = ctx.compress_mode(mode, x, rr, workloads.C4_S, seed=7, step=k, out=buf)
+            C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=k, out=buf)
             t1 = time.perf_counter()
             ctx.decompress_mode(mode, C, M, out, accumulate=True)
             ctx.sync()
@@ -242,25 +247,26 @@ def report(torch, tlc, workloads, dev):
             te += t1 - t0
             td += t2 - t1
         kus = {}
-        for kid in (tlc.TLC_KERNEL_ABSMAX,) + kids:
+        for kid in (tlc.TLC_KERNEL_ABSMAX_CHECK, tlc.TLC_KERNEL_ABSMAX) + kids:
             ms, cnt = ctx.profile_get(kid)
-            kus[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
+            if cnt:
+                kus[tlc.tlc_kernel_name(kid)] = round(ms / cnt * 1e3, 1)
         ctx.profile(False)
         rh = np.zeros(xh.size, np.float32)
         t0 = time.perf_counter()
         if mode == tlc.TLC_MODE_NO_ZRE:
-            st, Ch, Mh = oracle.compress_nozre(xh, rh, workloads.C4_S)
+            st, Ch, Mh = oracle.compress_nozre(xh, rh, sm)
         elif mode == tlc.TLC_MODE_STOCHASTIC:
-            st, Ch, Mh = oracle.compress_stochastic(xh, workloads.C4_S, 7, 0)
+            st, Ch, Mh = oracle.compress_stochastic(xh, sm, 7, 0)
         else:
-            st, Ch, Mh = oracle.compress_int8(xh, rh, workloads.C4_S)
+            st, Ch, Mh = oracle.compress_int8(xh, rh, sm)
         t1 = time.perf_counter()
         if mode == tlc.TLC_MODE_INT8:
             oracle.decompress_int8(Ch, Mh, xh.size, rh, accumulate=True)
         else:
             oracle.decompress(Ch, Mh, xh.size, rh, accumulate=True)
         t2 = time.perf_counter()
-        rows.append(_row(f"C4 step 0, {name}", reps * x.numel(), workloads.C4_S, te, td,
+        rows.append(_row(f"C4 step 0, {name}", reps * x.numel(), sm, te, td,
                          reps * (C.numel() + 4), t1 - t0, t2 - t1, x.numel(),
                          kernel_us=kus))
     del x, r, out, buf, xh, rh
@@ -392,7 +398,12 @@ def report(torch, tlc, workloads, dev):
                  "oracle_aggregate_GBps": round(4 * n5 * len(s5) / 1e9 / (tb - ta), 4),
                  "oracle_reencode_GBps": round(4 * n5 / 1e9 / (tc - tb), 4),
                  "oracle_cores": 1})
-    for row in rows:
+    return rows
+
+
+def report(torch, tlc, workloads, dev):
+    """One JSON line per config (C1-C5 and the comparison encodings)."""
+    for row in config_rows(torch, tlc, workloads, dev, with_c4=True):
         print(json.dumps(row), flush=True)
 
 
@@ -407,6 +418,8 @@ def main():
                     help="only run 1 GiB device copies (counter calibration)")
     ap.add_argument("--report", action="store_true",
                     help="per-config report (C1-C5) instead of the headline line")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="leave the C1, C2, C3, C5 and comparison rows out of the line")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -482,24 +495,34 @@ def main():
     dom_ms_timed /= max(dom_cnt, 1)
     timed_lens = list(lens)
 
-    # A second, untimed pass over the same steps times every kernel.
-    kern_steps = min(args.steps, 5)
-    ctx.profile(True)
-    ctx.profile_reset()
-    for k in range(kern_steps):
-        step(args.warmup + args.steps + k)
-    ctx.sync()
-    ctx.profile(False)
+    # Further untimed steps time every kernel of a step, one kernel at a
+    # time: a single event pair per step, as for the roofline kernel (an
+    # event pair on every kernel would cost tens of microseconds per step).
+    # The ZRE_CHUNKS id brackets two launches (the chunk scan and the scan of
+    # the chunk summaries).
+    kern_steps = 3
+    names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
+    enc_k = ["tlc_absmax_check_kernel", "tlc_accum_quantize_kernel", "tlc_quant_encode_kernel",
+             "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
+    dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     kern = {}
-    for kid in range(tlc.TLC_KERNEL_COUNT):
+    base = args.warmup + args.steps
+    for name in enc_k + dec_k:
+        kid = names.index(name)
+        ctx.profile(True, kernels=[kid])
+        ctx.profile_reset()
+        for k in range(kern_steps):
+            step(base + k)
+        ctx.sync()
+        ctx.profile(False)
         ms, cnt = ctx.profile_get(kid)
-        kern[tlc.tlc_kernel_name(kid)] = (ms / cnt if cnt else 0.0, cnt)
+        kern[name] = (ms / cnt if cnt else 0.0, cnt)
+        base += kern_steps
 
     # The same steps with TLC_OPT_IN_PLACE_FEEDBACK (no check pass before the
     # in-place max pass; only the residual after NaN/Inf differs), timed the
     # same way without any events.
     ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
-    base = args.warmup + args.steps + kern_steps
     for k in range(2):
         step(base + k)
     ctx.sync()
@@ -530,9 +553,6 @@ def main():
     achieved = algo[dom] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(n)
 
-    enc_k = ["tlc_absmax_check_kernel", "tlc_accum_absmax_kernel", "tlc_quant_encode_kernel",
-             "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
-    dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
     enc_kernel_ms = sum(kern[k][0] for k in enc_k)
     dec_kernel_ms = sum(kern[k][0] for k in dec_k)
     enc_bytes = sum(algo[k] for k in enc_k)
@@ -577,9 +597,15 @@ def main():
         # a decoder that stores every sum moves c + 8n bytes; this is its time at
         # the 8 TB/s peak, for comparison with the store-what-changes decoder above
         "decode_dense_form_ms_at_peak": round((c_avg + 8 * n) / (PEAK_HBM_GBPS * 1e9) * 1e3, 5),
+        # the same as a fraction of peak: (c + 8n) bytes over the decode kernels'
+        # time, the figure the >= 60 % decode + accumulate target is read on
+        # (decode_kernels_hbm_frac counts the bytes this decoder moves)
+        "decode_dense_equiv_hbm_frac": round((c_avg + 8 * n) / (dec_kernel_ms * 1e-3) / 1e9
+                                             / PEAK_HBM_GBPS, 4),
         "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
-        "kernels_avg_ms_note": "every kernel timed over %d further steps after the timed "
-                               "region; the roofline kernel is timed inside it" % kern_steps,
+        "kernels_avg_ms_note": "each kernel timed alone (one event pair per step) over %d "
+                               "further steps after the timed region; the roofline kernel "
+                               "is timed inside it" % kern_steps,
         "in_place_feedback": {
             "value": round(4 * n * args.steps / (t1_ip - t0_ip) / 1e9, 2),
             "ms_per_step": round((t1_ip - t0_ip) / args.steps * 1e3, 4),
@@ -592,11 +618,17 @@ def main():
         "compression_ratio_payload_only": round(4 * n / c_avg, 2),
         "kernel_source_sha256_16": kernel_source_hash(),
     }
+    ctx.close()
+    del xs, resid, model, payload
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        # the other configs (and the comparison encodings) in the same line
+        result["configs"] = {row.pop("config"): row
+                             for row in config_rows(torch, tlc, workloads, dev, with_c4=False)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(host_inputs[0], s)
     else:
         result["cpu_baseline"] = None
-    ctx.close()
     print(json.dumps(result), flush=True)
 
 

@@ -227,6 +227,23 @@ int tlc_ctx_set_options(tlc_ctx* ctx, uint32_t options);
  * status of asynchronous decodes: TLC_OK or TLC_E_CORRUPT. */
 int tlc_sync(tlc_ctx* ctx);
 
+/* Look-back epochs.  Every launch of a chained or batched encode and every
+ * decode tags the status words of its scan with the next value of a
+ * per-context counter (encode 1 .. TLC_ENC_EPOCH_MAX, decode 1 ..
+ * TLC_DEC_EPOCH_MAX), so the words need no clearing between launches;
+ * when a counter wraps, its status words are cleared first (and for the
+ * decode counter the mark that flags a corrupt stream's launch). */
+#define TLC_ENC_EPOCH_MAX 8388607  /* 2^23 - 1 */
+#define TLC_DEC_EPOCH_MAX 67108863 /* 2^26 - 1 */
+
+/* For tests of the wrap: wait for the context's work, clear the status
+ * words of both scans (no word of an earlier launch can then carry a
+ * future epoch) and set the counters to the last epochs used, enc_epoch
+ * <= TLC_ENC_EPOCH_MAX and dec_epoch <= TLC_DEC_EPOCH_MAX (else
+ * TLC_E_INVALID).  The corrupt-stream mark is left as it is: only the wrap
+ * clears it. */
+int tlc_ctx_set_epochs(tlc_ctx* ctx, uint32_t enc_epoch, uint32_t dec_epoch);
+
 /* Text of the calling thread's most recent error (never NULL). */
 const char* tlc_last_error_string(void);
 
@@ -250,7 +267,9 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_QUANT_ENCODE_CHAINED 14 /* a small tensor's encode in one chained pass */
 #define TLC_KERNEL_ABSMAX_CHECK 15  /* partial max of |tensor + residual|, nothing written */
 #define TLC_KERNEL_ABSMAX_CHECK_BATCH 16
-#define TLC_KERNEL_COUNT 17
+#define TLC_KERNEL_ACCUM_QUANTIZE 17 /* after the check pass: step 1, Eq. 2 and the residual
+                                        for every value, 2-bit trits (large tensors) */
+#define TLC_KERNEL_COUNT 18
 
 /* Enable (on != 0) or disable recording of a start/stop event pair around
  * every kernel launch of the context (of the kernels selected by

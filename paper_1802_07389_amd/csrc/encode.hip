@@ -7,6 +7,10 @@
 //       step 1 of error accumulation (the tensor is added into the buffer,
 //       in place) and partial maxima of the sums               (Section 3.1,
 //                                                               Fig. 3, Eq. 1)
+//   tlc_accum_quantize_kernel
+//       after the check pass, on large aligned tensors: acc = x + r,
+//       3-value quantization, the residual stored in place and 2-bit
+//       trits for the quartic pack                  (Section 3.1, Eq. 1-2)
 //   tlc_quant_encode_kernel, tlc_zre_chunk(_scan)_kernel, tlc_zre_compact_kernel
 //       one tensor: M, 3-value quantization of the buffer, residual
 //       write-back where q != 0, quartic pack and each tile's own zero-run
@@ -181,31 +185,36 @@ __device__ __forceinline__ bool refused_by_guard(const uint32_t* __restrict__ gu
   return true;
 }
 
-// kTrit (float4 path, after the check pass): the check pass's maxima give
-// M, the buffer receives the final residuals and `summ` the trits
-// (accum_quantize_part); the block's partial is the check pass's own.
-template <bool kVec, bool kResid, bool kSum, bool kTrit = false>
+template <bool kVec, bool kResid, bool kSum>
 __global__ __launch_bounds__(kThreads) void tlc_accum_absmax_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n,
     uint32_t* __restrict__ partials, uint16_t* __restrict__ summ,
     const uint32_t* __restrict__ guard, uint32_t guard_np, float s) {
   __shared__ uint32_t lds[kWaves];
-  if (kTrit) {
-    static_assert(!kTrit || (kVec && kResid && !kSum), "trits come from the float4 buffer path");
-    const Scale g = finish_scale(guard, guard_np, s, lds);
-    if (g.bad) {  // NaN/Inf or overflow: nothing written, later kernels refuse too
-      if (threadIdx.x == 0) partials[blockIdx.x] = 0xffffffffu;
-      return;
-    }
-    accum_quantize_part(x, r, n, blockIdx.x, gridDim.x, g.M, g.U,
-                        reinterpret_cast<uint8_t*>(summ));
-    if (threadIdx.x == 0) partials[blockIdx.x] = guard[blockIdx.x];
-    return;
-  }
   if (refused_by_guard(guard, guard_np, s, lds, &partials[blockIdx.x])) return;
   const uint32_t mx =
       block_max(absmax_part<kVec, kResid, kSum>(x, r, n, blockIdx.x, gridDim.x, summ), lds);
   if (threadIdx.x == 0) partials[blockIdx.x] = mx;
+}
+
+// The writing pass of the default error policy on the float4 path of large
+// tensors (steps 1, a and b of Section 3.1 with Eq. 2): the check pass's
+// partial maxima give M (Eq. 1), then every value's acc = x + r is
+// quantized, its residual stored in place and q + 1 kept as a 2-bit trit
+// (accum_quantize_part).  A scale that is NaN/Inf or overflows leaves the
+// buffer untouched.  The block's partial is the check pass's own.
+__global__ __launch_bounds__(kThreads) void tlc_accum_quantize_kernel(
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n,
+    uint32_t* __restrict__ partials, uint8_t* __restrict__ trits,
+    const uint32_t* __restrict__ guard, uint32_t guard_np, float s) {
+  __shared__ uint32_t lds[kWaves];
+  const Scale g = finish_scale(guard, guard_np, s, lds);
+  if (g.bad) {  // NaN/Inf or overflow: nothing written, later kernels refuse too
+    if (threadIdx.x == 0) partials[blockIdx.x] = 0xffffffffu;
+    return;
+  }
+  accum_quantize_part(x, r, n, blockIdx.x, gridDim.x, g.M, g.U, trits);
+  if (threadIdx.x == 0) partials[blockIdx.x] = guard[blockIdx.x];
 }
 
 // One block of the batch's max passes.  kStore false: the check pass.
@@ -1116,8 +1125,8 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* p
   if (guard && guard_np != blocks) return hipErrorInvalidValue;  // same launch as the check
   *nblocks = blocks;
   if (trit) {
-    tlc_accum_absmax_kernel<true, true, false, true><<<blocks, kThreads, 0, st>>>(
-        x, r, n, partials, summ, guard, guard_np, s);
+    tlc_accum_quantize_kernel<<<blocks, kThreads, 0, st>>>(
+        x, r, n, partials, reinterpret_cast<uint8_t*>(summ), guard, guard_np, s);
     return hipGetLastError();
   }
 #define TLC_LAUNCH(V, R, S)                                                                 \

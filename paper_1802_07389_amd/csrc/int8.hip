@@ -47,11 +47,14 @@ __device__ __forceinline__ float int8_acc(float out, uint32_t byte, float D) {
   return __fadd_rn(out, int8_value(byte, D));
 }
 
-// One value: code byte and (kResid) residual acc - fl(code * D).
+// One value: code byte and (kResid) residual acc - fl(code * D).  The
+// product is taken from the integer code: rint leaves -0.0 for acc = -0.0,
+// whose product -0 would turn the residual -0.0 - (-0) into +0.0, while
+// the integer 0 gives +0 and keeps acc = -0.0 as its residual.
 template <bool kResid>
 __device__ __forceinline__ uint32_t int8_one(float acc, float D, float& res) {
   const float code = int8_code(acc, D);
-  if (kResid) res = __fsub_rn(acc, __fmul_rn(code, D));
+  if (kResid) res = __fsub_rn(acc, __fmul_rn((float)(int32_t)code, D));
   return int8_byte(code);
 }
 

@@ -18,16 +18,18 @@
 using namespace tlc;
 
 namespace {
-
 thread_local char g_err[512] = "no error";
+}  // namespace
 
-int fail(int code, const char* fmt, ...) {
+int tlc::fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
   vsnprintf(g_err, sizeof(g_err), fmt, ap);
   va_end(ap);
   return code;
 }
+
+namespace {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(TLC_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
@@ -55,7 +57,35 @@ const char* const kKernelNames[TLC_KERNEL_COUNT] = {
     "tlc_int8_quant_kernel",         "tlc_int8_dequant_kernel",
     "tlc_zre_chunk_kernel",          "tlc_zre_compact_kernel",
     "tlc_quant_encode_chained_kernel", "tlc_absmax_check_kernel",
-    "tlc_absmax_check_batch_kernel"};
+    "tlc_absmax_check_batch_kernel", "tlc_accum_quantize_kernel"};
+
+// A device address range of one call's arguments; `written` ranges must
+// not overlap any other range of the call.
+struct Span {
+  uintptr_t lo, hi;
+  bool written;
+};
+
+// Sorts the spans by start address and reports whether a written span
+// overlaps another span (read-only spans may overlap each other: one stream
+// decoded into several outputs, one tensor read twice).  In start order a
+// span overlaps an earlier one exactly when it starts below that one's end,
+// so it suffices to keep the largest end of all earlier spans and of the
+// earlier written ones.  std::sort works in place: nothing is allocated.
+bool spans_conflict(std::vector<Span>& v) {
+  std::sort(v.begin(), v.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+  uintptr_t end_all = 0, end_written = 0;
+  for (const Span& sp : v) {
+    if (sp.lo < (sp.written ? end_all : end_written)) return true;
+    end_all = std::max(end_all, sp.hi);
+    if (sp.written) end_written = std::max(end_written, sp.hi);
+  }
+  return false;
+}
+
+void add_span(std::vector<Span>& v, const void* p, size_t bytes, bool written) {
+  if (bytes) v.push_back(Span{(uintptr_t)p, (uintptr_t)p + bytes, written});
+}
 
 struct PendingTiming {
   int kernel;
@@ -113,6 +143,7 @@ struct tlc_ctx {
   std::vector<EncDesc> enc_host;
   std::vector<DecDesc> dec_host;
   std::vector<size_t> which;
+  std::vector<Span> spans;  // address ranges of a batched call (3 per tensor)
   std::vector<hipEvent_t> free_events;
   std::vector<PendingTiming> pending;
   double total_ms[TLC_KERNEL_COUNT] = {};
@@ -405,6 +436,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
     c->enc_host.reserve(max_tensors);
     c->dec_host.reserve(max_tensors);
     c->which.reserve(max_tensors);
+    c->spans.reserve(3 * max_tensors);
   } catch (...) {
     tlc_ctx_destroy(c);
     return fail(TLC_E_DEVICE, "tlc_ctx_create: out of host memory");
@@ -457,7 +489,7 @@ int launch_max_passes(tlc_ctx* c, const float* x, float* r, size_t n, float s, u
   }
   const bool quantize = summ != nullptr && guard != nullptr;
   if (trit) *trit = quantize;
-  return timed_launch(c, TLC_KERNEL_ABSMAX, [&] {
+  return timed_launch(c, quantize ? TLC_KERNEL_ACCUM_QUANTIZE : TLC_KERNEL_ABSMAX, [&] {
     return launch_accum_absmax(x, r, n, c->partials, np, summ, guard, guard_np, s, quantize,
                                c->stream);
   });
@@ -684,6 +716,16 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   if (total_n > c->max_n)
     return fail(TLC_E_INVALID, "tlc_compress_batch: %zu values exceed the context's max_n %zu",
                 total_n, c->max_n);
+  c->spans.clear();
+  for (size_t t = 0; t < count; ++t) {
+    if (ns[t] == 0) continue;
+    add_span(c->spans, tensors[t], ns[t] * 4, false);
+    add_span(c->spans, residuals[t], ns[t] * 4, true);
+    add_span(c->spans, bytes[t], quartic_len(ns[t]), true);
+  }
+  if (spans_conflict(c->spans))
+    return fail(TLC_E_INVALID,
+                "tlc_compress_batch: a residual or byte buffer overlaps another tensor's buffer");
   std::vector<EncDesc>& d = c->enc_host;
   std::vector<size_t>& which = c->which;  // batch position of each launched tensor
   d.clear();
@@ -892,6 +934,14 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
     return fail(TLC_E_INVALID, "tlc_decompress_batch: %zu values exceed the context's max_n %zu",
                 total_n, c->max_n);
   if (d.empty()) return TLC_OK;
+  c->spans.clear();
+  for (const DecDesc& e : d) {
+    add_span(c->spans, e.C, e.c, false);
+    add_span(c->spans, e.out, e.n * 4, true);
+  }
+  if (spans_conflict(c->spans))
+    return fail(TLC_E_INVALID, "tlc_decompress_batch: an output overlaps another stream's "
+                               "output or bytes");
   if (tiles > c->dec_status_words || ranges > c->start_words)
     return fail(TLC_E_INVALID, "tlc_decompress_batch: batch exceeds the context's workspace");
   DeviceScope dev(c->device);
@@ -996,6 +1046,26 @@ TLC_API int tlc_sync(tlc_ctx* c) {
     if (e != hipSuccess) return hip_fail(e, "tlc_sync: clearing status");
     return fail(TLC_E_CORRUPT, "a decoded stream did not expand to ceil(n/5) bytes");
   }
+  return TLC_OK;
+}
+
+TLC_API int tlc_ctx_set_epochs(tlc_ctx* c, uint32_t enc_epoch, uint32_t dec_epoch) {
+  int st = check_usable(c, "tlc_ctx_set_epochs");
+  if (st) return st;
+  if (enc_epoch > kEncEpochMax || dec_epoch > kDecEpochMax)
+    return fail(TLC_E_INVALID, "tlc_ctx_set_epochs: epochs %u, %u above %u, %u", enc_epoch,
+                dec_epoch, kEncEpochMax, kDecEpochMax);
+  DeviceScope dev(c->device);
+  st = dev.status();
+  if (st) return st;
+  hipError_t e = hipMemsetAsync(c->enc_status, 0, c->enc_status_words * sizeof(uint64_t),
+                                c->stream);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->dec_status, 0, c->dec_status_words * sizeof(uint64_t), c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "tlc_ctx_set_epochs");
+  c->enc_epoch = enc_epoch;
+  c->dec_epoch = dec_epoch;
   return TLC_OK;
 }
 

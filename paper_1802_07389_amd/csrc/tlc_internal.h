@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "tlc.h"
+
 namespace tlc {
 
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
@@ -172,5 +174,11 @@ hipError_t launch_expand_sum(const DecDesc* descs, uint32_t count, const uint64_
 // Epoch widths of the two look-back status layouts.
 constexpr uint32_t kEncEpochMax = (1u << 23) - 1u;
 constexpr uint32_t kDecEpochMax = (1u << 26) - 1u;
+static_assert(kEncEpochMax == TLC_ENC_EPOCH_MAX && kDecEpochMax == TLC_DEC_EPOCH_MAX,
+              "the header states the epoch maxima");
+
+// Sets the calling thread's error text (tlc_last_error_string) and returns
+// code.
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 }  // namespace tlc

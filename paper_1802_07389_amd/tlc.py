@@ -41,9 +41,13 @@ TLC_KERNEL_ZRE_COMPACT = 13
 TLC_KERNEL_QUANT_ENCODE_CHAINED = 14
 TLC_KERNEL_ABSMAX_CHECK = 15
 TLC_KERNEL_ABSMAX_CHECK_BATCH = 16
-TLC_KERNEL_COUNT = 17
+TLC_KERNEL_ACCUM_QUANTIZE = 17
+TLC_KERNEL_COUNT = 18
 
 TLC_OPT_IN_PLACE_FEEDBACK = 1
+
+TLC_ENC_EPOCH_MAX = 8388607
+TLC_DEC_EPOCH_MAX = 67108863
 
 TLC_MODE_3LC = 0
 TLC_MODE_NO_ZRE = 1
@@ -57,6 +61,7 @@ EXPORTS = (
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
     "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_mask", "tlc_profile_get",
     "tlc_profile_reset", "tlc_kernel_name", "tlc_ctx_set_options",
+    "tlc_ctx_set_epochs",
 )
 
 
@@ -116,6 +121,8 @@ def _load():
     L.tlc_ctx_set_options.restype = i
     L.tlc_kernel_name.argtypes = [i]
     L.tlc_kernel_name.restype = ctypes.c_char_p
+    L.tlc_ctx_set_epochs.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32]
+    L.tlc_ctx_set_epochs.restype = i
     return L
 
 
@@ -218,6 +225,10 @@ def tlc_decompress_ex(ctx, mode, bytes_, bytes_len, scale, n, out, accumulate):
 
 def tlc_sync(ctx):
     return lib.tlc_sync(ctx)
+
+
+def tlc_ctx_set_epochs(ctx, enc_epoch, dec_epoch):
+    return lib.tlc_ctx_set_epochs(ctx, int(enc_epoch), int(dec_epoch))
 
 
 def tlc_profile_enable(ctx, on):

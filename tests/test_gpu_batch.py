@@ -145,39 +145,89 @@ def test_batch_argument_errors(bctx):
 
 
 def test_batch_c2_ten_steps_and_batch_decode(bctx):
-    """C2 through the batched calls: 335 tensors, 10 steps, residuals carried."""
+    """C2 through the batched calls: 335 tensors, 10 steps, residuals carried;
+    every step's streams decoded in one batch (odd steps accumulate).  Every
+    tensor's stream, scale, residual and decoded output is compared with the
+    oracle after every step."""
     import torch
     g = G()
     sizes = workloads.c2_sizes()
     rs_gpu = [torch.zeros(n, device="cuda") for n in sizes]
     rs_ref = [np.zeros(n, F32) for n in sizes]
     outs = [torch.full((n,), -0.0, device="cuda") for n in sizes]
+    outs_ref = [np.full(n, -0.0, F32) for n in sizes]
     for step in range(workloads.C2_STEPS):
         xs = [workloads.c2_gradient(step, t, n) for t, n in enumerate(sizes)]
         xd = [torch.from_numpy(x).cuda() for x in xs]
         pays = bctx.compress_batch(xd, rs_gpu, workloads.C2_S)
+        acc = step % 2 == 1
         for t, x in enumerate(xs):
             st, C_ref, M_ref = oracle.compress(x, rs_ref[t], workloads.C2_S)
             C, M = pays[t]
             assert st == 0 and M == M_ref, (step, t)
             assert np.array_equal(C.cpu().numpy(), C_ref), (step, t)
-        acc = step % 2 == 1
+            st, outs_ref[t] = oracle.decompress(C_ref, M_ref, sizes[t], outs_ref[t],
+                                                accumulate=acc)
+            assert st == 0, (step, t)
         bctx.decompress_batch([p[0] for p in pays], [p[1] for p in pays], outs, accumulate=acc)
         bctx.sync()
-        for t in range(0, len(sizes), 7):
-            assert np.array_equal(g.bits(rs_gpu[t].cpu().numpy()), g.bits(rs_ref[t])), (step, t)
-        g.log(f"batched C2 step {step} ok")
-    # the last decode was accumulate=True on top of step 8's values: check a few
-    # tensors end to end against the oracle
-    for t in range(0, len(sizes), 41):
-        n = sizes[t]
-        out_ref = np.full(n, -0.0, F32)
-        rr = np.zeros(n, F32)
-        for step in range(workloads.C2_STEPS):
-            x = workloads.c2_gradient(step, t, n)
-            st, C, M = oracle.compress(x, rr, workloads.C2_S)
-            st, out_ref = oracle.decompress(C, M, n, out_ref, accumulate=(step % 2 == 1))
-        assert np.array_equal(g.bits(outs[t].cpu().numpy()), g.bits(out_ref)), t
+        r_all = g.bits(torch.cat(rs_gpu).cpu().numpy())
+        o_all = g.bits(torch.cat(outs).cpu().numpy())
+        assert np.array_equal(r_all, g.bits(np.concatenate(rs_ref))), step
+        assert np.array_equal(o_all, g.bits(np.concatenate(outs_ref))), step
+        g.log(f"batched C2 step {step} ok: all 335 residuals and outputs")
+
+
+def test_batch_overlapping_buffers_are_refused(bctx):
+    """A residual or byte buffer shared between two tensors of one batch, or
+    an output shared between two streams (or overlapping a stream's bytes),
+    is an argument error: nothing runs.  One stream decoded into several
+    outputs (read-only bytes shared) stays allowed."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    n = 5000
+    m = tlc.tlc_max_compressed_bytes(n)
+    x = torch.from_numpy(workloads.normal([990, 0], 2 * n, 1e-3)).cuda()
+    r = torch.zeros(2 * n, device="cuda")
+    b = torch.zeros(2 * m, dtype=torch.uint8, device="cuda")
+    xp, rp, bp = x.data_ptr(), r.data_ptr(), b.data_ptr()
+    r_before = r.clone()
+    # the second tensor's residual starts inside the first one's
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [xp, xp + 4 * n], [rp, rp + 4 * (n - 1)],
+                                    [n, n], [1.5, 1.5], [bp, bp + m], [m, m])
+    assert st == tlc.TLC_E_INVALID
+    # both tensors write the same bytes
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [xp, xp + 4 * n], [rp, rp + 4 * n],
+                                    [n, n], [1.5, 1.5], [bp, bp], [m, m])
+    assert st == tlc.TLC_E_INVALID
+    # a residual over another tensor's input
+    x2 = torch.from_numpy(workloads.normal([990, 1], n, 1e-3)).cuda()
+    st, *_ = tlc.tlc_compress_batch(bctx.handle, [xp, x2.data_ptr()], [rp, xp + 8],
+                                    [n, n], [1.5, 1.5], [bp, bp + m], [m, m])
+    assert st == tlc.TLC_E_INVALID
+    assert torch.equal(r, r_before)
+    # disjoint buffers: accepted, and the same input read by both tensors is fine
+    st, lens, scales, stat = tlc.tlc_compress_batch(
+        bctx.handle, [xp, xp], [rp, rp + 4 * n], [n, n], [1.5, 1.5], [bp, bp + m], [m, m])
+    assert st == tlc.TLC_OK and lens[0] == lens[1] and scales[0] == scales[1]
+    o = torch.zeros(2 * n, device="cuda")
+    op = o.data_ptr()
+    # overlapping outputs
+    st = tlc.tlc_decompress_batch(bctx.handle, [bp, bp], lens, scales, [n, n],
+                                  [op, op + 4 * (n - 3)], 0)
+    assert st == tlc.TLC_E_INVALID
+    # an output over the other stream's bytes
+    bb = torch.zeros(4 * n + m, dtype=torch.uint8, device="cuda")
+    bb[:lens[0]].copy_(b[:lens[0]])
+    st = tlc.tlc_decompress_batch(bctx.handle, [bb.data_ptr(), bp], lens, scales, [n, n],
+                                  [op, bb.data_ptr() + 4], 0)
+    assert st == tlc.TLC_E_INVALID
+    assert tlc.tlc_sync(bctx.handle) == tlc.TLC_OK
+    # one stream into two disjoint outputs: accepted, both decode the same values
+    st = tlc.tlc_decompress_batch(bctx.handle, [bp, bp], [lens[0]] * 2, [scales[0]] * 2,
+                                  [n, n], [op, op + 4 * n], 0)
+    assert st == tlc.TLC_OK and tlc.tlc_sync(bctx.handle) == tlc.TLC_OK
+    assert torch.equal(o[:n], o[n:])
 
 
 def test_batch_decode_corrupt_writes_nothing(bctx):

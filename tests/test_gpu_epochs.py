@@ -1,0 +1,130 @@
+"""The look-back epoch counters across their wrap, through the C ABI.
+
+Every chained or batched encode and every decode tags its scan's status
+words with the next epoch; at the wrap the words (and, for decodes, the
+mark of the launch with a corrupt stream) are cleared.  tlc_ctx_set_epochs
+moves the counters next to the wrap; every call on either side of it must
+still match the oracle bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_07389_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+def G():
+    import gpuutil
+    return gpuutil
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_1802_07389_amd import tlc
+    c = tlc.Context(max_n=4 * 2_000_000, max_tensors=8)
+    yield c
+    c.close()
+
+
+def chained_encode_check(ctx, n, seed):
+    """A tensor on the chained (look-back) path, against the oracle."""
+    g = G()
+    x = workloads.normal([85, seed], n, 1e-3)
+    r = workloads.normal([86, seed], n, 1e-4)
+    st, C, M, r_gpu = g.gpu_compress(ctx, x, r.copy(), 1.5)
+    r_ref = r.copy()
+    st_ref, C_ref, M_ref = oracle.compress(x, r_ref, 1.5)
+    assert st == st_ref == 0 and M == M_ref and np.array_equal(C, C_ref), seed
+    assert np.array_equal(g.bits(r_gpu), g.bits(r_ref)), seed
+    return C_ref, M_ref
+
+
+def test_encode_epochs_wrap(ctx):
+    import torch
+    from paper_1802_07389_amd import tlc
+    E = tlc.TLC_ENC_EPOCH_MAX
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, E + 1, 0) == tlc.TLC_E_INVALID
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, E - 2, 0) == tlc.TLC_OK
+    # epochs E - 1, E, then the wrap: 1, 2; 600,001 values make 30 tiles
+    for k in range(4):
+        chained_encode_check(ctx, 600_001, k)
+    # batched encodes: one at E, one after the wrap
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, E - 1, 0) == tlc.TLC_OK
+    sizes = [70_001, 5, 400_000, 1_000_003]
+    for step in range(2):
+        xs = [workloads.normal([87, step, t], n, 1e-3) for t, n in enumerate(sizes)]
+        rs = [workloads.normal([88, step, t], n, 1e-4) for t, n in enumerate(sizes)]
+        rd = [torch.from_numpy(r.copy()).cuda() for r in rs]
+        pays = ctx.compress_batch([torch.from_numpy(x).cuda() for x in xs], rd, 1.75)
+        for t, (x, r) in enumerate(zip(xs, rs)):
+            st, C_ref, M_ref = oracle.compress(x, r, 1.75)
+            assert st == 0 and pays[t][1] == M_ref, (step, t)
+            assert np.array_equal(pays[t][0].cpu().numpy(), C_ref), (step, t)
+            assert np.array_equal(G().bits(rd[t].cpu().numpy()), G().bits(r)), (step, t)
+        G().log(f"batched encode across the wrap, call {step} ok")
+
+
+def test_decode_epochs_wrap_and_corrupt_mark(ctx):
+    """A corrupt stream decoded at epoch 3 marks that epoch; the counter is
+    then moved next to the wrap (the mark stays), and after the wrap the
+    decodes at epochs 1, 2, 3, 4 must all write their output: the wrap
+    cleared the mark.  A corrupt stream in the last epoch before a wrap is
+    refused, and good streams after the wrap decode.  Single, batched and
+    summed decodes each take an epoch."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    D = tlc.TLC_DEC_EPOCH_MAX
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, 0, D + 1) == tlc.TLC_E_INVALID
+    n = 1_500_007
+    streams = [chained_encode_check(ctx, n, 10 + k) for k in range(3)]
+    out0 = workloads.normal([89, 0], n, 1e-3)
+    bad = np.append(streams[0][0], streams[0][0][-1:])
+
+    def single(C, M, expect):
+        st, out = g.gpu_decompress(ctx, C, M, n, out0.copy(), accumulate=True)
+        if expect == 0:
+            st_ref, out_ref = oracle.decompress(C, M, n, out0.copy(), True)
+            assert st == st_ref == 0
+            assert np.array_equal(g.bits(out), g.bits(out_ref))
+        else:
+            assert st == tlc.TLC_E_CORRUPT
+            assert np.array_equal(g.bits(out), g.bits(out0))
+
+    def batch():
+        outs = [torch.from_numpy(out0.copy()).cuda() for _ in streams]
+        ctx.decompress_batch([torch.from_numpy(C).cuda() for C, _ in streams],
+                             [M for _, M in streams], outs, accumulate=True)
+        ctx.sync()
+        for (C, M), o in zip(streams, outs):
+            st, out_ref = oracle.decompress(C, M, n, out0.copy(), True)
+            assert np.array_equal(g.bits(o.cpu().numpy()), g.bits(out_ref))
+
+    def summed():
+        total = torch.from_numpy(out0.copy()).cuda()
+        ctx.decompress_sum([torch.from_numpy(C).cuda() for C, _ in streams],
+                           [M for _, M in streams], total, accumulate=True)
+        ctx.sync()
+        ref = out0.copy()
+        for C, M in streams:
+            st, ref = oracle.decompress(C, M, n, ref, True)
+        assert np.array_equal(g.bits(total.cpu().numpy()), g.bits(ref))
+
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, 0, 2) == tlc.TLC_OK
+    single(bad, streams[0][1], tlc.TLC_E_CORRUPT)  # epoch 3 marked
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, 0, D - 1) == tlc.TLC_OK
+    single(*streams[1], 0)  # epoch D
+    single(*streams[0], 0)  # wrap: epoch 1
+    batch()                 # 2
+    single(*streams[2], 0)  # 3: the old mark is gone
+    summed()                # 4
+    g.log("decodes across the wrap after a marked epoch ok")
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, 0, D - 2) == tlc.TLC_OK
+    summed()                                        # D - 1
+    single(bad, streams[0][1], tlc.TLC_E_CORRUPT)  # D: the last epoch before the wrap
+    batch()                                         # wrap: 1
+    single(*streams[1], 0)                          # 2
+    g.log("corrupt stream in the last epoch, good streams after the wrap ok")

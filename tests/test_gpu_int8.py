@@ -100,6 +100,11 @@ def test_int8_special_scales(ctx):
     acc = (np.arange(-127 * 4, 127 * 4 + 1) / 4.0).astype(F32)  # ties at M = 127
     check(ctx, acc, None, 1.0, tag="ties")
     check(ctx, acc, np.zeros_like(acc), 1.0, tag="ties feedback")
+    # sums of -0.0 (tensor -0.0, residual -0.0) keep -0.0 as their residual
+    x = np.array([1.0, -0.0, -0.0, 0.5, 0.0] * 1000, F32)
+    r = np.array([0.0, -0.0, 0.0, 0.0, -0.0] * 1000, F32)
+    check(ctx, x, r, 1.0, tag="signed zeros")
+    check(ctx, x, r, 1.0, offset=1, tag="signed zeros, unaligned")
 
 
 def test_int8_c4_size(ctx):

@@ -2,8 +2,8 @@
 (m = 858,993,459 quartic bytes; 16 GiB per fp32 buffer).  Sparse input so
 the host side stays cheap: zeros with spikes at the five partition starts,
 quartic-tile edges and the last value.  Bar: the whole stream byte for
-byte, M, and the residual and decoded output bit for bit at every spike
-plus their counts of non-zeros (every other value is zero on both sides)."""
+byte, M, and the whole residual and decoded output bit for bit (compared
+in chunks of 2^28 values, so a -0.0/+0.0 flip anywhere fails)."""
 import numpy as np
 import pytest
 
@@ -27,6 +27,16 @@ def spike_positions(n, m):
     rng = np.random.default_rng(123)
     pos.update(int(v) for v in rng.integers(0, n, 2000))
     return np.array(sorted(p for p in pos if 0 <= p < n), dtype=np.int64)
+
+
+def same_bits(a, b, chunk=1 << 28):
+    """Index of the first value whose bits differ, or -1."""
+    assert a.size == b.size
+    for i in range(0, a.size, chunk):
+        d = np.flatnonzero(a[i:i + chunk].view(np.uint32) != b[i:i + chunk].view(np.uint32))
+        if d.size:
+            return i + int(d[0])
+    return -1
 
 
 def test_max_n_round_trip():
@@ -57,10 +67,10 @@ def test_max_n_round_trip():
         assert C.size == C_ref.size and np.array_equal(C, C_ref)
         r_gpu = rd.cpu().numpy()
         del rd
-        assert np.array_equal(g.bits(r_gpu[P]), g.bits(r_ref[P]))
-        assert np.count_nonzero(r_gpu) == np.count_nonzero(r_ref)
-        del r_gpu
-        g.log("stream and residual match")
+        i = same_bits(r_gpu, r_ref)
+        assert i < 0, (i, r_gpu[i], r_ref[i])
+        del r_gpu, r_ref
+        g.log("stream and the whole residual match")
 
         od = torch.zeros(n, dtype=torch.float32, device="cuda")
         ctx.decompress(torch.from_numpy(C_ref).cuda(), M_ref, n, od, accumulate=True)
@@ -69,8 +79,8 @@ def test_max_n_round_trip():
         del od
         st, out_ref = oracle.decompress(C_ref, M_ref, n, np.zeros(n, F32), accumulate=True)
         assert st == 0
-        assert np.array_equal(g.bits(out[P]), g.bits(out_ref[P]))
-        assert np.count_nonzero(out) == np.count_nonzero(out_ref)
-        g.log("decode matches")
+        i = same_bits(out, out_ref)
+        assert i < 0, (i, out[i], out_ref[i])
+        g.log("the whole decoded output matches")
     finally:
         ctx.close()

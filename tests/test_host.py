@@ -69,8 +69,14 @@ def test_host_only_entry_points():
                      "tlc_quant_pack_kernel", "tlc_int8_quant_kernel",
                      "tlc_int8_dequant_kernel", "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel",
                      "tlc_quant_encode_chained_kernel", "tlc_absmax_check_kernel",
-                     "tlc_absmax_check_batch_kernel"]
+                     "tlc_absmax_check_batch_kernel", "tlc_accum_quantize_kernel"]
     assert tlc.tlc_kernel_name(99) is None
+    # every name is a __global__ function of the library's sources
+    csrc = os.path.join(ROOT, "paper_1802_07389_amd", "csrc")
+    src = "".join(open(os.path.join(csrc, f)).read() for f in os.listdir(csrc)
+                  if f.endswith(".hip"))
+    for name in names:
+        assert re.search(r"__global__[^;{]*\b" + name + r"\s*\(", src, flags=re.S), name
 
 
 def test_ctx_create_fails_cleanly_without_gpu():

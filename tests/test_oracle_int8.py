@@ -136,3 +136,17 @@ def test_error_feedback_telescopes():
         sd += codes(C) * float(oracle.int8_step(M))
     assert np.abs(sx - sd - r).max() <= 8 * 2 ** -24 * np.abs(sx).max() * 4 + 1e-12
     assert np.abs(r).max() <= 0.5 * 2e-3 / 127 * 5  # residual stays about half a step
+
+
+def test_signed_zero_residual():
+    """A value whose sum is -0.0 takes code 0, and its residual is
+    -0.0 - 0 * D: the integer code 0 times D > 0 is +0, and -0.0 - (+0.0)
+    is -0.0 in round-to-nearest, so the residual keeps the sign bit
+    (0x80000000).  A sum of +0.0 keeps +0.0."""
+    x = np.array([1.0, -0.0, -0.0, 0.5, 0.0], F32)
+    r = np.array([0.0, -0.0, 0.0, 0.0, -0.0], F32)  # sums: 1, -0, +0, 0.5, +0
+    st, C, M = oracle.compress_int8(x, r, 1.0)
+    assert st == 0 and M == 1.0
+    assert list(codes(C)) == [127, 0, 0, 64, 0]
+    assert list(r.view(np.uint32)[1:3]) == [0x80000000, 0]
+    assert r.view(np.uint32)[4] == 0
