@@ -207,6 +207,49 @@ int tlc_decompress_sum(tlc_ctx* ctx, size_t count, const uint8_t* const* bytes,
                        const size_t* bytes_len, const float* scales, size_t n, float* out,
                        int accumulate);
 
+/* ---- encoding without a context (no allocation) ------------------------ */
+
+/* Result of tlc_compress_noalloc, written to device memory by the call's
+ * last kernel: status is TLC_OK, TLC_E_NONFINITE (residual and bytes left
+ * unchanged, as for tlc_compress) or TLC_E_DEVICE (a look-back wait gave
+ * up; the residual may then already hold its new values and no stream was
+ * written); bytes_len and scale are those tlc_compress returns (0 unless
+ * status is TLC_OK). */
+typedef struct tlc_result {
+  int32_t status;
+  uint32_t bytes_len;
+  float scale;
+  uint32_t reserved; /* 0 */
+} tlc_result;
+
+/* Largest n tlc_compress_noalloc accepts: 2^23 values (at most 410 encoder
+ * tiles, whose scratch is 8 KiB of device memory). */
+#define TLC_NOALLOC_MAX_N ((size_t)8388608u)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * tlc_compress without a context.  Same encoding, bit for bit, with the
+ * default error policy (the check pass leaves residual and bytes unchanged
+ * on NaN/Inf), for n <= TLC_NOALLOC_MAX_N (larger n: TLC_E_INVALID, nothing
+ * runs).
+ *   tensor, residual, n, s, bytes, bytes_cap   as for tlc_compress.
+ *   result      device pointer to one tlc_result (16 bytes), written last.
+ *   hip_stream  a hipStream_t of the calling thread's current device (or
+ *               NULL, the default stream); every pointer belongs to that
+ *               device.
+ * Asynchronous: returns after queueing its kernels (argument errors are
+ * returned at once, and nothing runs); read *result after the stream has
+ * reached it.  No device or pinned memory is allocated, and no library
+ * routine that allocates is called: the scratch (a control block, partial
+ * maxima, look-back status words) is a static device array of 8 KiB per
+ * device, located once per device on the first call there.  Every call on
+ * a device shares that array and clears it first, so calls that may
+ * overlap on one device (other streams, other host threads) race and must
+ * be ordered by the caller. */
+int tlc_compress_noalloc(const float* tensor, float* residual, size_t n, float s,
+                         uint8_t* bytes, size_t bytes_cap, tlc_result* result,
+                         void* hip_stream);
+
 /* ---- options ------------------------------------------------------------ */
 
 /* TLC_OPT_IN_PLACE_FEEDBACK: take step 1 of error accumulation (Section

@@ -7,7 +7,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtlc.so")
-SOURCES = ["encode.hip", "decode.hip", "int8.hip", "tlc_api.hip"]
+SOURCES = ["encode.hip", "decode.hip", "int8.hip", "tlc_api.hip", "noalloc.hip"]
 HEADERS = ["tlc_internal.h", "device_common.hpp", "lookback.hpp", "zre_scan.hpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

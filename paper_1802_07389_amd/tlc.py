@@ -46,6 +46,7 @@ TLC_KERNEL_COUNT = 18
 
 TLC_OPT_IN_PLACE_FEEDBACK = 1
 
+TLC_NOALLOC_MAX_N = 8388608
 TLC_ENC_EPOCH_MAX = 8388607
 TLC_DEC_EPOCH_MAX = 67108863
 
@@ -61,8 +62,15 @@ EXPORTS = (
     "tlc_decompress_batch", "tlc_decompress_sum", "tlc_sync",
     "tlc_last_error_string", "tlc_profile_enable", "tlc_profile_mask", "tlc_profile_get",
     "tlc_profile_reset", "tlc_kernel_name", "tlc_ctx_set_options",
-    "tlc_ctx_set_epochs",
+    "tlc_compress_noalloc", "tlc_ctx_set_epochs",
 )
+
+
+class tlc_result(ctypes.Structure):
+    """struct tlc_result of tlc.h (written to device memory by
+    tlc_compress_noalloc; this layout reads a host copy of it)."""
+    _fields_ = [("status", ctypes.c_int32), ("bytes_len", ctypes.c_uint32),
+                ("scale", ctypes.c_float), ("reserved", ctypes.c_uint32)]
 
 
 class TLCError(RuntimeError):
@@ -121,6 +129,8 @@ def _load():
     L.tlc_ctx_set_options.restype = i
     L.tlc_kernel_name.argtypes = [i]
     L.tlc_kernel_name.restype = ctypes.c_char_p
+    L.tlc_compress_noalloc.argtypes = [vp, vp, sz, f, vp, sz, vp, vp]
+    L.tlc_compress_noalloc.restype = i
     L.tlc_ctx_set_epochs.argtypes = [vp, ctypes.c_uint32, ctypes.c_uint32]
     L.tlc_ctx_set_epochs.restype = i
     return L
@@ -225,6 +235,13 @@ def tlc_decompress_ex(ctx, mode, bytes_, bytes_len, scale, n, out, accumulate):
 
 def tlc_sync(ctx):
     return lib.tlc_sync(ctx)
+
+
+def tlc_compress_noalloc(tensor, residual, n, s, bytes_, bytes_cap, result, hip_stream):
+    """Device pointers in (result: device address of a 16-byte tlc_result);
+    returns the status of the call (the encode's own status is in *result)."""
+    return lib.tlc_compress_noalloc(tensor, residual, n, s, bytes_, bytes_cap, result,
+                                    hip_stream)
 
 
 def tlc_ctx_set_epochs(ctx, enc_epoch, dec_epoch):
