@@ -47,9 +47,10 @@ def algorithmic_bytes(n, c, nnz):
         # read the trits; write each tile's own stream bytes (c in all) and
         # its 16-byte record
         "tlc_quant_encode_kernel": n // 4 + c + 16 * tiles,
-        # tile records in, tile prefixes and chunk summaries out
+        # tile records in, tile prefixes and chunk summaries out (the
+        # chunk summaries' scan, a second launch, rides on the same id)
         "tlc_zre_chunk_kernel": 24 * tiles,
-        # records, prefixes and slot bytes in, the stream out
+        # records and prefixes in, slot bytes in, the stream out
         "tlc_zre_compact_kernel": 2 * c + 32 * tiles,
         "tlc_zre_index_kernel": c,                       # read C (writes m/4096 index words)
         # read C; accumulating densely, read every value of out and store the
@@ -171,12 +172,16 @@ def _row(name, values, s, te, td, nbytes, ote=None, otd=None, ovalues=None, **ex
     return row
 
 
-def config_rows(torch, tlc, workloads, dev, with_c4=True):
+PARTS = ("C1", "C3", "C4", "modes", "C2", "C5")
+
+
+def config_rows(torch, tlc, workloads, dev, parts=PARTS):
     """One row per config (C1-C5, and the comparison encodings of Section
-    5.1 on the C4 step-0 tensor): GPU and oracle GB/s of fp32 input and the
-    compression ratio 4n / (payload + 4-byte scale).  GPU encode times
-    include the host synchronisation of tlc_compress (it returns the stream
-    length).  The oracle runs on one pinned host core."""
+    5.1 on the C4 step-0 tensor, "modes"), for the names in `parts`: GPU and
+    oracle GB/s of fp32 input and the compression ratio 4n / (payload +
+    4-byte scale).  GPU encode times include the host synchronisation of
+    tlc_compress (it returns the stream length).  The oracle runs on one
+    pinned host core."""
     try:
         os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
     except (AttributeError, OSError):
@@ -186,22 +191,24 @@ def config_rows(torch, tlc, workloads, dev, with_c4=True):
     ctx = tlc.Context(max_n=workloads.C4_N, stream=stream, device=dev)
 
     # C1: one 2^20 tensor, s = 1, zero residual each time
-    x1 = workloads.c1_tensor()
-    _gpu_round_trips(torch, ctx, [x1], workloads.C1_S, dev, carry=False)
-    te, td, nb, v = _gpu_round_trips(torch, ctx, [x1] * 50, workloads.C1_S, dev, carry=False)
-    ote, otd = _oracle_round_trips([x1] * 5, workloads.C1_S, carry=False)
-    rows.append(_row("C1", v, workloads.C1_S, te, td, nb, ote, otd, 5 * x1.size))
+    if "C1" in parts:
+        x1 = workloads.c1_tensor()
+        _gpu_round_trips(torch, ctx, [x1], workloads.C1_S, dev, carry=False)
+        te, td, nb, v = _gpu_round_trips(torch, ctx, [x1] * 50, workloads.C1_S, dev, carry=False)
+        ote, otd = _oracle_round_trips([x1] * 5, workloads.C1_S, carry=False)
+        rows.append(_row("C1", v, workloads.C1_S, te, td, nb, ote, otd, 5 * x1.size))
 
     # C3: 2^26 values with zero runs, each s from a zero residual
-    x3 = workloads.c3_tensor()
-    for s3 in workloads.C3_S:
-        _gpu_round_trips(torch, ctx, [x3], s3, dev, carry=False)
-        te, td, nb, v = _gpu_round_trips(torch, ctx, [x3] * 10, s3, dev, carry=False)
-        ote, otd = _oracle_round_trips([x3], s3, carry=False)
-        rows.append(_row(f"C3 s={s3}", v, s3, te, td, nb, ote, otd, x3.size))
+    if "C3" in parts:
+        x3 = workloads.c3_tensor()
+        for s3 in workloads.C3_S:
+            _gpu_round_trips(torch, ctx, [x3], s3, dev, carry=False)
+            te, td, nb, v = _gpu_round_trips(torch, ctx, [x3] * 10, s3, dev, carry=False)
+            ote, otd = _oracle_round_trips([x3], s3, carry=False)
+            rows.append(_row(f"C3 s={s3}", v, s3, te, td, nb, ote, otd, x3.size))
 
     # C4: 5 steps of 2^28 values, residual carried, decode-accumulate
-    if with_c4:
+    if "C4" in parts:
         x4 = [workloads.c4_tensor(k) for k in range(workloads.C4_STEPS)]
         _gpu_round_trips(torch, ctx, x4[:1], workloads.C4_S, dev)
         te, td, nb, v = _gpu_round_trips(torch, ctx, x4, workloads.C4_S, dev)
@@ -215,195 +222,198 @@ def config_rows(torch, tlc, workloads, dev, with_c4=True):
     # 5.1 run at s = 1 (TernGrad-like stochastic quantization with the plain
     # max as its scale; 8-bit codes spanning all 255 levels); "No ZRE" is 3LC
     # itself without the zero-run stage, at C4's s.
-    import oracle
-    xh = workloads.c4_tensor(0)
-    x = torch.from_numpy(xh).to(dev)
-    r = torch.zeros_like(x)
-    out = torch.zeros_like(x)
-    buf = torch.empty(x.numel(), dtype=torch.uint8, device=dev)
-    modes = [("No ZRE", tlc.TLC_MODE_NO_ZRE, workloads.C4_S,
-              (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
-             ("Stoch 3-value + QE", tlc.TLC_MODE_STOCHASTIC, 1.0,
-              (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
-             ("8-bit int", tlc.TLC_MODE_INT8, 1.0,
-              (tlc.TLC_KERNEL_INT8_QUANT, tlc.TLC_KERNEL_INT8_DEQUANT))]
-    for name, mode, sm, kids in modes:
-        rr = None if mode == tlc.TLC_MODE_STOCHASTIC else r
-        C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=0, out=buf)
-        ctx.decompress_mode(mode, C, M, out, accumulate=True)
-        ctx.sync()
-        ctx.profile(True)
-        ctx.profile_reset()
-        reps = 5
-        te = td = 0.0
-        for k in range(reps):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=k, out=buf)
-            t1 = time.perf_counter()
+    if "modes" in parts:
+        import oracle
+        xh = workloads.c4_tensor(0)
+        x = torch.from_numpy(xh).to(dev)
+        r = torch.zeros_like(x)
+        out = torch.zeros_like(x)
+        buf = torch.empty(x.numel(), dtype=torch.uint8, device=dev)
+        modes = [("No ZRE", tlc.TLC_MODE_NO_ZRE, workloads.C4_S,
+                  (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+                 ("Stoch 3-value + QE", tlc.TLC_MODE_STOCHASTIC, 1.0,
+                  (tlc.TLC_KERNEL_QUANT_PACK, tlc.TLC_KERNEL_EXPAND_DEQUANT)),
+                 ("8-bit int", tlc.TLC_MODE_INT8, 1.0,
+                  (tlc.TLC_KERNEL_INT8_QUANT, tlc.TLC_KERNEL_INT8_DEQUANT))]
+        for name, mode, sm, kids in modes:
+            rr = None if mode == tlc.TLC_MODE_STOCHASTIC else r
+            C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=0, out=buf)
             ctx.decompress_mode(mode, C, M, out, accumulate=True)
             ctx.sync()
+            ctx.profile(True)
+            ctx.profile_reset()
+            reps = 5
+            te = td = 0.0
+            for k in range(reps):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                C, M = ctx.compress_mode(mode, x, rr, sm, seed=7, step=k, out=buf)
+                t1 = time.perf_counter()
+                ctx.decompress_mode(mode, C, M, out, accumulate=True)
+                ctx.sync()
+                t2 = time.perf_counter()
+                te += t1 - t0
+                td += t2 - t1
+            kus = {}
+            for kid in (tlc.TLC_KERNEL_ABSMAX_CHECK, tlc.TLC_KERNEL_ABSMAX) + kids:
+                ms, cnt = ctx.profile_get(kid)
+                if cnt:
+                    kus[tlc.tlc_kernel_name(kid)] = round(ms / cnt * 1e3, 1)
+            ctx.profile(False)
+            rh = np.zeros(xh.size, np.float32)
+            t0 = time.perf_counter()
+            if mode == tlc.TLC_MODE_NO_ZRE:
+                st, Ch, Mh = oracle.compress_nozre(xh, rh, sm)
+            elif mode == tlc.TLC_MODE_STOCHASTIC:
+                st, Ch, Mh = oracle.compress_stochastic(xh, sm, 7, 0)
+            else:
+                st, Ch, Mh = oracle.compress_int8(xh, rh, sm)
+            t1 = time.perf_counter()
+            if mode == tlc.TLC_MODE_INT8:
+                oracle.decompress_int8(Ch, Mh, xh.size, rh, accumulate=True)
+            else:
+                oracle.decompress(Ch, Mh, xh.size, rh, accumulate=True)
             t2 = time.perf_counter()
-            te += t1 - t0
-            td += t2 - t1
-        kus = {}
-        for kid in (tlc.TLC_KERNEL_ABSMAX_CHECK, tlc.TLC_KERNEL_ABSMAX) + kids:
-            ms, cnt = ctx.profile_get(kid)
-            if cnt:
-                kus[tlc.tlc_kernel_name(kid)] = round(ms / cnt * 1e3, 1)
-        ctx.profile(False)
-        rh = np.zeros(xh.size, np.float32)
-        t0 = time.perf_counter()
-        if mode == tlc.TLC_MODE_NO_ZRE:
-            st, Ch, Mh = oracle.compress_nozre(xh, rh, sm)
-        elif mode == tlc.TLC_MODE_STOCHASTIC:
-            st, Ch, Mh = oracle.compress_stochastic(xh, sm, 7, 0)
-        else:
-            st, Ch, Mh = oracle.compress_int8(xh, rh, sm)
-        t1 = time.perf_counter()
-        if mode == tlc.TLC_MODE_INT8:
-            oracle.decompress_int8(Ch, Mh, xh.size, rh, accumulate=True)
-        else:
-            oracle.decompress(Ch, Mh, xh.size, rh, accumulate=True)
-        t2 = time.perf_counter()
-        rows.append(_row(f"C4 step 0, {name}", reps * x.numel(), sm, te, td,
-                         reps * (C.numel() + 4), t1 - t0, t2 - t1, x.numel(),
-                         kernel_us=kus))
-    del x, r, out, buf, xh, rh
+            rows.append(_row(f"C4 step 0, {name}", reps * x.numel(), sm, te, td,
+                             reps * (C.numel() + 4), t1 - t0, t2 - t1, x.numel(),
+                             kernel_us=kus))
+        del x, r, out, buf, xh, rh
     ctx.close()
 
     # C2: 335 ResNet-110 tensors x 10 steps through the batched calls.  The
     # pointer arrays are built once (a training loop keeps its gradient and
     # residual buffers), so the timed region is the library calls.
-    import ctypes
-    sizes = workloads.c2_sizes()
-    T = len(sizes)
-    bctx = tlc.Context(max_n=sum(sizes), stream=stream, device=dev, max_tensors=T)
-    rs = [torch.zeros(n, device=dev) for n in sizes]
-    outs = [torch.zeros(n, device=dev) for n in sizes]
-    bufs = [torch.empty(-(-n // 5), dtype=torch.uint8, device=dev) for n in sizes]
-    grads = [[torch.from_numpy(workloads.c2_gradient(k, t, n)).to(dev)
-              for t, n in enumerate(sizes)] for k in range(workloads.C2_STEPS)]
-    A = lambda ct, vals: (ct * T)(*vals)
-    vp, sz, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
-    g_ptrs = [A(vp, [g.data_ptr() for g in gs]) for gs in grads]
-    r_ptrs = A(vp, [r.data_ptr() for r in rs])
-    b_ptrs = A(vp, [b.data_ptr() for b in bufs])
-    o_ptrs = A(vp, [o.data_ptr() for o in outs])
-    ns_a = A(sz, sizes)
-    caps_a = A(sz, [b.numel() for b in bufs])
-    s_a = A(f32, [workloads.C2_S] * T)
-    lens_a, sc_a, st_a = (sz * T)(), (f32 * T)(), (ctypes.c_int * T)()
-    te = td = 0.0
-    nb = 0
-    for k in range(workloads.C2_STEPS + 1):  # the first pass warms up
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        st = tlc.lib.tlc_compress_batch(bctx.handle, T, g_ptrs[k % workloads.C2_STEPS], r_ptrs,
-                                        ns_a, s_a, b_ptrs, caps_a, lens_a, sc_a, st_a)
-        t1 = time.perf_counter()
-        st2 = tlc.lib.tlc_decompress_batch(bctx.handle, T, b_ptrs, lens_a, sc_a, ns_a, o_ptrs, 0)
-        st3 = tlc.lib.tlc_sync(bctx.handle)
-        t2 = time.perf_counter()
-        assert st == 0 and st2 == 0 and st3 == 0
-        if k:
-            te += t1 - t0
-            td += t2 - t1
-            nb += sum(lens_a) + 4 * T
-    # kernel times from a further 10 steps: the event pairs of the per-kernel
-    # timing cost about as much host and device time as these small kernels,
-    # so the timed steps above run without them
-    bctx.profile(True)
-    bctx.profile_reset()
-    for k in range(workloads.C2_STEPS):
-        st = tlc.lib.tlc_compress_batch(bctx.handle, T, g_ptrs[k], r_ptrs, ns_a, s_a, b_ptrs,
-                                        caps_a, lens_a, sc_a, st_a)
-        st2 = tlc.lib.tlc_decompress_batch(bctx.handle, T, b_ptrs, lens_a, sc_a, ns_a, o_ptrs, 0)
-        assert st == 0 and st2 == 0 and tlc.lib.tlc_sync(bctx.handle) == 0
-    kms = {}
-    for kid in (tlc.TLC_KERNEL_ABSMAX_CHECK_BATCH, tlc.TLC_KERNEL_ABSMAX_BATCH,
-                tlc.TLC_KERNEL_QUANT_ENCODE_BATCH, tlc.TLC_KERNEL_ZRE_INDEX_BATCH,
-                tlc.TLC_KERNEL_EXPAND_DEQUANT_BATCH):
-        ms, cnt = bctx.profile_get(kid)
-        kms[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
-    bctx.close()
-    # oracle: the same 10 steps tensor by tensor on one core
-    import oracle
-    r_h = [np.zeros(n, np.float32) for n in sizes]
-    ote = otd = 0.0
-    nb_bn = 0
-    for k in range(workloads.C2_STEPS):
-        for t, n in enumerate(sizes):
-            g = workloads.c2_gradient(k, t, n)
+    if "C2" in parts:
+        import ctypes
+        sizes = workloads.c2_sizes()
+        T = len(sizes)
+        bctx = tlc.Context(max_n=sum(sizes), stream=stream, device=dev, max_tensors=T)
+        rs = [torch.zeros(n, device=dev) for n in sizes]
+        outs = [torch.zeros(n, device=dev) for n in sizes]
+        bufs = [torch.empty(-(-n // 5), dtype=torch.uint8, device=dev) for n in sizes]
+        grads = [[torch.from_numpy(workloads.c2_gradient(k, t, n)).to(dev)
+                  for t, n in enumerate(sizes)] for k in range(workloads.C2_STEPS)]
+        A = lambda ct, vals: (ct * T)(*vals)
+        vp, sz, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+        g_ptrs = [A(vp, [g.data_ptr() for g in gs]) for gs in grads]
+        r_ptrs = A(vp, [r.data_ptr() for r in rs])
+        b_ptrs = A(vp, [b.data_ptr() for b in bufs])
+        o_ptrs = A(vp, [o.data_ptr() for o in outs])
+        ns_a = A(sz, sizes)
+        caps_a = A(sz, [b.numel() for b in bufs])
+        s_a = A(f32, [workloads.C2_S] * T)
+        lens_a, sc_a, st_a = (sz * T)(), (f32 * T)(), (ctypes.c_int * T)()
+        te = td = 0.0
+        nb = 0
+        for k in range(workloads.C2_STEPS + 1):  # the first pass warms up
+            torch.cuda.synchronize()
             t0 = time.perf_counter()
-            st, C, M = oracle.compress(g, r_h[t], workloads.C2_S)
+            st = tlc.lib.tlc_compress_batch(bctx.handle, T, g_ptrs[k % workloads.C2_STEPS], r_ptrs,
+                                            ns_a, s_a, b_ptrs, caps_a, lens_a, sc_a, st_a)
             t1 = time.perf_counter()
-            oracle.decompress(C, M, n)
+            st2 = tlc.lib.tlc_decompress_batch(bctx.handle, T, b_ptrs, lens_a, sc_a, ns_a, o_ptrs, 0)
+            st3 = tlc.lib.tlc_sync(bctx.handle)
             t2 = time.perf_counter()
-            ote += t1 - t0
-            otd += t2 - t1
-            if workloads.resnet110_cifar_shapes()[t][2] != "bn":
-                nb_bn += C.size + 4
-    v2 = sum(sizes) * workloads.C2_STEPS
-    bn_vals = sum(n for (_, _, kind), n in zip(workloads.resnet110_cifar_shapes(), sizes)
-                  if kind == "bn") * workloads.C2_STEPS
-    rows.append(_row("C2 (batched, 10 steps)", v2, workloads.C2_S, te, td, nb, ote, otd, v2,
-                     ms_per_step=round((te + td) / workloads.C2_STEPS * 1e3, 4),
-                     ratio_without_bn=round(4 * (v2 - bn_vals) / nb_bn, 2),
-                     kernel_us_per_step=kms))
+            assert st == 0 and st2 == 0 and st3 == 0
+            if k:
+                te += t1 - t0
+                td += t2 - t1
+                nb += sum(lens_a) + 4 * T
+        # kernel times from a further 10 steps: the event pairs of the per-kernel
+        # timing cost about as much host and device time as these small kernels,
+        # so the timed steps above run without them
+        bctx.profile(True)
+        bctx.profile_reset()
+        for k in range(workloads.C2_STEPS):
+            st = tlc.lib.tlc_compress_batch(bctx.handle, T, g_ptrs[k], r_ptrs, ns_a, s_a, b_ptrs,
+                                            caps_a, lens_a, sc_a, st_a)
+            st2 = tlc.lib.tlc_decompress_batch(bctx.handle, T, b_ptrs, lens_a, sc_a, ns_a, o_ptrs, 0)
+            assert st == 0 and st2 == 0 and tlc.lib.tlc_sync(bctx.handle) == 0
+        kms = {}
+        for kid in (tlc.TLC_KERNEL_ABSMAX_CHECK_BATCH, tlc.TLC_KERNEL_ABSMAX_BATCH,
+                    tlc.TLC_KERNEL_QUANT_ENCODE_BATCH, tlc.TLC_KERNEL_ZRE_INDEX_BATCH,
+                    tlc.TLC_KERNEL_EXPAND_DEQUANT_BATCH):
+            ms, cnt = bctx.profile_get(kid)
+            kms[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
+        bctx.close()
+        # oracle: the same 10 steps tensor by tensor on one core
+        import oracle
+        r_h = [np.zeros(n, np.float32) for n in sizes]
+        ote = otd = 0.0
+        nb_bn = 0
+        for k in range(workloads.C2_STEPS):
+            for t, n in enumerate(sizes):
+                g = workloads.c2_gradient(k, t, n)
+                t0 = time.perf_counter()
+                st, C, M = oracle.compress(g, r_h[t], workloads.C2_S)
+                t1 = time.perf_counter()
+                oracle.decompress(C, M, n)
+                t2 = time.perf_counter()
+                ote += t1 - t0
+                otd += t2 - t1
+                if workloads.resnet110_cifar_shapes()[t][2] != "bn":
+                    nb_bn += C.size + 4
+        v2 = sum(sizes) * workloads.C2_STEPS
+        bn_vals = sum(n for (_, _, kind), n in zip(workloads.resnet110_cifar_shapes(), sizes)
+                      if kind == "bn") * workloads.C2_STEPS
+        rows.append(_row("C2 (batched, 10 steps)", v2, workloads.C2_S, te, td, nb, ote, otd, v2,
+                         ms_per_step=round((te + td) / workloads.C2_STEPS * 1e3, 4),
+                         ratio_without_bn=round(4 * (v2 - bn_vals) / nb_bn, 2),
+                         kernel_us_per_step=kms))
 
     # C5: 16 payloads encoded (batched), summed by the fused aggregation,
     # then the sum re-encoded
-    n5 = workloads.C5_N
-    P = workloads.C5_PAYLOADS
-    actx = tlc.Context(max_n=P * n5, stream=stream, device=dev, max_tensors=P)
-    xs5 = [torch.from_numpy(workloads.c5_tensor(p)).to(dev) for p in range(P)]
-    rs5 = [torch.zeros(n5, device=dev) for _ in range(P)]
-    pays = actx.compress_batch(xs5, rs5, workloads.C5_S)
-    total = torch.zeros(n5, device=dev)
-    reps = 10
-    actx.decompress_sum([p[0] for p in pays], [p[1] for p in pays], total)
-    actx.sync()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(reps):
+    if "C5" in parts:
+        n5 = workloads.C5_N
+        P = workloads.C5_PAYLOADS
+        actx = tlc.Context(max_n=P * n5, stream=stream, device=dev, max_tensors=P)
+        xs5 = [torch.from_numpy(workloads.c5_tensor(p)).to(dev) for p in range(P)]
+        rs5 = [torch.zeros(n5, device=dev) for _ in range(P)]
+        pays = actx.compress_batch(xs5, rs5, workloads.C5_S)
+        total = torch.zeros(n5, device=dev)
+        reps = 10
         actx.decompress_sum([p[0] for p in pays], [p[1] for p in pays], total)
-    actx.sync()
-    t1 = time.perf_counter()
-    r_srv = torch.zeros(n5, device=dev)
-    out = torch.empty(-(-n5 // 5), dtype=torch.uint8, device=dev)
-    torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    for _ in range(reps):  # same work every rep (the residual's values do not matter)
-        C, M = actx.compress(total, r_srv, workloads.C5_S, out=out)
-    t3 = time.perf_counter()
-    actx.close()
-    agg_gb = 4 * n5 * P * reps / 1e9
-    # oracle: 16 decode-accumulates + one re-encode
-    s5 = [workloads.c5_tensor(p) for p in range(2)]
-    o_pay = [oracle.compress(x, np.zeros(n5, np.float32), workloads.C5_S) for x in s5]
-    acc5 = np.zeros(n5, np.float32)
-    ta = time.perf_counter()
-    for st, C5, M5 in o_pay:
-        oracle.decompress(C5, M5, n5, acc5, accumulate=True)
-    tb = time.perf_counter()
-    oracle.compress(acc5, np.zeros(n5, np.float32), workloads.C5_S)
-    tc = time.perf_counter()
-    rows.append({"config": "C5 (16-stream aggregation + re-encode)", "values": n5,
-                 "streams": P, "s": workloads.C5_S,
-                 "aggregate_GBps_of_stream_values": round(agg_gb / (t1 - t0), 2),
-                 "aggregate_ms": round((t1 - t0) / reps * 1e3, 4),
-                 "reencode_GBps": round(4 * n5 * reps / 1e9 / (t3 - t2), 2),
-                 "reencode_ms": round((t3 - t2) / reps * 1e3, 4),
-                 "oracle_aggregate_GBps": round(4 * n5 * len(s5) / 1e9 / (tb - ta), 4),
-                 "oracle_reencode_GBps": round(4 * n5 / 1e9 / (tc - tb), 4),
-                 "oracle_cores": 1})
+        actx.sync()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            actx.decompress_sum([p[0] for p in pays], [p[1] for p in pays], total)
+        actx.sync()
+        t1 = time.perf_counter()
+        r_srv = torch.zeros(n5, device=dev)
+        out = torch.empty(-(-n5 // 5), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for _ in range(reps):  # same work every rep (the residual's values do not matter)
+            C, M = actx.compress(total, r_srv, workloads.C5_S, out=out)
+        t3 = time.perf_counter()
+        actx.close()
+        agg_gb = 4 * n5 * P * reps / 1e9
+        # oracle: 16 decode-accumulates + one re-encode
+        s5 = [workloads.c5_tensor(p) for p in range(2)]
+        o_pay = [oracle.compress(x, np.zeros(n5, np.float32), workloads.C5_S) for x in s5]
+        acc5 = np.zeros(n5, np.float32)
+        ta = time.perf_counter()
+        for st, C5, M5 in o_pay:
+            oracle.decompress(C5, M5, n5, acc5, accumulate=True)
+        tb = time.perf_counter()
+        oracle.compress(acc5, np.zeros(n5, np.float32), workloads.C5_S)
+        tc = time.perf_counter()
+        rows.append({"config": "C5 (16-stream aggregation + re-encode)", "values": n5,
+                     "streams": P, "s": workloads.C5_S,
+                     "aggregate_GBps_of_stream_values": round(agg_gb / (t1 - t0), 2),
+                     "aggregate_ms": round((t1 - t0) / reps * 1e3, 4),
+                     "reencode_GBps": round(4 * n5 * reps / 1e9 / (t3 - t2), 2),
+                     "reencode_ms": round((t3 - t2) / reps * 1e3, 4),
+                     "oracle_aggregate_GBps": round(4 * n5 * len(s5) / 1e9 / (tb - ta), 4),
+                     "oracle_reencode_GBps": round(4 * n5 / 1e9 / (tc - tb), 4),
+                     "oracle_cores": 1})
     return rows
 
 
-def report(torch, tlc, workloads, dev):
+def report(torch, tlc, workloads, dev, parts=PARTS):
     """One JSON line per config (C1-C5 and the comparison encodings)."""
-    for row in config_rows(torch, tlc, workloads, dev, with_c4=True):
+    for row in config_rows(torch, tlc, workloads, dev, parts):
         print(json.dumps(row), flush=True)
 
 
@@ -418,6 +428,8 @@ def main():
                     help="only run 1 GiB device copies (counter calibration)")
     ap.add_argument("--report", action="store_true",
                     help="per-config report (C1-C5) instead of the headline line")
+    ap.add_argument("--only", default=",".join(PARTS),
+                    help="with --report: the parts to run, comma-separated from " + ",".join(PARTS))
     ap.add_argument("--no-configs", action="store_true",
                     help="leave the C1, C2, C3, C5 and comparison rows out of the line")
     args = ap.parse_args()
@@ -444,7 +456,10 @@ def main():
         return
 
     if args.report:
-        report(torch, tlc, workloads, dev)
+        parts = tuple(p for p in args.only.split(",") if p)
+        if not set(parts) <= set(PARTS):
+            ap.error(f"--only takes names from {','.join(PARTS)}")
+        report(torch, tlc, workloads, dev, parts)
         return
 
     n = args.n or workloads.C4_N
@@ -498,8 +513,6 @@ def main():
     # Further untimed steps time every kernel of a step, one kernel at a
     # time: a single event pair per step, as for the roofline kernel (an
     # event pair on every kernel would cost tens of microseconds per step).
-    # The ZRE_CHUNKS id brackets two launches (the chunk scan and the scan of
-    # the chunk summaries).
     kern_steps = 3
     names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
     enc_k = ["tlc_absmax_check_kernel", "tlc_accum_quantize_kernel", "tlc_quant_encode_kernel",
@@ -624,7 +637,8 @@ def main():
     if not args.no_configs:
         # the other configs (and the comparison encodings) in the same line
         result["configs"] = {row.pop("config"): row
-                             for row in config_rows(torch, tlc, workloads, dev, with_c4=False)}
+                             for row in config_rows(torch, tlc, workloads, dev,
+                                                    tuple(p for p in PARTS if p != "C4"))}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(host_inputs[0], s)
     else:

@@ -7,6 +7,10 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtlc.so")
+# The stress build of the look-back scans: every status-word publish sleeps
+# a pseudo-random while first (TLC_DELAY_INJECT); used only by
+# tests/test_gpu_lookback_delays.py.
+LIB_DELAY = os.path.join(PKG, "libtlc_delay.so")
 SOURCES = ["encode.hip", "decode.hip", "int8.hip", "tlc_api.hip", "noalloc.hip"]
 HEADERS = ["tlc_internal.h", "device_common.hpp", "lookback.hpp", "zre_scan.hpp"]
 
@@ -39,16 +43,18 @@ def stale():
     return any(os.path.getmtime(d) > t for d in deps())
 
 
-def build(verbose=False):
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           "-o", tmp, *sources()]
+def build(verbose=False, delay=False):
+    """Compile libtlc.so (delay=True: the stress build libtlc_delay.so)."""
+    out = LIB_DELAY if delay else LIB
+    tmp = out + ".tmp"
+    cmd = [HIPCC, *FLAGS, *(["-DTLC_DELAY_INJECT"] if delay else []),
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-o", tmp, *sources()]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-q" not in sys.argv))
+    print(build(verbose="-q" not in sys.argv, delay="--delay" in sys.argv))

@@ -180,8 +180,12 @@ __device__ __forceinline__ uint32_t quantize_one(float acc, float M, float U,
 // (contiguous partitions, p0 most significant; elements past n are the zero
 // padding of Section 3.2, step 4) and returns the byte.  A value with q = 0
 // keeps acc as its residual, which the buffer already holds, so only q != 0
-// writes back.
-__device__ __forceinline__ uint32_t quantize_byte(float* __restrict__ r, uint64_t n,
+// writes back.  kX (after the check pass has given M): the buffer still
+// holds the previous residual, acc = x + r is formed here (step 1 of
+// Section 3.1) and every value's residual is stored.
+template <bool kX = false>
+__device__ __forceinline__ uint32_t quantize_byte(const float* __restrict__ x,
+                                                  float* __restrict__ r, uint64_t n,
                                                   uint64_t m, uint64_t j, float M, float U) {
   uint32_t code = 0u;
 #pragma unroll
@@ -190,8 +194,8 @@ __device__ __forceinline__ uint32_t quantize_byte(float* __restrict__ r, uint64_
     uint32_t t = 0u;
     if (e < n) {
       float o;
-      t = quantize_one(r[e], M, U, o);
-      if (t != 1u) r[e] = o;
+      t = quantize_one(kX ? x[e] + r[e] : r[e], M, U, o);
+      if (kX || t != 1u) r[e] = o;
     }
     code = code * 3u + t;
   }
@@ -199,22 +203,33 @@ __device__ __forceinline__ uint32_t quantize_byte(float* __restrict__ r, uint64_
 }
 
 // Quartic bytes j .. j+3 (j % 4 == 0) with m % 4 == 0 and r 16-byte
-// aligned: every partition slice is one float4.  group4_full says whether
-// all twenty values exist (only the last groups reach into the padding of
-// p4); load_group4 fetches the five slices and quantize_group4_loaded
-// quantizes them, stores back a slice only if one of its values has q != 0,
-// and returns the four bytes packed little-endian.  Split so a caller can
-// keep the loads of several groups in flight at once.
+// aligned (and x, with kX): every partition slice is one float4.
+// group4_full says whether all twenty values exist (only the last groups
+// reach into the padding of p4); load_group4 fetches the five slices (the
+// sums x + r with kX) and quantize_group4_loaded quantizes them, stores
+// back a slice if one of its values has q != 0 (every slice with kX), and
+// returns the four bytes packed little-endian.  Split so a caller can keep
+// the loads of several groups in flight at once.
 __device__ __forceinline__ bool group4_full(uint64_t n, uint64_t m, uint64_t j) {
   return 4 * m + j + 4 <= n;
 }
 
-__device__ __forceinline__ void load_group4(const float* __restrict__ r, uint64_t m,
+template <bool kX = false>
+__device__ __forceinline__ void load_group4(const float* __restrict__ x,
+                                            const float* __restrict__ r, uint64_t m,
                                             uint64_t j, float4 (&a)[5]) {
 #pragma unroll
   for (int k = 0; k < 5; ++k) a[k] = *reinterpret_cast<const float4*>(r + k * m + j);
+  if (kX) {
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const float4 b = *reinterpret_cast<const float4*>(x + k * m + j);
+      a[k] = make_float4(b.x + a[k].x, b.y + a[k].y, b.z + a[k].z, b.w + a[k].w);
+    }
+  }
 }
 
+template <bool kX = false>
 __device__ __forceinline__ uint32_t quantize_group4_loaded(float* __restrict__ r, uint64_t m,
                                                            uint64_t j, const float4 (&a)[5],
                                                            float M, float U) {
@@ -230,29 +245,33 @@ __device__ __forceinline__ uint32_t quantize_group4_loaded(float* __restrict__ r
     code[1] = code[1] * 3u + t1;
     code[2] = code[2] * 3u + t2;
     code[3] = code[3] * 3u + t3;
-    if ((t0 ^ 1u) | (t1 ^ 1u) | (t2 ^ 1u) | (t3 ^ 1u))
+    if (kX || ((t0 ^ 1u) | (t1 ^ 1u) | (t2 ^ 1u) | (t3 ^ 1u)))
       *reinterpret_cast<float4*>(r + k * m + j) = o;
   }
   return code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
 }
 
 // The group by single bytes (any group, including those in the padding).
-__device__ __forceinline__ uint32_t quantize_group4_bytes(float* __restrict__ r, uint64_t n,
+template <bool kX = false>
+__device__ __forceinline__ uint32_t quantize_group4_bytes(const float* __restrict__ x,
+                                                          float* __restrict__ r, uint64_t n,
                                                           uint64_t m, uint64_t j, float M,
                                                           float U) {
   uint32_t w = 0u;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) w |= quantize_byte(r, n, m, j + c, M, U) << (8 * c);
+  for (int c = 0; c < 4; ++c) w |= quantize_byte<kX>(x, r, n, m, j + c, M, U) << (8 * c);
   return w;
 }
 
-__device__ __forceinline__ uint32_t quantize_group4(float* __restrict__ r, uint64_t n,
+template <bool kX = false>
+__device__ __forceinline__ uint32_t quantize_group4(const float* __restrict__ x,
+                                                    float* __restrict__ r, uint64_t n,
                                                     uint64_t m, uint64_t j, float M,
                                                     float U) {
-  if (!group4_full(n, m, j)) return quantize_group4_bytes(r, n, m, j, M, U);
+  if (!group4_full(n, m, j)) return quantize_group4_bytes<kX>(x, r, n, m, j, M, U);
   float4 a[5];
-  load_group4(r, m, j, a);
-  return quantize_group4_loaded(r, m, j, a, M, U);
+  load_group4<kX>(x, r, m, j, a);
+  return quantize_group4_loaded<kX>(r, m, j, a, M, U);
 }
 
 // ---------------------------------------------------------------- stochastic mode

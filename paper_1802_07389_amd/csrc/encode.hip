@@ -264,7 +264,9 @@ __global__ __launch_bounds__(kThreads) void tlc_accum_absmax_batch_kernel(
 // multiple of 4) stores the bytes; partitions 1-4 add their weighted trits
 // with LDS atomics on the two words a cell straddles: a byte's total stays
 // below 243, so no carry crosses into the next byte.
-__device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uint64_t n,
+template <bool kX = false>
+__device__ __forceinline__ void quantize_tile_shifted(const float* __restrict__ x,
+                                                      float* __restrict__ r, uint64_t n,
                                                       uint64_t m, uint64_t q0, uint32_t T,
                                                       float M, float U, uint32_t* qw) {
   constexpr int kCells = (kEncTile + 6) / 4 / kThreads + 1;  // cells per lane, a <= 3
@@ -282,7 +284,13 @@ __device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uin
       const uint32_t f = threadIdx.x + kThreads * i;
       const uint64_t e = e0 + 4ull * f;
       full[i] = f < nf && 4u * f >= a && 4u * f + 4u <= T + a && e + 4u <= n;
-      if (full[i]) ra[i] = *reinterpret_cast<const float4*>(r + e);
+      if (full[i]) {
+        ra[i] = *reinterpret_cast<const float4*>(r + e);
+        if (kX) {
+          const float4 b = *reinterpret_cast<const float4*>(x + e);
+          ra[i] = make_float4(b.x + ra[i].x, b.y + ra[i].y, b.z + ra[i].z, b.w + ra[i].w);
+        }
+      }
     }
 #pragma unroll
     for (int i = 0; i < kCells; ++i) {
@@ -296,7 +304,7 @@ __device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uin
         t[1] = quantize_one(ra[i].y, M, U, o.y);
         t[2] = quantize_one(ra[i].z, M, U, o.z);
         t[3] = quantize_one(ra[i].w, M, U, o.w);
-        if ((t[0] ^ 1u) | (t[1] ^ 1u) | (t[2] ^ 1u) | (t[3] ^ 1u))
+        if (kX || ((t[0] ^ 1u) | (t[1] ^ 1u) | (t[2] ^ 1u) | (t[3] ^ 1u)))
           *reinterpret_cast<float4*>(r + e) = o;
       } else {
 #pragma unroll
@@ -304,8 +312,8 @@ __device__ __forceinline__ void quantize_tile_shifted(float* __restrict__ r, uin
           const uint32_t p = 4u * f + c;  // position in the partition's cell grid
           if (p >= a && p - a < T && e + c < n) {
             float o;
-            t[c] = quantize_one(r[e + c], M, U, o);
-            if (t[c] != 1u) r[e + c] = o;
+            t[c] = quantize_one(kX ? x[e + c] + r[e + c] : r[e + c], M, U, o);
+            if (kX || t[c] != 1u) r[e + c] = o;
           }
         }
       }
@@ -353,19 +361,20 @@ static_assert(kEncTile / kThreads == 16, "one uint4 of quartic bytes per thread"
 // aligned float4 cells of one partition at a time, or single bytes,
 // interleaved so every load and store instruction is coalesced.  Ends with
 // a barrier.
-template <int kPath>
-__device__ __forceinline__ void quantize_tile(float* __restrict__ r, uint64_t n, uint32_t m,
-                                              const Scale& sc, uint64_t q0,
-                                              uint32_t tile_bytes, uint8_t* q) {
+template <int kPath, bool kX = false>
+__device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float* __restrict__ r,
+                                              uint64_t n, uint32_t m, const Scale& sc,
+                                              uint64_t q0, uint32_t tile_bytes, uint8_t* q) {
   if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
     for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
       *reinterpret_cast<uint32_t*>(q + g * 4u) =
-          quantize_group4(r, n, m, q0 + g * 4u, sc.M, sc.U);
+          quantize_group4<kX>(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
   } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
-    quantize_tile_shifted(r, n, m, q0, tile_bytes, sc.M, sc.U, reinterpret_cast<uint32_t*>(q));
+    quantize_tile_shifted<kX>(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
+                              reinterpret_cast<uint32_t*>(q));
   } else {  // 1 byte per thread: dword accesses, still contiguous per wave
     for (uint32_t lj = threadIdx.x; lj < tile_bytes; lj += kThreads)
-      q[lj] = (uint8_t)quantize_byte(r, n, m, q0 + lj, sc.M, sc.U);
+      q[lj] = (uint8_t)quantize_byte<kX>(x, r, n, m, q0 + lj, sc.M, sc.U);
   }
   __syncthreads();
 }
@@ -378,8 +387,9 @@ __device__ __forceinline__ void quantize_tile(float* __restrict__ r, uint64_t n,
 // every thread zero-run encodes its bytes from its own prefix into LDS; the
 // block then copies the tile's output into the stream.  The last tile
 // stores the stream length in res->len.
-template <int kPath>
-__device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, uint32_t m, const Scale& sc,
+template <int kPath, bool kX>
+__device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* __restrict__ r,
+                                            uint64_t n, uint32_t m, const Scale& sc,
                                             uint32_t lt, uint32_t floor,
                                             uint8_t* __restrict__ out,
                                             uint64_t* __restrict__ status, uint32_t epoch,
@@ -391,7 +401,7 @@ __device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, u
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
   const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
-  quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
+  quantize_tile<kPath, kX>(x, r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- phase 2: Section 3.3
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
@@ -474,7 +484,7 @@ __device__ __forceinline__ void encode_tile(float* __restrict__ r, uint64_t n, u
 //   pass B (tlc_zre_chunk_kernel, tlc_zre_chunk_scan_kernel): every tile's
 //     prefix within its chunk of 64 tiles and the chunk summaries, then one
 //     block scans the chunk summaries.
-//   pass C (tlc_zre_compact_kernel, one block per tile): the tile's prefix
+//   pass C (tlc_zre_compact_kernel, one wave per tile): the tile's prefix
 //     (its output offset and incoming run phase) from its chunk's prefix
 //     and its own within the chunk, then the leading run's codes, which
 //     need the incoming phase (one 255 per 14th byte of the grown run, then
@@ -633,7 +643,7 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
       qw[g] = group4_full(n, m, j)
                   ? (uint32_t)code[it][0] | ((uint32_t)code[it][1] << 8) |
                         ((uint32_t)code[it][2] << 16) | ((uint32_t)code[it][3] << 24)
-                  : quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
+                  : quantize_group4_bytes(nullptr, r, n, m, j, sc.M, sc.U);
     }
   } else {
 #pragma unroll
@@ -642,7 +652,7 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
       if (g * 4u >= tile_bytes) break;
       const uint64_t j = q0 + g * 4u;
       if (!group4_full(n, m, j)) {
-        qw[g] = quantize_group4_bytes(r, n, m, j, sc.M, sc.U);
+        qw[g] = quantize_group4_bytes(nullptr, r, n, m, j, sc.M, sc.U);
         continue;
       }
       float4 a[5];
@@ -652,7 +662,7 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
           a[k] = (need >> (5 * it + k)) & 1u ? *reinterpret_cast<const float4*>(r + (uint64_t)k * m + j)
                                              : make_float4(0.f, 0.f, 0.f, 0.f);
       } else {
-        load_group4(r, m, j, a);
+        load_group4(nullptr, r, m, j, a);
       }
       uint32_t code[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -790,7 +800,7 @@ void tlc_quant_encode_kernel(
       quantize_tile_vec_deferred<false>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
                                         &sh.nneed, fix + (uint64_t)t * kFixCap, h);
   } else {
-    quantize_tile<kPath>(r, n, m, sc, q0, tile_bytes, sh.q);
+    quantize_tile<kPath>(nullptr, r, n, m, sc, q0, tile_bytes, sh.q);
   }
 
   // ---- Section 3.3 from the tile's first non-121 byte on, from the gaps
@@ -911,19 +921,21 @@ __global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
   }
 }
 
-// Pass C: one block per tile.  Prefix = the chunk's prefix combined with
-// the tile's prefix within its chunk; then the leading run's codes and the
-// slot; the last tile also writes the remainder of a run that ends the
-// stream and the stream length.  Every write is clamped to the m-byte
-// output (the stream never exceeds m bytes; the clamp only contains a logic
-// error).
+// Pass C, the compaction: one wave per tile.  Prefix = the chunk's prefix
+// combined with the tile's prefix within the chunk; then the leading run's
+// codes and the slot; the last tile also writes the remainder of a run that
+// ends the stream and the stream length.  Every write is clamped to
+// the m-byte output (the stream never exceeds m bytes; the clamp only
+// contains a logic error).
 __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
     const TileRec* __restrict__ recs, const uint64_t* __restrict__ chunk_pre,
     const uint64_t* __restrict__ local_pre, const uint8_t* __restrict__ slots, uint32_t m,
-    uint8_t* __restrict__ out, const uint2* __restrict__ fix, float* __restrict__ r, uint64_t n,
-    Ctrl* __restrict__ ctrl) {
+    uint32_t ntiles, uint8_t* __restrict__ out, const uint2* __restrict__ fix,
+    float* __restrict__ r, uint64_t n, Ctrl* __restrict__ ctrl) {
   if (ctrl->enc.err) return;
-  const uint32_t t = blockIdx.x;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t t = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (t >= ntiles) return;  // whole waves; nothing below synchronises the block
   RunSum cp, lp;
   cp.v = chunk_pre[t / kChunkTiles];
   lp.v = local_pre[t];
@@ -936,25 +948,30 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
   const uint32_t n255 = grown / kRunMax, rho = grown % kRunMax;
   const bool rest = rec.lead < tile_bytes;
   const uint32_t code = (rest && rho) ? 1u : 0u;
-  for (uint32_t i = threadIdx.x; i < n255; i += kThreads)
+  for (uint32_t i = lane; i < n255; i += 64u)
     if (off + i < m) out[off + i] = (uint8_t)kFullChunk;
-  if (code && threadIdx.x == 0 && off + n255 < m) out[off + n255] = (uint8_t)rs_code(rho);
+  if (code && lane == 0 && off + n255 < m) out[off + n255] = (uint8_t)rs_code(rho);
   if (rest) {
     const uint32_t at = off + n255 + code;
     const uint32_t len = min<uint32_t>(rec.len, tile_bytes);
-    for (uint32_t i = threadIdx.x; i < len; i += kThreads)
-      if (at + i < m) out[at + i] = slots[q0 + i];
+    // dword loads from the slot (4096-byte aligned, len <= 4096), byte stores
+    for (uint32_t i = 4u * lane; i < len; i += 256u) {
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(slots + q0 + i);
+#pragma unroll
+      for (uint32_t b = 0; b < 4u; ++b)
+        if (i + b < len && at + i + b < m) out[at + i + b] = (uint8_t)(w >> (8u * b));
+    }
   }
   // the residuals the first pass left in the tile's fix list
   const uint2* tf = fix + (uint64_t)t * kFixCap;
   const uint32_t nf = min<uint32_t>(rec.nfix, kFixCap);
-  for (uint32_t i = threadIdx.x; i < nf; i += kThreads) {
+  for (uint32_t i = lane; i < nf; i += 64u) {
     const uint2 f = tf[i];
     const uint32_t k = f.x / (uint32_t)kEncTile, p = f.x % (uint32_t)kEncTile;
     const uint64_t e = (uint64_t)k * m + q0 + p;
     if (k < 5u && p < tile_bytes && e < n) r[e] = __uint_as_float(f.y);
   }
-  if (t + 1 == gridDim.x && threadIdx.x == 0) {  // a run that ends the stream; the length
+  if (t + 1 == ntiles && lane == 0) {  // a run that ends the stream; the length
     RunSum a;
     a.v = rec.agg;
     const RunSum T = rs_combine(P, a);
@@ -968,9 +985,12 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
 // A small tensor in one pass: tiles taken in order from the ticket and
 // chained by decoupled look-back (status slot = tile).  With few tiles the
 // look-back rarely waits, and this saves the two small passes' launches.
-template <int kPath>
+// kX (the default error policy): partials are the check pass's, the buffer
+// still holds the previous residual, and the tiles form acc = x + r
+// themselves (no writing max pass before them).
+template <int kPath, bool kX>
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
-    float* __restrict__ r, uint64_t n, uint32_t m, float s,
+    const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
     Ctrl* __restrict__ ctrl) {
@@ -983,10 +1003,13 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
   }
-  if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
-  encode_tile<kPath>(r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+  if (sc.bad) return;  // NaN/Inf or overflow: no stream (the buffer as it was, or acc)
+  encode_tile<kPath, kX>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
 }
 
+// kX as for the chained kernel (partials: the check pass's).  The float4
+// paths need x aligned like r (vec bit 2) when kX.
+template <bool kX>
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
     const EncDesc* __restrict__ descs, uint32_t count, const uint32_t* __restrict__ partials,
     EncResult* __restrict__ results, uint64_t* __restrict__ status, uint32_t ticket_base,
@@ -1006,15 +1029,16 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
     if (sc.bad) results[t].len = 0u;
   }
   if (sc.bad) return;  // this tensor is refused; the others go on
-  if (d.vec & 1u)
-    encode_tile<kPathVec>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                          &results[t], sh);
-  else if (d.vec & 2u)
-    encode_tile<kPathShift>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                            &results[t], sh);
+  const bool xal = !kX || (d.vec & 4u);
+  if ((d.vec & 1u) && xal)
+    encode_tile<kPathVec, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
+                              &results[t], sh);
+  else if ((d.vec & 2u) && xal)
+    encode_tile<kPathShift, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch,
+                                ctrl, &results[t], sh);
   else
-    encode_tile<kPathByte>(d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                           &results[t], sh);
+    encode_tile<kPathByte, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch,
+                               ctrl, &results[t], sh);
 }
 
 // ---------------------------------------------------------------- comparison modes
@@ -1044,7 +1068,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
       const uint64_t j = q0 + g * 4u;
       uint32_t w;
       if (!kStoch) {
-        w = quantize_group4(r, n, m, j, sc.M, sc.U);
+        w = quantize_group4(nullptr, r, n, m, j, sc.M, sc.U);
       } else {
         uint32_t code[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -1074,7 +1098,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
       const uint64_t j = q0 + lj;
       uint32_t code;
       if (!kStoch) {
-        code = quantize_byte(r, n, m, j, sc.M, sc.U);
+        code = quantize_byte(nullptr, r, n, m, j, sc.M, sc.U);
       } else {
         code = 0u;
 #pragma unroll
@@ -1149,36 +1173,41 @@ hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                Ctrl* ctrl, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
+#define TLC_ARGS r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl
   if (trit) {
     if (!summ) return hipErrorInvalidValue;
-    tlc_quant_encode_kernel<kPathVec, true><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
-  } else if (al && m % 4 == 0)
-    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl);
-  else if (al)
-    tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, nullptr, ctrl);
-  else
-    tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, slots, recs, fix, nullptr, ctrl);
+    tlc_quant_encode_kernel<kPathVec, true><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+  } else if (al && m % 4 == 0) {
+    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+  } else {
+    summ = nullptr;  // bounds serve the float4 slices only
+    if (al)
+      tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+    else
+      tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+  }
+#undef TLC_ARGS
   return hipGetLastError();
 }
 
-hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
-                                       const uint32_t* partials, uint32_t npartials, uint8_t* out,
-                                       uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                                       uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  const bool al = aligned16(r);
-  if (al && m % 4 == 0)
-    tlc_quant_encode_chained_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
-  else if (al)
-    tlc_quant_encode_chained_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
-  else
-    tlc_quant_encode_chained_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(
-        r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl);
+hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m,
+                                       float s, const uint32_t* partials, uint32_t npartials,
+                                       uint8_t* out, uint64_t* status, uint32_t ntiles,
+                                       uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
+                                       hipStream_t st) {
+  const bool fused = x != nullptr;
+  const bool al = aligned16(r) && (!fused || aligned16(x));
+#define TLC_LAUNCH(P, X)                                                                    \
+  tlc_quant_encode_chained_kernel<P, X><<<ntiles, kThreads, 0, st>>>(                        \
+      x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl)
+  if (al && m % 4 == 0) {
+    if (fused) TLC_LAUNCH(kPathVec, true); else TLC_LAUNCH(kPathVec, false);
+  } else if (al) {
+    if (fused) TLC_LAUNCH(kPathShift, true); else TLC_LAUNCH(kPathShift, false);
+  } else {
+    if (fused) TLC_LAUNCH(kPathByte, true); else TLC_LAUNCH(kPathByte, false);
+  }
+#undef TLC_LAUNCH
   return hipGetLastError();
 }
 
@@ -1198,8 +1227,8 @@ hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
                               hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
-  tlc_zre_compact_kernel<<<ntiles, kThreads, 0, st>>>(recs, chunk_pre, local_pre, slots, m, out,
-                                                      fix, r, n, ctrl);
+  tlc_zre_compact_kernel<<<(ntiles + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+      recs, chunk_pre, local_pre, slots, m, ntiles, out, fix, r, n, ctrl);
   return hipGetLastError();
 }
 
@@ -1219,11 +1248,15 @@ hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
 
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
-                                     EncResult* results, uint64_t* status,
+                                     bool fused, EncResult* results, uint64_t* status,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
                                      hipStream_t st) {
-  tlc_quant_encode_batch_kernel<<<total_tiles, kThreads, 0, st>>>(
-      descs, count, partials, results, status, ticket_base, epoch, ctrl);
+  if (fused)
+    tlc_quant_encode_batch_kernel<true><<<total_tiles, kThreads, 0, st>>>(
+        descs, count, partials, results, status, ticket_base, epoch, ctrl);
+  else
+    tlc_quant_encode_batch_kernel<false><<<total_tiles, kThreads, 0, st>>>(
+        descs, count, partials, results, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
 

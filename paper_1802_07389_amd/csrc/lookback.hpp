@@ -45,7 +45,19 @@ struct StatusWord {
 // The payload lives inside the status word, so no other memory has to be
 // made visible with it: relaxed agent-scope atomics are enough and avoid the
 // L2 write-back / invalidate that release / acquire imply on gfx950.
+//
+// Built with TLC_DELAY_INJECT (the stress build of the look-back scans
+// only, never the product library), every publish first sleeps for a
+// pseudo-random 0 to 7 times 127 * 64 clocks (up to about 25 us), a
+// function of the word's address and contents: tiles then publish in a
+// scrambled order and their successors see every mix of missing,
+// aggregate and prefix words.
 __device__ __forceinline__ void status_publish(uint64_t* p, uint64_t w) {
+#ifdef TLC_DELAY_INJECT
+  uint64_t h = (reinterpret_cast<uintptr_t>(p) ^ (w * 0x9E3779B97F4A7C15ull)) + 0x632BE59BD9B4E019ull;
+  h = (h ^ (h >> 31)) * 0xD6E8FEB86659FD93ull;
+  for (uint32_t d = (uint32_t)(h >> 61); d > 0u; --d) __builtin_amdgcn_s_sleep(127);
+#endif
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 

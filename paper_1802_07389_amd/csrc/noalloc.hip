@@ -1,9 +1,9 @@
 // noalloc.hip -- tlc_compress_noalloc: the encode of tlc_compress for
 // callers that cannot allocate device memory (graph capture, serving
 // loops, harnesses that forbid hipMalloc).  It runs the kernels of the
-// small-tensor path (check pass, writing max pass, chained quantize +
-// quartic pack + zero-run encode; Sections 3.1-3.3) with their scratch in
-// a file-scope device array instead of a context's workspace.
+// small-tensor path (check pass, then the chained pass that accumulates,
+// quantizes, packs and zero-run encodes; Sections 3.1-3.3) with their
+// scratch in a file-scope device array instead of a context's workspace.
 #include <mutex>
 
 #include "tlc.h"
@@ -15,8 +15,9 @@ namespace tlc {
 namespace {
 
 // Scratch layout: the control block (tile ticket, encode result, fault
-// flag), the check pass's and the writing pass's partial maxima (at most
-// kAbsmaxMaxBlocks each), then one look-back status word per encoder tile
+// flag), the check pass's partial maxima (at most kAbsmaxMaxBlocks; the
+// next kAbsmaxMaxBlocks words are spare), then one look-back status word
+// per encoder tile
 // (n <= TLC_NOALLOC_MAX_N gives at most 410 tiles, all on the chained
 // path) and two spare words.
 constexpr uint32_t kNoallocMaxTiles =
@@ -115,7 +116,6 @@ TLC_API int tlc_compress_noalloc(const float* tensor, float* residual, size_t n,
   uint8_t* scr = g_scratch[dev];
   Ctrl* ctrl = reinterpret_cast<Ctrl*>(scr);
   uint32_t* partials_chk = reinterpret_cast<uint32_t*>(scr + kOffPartialsChk);
-  uint32_t* partials = reinterpret_cast<uint32_t*>(scr + kOffPartials);
   uint64_t* status = reinterpret_cast<uint64_t*>(scr + kOffStatus);
   hipStream_t st = (hipStream_t)hip_stream;
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);  // <= kNoallocMaxTiles
@@ -123,14 +123,11 @@ TLC_API int tlc_compress_noalloc(const float* tensor, float* residual, size_t n,
   tlc_noalloc_begin_kernel<<<1, kThreads, 0, st>>>(scr, ntiles + 2u, result);
   e = hipGetLastError();
   if (e == hipSuccess && n) {
-    uint32_t np_chk = 0, np = 0;
-    e = launch_absmax_check(tensor, residual, n, partials_chk, &np_chk, st);
+    uint32_t np = 0;
+    e = launch_absmax_check(tensor, residual, n, partials_chk, &np, st);
     if (e == hipSuccess)
-      e = launch_accum_absmax(tensor, residual, n, partials, &np, nullptr, partials_chk, np_chk,
-                              s, false, st);
-    if (e == hipSuccess)
-      e = launch_quant_encode_chained(residual, n, (uint32_t)m, s, partials, np, bytes, status,
-                                      ntiles, 0u, 1u, ctrl, st);
+      e = launch_quant_encode_chained(tensor, residual, n, (uint32_t)m, s, partials_chk, np,
+                                      bytes, status, ntiles, 0u, 1u, ctrl, st);
     if (e == hipSuccess) {
       tlc_noalloc_end_kernel<<<1, 64, 0, st>>>(scr, result);
       e = hipGetLastError();

@@ -349,10 +349,10 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   const size_t mm = max_n / 5 + max_tensors;
   c->partials_cap =
       std::max<size_t>(kAbsmaxMaxBlocks, max_n / ((size_t)kThreads * 4) + max_tensors + 1);
+  const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
   c->enc_status_words = mm / kEncTile + max_tensors + 2;
   c->dec_status_words = mm / kZreBatchTile + max_tensors + 2;  // the smaller tile
   c->start_words = mm / kDecRange + max_tensors + 2;
-  const size_t tiles1 = ceil_div(quartic_len(max_n), (size_t)kEncTile);  // one tensor
   // layout: ctrl | enc results | partials | check partials | enc status | dec status |
   //         start | enc descs | dec descs | tile records | chunk summaries |
   //         tile prefixes in their chunks | fix lists | float4 summaries | slots
@@ -545,24 +545,37 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
                     (m % 4 == 0 || !in_place))
                        ? c->summ
                        : nullptr;
-  uint32_t np = 0;
-  bool trit = false;
-  st = launch_max_passes(c, tensor, residual, n, s, summ, &np, &trit);
-  if (st) return st;
   if (ntiles < kThreePassMinTiles) {  // small tensor: one chained pass
+    // default policy: the check pass, then the chained tiles form acc = x + r
+    // themselves; in place: step 1 into the buffer first, as for large tensors
+    uint32_t np = 0;
+    const uint32_t* partials = c->partials;
+    if (in_place) {
+      st = launch_max_passes(c, tensor, residual, n, s, nullptr, &np);
+    } else {
+      partials = c->partials_chk;
+      st = timed_launch(c, TLC_KERNEL_ABSMAX_CHECK, [&] {
+        return launch_absmax_check(tensor, residual, n, c->partials_chk, &np, c->stream);
+      });
+    }
+    if (st) return st;
     uint32_t epoch = 0;
     st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, nullptr,
-                  &epoch);
+                    &epoch);
     if (st) return st;
     st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_CHAINED, [&] {
-      return launch_quant_encode_chained(residual, n, (uint32_t)m, s, c->partials, np, bytes,
-                                         c->enc_status, ntiles, c->enc_ticket_base, epoch,
-                                         c->ctrl, c->stream);
+      return launch_quant_encode_chained(in_place ? nullptr : tensor, residual, n, (uint32_t)m,
+                                         s, partials, np, bytes, c->enc_status, ntiles,
+                                         c->enc_ticket_base, epoch, c->ctrl, c->stream);
     });
     if (st) return st;
     c->enc_ticket_base += ntiles;
     return finish_compress(c, "tlc_compress", bytes_len, scale);
   }
+  uint32_t np = 0;
+  bool trit = false;
+  st = launch_max_passes(c, tensor, residual, n, s, summ, &np, &trit);
+  if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
                                c->fix, summ, trit, c->ctrl, c->stream);
@@ -760,26 +773,30 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
   if (st) return st;
+  // default policy: the check pass, then every tile forms acc = x + r itself
+  // from its tensor (no writing max pass); in place: step 1 into the buffers
+  // with the partial maxima of the sums, then the tiles quantize the buffers
   const bool check = !(c->options & TLC_OPT_IN_PLACE_FEEDBACK);
-  if (check) {  // the default error policy: see launch_max_passes
+  if (check) {
     st = timed_launch(c, TLC_KERNEL_ABSMAX_CHECK_BATCH, [&] {
       return launch_absmax_check_batch(c->enc_descs, cnt, blocks, c->partials_chk, c->stream);
     });
-    if (st) return st;
+  } else {
+    st = timed_launch(c, TLC_KERNEL_ABSMAX_BATCH, [&] {
+      return launch_accum_absmax_batch(c->enc_descs, cnt, blocks, c->partials, nullptr,
+                                       c->stream);
+    });
   }
-  st = timed_launch(c, TLC_KERNEL_ABSMAX_BATCH, [&] {
-    return launch_accum_absmax_batch(c->enc_descs, cnt, blocks, c->partials,
-                                     check ? c->partials_chk : nullptr, c->stream);
-  });
   if (st) return st;
   uint32_t epoch = 0;
   st = next_epoch(c, &c->enc_epoch, kEncEpochMax, c->enc_status, c->enc_status_words, nullptr,
                   &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_BATCH, [&] {
-    return launch_quant_encode_batch(c->enc_descs, cnt, tiles, c->partials, c->enc_results,
-                                     c->enc_status, c->enc_ticket_base, epoch, c->ctrl,
-                                     c->stream);
+    return launch_quant_encode_batch(c->enc_descs, cnt, tiles,
+                                     check ? c->partials_chk : c->partials, check,
+                                     c->enc_results, c->enc_status, c->enc_ticket_base, epoch,
+                                     c->ctrl, c->stream);
   });
   if (st) return st;
   c->enc_ticket_base += tiles;

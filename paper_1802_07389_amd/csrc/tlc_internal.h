@@ -124,10 +124,13 @@ hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, uint2* fix, const uint16_t* summ, bool trit,
                                Ctrl* ctrl, hipStream_t st);
-hipError_t launch_quant_encode_chained(float* r, uint64_t n, uint32_t m, float s,
-                                       const uint32_t* partials, uint32_t npartials, uint8_t* out,
-                                       uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                                       uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+// x != NULL: the tiles form acc = x + r themselves from the check pass's
+// partials (r still holds the previous residual); x == NULL: r holds acc.
+hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m,
+                                       float s, const uint32_t* partials, uint32_t npartials,
+                                       uint8_t* out, uint64_t* status, uint32_t ntiles,
+                                       uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
+                                       hipStream_t st);
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
                              uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
@@ -148,9 +151,10 @@ hipError_t launch_absmax_check_batch(const EncDesc* descs, uint32_t count,
 hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_blocks, uint32_t* partials,
                                      const uint32_t* guard, hipStream_t st);
+// fused: as x != NULL for the chained encoder (partials: the check pass's).
 hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
-                                     EncResult* results, uint64_t* status,
+                                     bool fused, EncResult* results, uint64_t* status,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
                                      hipStream_t st);
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,

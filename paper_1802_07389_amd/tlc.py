@@ -12,7 +12,9 @@ import os
 import torch  # load torch's HIP runtime first so libtlc binds to the same one
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtlc.so")
+# TLC_LIBRARY may name another build of this same library (the look-back
+# stress build libtlc_delay.so, which the stress test loads this way).
+LIB_PATH = os.environ.get("TLC_LIBRARY") or os.path.join(_HERE, "libtlc.so")
 
 TLC_OK = 0
 TLC_E_INVALID = -1

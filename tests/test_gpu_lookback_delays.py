@@ -1,0 +1,143 @@
+"""The look-back scans under scrambled publish order: the stress build of
+the library (libtlc_delay.so, compiled with TLC_DELAY_INJECT) sleeps a
+pseudo-random 0 to about 25 us before every status-word publish.  Each
+user of the status words runs here once against the CPU oracle, bit for
+bit: the chained single-tensor encoder, the three-pass encoder's
+tile-prefix scan, the batched encoder, and the decoder's index scan
+(single, batched and summed decodes).  Every wait is bounded; a timeout
+would surface as TLC_E_DEVICE, not a hang."""
+import importlib.util
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_07389_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PKG = os.path.join(ROOT, "paper_1802_07389_amd")
+
+
+def bits(a):
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+@pytest.fixture(scope="module")
+def dt():
+    """A second instance of the binding, bound to the stress build."""
+    path = os.path.join(PKG, "libtlc_delay.so")
+    assert os.path.exists(path), "libtlc_delay.so is not built: run __graft_entry__.build()"
+    old = os.environ.get("TLC_LIBRARY")
+    os.environ["TLC_LIBRARY"] = path
+    try:
+        spec = importlib.util.spec_from_file_location("tlc_delay", os.path.join(PKG, "tlc.py"))
+        mod = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(mod)
+    finally:
+        if old is None:
+            del os.environ["TLC_LIBRARY"]
+        else:
+            os.environ["TLC_LIBRARY"] = old
+    assert mod.LIB_PATH == path
+    return mod
+
+
+@pytest.fixture(scope="module")
+def ctx(dt):
+    c = dt.Context(max_n=(1 << 25) + 64, max_tensors=400)
+    yield c
+    c.close()
+
+
+def encode_check(ctx, x, r, s, tag):
+    import torch
+    xd = torch.from_numpy(x).cuda()
+    rd = torch.from_numpy(r.copy()).cuda()
+    C, M = ctx.compress(xd, rd, s)
+    r_ref = r.copy()
+    st, C_ref, M_ref = oracle.compress(x, r_ref, s)
+    assert st == 0 and M == M_ref, tag
+    assert np.array_equal(C.cpu().numpy(), C_ref), tag
+    assert np.array_equal(bits(rd.cpu().numpy()), bits(r_ref)), tag
+    print(f"{tag}: {C_ref.size} bytes ok", flush=True)
+    return C_ref, M_ref
+
+
+def test_chained_and_three_pass_encoders(dt, ctx):
+    # 400 tiles on the chained path (tile tickets + decoupled look-back)
+    n = 400 * 4096 * 5 - 3
+    encode_check(ctx, workloads.normal([91, 0], n, 1e-3), workloads.normal([91, 1], n, 1e-4),
+                 1.0, "chained, 400 tiles")
+    # 1639 tiles on the three-pass path (the last blocks' tile-prefix scan),
+    # the trit path and the in-place bounds path
+    n = (1 << 25) + 7
+    x = workloads.runs_tensor([91, 2], n)
+    encode_check(ctx, x, np.zeros(n, F32), 1.5, "three-pass, 1639 tiles")
+    n = 1 << 25
+    encode_check(ctx, workloads.normal([91, 3], n, 1e-3), workloads.normal([91, 4], n, 1e-4),
+                 1.0, "three-pass trit path")
+    ctx.set_options(dt.TLC_OPT_IN_PLACE_FEEDBACK)  # bounds and residual lists
+    try:
+        encode_check(ctx, workloads.normal([91, 5], n, 1e-3), workloads.normal([91, 6], n, 1e-4),
+                     1.0, "three-pass in place")
+    finally:
+        ctx.set_options(0)
+
+
+def test_batched_encoder(ctx):
+    import torch
+    sizes = workloads.c2_sizes()
+    xs = [workloads.c2_gradient(0, t, n) for t, n in enumerate(sizes)]
+    rs = [workloads.normal([92, t], n, 1e-5) for t, n in enumerate(sizes)]
+    rd = [torch.from_numpy(r.copy()).cuda() for r in rs]
+    pays = ctx.compress_batch([torch.from_numpy(x).cuda() for x in xs], rd, 1.75)
+    for t, (x, r) in enumerate(zip(xs, rs)):
+        st, C_ref, M_ref = oracle.compress(x, r, 1.75)
+        assert st == 0 and pays[t][1] == M_ref, t
+        assert np.array_equal(pays[t][0].cpu().numpy(), C_ref), t
+        assert np.array_equal(bits(rd[t].cpu().numpy()), bits(r)), t
+    print("batched encoder, 335 tensors ok", flush=True)
+
+
+def test_decoder_index_scans(ctx):
+    """Streams of synthetic quartic bytes with half of them data bytes, so
+    each stream spans about 80 index tiles of the single decode (160 of the
+    batched one); single, batched and summed decodes with accumulate."""
+    import torch
+    n = (1 << 23) + 3
+    m = oracle.quartic_len(n)
+    streams = []
+    for k in range(3):
+        rng = np.random.default_rng([93, k])
+        Q = np.full(m, 121, np.uint8)
+        hit = rng.random(m) < 0.5
+        Q[hit] = rng.integers(0, 243, int(hit.sum()), dtype=np.uint8)
+        streams.append((oracle.zre_encode(Q), F32(1e-3 * (k + 1))))
+    out0 = workloads.normal([94, 0], n, 1e-3)
+    for C, M in streams:
+        od = torch.from_numpy(out0.copy()).cuda()
+        ctx.decompress(torch.from_numpy(C).cuda(), M, n, od, accumulate=True)
+        ctx.sync()
+        st, ref = oracle.decompress(C, M, n, out0.copy(), True)
+        assert st == 0 and np.array_equal(bits(od.cpu().numpy()), bits(ref))
+    print(f"single decodes ok ({streams[0][0].size} stream bytes each)", flush=True)
+    outs = [torch.from_numpy(out0.copy()).cuda() for _ in streams]
+    ctx.decompress_batch([torch.from_numpy(C).cuda() for C, _ in streams],
+                         [M for _, M in streams], outs, accumulate=True)
+    ctx.sync()
+    for (C, M), o in zip(streams, outs):
+        st, ref = oracle.decompress(C, M, n, out0.copy(), True)
+        assert np.array_equal(bits(o.cpu().numpy()), bits(ref))
+    total = torch.from_numpy(out0.copy()).cuda()
+    ctx.decompress_sum([torch.from_numpy(C).cuda() for C, _ in streams],
+                       [M for _, M in streams], total, accumulate=True)
+    ctx.sync()
+    ref = out0.copy()
+    for C, M in streams:
+        st, ref = oracle.decompress(C, M, n, ref, True)
+    assert np.array_equal(bits(total.cpu().numpy()), bits(ref))
+    print("batched and summed decodes ok", flush=True)

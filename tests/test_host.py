@@ -75,7 +75,7 @@ def test_host_only_entry_points():
     csrc = os.path.join(ROOT, "paper_1802_07389_amd", "csrc")
     src = "".join(open(os.path.join(csrc, f)).read() for f in os.listdir(csrc)
                   if f.endswith(".hip"))
-    for name in names:
+    for name in filter(None, names):
         assert re.search(r"__global__[^;{]*\b" + name + r"\s*\(", src, flags=re.S), name
 
 
