@@ -25,15 +25,20 @@ _lib = None
 
 
 def lib():
-    """Load (building first if needed) the oracle shared library."""
+    """Load (building first if needed) the oracle shared library.
+    TLC_REF_LIBRARY may name a build of a changed copy of tlc_ref.c: the
+    mutation test plants mistakes that way and runs the pins against them."""
     global _lib
     if _lib is not None:
         return _lib
-    src = os.path.join(_build.HERE, "tlc_ref.c")
-    if (not os.path.exists(_build.LIB)
-            or os.path.getmtime(_build.LIB) < os.path.getmtime(src)):
-        _build.build()
-    L = ctypes.CDLL(_build.LIB)
+    path = os.environ.get("TLC_REF_LIBRARY")
+    if not path:
+        path = _build.LIB
+        src = os.path.join(_build.HERE, "tlc_ref.c")
+        if (not os.path.exists(_build.LIB)
+                or os.path.getmtime(_build.LIB) < os.path.getmtime(src)):
+            _build.build()
+    L = ctypes.CDLL(path)
     c_sz, c_f, c_i = ctypes.c_size_t, ctypes.c_float, ctypes.c_int
     vp = ctypes.c_void_p
     L.tlc_ref_quartic_len.argtypes = [c_sz]
