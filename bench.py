@@ -182,6 +182,9 @@ def config_rows(torch, tlc, workloads, dev, parts=PARTS):
     4-byte scale).  GPU encode times include the host synchronisation of
     tlc_compress (it returns the stream length).  The oracle runs on one
     pinned host core."""
+    import ctypes
+
+    import oracle
     try:
         os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
     except (AttributeError, OSError):
@@ -223,7 +226,6 @@ def config_rows(torch, tlc, workloads, dev, parts=PARTS):
     # max as its scale; 8-bit codes spanning all 255 levels); "No ZRE" is 3LC
     # itself without the zero-run stage, at C4's s.
     if "modes" in parts:
-        import oracle
         xh = workloads.c4_tensor(0)
         x = torch.from_numpy(xh).to(dev)
         r = torch.zeros_like(x)
@@ -284,7 +286,6 @@ def config_rows(torch, tlc, workloads, dev, parts=PARTS):
     # pointer arrays are built once (a training loop keeps its gradient and
     # residual buffers), so the timed region is the library calls.
     if "C2" in parts:
-        import ctypes
         sizes = workloads.c2_sizes()
         T = len(sizes)
         bctx = tlc.Context(max_n=sum(sizes), stream=stream, device=dev, max_tensors=T)
@@ -337,7 +338,6 @@ def config_rows(torch, tlc, workloads, dev, parts=PARTS):
             kms[tlc.tlc_kernel_name(kid)] = round(ms / max(cnt, 1) * 1e3, 1)
         bctx.close()
         # oracle: the same 10 steps tensor by tensor on one core
-        import oracle
         r_h = [np.zeros(n, np.float32) for n in sizes]
         ote = otd = 0.0
         nb_bn = 0
