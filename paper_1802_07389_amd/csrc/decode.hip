@@ -159,54 +159,79 @@ __device__ __forceinline__ uint32_t range_end(const uint64_t* __restrict__ start
   return c;
 }
 
-// Expands quartic bytes [k*kDecRange, k*kDecRange + qn) of one stream into
-// s_q.  The stream bytes covering the range (found through the start
-// entries) are spread over the threads; a block scan of their expansion
-// lengths gives each one its position and each thread writes its own
-// expansions.  The same scan counts the slice's data bytes other than 121
-// (packed as length + (count << 16): a slice expands to fewer than
-// kDecRange + 28 bytes and holds at most kDecRange bytes, so no carry
-// crosses), which is returned.  Ends with a barrier.
-__device__ __forceinline__ uint32_t expand_range(const uint8_t* __restrict__ C, uint32_t c,
-                                             const uint64_t* __restrict__ starts, uint32_t k,
-                                             uint64_t m, uint32_t qn, uint8_t* s_q,
-                                             uint32_t* red) {
-  constexpr int kBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
+// The stream bytes that expand into range k of one stream: the first one,
+// how far into its expansion the range starts, and how many (at most
+// kDecRange: the range's qn quartic bytes come from at most qn stream bytes).
+struct Slice {
+  uint32_t i0, skip, count;
+};
+
+__device__ __forceinline__ Slice slice_of(const uint64_t* __restrict__ starts, uint32_t k,
+                                          uint64_t m, uint32_t c) {
   const uint64_t s0 = starts[k];
-  const uint32_t i0 = (uint32_t)(s0 >> 8);
-  const uint32_t skip = (uint32_t)(s0 & 255u);
+  Slice r;
+  r.i0 = (uint32_t)(s0 >> 8);
+  r.skip = (uint32_t)(s0 & 255u);
   const uint32_t i1 = range_end(starts, k, m, c);
-  const uint32_t count = i1 > i0 ? min<uint32_t>(i1 - i0, kDecRange) : 0u;
-  const uint32_t lo = threadIdx.x * kBytes;
-  const uint32_t cnt = lo < count ? min<uint32_t>(kBytes, count - lo) : 0u;
-  uint8_t b[kBytes];
-#pragma unroll
-  for (int i = 0; i < kBytes; ++i) b[i] = (uint32_t)i < cnt ? C[i0 + lo + i] : (uint8_t)0;
+  r.count = i1 > r.i0 ? min<uint32_t>(i1 - r.i0, kDecRange) : 0u;
+  return r;
+}
+
+constexpr int kSliceBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
+
+// Expands a slice into s_q, the range's quartic bytes [0, qn): the thread
+// holds slice bytes lo .. lo + cnt - 1 (lo = threadIdx.x * kSliceBytes),
+// byte(i) giving byte lo + i.  Every run code expands to bytes of 121, so
+// the range is first filled with 121 (one 16-byte store per thread, before
+// the scan's barrier) and only the data bytes other than 121 are written,
+// each at the position a block scan of the expansion lengths gives it: the
+// work no longer follows the length of the runs a thread holds.  The same
+// scan counts those data bytes (packed as length + (count << 16): a slice
+// expands to fewer than kDecRange + 28 bytes and holds at most kDecRange
+// bytes, so no carry crosses), which is returned.  Ends with a barrier.
+static_assert(kDecRange == 16 * kThreads, "the fill of s_q is one uint4 per thread");
+template <class ByteAt>
+__device__ __forceinline__ uint32_t expand_slice(ByteAt byte, uint32_t cnt, uint32_t skip,
+                                                 uint32_t qn, uint8_t* s_q, uint32_t* red) {
+  reinterpret_cast<uint4*>(s_q)[threadIdx.x] =
+      make_uint4(0x79797979u, 0x79797979u, 0x79797979u, 0x79797979u);
   uint32_t sum = 0;
 #pragma unroll
-  for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt)
-      sum += expanded_len(b[i]) + (b[i] < kRunBase && b[i] != kZeroGroup ? 1u << 16 : 0u);
-  const ScanU32 sc = block_scan_u32(sum, red);
-  int pos = (int)(sc.excl & 0xffffu) - (int)skip;  // range-relative start of b[0]
-#pragma unroll
-  for (int i = 0; i < kBytes; ++i) {
+  for (int i = 0; i < kSliceBytes; ++i) {
     if ((uint32_t)i < cnt) {
-      const uint32_t x = b[i];
-      const int len = (int)expanded_len(x);
-      const uint32_t a = (uint32_t)max(pos, 0);
-      const uint32_t e = (uint32_t)min(pos + len, (int)qn);
-      if (a < e) {
-        if (x < kRunBase)
-          s_q[a] = (uint8_t)x;
-        else
-          fill_zero_groups(s_q, a, e);
-      }
-      pos += len;
+      const uint32_t x = byte(i);
+      sum += expanded_len(x) + (x < kRunBase && x != kZeroGroup ? 1u << 16 : 0u);
+    }
+  }
+  const ScanU32 sc = block_scan_u32(sum, red);
+  int pos = (int)(sc.excl & 0xffffu) - (int)skip;  // range-relative start of byte 0
+#pragma unroll
+  for (int i = 0; i < kSliceBytes; ++i) {
+    if ((uint32_t)i < cnt) {
+      const uint32_t x = byte(i);
+      if (x < kRunBase && x != kZeroGroup && pos >= 0 && pos < (int)qn) s_q[pos] = (uint8_t)x;
+      pos += (int)expanded_len(x);
     }
   }
   __syncthreads();
   return sc.total >> 16;
+}
+
+// Expands quartic bytes [k*kDecRange, k*kDecRange + qn) of one stream into
+// s_q (the stream bytes covering the range found through the start entries,
+// spread over the threads); returns the slice's count of data bytes other
+// than 121.  Ends with a barrier.
+__device__ __forceinline__ uint32_t expand_range(const uint8_t* __restrict__ C, uint32_t c,
+                                             const uint64_t* __restrict__ starts, uint32_t k,
+                                             uint64_t m, uint32_t qn, uint8_t* s_q,
+                                             uint32_t* red) {
+  const Slice sl = slice_of(starts, k, m, c);
+  const uint32_t lo = threadIdx.x * kSliceBytes;
+  const uint32_t cnt = lo < sl.count ? min<uint32_t>(kSliceBytes, sl.count - lo) : 0u;
+  uint8_t b[kSliceBytes];
+#pragma unroll
+  for (int i = 0; i < kSliceBytes; ++i) b[i] = (uint32_t)i < cnt ? C[sl.i0 + lo + i] : (uint8_t)0;
+  return expand_slice([&](int i) -> uint32_t { return b[i]; }, cnt, sl.skip, qn, s_q, red);
 }
 
 // ---------------------------------------------------------------- Eq. 3
@@ -456,11 +481,56 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
 }
 
 // ---------------------------------------------------------------- aggregation
+// Streams whose slices a block stages per pass of the summed decode: one
+// wave reads their descriptors and start entries together.
+constexpr int kSumChunk = 64;
+
+struct SumSlice {
+  const uint8_t* C;  // the slice's first byte
+  uint32_t count;
+  uint32_t skip;
+  float scale;
+  uint32_t pad;
+};
+
+// The thread's bytes of a slice (lo = threadIdx.x * kSliceBytes onwards)
+// as kSliceBytes / 4 words, byte i in bits 8 * (i % 4) of word i / 4.
+// Reads the aligned dwords that hold them: each dword read holds at least
+// one byte of the slice, so no read leaves the pages the stream lies in.
+// Bytes past the slice's end are unspecified and never used.
+struct SliceWords {
+  uint32_t w[kSliceBytes / 4 + 1];
+  uint32_t sh;  // byte offset of the first byte inside w[0]
+};
+
+__device__ __forceinline__ SliceWords load_slice_words(const SumSlice& s) {
+  const uint32_t lo = threadIdx.x * kSliceBytes;
+  const uint32_t cnt = lo < s.count ? min<uint32_t>(kSliceBytes, s.count - lo) : 0u;
+  const uintptr_t first = reinterpret_cast<uintptr_t>(s.C) + lo;
+  const uint32_t* base = reinterpret_cast<const uint32_t*>(first & ~(uintptr_t)3);
+  SliceWords r;
+  r.sh = (uint32_t)(first & 3u);
+#pragma unroll
+  for (int j = 0; j <= kSliceBytes / 4; ++j)
+    r.w[j] = (uint32_t)(4 * j) < r.sh + cnt ? base[j] : 0u;
+  return r;
+}
+
+__device__ __forceinline__ uint32_t slice_word_byte(const SliceWords& s, int i) {
+  // byte i lies in w[(sh + i) / 4]; alignbyte selects it from a word pair
+  const uint32_t q = (uint32_t)i >> 2;
+  const uint32_t word = __builtin_amdgcn_alignbyte(s.w[q + 1], s.w[q], s.sh);
+  return (word >> (8 * (i & 3))) & 255u;
+}
+
 // Range k of `count` streams of the same n-value tensor, summed into out in
 // stream order per element (out = ((out + v0) + v1) + ..., or starting
 // from v0 without accumulate): the same fp32 additions, in the same order,
 // as decoding the streams one after another, but out is read and written
-// once.  Values stay in registers between streams.
+// once.  Values stay in registers between streams.  The descriptors and
+// start entries of up to kSumChunk streams are read in one round trip; the
+// next stream's bytes load while the current one expands, into the other
+// half of a double-buffered LDS range.
 template <bool kVec, bool kAcc>
 __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
     const DecDesc* __restrict__ descs, uint32_t count, const uint64_t* __restrict__ start,
@@ -468,12 +538,15 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
     const Ctrl* __restrict__ ctrl) {
   constexpr int kPer = kVec ? kDecRange / kThreads / 4 : kDecRange / kThreads;  // slots
   constexpr int kW = kVec ? 4 : 1;                                              // bytes/slot
+  constexpr uint32_t kZeroWord = kVec ? 0x79797979u : kZeroGroup;  // a slot of zero groups
   __shared__ uint32_t red[kWaves];
-  __shared__ __align__(16) uint8_t s_q[kDecRange];
+  __shared__ __align__(16) uint8_t s_q[2][kDecRange];
+  __shared__ SumSlice s_sl[kSumChunk];
   if (ctrl->dec_bad_epoch == epoch) return;  // a corrupt stream: out untouched
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  const uint32_t lo = threadIdx.x * kSliceBytes;
 
   // slot g covers quartic bytes jl(g) .. jl(g) + kW - 1 and their 5 partitions
   float acc[kPer][5][kW];
@@ -505,25 +578,52 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
     }
   }
 
-  for (uint32_t p = 0; p < count; ++p) {
-    const DecDesc d = descs[p];
-    expand_range(d.C, d.c, start + d.range0, k, m, qn, s_q, red);
-#pragma unroll
-    for (int g = 0; g < kPer; ++g) {
-      const uint32_t jl = jl_of(g);
-      if (jl >= qn) continue;
-      uint32_t w = kVec ? *reinterpret_cast<const uint32_t*>(s_q + jl) : s_q[jl];
-#pragma unroll
-      for (int cc = 0; cc < kW; ++cc) {
-        uint32_t t[5];
-        digits5((w >> (8 * cc)) & 0xffu, t);
-#pragma unroll
-        for (int kk = 0; kk < 5; ++kk)
-          acc[g][kk][cc] = (!kAcc && p == 0) ? trit_value(t[kk], d.scale)
-                                             : acc_trit(acc[g][kk][cc], t[kk], d.scale);
-      }
+  bool clean = false;  // no value is -0.0 and every NaN is quiet
+  for (uint32_t p0 = 0; p0 < count; p0 += kSumChunk) {
+    const uint32_t pc = min<uint32_t>(kSumChunk, count - p0);
+    if (threadIdx.x < pc) {
+      const DecDesc d = descs[p0 + threadIdx.x];
+      const Slice sl = slice_of(start + d.range0, k, m, d.c);
+      s_sl[threadIdx.x] = SumSlice{d.C + sl.i0, sl.count, sl.skip, d.scale, 0u};
     }
-    __syncthreads();  // s_q is rewritten by the next stream
+    __syncthreads();
+    SliceWords cur = load_slice_words(s_sl[0]);
+    for (uint32_t q = 0; q < pc; ++q) {
+      const SumSlice sl = s_sl[q];
+      SliceWords nxt;
+      if (q + 1 < pc) nxt = load_slice_words(s_sl[q + 1]);
+      uint8_t* sq = s_q[q & 1u];
+      // Barriers: the scan inside expand_slice is passed only once every
+      // thread has finished reading s_q[q & 1] for stream q - 2 (two
+      // streams back), so the halves alternate without a barrier of their own.
+      const uint32_t cnt = lo < sl.count ? min<uint32_t>(kSliceBytes, sl.count - lo) : 0u;
+      expand_slice([&](int i) { return slice_word_byte(cur, i); }, cnt, sl.skip, qn, sq, red);
+      const bool first = !kAcc && p0 + q == 0;
+      const bool dense = first || !clean;
+#pragma unroll
+      for (int g = 0; g < kPer; ++g) {
+        const uint32_t jl = jl_of(g);
+        if (jl >= qn) continue;
+        const uint32_t w = kVec ? *reinterpret_cast<const uint32_t*>(sq + jl) : sq[jl];
+        if (!dense && w == kZeroWord) continue;  // every term +-0: no value changes
+#pragma unroll
+        for (int cc = 0; cc < kW; ++cc) {
+          uint32_t t[5];
+          digits5((w >> (8 * cc)) & 0xffu, t);
+#pragma unroll
+          for (int kk = 0; kk < 5; ++kk)
+            acc[g][kk][cc] = first ? trit_value(t[kk], sl.scale)
+                                   : acc_trit(acc[g][kk][cc], t[kk], sl.scale);
+        }
+      }
+      // After a dense pass with M > 0 every value was given one of -M, +0,
+      // M, so none is -0.0 (a rounded-to-nearest sum that is zero is +0)
+      // and every NaN is quiet; no later term of +-0 (a zero group, with
+      // any M >= 0) then changes a value, and none makes a -0.0 again.
+      if (dense && sl.scale > 0.0f) clean = true;
+      if (q + 1 < pc) cur = nxt;
+    }
+    __syncthreads();  // s_sl is rewritten for the next chunk
   }
 
 #pragma unroll

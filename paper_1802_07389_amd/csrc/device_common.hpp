@@ -365,13 +365,6 @@ __device__ __forceinline__ uint32_t expanded_len(uint32_t b) {
   return b < kRunBase ? 1u : b - (kRunBase - 2u);
 }
 
-// Writes bytes of 121 at lds[lo..hi).
-__device__ __forceinline__ void fill_zero_groups(uint8_t* lds, uint32_t lo, uint32_t hi) {
-  while (lo < hi && (lo & 3u)) lds[lo++] = (uint8_t)kZeroGroup;
-  for (; lo + 4 <= hi; lo += 4) *reinterpret_cast<uint32_t*>(lds + lo) = 0x79797979u;
-  while (lo < hi) lds[lo++] = (uint8_t)kZeroGroup;
-}
-
 // ---------------------------------------------------------------- Eq. 3
 // The dequantized value M*q for trit t = q + 1 is -M, M*0 or M (M*(-1) is
 // the exact negation; M*0 is +0, or -0 for a scale of -0.0, which the

@@ -276,6 +276,36 @@ def test_decompress_sum_small(bctx, n, count, offset):
         assert np.array_equal(g.bits(od.cpu().numpy()), g.bits(ref)), (n, count, acc)
 
 
+@pytest.mark.parametrize("count", [64, 65, 131])
+def test_decompress_sum_many_streams_odd_offsets(bctx, count):
+    """More streams than one block stages at once, each stream starting at
+    an odd byte offset of one shared buffer (slices at every alignment);
+    summed in order, bit for bit against sequential decode-accumulate."""
+    import torch
+    g = G()
+    n = 4096 * 5 * 2 + 11
+    pays = []
+    for p in range(count):
+        x = workloads.runs_tensor([733, p], n) if p % 3 else workloads.normal([734, p], n)
+        st, C, M = oracle.compress(x, np.zeros(n, F32), [1.0, 1.75, 1.5][p % 3])
+        pays.append((C, M))
+    buf = torch.zeros(sum(C.size + 3 for C, _ in pays) + 16, dtype=torch.uint8, device="cuda")
+    views, at = [], 1
+    for p, (C, _) in enumerate(pays):
+        at += p % 4  # offsets of every residue mod 4
+        buf[at:at + C.size] = torch.from_numpy(C).cuda()
+        views.append(buf[at:at + C.size])
+        at += C.size
+    out0 = workloads.normal([735, count], n, 1e-3)
+    ref = out0.copy()
+    for C, M in pays:
+        st, ref = oracle.decompress(C, M, n, ref, accumulate=True)
+    od = torch.from_numpy(out0.copy()).cuda()
+    bctx.decompress_sum(views, [M for _, M in pays], od, accumulate=True)
+    bctx.sync()
+    assert np.array_equal(g.bits(od.cpu().numpy()), g.bits(ref)), count
+
+
 def test_decompress_sum_corrupt_leaves_out(bctx):
     import torch
     from paper_1802_07389_amd import tlc
