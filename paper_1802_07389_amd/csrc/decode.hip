@@ -484,6 +484,8 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
 // Streams whose slices a block stages per pass of the summed decode: one
 // wave reads their descriptors and start entries together.
 constexpr int kSumChunk = 64;
+// Stream bytes a wave expands per round (16 per lane).
+constexpr uint32_t kWaveSliceBytes = 64u * 16u;
 
 struct SumSlice {
   const uint8_t* C;  // the slice's first byte
@@ -493,26 +495,25 @@ struct SumSlice {
   uint32_t pad;
 };
 
-// The thread's bytes of a slice (lo = threadIdx.x * kSliceBytes onwards)
-// as kSliceBytes / 4 words, byte i in bits 8 * (i % 4) of word i / 4.
-// Reads the aligned dwords that hold them: each dword read holds at least
-// one byte of the slice, so no read leaves the pages the stream lies in.
-// Bytes past the slice's end are unspecified and never used.
+// Stream bytes lo .. lo + 15 of a slice (those below count) as words,
+// byte i in bits 8 * (i % 4) of word i / 4 once aligned by sh.  Reads only
+// the aligned dwords that hold them (none when lo >= count): each dword
+// read holds at least one byte of the slice, so no read leaves the pages
+// the stream lies in.  Bytes past the slice's end are unspecified and
+// never used.
 struct SliceWords {
-  uint32_t w[kSliceBytes / 4 + 1];
+  uint32_t w[5];
   uint32_t sh;  // byte offset of the first byte inside w[0]
 };
 
-__device__ __forceinline__ SliceWords load_slice_words(const SumSlice& s) {
-  const uint32_t lo = threadIdx.x * kSliceBytes;
-  const uint32_t cnt = lo < s.count ? min<uint32_t>(kSliceBytes, s.count - lo) : 0u;
+__device__ __forceinline__ SliceWords load_slice_words(const SumSlice& s, uint32_t lo) {
+  const uint32_t cnt = lo < s.count ? min<uint32_t>(16u, s.count - lo) : 0u;
   const uintptr_t first = reinterpret_cast<uintptr_t>(s.C) + lo;
   const uint32_t* base = reinterpret_cast<const uint32_t*>(first & ~(uintptr_t)3);
   SliceWords r;
   r.sh = (uint32_t)(first & 3u);
 #pragma unroll
-  for (int j = 0; j <= kSliceBytes / 4; ++j)
-    r.w[j] = (uint32_t)(4 * j) < r.sh + cnt ? base[j] : 0u;
+  for (int j = 0; j < 5; ++j) r.w[j] = cnt && (uint32_t)(4 * j) < r.sh + cnt ? base[j] : 0u;
   return r;
 }
 
@@ -523,14 +524,56 @@ __device__ __forceinline__ uint32_t slice_word_byte(const SliceWords& s, int i) 
   return (word >> (8 * (i & 3))) & 255u;
 }
 
+// One wave expands a slice into s_q (the range's quartic bytes [0, qn)):
+// it fills the range with 121, then each lane takes 16 stream bytes per
+// round, a wave scan of their expansion lengths places them, and the data
+// bytes other than 121 are written.  `pre` holds the lane's bytes of the
+// first round.  No block barrier: the caller's barrier publishes s_q.
+__device__ __forceinline__ void wave_expand(const SumSlice& sl, const SliceWords& pre,
+                                            uint32_t qn, uint8_t* s_q) {
+  const uint32_t lane = threadIdx.x & 63u;
+#pragma unroll
+  for (int i = 0; i < kDecRange / (16 * 64); ++i)
+    reinterpret_cast<uint4*>(s_q)[lane + 64 * i] =
+        make_uint4(0x79797979u, 0x79797979u, 0x79797979u, 0x79797979u);
+  int base = -(int)sl.skip;  // range-relative start of the round's first byte
+  for (uint32_t r0 = 0; r0 < sl.count; r0 += kWaveSliceBytes) {
+    const uint32_t lo = r0 + 16u * lane;
+    const SliceWords w = r0 == 0 ? pre : load_slice_words(sl, lo);
+    const uint32_t cnt = lo < sl.count ? min<uint32_t>(16u, sl.count - lo) : 0u;
+    uint32_t len = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if ((uint32_t)i < cnt) len += expanded_len(slice_word_byte(w, i));
+    uint32_t incl = len;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t o = __shfl_up(incl, d, 64);
+      if (lane >= (uint32_t)d) incl += o;
+    }
+    int pos = base + (int)(incl - len);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if ((uint32_t)i < cnt) {
+        const uint32_t x = slice_word_byte(w, i);
+        if (x < kRunBase && x != kZeroGroup && pos >= 0 && pos < (int)qn) s_q[pos] = (uint8_t)x;
+        pos += (int)expanded_len(x);
+      }
+    }
+    base += (int)__shfl(incl, 63, 64);
+  }
+}
+
 // Range k of `count` streams of the same n-value tensor, summed into out in
 // stream order per element (out = ((out + v0) + v1) + ..., or starting
 // from v0 without accumulate): the same fp32 additions, in the same order,
 // as decoding the streams one after another, but out is read and written
 // once.  Values stay in registers between streams.  The descriptors and
 // start entries of up to kSumChunk streams are read in one round trip; the
-// next stream's bytes load while the current one expands, into the other
-// half of a double-buffered LDS range.
+// streams then go in groups of kWaves, one per wave, each expanded by its
+// wave into its own LDS range, with one block barrier per group; the next
+// group's bytes load while the current group is summed, and the groups'
+// LDS ranges alternate between two sets.
 template <bool kVec, bool kAcc>
 __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
     const DecDesc* __restrict__ descs, uint32_t count, const uint64_t* __restrict__ start,
@@ -539,14 +582,13 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
   constexpr int kPer = kVec ? kDecRange / kThreads / 4 : kDecRange / kThreads;  // slots
   constexpr int kW = kVec ? 4 : 1;                                              // bytes/slot
   constexpr uint32_t kZeroWord = kVec ? 0x79797979u : kZeroGroup;  // a slot of zero groups
-  __shared__ uint32_t red[kWaves];
-  __shared__ __align__(16) uint8_t s_q[2][kDecRange];
+  __shared__ __align__(16) uint8_t s_q[2][kWaves][kDecRange];
   __shared__ SumSlice s_sl[kSumChunk];
   if (ctrl->dec_bad_epoch == epoch) return;  // a corrupt stream: out untouched
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
-  const uint32_t lo = threadIdx.x * kSliceBytes;
+  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
 
   // slot g covers quartic bytes jl(g) .. jl(g) + kW - 1 and their 5 partitions
   float acc[kPer][5][kW];
@@ -587,43 +629,49 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
       s_sl[threadIdx.x] = SumSlice{d.C + sl.i0, sl.count, sl.skip, d.scale, 0u};
     }
     __syncthreads();
-    SliceWords cur = load_slice_words(s_sl[0]);
-    for (uint32_t q = 0; q < pc; ++q) {
-      const SumSlice sl = s_sl[q];
-      SliceWords nxt;
-      if (q + 1 < pc) nxt = load_slice_words(s_sl[q + 1]);
-      uint8_t* sq = s_q[q & 1u];
-      // Barriers: the scan inside expand_slice is passed only once every
-      // thread has finished reading s_q[q & 1] for stream q - 2 (two
-      // streams back), so the halves alternate without a barrier of their own.
-      const uint32_t cnt = lo < sl.count ? min<uint32_t>(kSliceBytes, sl.count - lo) : 0u;
-      expand_slice([&](int i) { return slice_word_byte(cur, i); }, cnt, sl.skip, qn, sq, red);
-      const bool first = !kAcc && p0 + q == 0;
-      const bool dense = first || !clean;
+    SliceWords cur{};
+    if (wid < pc) cur = load_slice_words(s_sl[wid], 16u * lane);
+    for (uint32_t g0 = 0; g0 < pc; g0 += kWaves) {
+      const uint32_t gn = min<uint32_t>(kWaves, pc - g0);
+      SliceWords nxt{};
+      if (g0 + kWaves + wid < pc) nxt = load_slice_words(s_sl[g0 + kWaves + wid], 16u * lane);
+      // Group g0 / kWaves fills set (g0 / kWaves) & 1.  A wave reaches that
+      // fill only past the barrier of the previous group, which every
+      // thread passes only after summing the group two back from the same
+      // set, so the sets alternate without a barrier of their own.
+      uint8_t(*set)[kDecRange] = s_q[(g0 / kWaves) & 1u];
+      if (wid < gn) wave_expand(s_sl[g0 + wid], cur, qn, set[wid]);
+      __syncthreads();
+      for (uint32_t s = 0; s < gn; ++s) {
+        const float scale = s_sl[g0 + s].scale;
+        const bool first = !kAcc && p0 + g0 + s == 0;
+        const bool dense = first || !clean;
+        const uint8_t* sq = set[s];
 #pragma unroll
-      for (int g = 0; g < kPer; ++g) {
-        const uint32_t jl = jl_of(g);
-        if (jl >= qn) continue;
-        const uint32_t w = kVec ? *reinterpret_cast<const uint32_t*>(sq + jl) : sq[jl];
-        if (!dense && w == kZeroWord) continue;  // every term +-0: no value changes
+        for (int g = 0; g < kPer; ++g) {
+          const uint32_t jl = jl_of(g);
+          if (jl >= qn) continue;
+          const uint32_t w = kVec ? *reinterpret_cast<const uint32_t*>(sq + jl) : sq[jl];
+          if (!dense && w == kZeroWord) continue;  // every term +-0: no value changes
 #pragma unroll
-        for (int cc = 0; cc < kW; ++cc) {
-          uint32_t t[5];
-          digits5((w >> (8 * cc)) & 0xffu, t);
+          for (int cc = 0; cc < kW; ++cc) {
+            uint32_t t[5];
+            digits5((w >> (8 * cc)) & 0xffu, t);
 #pragma unroll
-          for (int kk = 0; kk < 5; ++kk)
-            acc[g][kk][cc] = first ? trit_value(t[kk], sl.scale)
-                                   : acc_trit(acc[g][kk][cc], t[kk], sl.scale);
+            for (int kk = 0; kk < 5; ++kk)
+              acc[g][kk][cc] = first ? trit_value(t[kk], scale)
+                                     : acc_trit(acc[g][kk][cc], t[kk], scale);
+          }
         }
+        // After a dense pass with M > 0 every value was given one of -M,
+        // +0, M, so none is -0.0 (a rounded-to-nearest sum that is zero is
+        // +0) and every NaN is quiet; no later term of +-0 (a zero group,
+        // with any M >= 0) then changes a value, and none makes a -0.0 again.
+        if (dense && scale > 0.0f) clean = true;
       }
-      // After a dense pass with M > 0 every value was given one of -M, +0,
-      // M, so none is -0.0 (a rounded-to-nearest sum that is zero is +0)
-      // and every NaN is quiet; no later term of +-0 (a zero group, with
-      // any M >= 0) then changes a value, and none makes a -0.0 again.
-      if (dense && sl.scale > 0.0f) clean = true;
-      if (q + 1 < pc) cur = nxt;
+      cur = nxt;
     }
-    __syncthreads();  // s_sl is rewritten for the next chunk
+    __syncthreads();  // s_sl and the sets are rewritten for the next chunk
   }
 
 #pragma unroll
