@@ -40,7 +40,7 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
   constexpr uint32_t kTile = kThreads * kBytes;
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint64_t j0 = (uint64_t)lt * kTile + threadIdx.x * kBytes;
-  const uint32_t cnt = j0 < c ? (uint32_t)min<uint64_t>(kBytes, c - j0) : 0u;
+  const uint32_t cnt = j0 < c ? (uint32_t)umin64(kBytes, c - j0) : 0u;
 
   // the thread's bytes stay packed four to a word; byte i is bits 8*(i%4) of w[i/4]
   uint32_t w[kBytes / 4];
@@ -154,7 +154,7 @@ __device__ __forceinline__ uint32_t range_end(const uint64_t* __restrict__ start
                                               uint64_t m, uint32_t c) {
   if ((uint64_t)(k + 1) * kDecRange < m) {
     const uint64_t s1 = starts[k + 1];
-    return min<uint32_t>((uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u), c);
+    return umin32((uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u), c);
   }
   return c;
 }
@@ -173,7 +173,7 @@ __device__ __forceinline__ Slice slice_of(const uint64_t* __restrict__ starts, u
   r.i0 = (uint32_t)(s0 >> 8);
   r.skip = (uint32_t)(s0 & 255u);
   const uint32_t i1 = range_end(starts, k, m, c);
-  r.count = i1 > r.i0 ? min<uint32_t>(i1 - r.i0, kDecRange) : 0u;
+  r.count = i1 > r.i0 ? umin32(i1 - r.i0, kDecRange) : 0u;
   return r;
 }
 
@@ -227,7 +227,7 @@ __device__ __forceinline__ uint32_t expand_range(const uint8_t* __restrict__ C, 
                                              uint32_t* red) {
   const Slice sl = slice_of(starts, k, m, c);
   const uint32_t lo = threadIdx.x * kSliceBytes;
-  const uint32_t cnt = lo < sl.count ? min<uint32_t>(kSliceBytes, sl.count - lo) : 0u;
+  const uint32_t cnt = lo < sl.count ? umin32(kSliceBytes, sl.count - lo) : 0u;
   uint8_t b[kSliceBytes];
 #pragma unroll
   for (int i = 0; i < kSliceBytes; ++i) b[i] = (uint32_t)i < cnt ? C[sl.i0 + lo + i] : (uint8_t)0;
@@ -437,7 +437,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
   if (ctrl->dec_bad_epoch == epoch) return;  // corrupt stream: out untouched
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
-  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  const uint32_t qn = (uint32_t)umin64(kDecRange, m - q0);
   if (kPath == kPathShift && kAcc && kNT) {
     // large outputs: the first two partitions' loads overlap the expansion
     // (on gfx950 15 us of 410 on a 2^28-value decode; outputs that fit the
@@ -469,7 +469,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_batch_kernel(
   const DecDesc d = descs[t];
   const uint32_t k = blockIdx.x - d.range0;
   const uint64_t q0 = (uint64_t)k * kDecRange;
-  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, (uint64_t)d.m - q0);
+  const uint32_t qn = (uint32_t)umin64(kDecRange, (uint64_t)d.m - q0);
   const bool dense =
       expand_range(d.C, d.c, start + d.range0, k, d.m, qn, s_q, red) > kDenseLiterals;
   if (d.vec & 1u)
@@ -507,7 +507,7 @@ struct SliceWords {
 };
 
 __device__ __forceinline__ SliceWords load_slice_words(const SumSlice& s, uint32_t lo) {
-  const uint32_t cnt = lo < s.count ? min<uint32_t>(16u, s.count - lo) : 0u;
+  const uint32_t cnt = lo < s.count ? umin32(16u, s.count - lo) : 0u;
   const uintptr_t first = reinterpret_cast<uintptr_t>(s.C) + lo;
   const uint32_t* base = reinterpret_cast<const uint32_t*>(first & ~(uintptr_t)3);
   SliceWords r;
@@ -540,7 +540,7 @@ __device__ __forceinline__ void wave_expand(const SumSlice& sl, const SliceWords
   for (uint32_t r0 = 0; r0 < sl.count; r0 += kWaveSliceBytes) {
     const uint32_t lo = r0 + 16u * lane;
     const SliceWords w = r0 == 0 ? pre : load_slice_words(sl, lo);
-    const uint32_t cnt = lo < sl.count ? min<uint32_t>(16u, sl.count - lo) : 0u;
+    const uint32_t cnt = lo < sl.count ? umin32(16u, sl.count - lo) : 0u;
     uint32_t len = 0;
 #pragma unroll
     for (int i = 0; i < 16; ++i)
@@ -587,7 +587,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
   if (ctrl->dec_bad_epoch == epoch) return;  // a corrupt stream: out untouched
   const uint32_t k = blockIdx.x;
   const uint64_t q0 = (uint64_t)k * kDecRange;
-  const uint32_t qn = (uint32_t)min<uint64_t>(kDecRange, m - q0);
+  const uint32_t qn = (uint32_t)umin64(kDecRange, m - q0);
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
 
   // slot g covers quartic bytes jl(g) .. jl(g) + kW - 1 and their 5 partitions
@@ -622,7 +622,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
 
   bool clean = false;  // no value is -0.0 and every NaN is quiet
   for (uint32_t p0 = 0; p0 < count; p0 += kSumChunk) {
-    const uint32_t pc = min<uint32_t>(kSumChunk, count - p0);
+    const uint32_t pc = umin32(kSumChunk, count - p0);
     if (threadIdx.x < pc) {
       const DecDesc d = descs[p0 + threadIdx.x];
       const Slice sl = slice_of(start + d.range0, k, m, d.c);
@@ -632,7 +632,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_sum_kernel(
     SliceWords cur{};
     if (wid < pc) cur = load_slice_words(s_sl[wid], 16u * lane);
     for (uint32_t g0 = 0; g0 < pc; g0 += kWaves) {
-      const uint32_t gn = min<uint32_t>(kWaves, pc - g0);
+      const uint32_t gn = umin32(kWaves, pc - g0);
       SliceWords nxt{};
       if (g0 + kWaves + wid < pc) nxt = load_slice_words(s_sl[g0 + kWaves + wid], 16u * lane);
       // Group g0 / kWaves fills set (g0 / kWaves) & 1.  A wave reaches that

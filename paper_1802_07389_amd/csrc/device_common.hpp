@@ -12,6 +12,14 @@ namespace tlc {
 
 constexpr int kWaves = kThreads / 64;
 
+// Unsigned min/max with both operands of one type.  HIP's mixed-type
+// min/max (what min<T>(a, b) selects when b has another type, an int
+// constant for instance) converts to double and calls fmin: several f64
+// instructions, and values from 2^53 on would round.
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ uint32_t abs_bits(float v) {
   return __float_as_uint(v) & 0x7fffffffu;

@@ -13,9 +13,10 @@
 //       trits for the quartic pack                  (Section 3.1, Eq. 1-2)
 //   tlc_quant_encode_kernel, tlc_zre_chunk(_scan)_kernel, tlc_zre_compact_kernel
 //       one tensor: M, 3-value quantization of the buffer, residual
-//       write-back where q != 0, quartic pack and each tile's own zero-run
-//       encoding; then a scan of the tile summaries and the compaction into
-//       one stream                             (Eq. 1-2, Sections 3.2-3.3)
+//       write-back where q != 0 (or the quartic pack from the writing
+//       pass's trits), each tile's own zero-run encoding; then a scan of the
+//       tile summaries and the compaction into one stream
+//                                              (Eq. 1-2, Sections 3.2-3.3)
 //   tlc_quant_encode_chained_kernel, tlc_quant_encode_batch_kernel
 //       a small tensor, or many tensors, in one pass: tiles chained by
 //       decoupled look-back
@@ -400,13 +401,13 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
 
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
-  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
   quantize_tile<kPath, kX>(x, r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- phase 2: Section 3.3
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t lo = threadIdx.x * kBytes;
-  const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
+  const uint32_t cnt = lo < tile_bytes ? umin32(kBytes, tile_bytes - lo) : 0u;
   const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
   const RunSum sum = rs_mask_summary(nz, cnt);
 
@@ -467,7 +468,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   // a tile emits at most kEncTile + 1 bytes; the clamps only keep a logic
   // error from writing outside the m-byte output buffer
   const uint32_t count =
-      tile_end >= tile_begin ? min<uint32_t>(tile_end - tile_begin, kEncTile + 1) : 0u;
+      tile_end >= tile_begin ? umin32(tile_end - tile_begin, kEncTile + 1) : 0u;
   for (uint32_t i = threadIdx.x; i < count; i += kThreads)
     if (tile_begin + i < m) out[tile_begin + i] = sh.out[i];
   if (last_tile && threadIdx.x == 0) res->len = tile_end;
@@ -676,7 +677,7 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
     }
   }
   __syncthreads();
-  const uint32_t nf = min<uint32_t>(*nfix, kFixCap);
+  const uint32_t nf = umin32(*nfix, kFixCap);
   for (uint32_t i = threadIdx.x; i < nf; i += kThreads) fix[i] = s_fix[i];
 }
 
@@ -701,8 +702,8 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
     const uint32_t a = (uint32_t)(base & 3u);
     const uint8_t* tp = trits + (base >> 2);
     const uint64_t left = n > base ? n - base : 0u;  // values of the partition from base on
-    const uint32_t lim = (uint32_t)min<uint64_t>(left, tile_bytes);
-    const uint32_t cap = (uint32_t)min<uint64_t>(left + a, 2u * kEncTile);
+    const uint32_t lim = (uint32_t)umin64(left, tile_bytes);
+    const uint32_t cap = (uint32_t)umin64(left + a, 2u * kEncTile);
 #pragma unroll
     for (int it = 0; it < kGroupsPerThread; ++it) {
       const uint32_t g = threadIdx.x + kThreads * it;
@@ -721,15 +722,46 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
   }
 }
 
+// A tile whose partitions all start on a trit-byte boundary (m % 4 == 0),
+// that is whole and whose 5 * kEncTile values all lie before n: every trit
+// byte it needs exists and none needs shifting, so the loads go without
+// guards (one scalar base per partition, the group in the offset).
+__device__ __forceinline__ void load_trits_interior(const uint8_t* __restrict__ trits,
+                                                    uint32_t m, uint64_t q0,
+                                                    uint32_t (&tb)[kGroupsPerThread][5]) {
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    const uint8_t* tp = trits + (((uint64_t)k * m + q0) >> 2);
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it) tb[it][k] = tp[threadIdx.x + kThreads * it];
+  }
+}
+
 __device__ __forceinline__ uint32_t spread_trits(uint32_t tb) {
   // the four 2-bit trits of one byte into the low bits of four bytes
   tb = (tb | (tb << 12)) & 0x000f000fu;
   return (tb | (tb << 6)) & 0x03030303u;
 }
 
+// Tables of spread trits times the partition's weight (Section 3.2: 81, 27,
+// 9, 3, 1): lut[k][b] holds, in byte lane c, 3^(4-k) times trit c of trit
+// byte b.  The sum of one entry per partition is the four quartic bytes of
+// a group (each at most 242, so no carry crosses a lane): five LDS reads
+// and four adds instead of five spreads and four multiply-adds.  Written
+// before a barrier of the caller.
+__device__ __forceinline__ void init_trit_luts(uint32_t (*lut)[256]) {
+  static_assert(kThreads == 256, "one table entry per thread and partition");
+  const uint32_t sp = spread_trits(threadIdx.x);
+  lut[0][threadIdx.x] = 81u * sp;
+  lut[1][threadIdx.x] = 27u * sp;
+  lut[2][threadIdx.x] = 9u * sp;
+  lut[3][threadIdx.x] = 3u * sp;
+  lut[4][threadIdx.x] = sp;
+}
+
 __device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread][5], uint64_t n,
                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
-                                           uint8_t* q) {
+                                           const uint32_t (*lut)[256], uint8_t* q) {
   uint32_t* qw = reinterpret_cast<uint32_t*>(q);
 #pragma unroll
   for (int it = 0; it < kGroupsPerThread; ++it) {
@@ -737,11 +769,9 @@ __device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread
     if (g * 4u >= tile_bytes) break;
     const uint64_t j = q0 + g * 4u;
     if (4ull * m + j + 4u <= n) {
-      // all 20 values exist: the four bytes at once, 81*t0 + 27*t1 + 9*t2 +
-      // 3*t3 + t4 per byte lane (at most 242, so no carry crosses a lane)
-      qw[g] = 81u * spread_trits(tb[it][0]) + 27u * spread_trits(tb[it][1]) +
-              9u * spread_trits(tb[it][2]) + 3u * spread_trits(tb[it][3]) +
-              spread_trits(tb[it][4]);
+      // all 20 values exist: the four bytes at once
+      qw[g] = lut[0][tb[it][0]] + lut[1][tb[it][1]] + lut[2][tb[it][2]] + lut[3][tb[it][3]] +
+              lut[4][tb[it][4]];
       continue;
     }
     uint32_t code[4] = {0u, 0u, 0u, 0u};
@@ -772,18 +802,25 @@ void tlc_quant_encode_kernel(
   static_assert(!kTrit || kPath == kPathVec, "trits are kept on the float4 path");
   __shared__ EncShared sh;
   __shared__ uint2 s_fix[(kPath == kPathVec && !kTrit) ? kFixCap : 1];
+  __shared__ uint32_t s_lut[kTrit ? 5 : 1][256];
   if (threadIdx.x == 0) {
     sh.nfix = 0u;
     sh.nneed = 0u;
   }
   const uint32_t t = blockIdx.x;
   const uint64_t q0 = (uint64_t)t * kEncTile;
-  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
   uint32_t h[kGroupsPerThread][5];  // bounds, or with kTrit the trit bytes
-  if (kTrit)
-    load_trits(reinterpret_cast<const uint8_t*>(summ), n, m, q0, tile_bytes, h);
-  else if (kPath == kPathVec && summ)
+  if (kTrit) {
+    const uint8_t* trits = reinterpret_cast<const uint8_t*>(summ);
+    if (m % 4u == 0u && tile_bytes == (uint32_t)kEncTile && 4ull * m + q0 + kEncTile <= n)
+      load_trits_interior(trits, m, q0, h);
+    else
+      load_trits(trits, n, m, q0, tile_bytes, h);
+    init_trit_luts(s_lut);
+  } else if (kPath == kPathVec && summ) {
     load_bounds(summ, n, m, q0, tile_bytes, h);
+  }
   const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
@@ -791,7 +828,7 @@ void tlc_quant_encode_kernel(
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
   if (kTrit) {
-    pack_trits(h, n, m, q0, tile_bytes, sh.q);
+    pack_trits(h, n, m, q0, tile_bytes, s_lut, sh.q);
   } else if (kPath == kPathVec) {
     if (summ)
       quantize_tile_vec_deferred<true>(r, n, m, sc, q0, tile_bytes, sh.q, s_fix, &sh.nfix,
@@ -810,7 +847,7 @@ void tlc_quant_encode_kernel(
   // rs_gaps_emit); the thread with the tile's last non-121 byte adds the
   // trailing run's codes 255 to its length.
   const uint32_t lo = threadIdx.x * kBytes;
-  const uint32_t cnt = lo < tile_bytes ? min<uint32_t>(kBytes, tile_bytes - lo) : 0u;
+  const uint32_t cnt = lo < tile_bytes ? umin32(kBytes, tile_bytes - lo) : 0u;
   const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
   const uint32_t last = nz ? lo + 31u - (uint32_t)__builtin_clz(nz) : 0u;
   const ScanU32 pm = block_scan_max_u32(nz ? last + 1u : 0u, sh.red);
@@ -835,7 +872,7 @@ void tlc_quant_encode_kernel(
                [&](uint32_t k) { o += k; });
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
-  const uint32_t len = min<uint32_t>(off.total, tile_bytes);
+  const uint32_t len = umin32(off.total, tile_bytes);
   __syncthreads();
   for (uint32_t i = 16u * threadIdx.x; i < len; i += 16u * kThreads)
     *reinterpret_cast<uint4*>(slots + q0 + i) = *reinterpret_cast<const uint4*>(sh.out + i);
@@ -850,7 +887,7 @@ void tlc_quant_encode_kernel(
       rec.lead = (uint16_t)sh.lead;
       rec.len = (uint16_t)len;
     }
-    rec.nfix = min<uint32_t>(sh.nfix, kFixCap);
+    rec.nfix = umin32(sh.nfix, kFixCap);
     recs[t] = rec;
   }
 }
@@ -942,7 +979,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
   const RunSum P = rs_combine(cp, lp);
   const TileRec rec = recs[t];
   const uint64_t q0 = (uint64_t)t * kEncTile;
-  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
   const uint32_t off = rs_emitted(P);
   const uint32_t grown = rs_phase(P) + rec.lead;  // the open run after the leading 121s
   const uint32_t n255 = grown / kRunMax, rho = grown % kRunMax;
@@ -953,7 +990,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
   if (code && lane == 0 && off + n255 < m) out[off + n255] = (uint8_t)rs_code(rho);
   if (rest) {
     const uint32_t at = off + n255 + code;
-    const uint32_t len = min<uint32_t>(rec.len, tile_bytes);
+    const uint32_t len = umin32(rec.len, tile_bytes);
     // dword loads from the slot (4096-byte aligned, len <= 4096), byte stores
     for (uint32_t i = 4u * lane; i < len; i += 256u) {
       const uint32_t w = *reinterpret_cast<const uint32_t*>(slots + q0 + i);
@@ -964,7 +1001,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
   }
   // the residuals the first pass left in the tile's fix list
   const uint2* tf = fix + (uint64_t)t * kFixCap;
-  const uint32_t nf = min<uint32_t>(rec.nfix, kFixCap);
+  const uint32_t nf = umin32(rec.nfix, kFixCap);
   for (uint32_t i = lane; i < nf; i += 64u) {
     const uint2 f = tf[i];
     const uint32_t k = f.x / (uint32_t)kEncTile, p = f.x % (uint32_t)kEncTile;
@@ -1062,7 +1099,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_pack_kernel(
   }
   if (sc.bad) return;
   const uint64_t q0 = (uint64_t)blockIdx.x * kEncTile;
-  const uint32_t tile_bytes = (uint32_t)min<uint64_t>(kEncTile, (uint64_t)m - q0);
+  const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
   if (kVec) {
     for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads) {
       const uint64_t j = q0 + g * 4u;
