@@ -708,7 +708,7 @@ static inline bool aligned16(const void* p) {
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                             uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  tlc_zre_index_kernel<<<ntiles, kThreads, 0, st>>>(C, c, m, start, status, ticket_base,
+  launch_k(tlc_zre_index_kernel, ntiles, kThreads, st, C, c, m, start, status, ticket_base,
                                                     epoch, ctrl);
   return hipGetLastError();
 }
@@ -721,7 +721,7 @@ hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* s
   const bool nt = al && n * sizeof(float) >= kNtMinBytes;
   const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
 #define TLC_LAUNCH(V, A, N)                                                                 \
-  tlc_expand_dequant_kernel<V, A, N><<<blocks, kThreads, 0, st>>>(C, c, start, n, m, scale, \
+  launch_k(tlc_expand_dequant_kernel<V, A, N>, blocks, kThreads, st, C, c, start, n, m, scale, \
                                                                   out, epoch, ctrl)
   if (nt) {
     if (accumulate) TLC_LAUNCH(kPathShift, true, true); else TLC_LAUNCH(kPathShift, false, true);
@@ -739,7 +739,7 @@ hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* s
 hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
                                   uint64_t* start, uint64_t* status, uint32_t ticket_base,
                                   uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
-  tlc_zre_index_batch_kernel<<<total_tiles, kThreads, 0, st>>>(descs, count, start, status,
+  launch_k(tlc_zre_index_batch_kernel, total_tiles, kThreads, st, descs, count, start, status,
                                                                ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
@@ -749,10 +749,10 @@ hipError_t launch_expand_dequant_batch(const DecDesc* descs, uint32_t count,
                                        int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                        hipStream_t st) {
   if (accumulate)
-    tlc_expand_dequant_batch_kernel<true><<<total_ranges, kThreads, 0, st>>>(descs, count,
+    launch_k(tlc_expand_dequant_batch_kernel<true>, total_ranges, kThreads, st, descs, count,
                                                                              start, epoch, ctrl);
   else
-    tlc_expand_dequant_batch_kernel<false><<<total_ranges, kThreads, 0, st>>>(
+    launch_k(tlc_expand_dequant_batch_kernel<false>, total_ranges, kThreads, st,
         descs, count, start, epoch, ctrl);
   return hipGetLastError();
 }
@@ -762,7 +762,7 @@ hipError_t launch_expand_sum(const DecDesc* descs, uint32_t count, const uint64_
                              uint32_t epoch, const Ctrl* ctrl, hipStream_t st) {
   const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
 #define TLC_LAUNCH(V, A)                                                                 \
-  tlc_expand_sum_kernel<V, A><<<blocks, kThreads, 0, st>>>(descs, count, start, n, m, out, \
+  launch_k(tlc_expand_sum_kernel<V, A>, blocks, kThreads, st, descs, count, start, n, m, out, \
                                                            epoch, ctrl)
   if (vec) {
     if (accumulate) TLC_LAUNCH(true, true); else TLC_LAUNCH(true, false);

@@ -1170,9 +1170,9 @@ hipError_t launch_absmax_check(const float* x, const float* r, uint64_t n, uint3
   const uint32_t blocks = absmax_blocks(n, vec);
   *nblocks = blocks;
   if (vec)
-    tlc_absmax_check_kernel<true><<<blocks, kThreads, 0, st>>>(x, r, n, partials);
+    launch_k(tlc_absmax_check_kernel<true>, blocks, kThreads, st, x, r, n, partials);
   else
-    tlc_absmax_check_kernel<false><<<blocks, kThreads, 0, st>>>(x, r, n, partials);
+    launch_k(tlc_absmax_check_kernel<false>, blocks, kThreads, st, x, r, n, partials);
   return hipGetLastError();
 }
 
@@ -1186,12 +1186,12 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* p
   if (guard && guard_np != blocks) return hipErrorInvalidValue;  // same launch as the check
   *nblocks = blocks;
   if (trit) {
-    tlc_accum_quantize_kernel<<<blocks, kThreads, 0, st>>>(
+    launch_k(tlc_accum_quantize_kernel, blocks, kThreads, st,
         x, r, n, partials, reinterpret_cast<uint8_t*>(summ), guard, guard_np, s);
     return hipGetLastError();
   }
 #define TLC_LAUNCH(V, R, S)                                                                 \
-  tlc_accum_absmax_kernel<V, R, S><<<blocks, kThreads, 0, st>>>(x, r, n, partials, summ, guard, \
+  launch_k(tlc_accum_absmax_kernel<V, R, S>, blocks, kThreads, st, x, r, n, partials, summ, guard, \
                                                                 guard_np, s)
   if (r == nullptr) {  // no error buffer: max |x|
     if (aligned16(x)) TLC_LAUNCH(true, false, false); else TLC_LAUNCH(false, false, false);
@@ -1213,15 +1213,15 @@ hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
 #define TLC_ARGS r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl
   if (trit) {
     if (!summ) return hipErrorInvalidValue;
-    tlc_quant_encode_kernel<kPathVec, true><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+    launch_k(tlc_quant_encode_kernel<kPathVec, true>, ntiles, kThreads, st, TLC_ARGS);
   } else if (al && m % 4 == 0) {
-    tlc_quant_encode_kernel<kPathVec><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+    launch_k(tlc_quant_encode_kernel<kPathVec>, ntiles, kThreads, st, TLC_ARGS);
   } else {
     summ = nullptr;  // bounds serve the float4 slices only
     if (al)
-      tlc_quant_encode_kernel<kPathShift><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+      launch_k(tlc_quant_encode_kernel<kPathShift>, ntiles, kThreads, st, TLC_ARGS);
     else
-      tlc_quant_encode_kernel<kPathByte><<<ntiles, kThreads, 0, st>>>(TLC_ARGS);
+      launch_k(tlc_quant_encode_kernel<kPathByte>, ntiles, kThreads, st, TLC_ARGS);
   }
 #undef TLC_ARGS
   return hipGetLastError();
@@ -1235,7 +1235,7 @@ hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uin
   const bool fused = x != nullptr;
   const bool al = aligned16(r) && (!fused || aligned16(x));
 #define TLC_LAUNCH(P, X)                                                                    \
-  tlc_quant_encode_chained_kernel<P, X><<<ntiles, kThreads, 0, st>>>(                        \
+  launch_k(tlc_quant_encode_chained_kernel<P, X>, ntiles, kThreads, st,                         \
       x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl)
   if (al && m % 4 == 0) {
     if (fused) TLC_LAUNCH(kPathVec, true); else TLC_LAUNCH(kPathVec, false);
@@ -1251,11 +1251,11 @@ hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uin
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
                              uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st) {
   const uint32_t nchunks = (ntiles + kChunkTiles - 1) / kChunkTiles;
-  tlc_zre_chunk_kernel<<<(nchunks + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+  launch_k(tlc_zre_chunk_kernel, (nchunks + kWaves - 1) / kWaves, kThreads, st,
       recs, ntiles, local_pre, chunk_agg, ctrl);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  tlc_zre_chunk_scan_kernel<<<1, kChunkScanThreads, 0, st>>>(nchunks, chunk_agg, ctrl);
+  launch_k(tlc_zre_chunk_scan_kernel, 1, kChunkScanThreads, st, nchunks, chunk_agg, ctrl);
   return hipGetLastError();
 }
 
@@ -1264,21 +1264,21 @@ hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
                               hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
-  tlc_zre_compact_kernel<<<(ntiles + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+  launch_k(tlc_zre_compact_kernel, (ntiles + kWaves - 1) / kWaves, kThreads, st,
       recs, chunk_pre, local_pre, slots, m, ntiles, out, fix, r, n, ctrl);
   return hipGetLastError();
 }
 
 hipError_t launch_absmax_check_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_blocks, uint32_t* partials, hipStream_t st) {
-  tlc_absmax_check_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials);
+  launch_k(tlc_absmax_check_batch_kernel, total_blocks, kThreads, st, descs, count, partials);
   return hipGetLastError();
 }
 
 hipError_t launch_accum_absmax_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_blocks, uint32_t* partials,
                                      const uint32_t* guard, hipStream_t st) {
-  tlc_accum_absmax_batch_kernel<<<total_blocks, kThreads, 0, st>>>(descs, count, partials,
+  launch_k(tlc_accum_absmax_batch_kernel, total_blocks, kThreads, st, descs, count, partials,
                                                                    guard);
   return hipGetLastError();
 }
@@ -1289,10 +1289,10 @@ hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
                                      hipStream_t st) {
   if (fused)
-    tlc_quant_encode_batch_kernel<true><<<total_tiles, kThreads, 0, st>>>(
+    launch_k(tlc_quant_encode_batch_kernel<true>, total_tiles, kThreads, st,
         descs, count, partials, results, status, ticket_base, epoch, ctrl);
   else
-    tlc_quant_encode_batch_kernel<false><<<total_tiles, kThreads, 0, st>>>(
+    launch_k(tlc_quant_encode_batch_kernel<false>, total_tiles, kThreads, st,
         descs, count, partials, results, status, ticket_base, epoch, ctrl);
   return hipGetLastError();
 }
@@ -1308,7 +1308,7 @@ hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, f
   const uint32_t blocks = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool vec = (m % 4 == 0) && aligned16(stochastic ? x : r);
 #define TLC_LAUNCH(V, S)                                                                      \
-  tlc_quant_pack_kernel<V, S><<<blocks, kThreads, 0, st>>>(x, r, n, m, s, seed, step, partials, \
+  launch_k(tlc_quant_pack_kernel<V, S>, blocks, kThreads, st, x, r, n, m, s, seed, step, partials, \
                                                            npartials, out, ctrl)
   if (stochastic) {
     if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);

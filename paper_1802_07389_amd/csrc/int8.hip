@@ -192,7 +192,7 @@ hipError_t launch_int8_quant(const float* x, float* r, uint64_t n, float s,
   const bool vec = aligned(r ? r : x, 16) && aligned(out, 4);
   if (r) x = nullptr;  // the buffer already holds x + r
 #define TLC_LAUNCH(V, R)                                                                 \
-  tlc_int8_quant_kernel<V, R><<<blocks, kThreads, 0, st>>>(x, r, n, s, partials, npartials, \
+  launch_k(tlc_int8_quant_kernel<V, R>, blocks, kThreads, st, x, r, n, s, partials, npartials, \
                                                            out, ctrl)
   if (r) {
     if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);
@@ -207,7 +207,7 @@ hipError_t launch_int8_dequant(const uint8_t* C, uint64_t n, float M, float* out
                                int accumulate, hipStream_t st) {
   const uint32_t blocks = int8_blocks(n);
   const bool vec = aligned(C, 4) && aligned(out, 16);
-#define TLC_LAUNCH(V, A) tlc_int8_dequant_kernel<V, A><<<blocks, kThreads, 0, st>>>(C, n, M, out)
+#define TLC_LAUNCH(V, A) launch_k(tlc_int8_dequant_kernel<V, A>, blocks, kThreads, st, C, n, M, out)
   if (accumulate) {
     if (vec) TLC_LAUNCH(true, true); else TLC_LAUNCH(false, true);
   } else {

@@ -21,6 +21,8 @@ namespace {
 thread_local char g_err[512] = "no error";
 }  // namespace
 
+thread_local LaunchEvents tlc::g_launch_events;
+
 int tlc::fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -202,19 +204,24 @@ void collect_timings(tlc_ctx* c) {
 }
 
 // Launch helper: brackets the launch with events when profiling is on.
+// The launcher's kernels record the event pair themselves (launch_k): the
+// first one's start and the last one's end.
 template <class F>
 int timed_launch(tlc_ctx* c, int kernel, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
   if (c->profiling && ((c->profile_mask >> kernel) & 1u)) {
     a = take_event(c);
     b = take_event(c);
-    if (a && b && hipEventRecord(a, c->stream) != hipSuccess) {
-      c->free_events.push_back(a);
-      c->free_events.push_back(b);
+    if (!a || !b) {
+      if (a) c->free_events.push_back(a);
+      if (b) c->free_events.push_back(b);
       a = b = nullptr;
     }
   }
+  g_launch_events = LaunchEvents{a, b};
   hipError_t e = launch();
+  const bool started = g_launch_events.start == nullptr;  // a kernel took the start event
+  g_launch_events = LaunchEvents{};
   if (e != hipSuccess) {
     c->broken = true;  // ticket counters may no longer match their bases
     if (a) c->free_events.push_back(a);
@@ -222,9 +229,9 @@ int timed_launch(tlc_ctx* c, int kernel, F&& launch) {
     return hip_fail(e, kKernelNames[kernel]);
   }
   if (a && b) {
-    if (hipEventRecord(b, c->stream) == hipSuccess) {
+    if (started) {
       c->pending.push_back(PendingTiming{kernel, a, b});
-    } else {
+    } else {  // the launcher dispatched no kernel
       c->free_events.push_back(a);
       c->free_events.push_back(b);
     }

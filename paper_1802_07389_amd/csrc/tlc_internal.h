@@ -2,6 +2,7 @@
 // the library (not part of the public ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -103,6 +104,31 @@ struct DecDesc {
   uint32_t pad[4];
 };
 static_assert(sizeof(DecDesc) == 64, "DecDesc is 64 bytes");
+
+// Kernel launches of the library.  While tlc_profile_* times a launcher
+// (timed_launch), g_launch_events holds its event pair: the first kernel
+// the launcher dispatches takes the start event and every kernel the stop
+// event (the last one's stands), recorded by the dispatches themselves
+// (hipExtLaunchKernelGGL), so timing adds no marker packets between
+// kernels.  Untimed launches are plain launches.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+template <class... Formals, class... Args>
+inline void launch_k(void (*kernel)(Formals...), dim3 grid, dim3 block, hipStream_t st,
+                     Args... args) {
+  LaunchEvents& ev = g_launch_events;
+  if (ev.start || ev.stop) {
+    hipEvent_t a = ev.start;
+    ev.start = nullptr;
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, a, ev.stop, 0, args...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+  }
+}
 
 // Launchers (encode.hip, decode.hip, int8.hip).  All return the hipError_t of the
 // launch.
