@@ -36,7 +36,7 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
                                            uint64_t* __restrict__ start,
                                            uint64_t* __restrict__ status, uint32_t floor,
                                            uint32_t lt, uint32_t epoch, Ctrl* __restrict__ ctrl,
-                                           IdxShared& sh) {
+                                           uint32_t* hfault, IdxShared& sh) {
   constexpr uint32_t kTile = kThreads * kBytes;
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint64_t j0 = (uint64_t)lt * kTile + threadIdx.x * kBytes;
@@ -81,8 +81,10 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
     if (lane == 0) {
       sh.excl = ex;
       sh.fault = fault ? 1u : 0u;
-      if (fault)
+      if (fault) {
         __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        host_put(hfault, 1u);
+      }
       const bool last_tile = (uint64_t)(lt + 1) * kTile >= c;
       if (last_tile && (fault || ex + agg != m)) {
         __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
@@ -124,18 +126,18 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
 __global__ __launch_bounds__(kThreads) void tlc_zre_index_kernel(
     const uint8_t* __restrict__ C, uint32_t c, uint32_t m, uint64_t* __restrict__ start,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
-    Ctrl* __restrict__ ctrl) {
+    Ctrl* __restrict__ ctrl, HostMirror hm) {
   __shared__ IdxShared sh;
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
   __syncthreads();
-  index_tile<kZreBytesPerThread>(C, c, m, start, status, 0, s_tile, epoch, ctrl, sh);
+  index_tile<kZreBytesPerThread>(C, c, m, start, status, 0, s_tile, epoch, ctrl, hm.fault, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
     const DecDesc* __restrict__ descs, uint32_t count, uint64_t* __restrict__ start,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
-    Ctrl* __restrict__ ctrl) {
+    Ctrl* __restrict__ ctrl, HostMirror hm) {
   __shared__ IdxShared sh;
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
   const uint32_t t = find_desc(descs, count, T, [](const DecDesc& d) { return d.tile0; });
   const DecDesc d = descs[t];
   index_tile<kZreBatchBytesPerThread>(d.C, d.c, d.m, start + d.range0, status, d.tile0,
-                                      T - d.tile0, epoch, ctrl, sh);
+                                      T - d.tile0, epoch, ctrl, hm.fault, sh);
 }
 
 // ---------------------------------------------------------------- expansion
@@ -707,9 +709,9 @@ static inline bool aligned16(const void* p) {
 
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                            uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+                            uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st) {
   launch_k(tlc_zre_index_kernel, ntiles, kThreads, st, C, c, m, start, status, ticket_base,
-                                                    epoch, ctrl);
+           epoch, ctrl, hm);
   return hipGetLastError();
 }
 
@@ -738,9 +740,9 @@ hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* s
 
 hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
                                   uint64_t* start, uint64_t* status, uint32_t ticket_base,
-                                  uint32_t epoch, Ctrl* ctrl, hipStream_t st) {
+                                  uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st) {
   launch_k(tlc_zre_index_batch_kernel, total_tiles, kThreads, st, descs, count, start, status,
-                                                               ticket_base, epoch, ctrl);
+           ticket_base, epoch, ctrl, hm);
   return hipGetLastError();
 }
 

@@ -20,6 +20,18 @@ __device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < 
 __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
+// A store into the pinned host readback (HostMirror) at system scope, so
+// that it is in host memory when the kernel completes; p null: nothing.
+__device__ __forceinline__ void host_put(uint32_t* p, uint32_t v) {
+  if (p) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+__device__ __forceinline__ void host_put_result(EncResult* h, uint32_t err, float scale) {
+  if (h) {
+    host_put(&h->err, err);
+    host_put(reinterpret_cast<uint32_t*>(&h->scale), __float_as_uint(scale));
+  }
+}
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ uint32_t abs_bits(float v) {
   return __float_as_uint(v) & 0x7fffffffu;

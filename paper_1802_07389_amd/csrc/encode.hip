@@ -395,6 +395,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
                                             uint8_t* __restrict__ out,
                                             uint64_t* __restrict__ status, uint32_t epoch,
                                             Ctrl* __restrict__ ctrl, EncResult* res,
+                                            EncResult* hres, uint32_t* hfault,
                                             EncShared& sh) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
@@ -442,8 +443,10 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
     if (lane == 0) {
       sh.excl = rs_from_payload(ex);
       sh.fault = fault ? 1u : 0u;
-      if (fault)
+      if (fault) {
         __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        host_put(hfault, 1u);
+      }
     }
   }
   __syncthreads();
@@ -471,7 +474,10 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
       tile_end >= tile_begin ? umin32(tile_end - tile_begin, kEncTile + 1) : 0u;
   for (uint32_t i = threadIdx.x; i < count; i += kThreads)
     if (tile_begin + i < m) out[tile_begin + i] = sh.out[i];
-  if (last_tile && threadIdx.x == 0) res->len = tile_end;
+  if (last_tile && threadIdx.x == 0) {
+    res->len = tile_end;
+    if (hres) host_put(&hres->len, tile_end);
+  }
 }
 
 // ---------------------------------------------------------------- single tensor, three passes
@@ -796,7 +802,7 @@ void tlc_quant_encode_kernel(
     float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ slots,
     TileRec* __restrict__ recs, uint2* __restrict__ fix, const uint16_t* __restrict__ summ,
-    Ctrl* __restrict__ ctrl) {
+    Ctrl* __restrict__ ctrl, HostMirror hm) {
   constexpr int kBytes = kEncTile / kThreads;  // zero-run bytes per thread
   static_assert(kBytes % 16 == 0, "threads read whole uint4s of quartic bytes");
   static_assert(!kTrit || kPath == kPathVec, "trits are kept on the float4 path");
@@ -825,6 +831,7 @@ void tlc_quant_encode_kernel(
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
+    host_put_result(hm.res, sc.bad, sc.M);
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
   if (kTrit) {
@@ -968,7 +975,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
     const TileRec* __restrict__ recs, const uint64_t* __restrict__ chunk_pre,
     const uint64_t* __restrict__ local_pre, const uint8_t* __restrict__ slots, uint32_t m,
     uint32_t ntiles, uint8_t* __restrict__ out, const uint2* __restrict__ fix,
-    float* __restrict__ r, uint64_t n, Ctrl* __restrict__ ctrl) {
+    float* __restrict__ r, uint64_t n, Ctrl* __restrict__ ctrl, HostMirror hm) {
   if (ctrl->enc.err) return;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t t = blockIdx.x * kWaves + (threadIdx.x >> 6);
@@ -1016,6 +1023,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_compact_kernel(
     if (rs_phase(T) && total >= 1u && total - 1u < m)
       out[total - 1u] = (uint8_t)rs_code(rs_phase(T));
     ctrl->enc.len = total;
+    if (hm.res) host_put(&hm.res->len, total);
   }
 }
 
@@ -1030,7 +1038,7 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
     const float* __restrict__ x, float* __restrict__ r, uint64_t n, uint32_t m, float s,
     const uint32_t* __restrict__ partials, uint32_t np, uint8_t* __restrict__ out,
     uint64_t* __restrict__ status, uint32_t ticket_base, uint32_t epoch,
-    Ctrl* __restrict__ ctrl) {
+    Ctrl* __restrict__ ctrl, HostMirror hm) {
   __shared__ EncShared sh;
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
@@ -1039,9 +1047,11 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_chained_kernel(
   if (tile == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
+    host_put_result(hm.res, sc.bad, sc.M);
   }
   if (sc.bad) return;  // NaN/Inf or overflow: no stream (the buffer as it was, or acc)
-  encode_tile<kPath, kX>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, sh);
+  encode_tile<kPath, kX>(x, r, n, m, sc, tile, 0, out, status, epoch, ctrl, &ctrl->enc, hm.res,
+                         hm.fault, sh);
 }
 
 // kX as for the chained kernel (partials: the check pass's).  The float4
@@ -1050,7 +1060,7 @@ template <bool kX>
 __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
     const EncDesc* __restrict__ descs, uint32_t count, const uint32_t* __restrict__ partials,
     EncResult* __restrict__ results, uint64_t* __restrict__ status, uint32_t ticket_base,
-    uint32_t epoch, Ctrl* __restrict__ ctrl) {
+    uint32_t epoch, Ctrl* __restrict__ ctrl, HostMirror hm) {
   __shared__ EncShared sh;
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->enc_ticket) - ticket_base;
@@ -1060,22 +1070,27 @@ __global__ __launch_bounds__(kThreads) void tlc_quant_encode_batch_kernel(
   const EncDesc d = descs[t];
   const Scale sc = finish_scale(partials + d.blk0, d.nblk, d.s, sh.red);
   const uint32_t lt = T - d.tile0;
+  EncResult* hres = hm.res ? hm.res + t : nullptr;
   if (lt == 0 && threadIdx.x == 0) {
     results[t].err = sc.bad;
     results[t].scale = sc.M;
-    if (sc.bad) results[t].len = 0u;
+    host_put_result(hres, sc.bad, sc.M);
+    if (sc.bad) {
+      results[t].len = 0u;
+      if (hres) host_put(&hres->len, 0u);
+    }
   }
   if (sc.bad) return;  // this tensor is refused; the others go on
   const bool xal = !kX || (d.vec & 4u);
   if ((d.vec & 1u) && xal)
     encode_tile<kPathVec, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch, ctrl,
-                              &results[t], sh);
+                              &results[t], hres, hm.fault, sh);
   else if ((d.vec & 2u) && xal)
     encode_tile<kPathShift, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch,
-                                ctrl, &results[t], sh);
+                                ctrl, &results[t], hres, hm.fault, sh);
   else
     encode_tile<kPathByte, kX>(d.x, d.r, d.n, d.m, sc, lt, d.tile0, d.out, status, epoch,
-                               ctrl, &results[t], sh);
+                               ctrl, &results[t], hres, hm.fault, sh);
 }
 
 // ---------------------------------------------------------------- comparison modes
@@ -1207,10 +1222,10 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n, uint32_t* p
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, uint2* fix, const uint16_t* summ, bool trit,
-                               Ctrl* ctrl, hipStream_t st) {
+                               Ctrl* ctrl, HostMirror hm, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   const bool al = aligned16(r);
-#define TLC_ARGS r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl
+#define TLC_ARGS r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl, hm
   if (trit) {
     if (!summ) return hipErrorInvalidValue;
     launch_k(tlc_quant_encode_kernel<kPathVec, true>, ntiles, kThreads, st, TLC_ARGS);
@@ -1231,12 +1246,12 @@ hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uin
                                        float s, const uint32_t* partials, uint32_t npartials,
                                        uint8_t* out, uint64_t* status, uint32_t ntiles,
                                        uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                                       hipStream_t st) {
+                                       HostMirror hm, hipStream_t st) {
   const bool fused = x != nullptr;
   const bool al = aligned16(r) && (!fused || aligned16(x));
 #define TLC_LAUNCH(P, X)                                                                    \
   launch_k(tlc_quant_encode_chained_kernel<P, X>, ntiles, kThreads, st,                         \
-      x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl)
+      x, r, n, m, s, partials, npartials, out, status, ticket_base, epoch, ctrl, hm)
   if (al && m % 4 == 0) {
     if (fused) TLC_LAUNCH(kPathVec, true); else TLC_LAUNCH(kPathVec, false);
   } else if (al) {
@@ -1262,10 +1277,10 @@ hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* loc
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
                               uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
-                              hipStream_t st) {
+                              HostMirror hm, hipStream_t st) {
   const uint32_t ntiles = (uint32_t)((m + kEncTile - 1) / kEncTile);
   launch_k(tlc_zre_compact_kernel, (ntiles + kWaves - 1) / kWaves, kThreads, st,
-      recs, chunk_pre, local_pre, slots, m, ntiles, out, fix, r, n, ctrl);
+      recs, chunk_pre, local_pre, slots, m, ntiles, out, fix, r, n, ctrl, hm);
   return hipGetLastError();
 }
 
@@ -1287,13 +1302,13 @@ hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
                                      bool fused, EncResult* results, uint64_t* status,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                                     hipStream_t st) {
+                                     HostMirror hm, hipStream_t st) {
   if (fused)
     launch_k(tlc_quant_encode_batch_kernel<true>, total_tiles, kThreads, st,
-        descs, count, partials, results, status, ticket_base, epoch, ctrl);
+        descs, count, partials, results, status, ticket_base, epoch, ctrl, hm);
   else
     launch_k(tlc_quant_encode_batch_kernel<false>, total_tiles, kThreads, st,
-        descs, count, partials, results, status, ticket_base, epoch, ctrl);
+        descs, count, partials, results, status, ticket_base, epoch, ctrl, hm);
   return hipGetLastError();
 }
 

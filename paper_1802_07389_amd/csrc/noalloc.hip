@@ -127,7 +127,7 @@ TLC_API int tlc_compress_noalloc(const float* tensor, float* residual, size_t n,
     e = launch_absmax_check(tensor, residual, n, partials_chk, &np, st);
     if (e == hipSuccess)
       e = launch_quant_encode_chained(tensor, residual, n, (uint32_t)m, s, partials_chk, np,
-                                      bytes, status, ntiles, 0u, 1u, ctrl, st);
+                                      bytes, status, ntiles, 0u, 1u, ctrl, HostMirror{}, st);
     if (e == hipSuccess) {
       tlc_noalloc_end_kernel<<<1, 64, 0, st>>>(scr, result);
       e = hipGetLastError();

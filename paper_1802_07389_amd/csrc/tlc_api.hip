@@ -85,6 +85,23 @@ bool spans_conflict(std::vector<Span>& v) {
   return false;
 }
 
+// spans_conflict for a call whose spans may repeat the previous call's
+// (`last`: the spans of the last call that passed, in call order).  A
+// training loop passes the same buffers every step: the list then equals
+// `last`, which was checked already, and the sort is skipped.  `last`
+// has the capacity of `v`, so nothing is allocated.
+bool spans_conflict_cached(std::vector<Span>& v, std::vector<Span>& last) {
+  if (v.size() == last.size() &&
+      std::equal(v.begin(), v.end(), last.begin(), [](const Span& a, const Span& b) {
+        return a.lo == b.lo && a.hi == b.hi && a.written == b.written;
+      }))
+    return false;
+  last = v;
+  if (!spans_conflict(v)) return false;
+  last.clear();
+  return true;
+}
+
 void add_span(std::vector<Span>& v, const void* p, size_t bytes, bool written) {
   if (bytes) v.push_back(Span{(uintptr_t)p, (uintptr_t)p + bytes, written});
 }
@@ -128,6 +145,7 @@ struct tlc_ctx {
   // pinned host memory: status readback, batch results, descriptor staging
   HostReadback* rb = nullptr;
   EncResult* host_results = nullptr;
+  HostReadback* rb_dev = nullptr;  // the same pinned memory, as the device addresses it
   uint8_t* staging = nullptr;  // kStagingSlots slots of max_tensors * 64 bytes
   hipEvent_t staging_done[kStagingSlots] = {};
   bool staging_used[kStagingSlots] = {};
@@ -146,6 +164,7 @@ struct tlc_ctx {
   std::vector<DecDesc> dec_host;
   std::vector<size_t> which;
   std::vector<Span> spans;  // address ranges of a batched call (3 per tensor)
+  std::vector<Span> enc_spans_ok, dec_spans_ok;  // the last batched calls that passed
   std::vector<hipEvent_t> free_events;
   std::vector<PendingTiming> pending;
   double total_ms[TLC_KERNEL_COUNT] = {};
@@ -280,12 +299,11 @@ int upload(tlc_ctx* c, void* dst, const void* src, size_t bytes) {
   return TLC_OK;
 }
 
-// Copies the control block's readback fields (and with `results` > 0 the
-// first `results` batch results after it) to the pinned block, then waits.
-int sync_and_read(tlc_ctx* c, size_t results = 0) {
-  const size_t bytes =
-      results ? sizeof(Ctrl) + results * sizeof(EncResult) : sizeof(HostReadback);
-  hipError_t e = hipMemcpyAsync(c->rb, c->ctrl, bytes, hipMemcpyDeviceToHost, c->stream);
+// Copies the control block's readback fields to the pinned block, then
+// waits.
+int sync_and_read(tlc_ctx* c) {
+  hipError_t e =
+      hipMemcpyAsync(c->rb, c->ctrl, sizeof(HostReadback), hipMemcpyDeviceToHost, c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(readback)");
   e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
@@ -293,9 +311,36 @@ int sync_and_read(tlc_ctx* c, size_t results = 0) {
   return TLC_OK;
 }
 
-// Waits for an encode and reports its result (the stream length and M).
-int finish_compress(tlc_ctx* c, const char* fn, size_t* bytes_len, float* scale) {
-  int st = sync_and_read(c);
+// Waits for the stream; for calls whose kernels wrote their result into the
+// pinned readback themselves (HostMirror), no copy is needed first.
+int sync_mirrored(tlc_ctx* c) {
+  hipError_t e = hipStreamSynchronize(c->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  collect_timings(c);
+  return TLC_OK;
+}
+
+// Where an encode's kernels mirror the single-tensor result and the fault
+// flag (the pinned readback, as the device addresses it).
+HostMirror enc_mirror(tlc_ctx* c) {
+  return HostMirror{&c->rb_dev->enc, &c->rb_dev->fault};
+}
+HostMirror fault_mirror(tlc_ctx* c) {
+  return HostMirror{nullptr, &c->rb_dev->fault};
+}
+// A batch: the per-tensor results follow the control block's slot in the
+// readback (as host_results does on the host).
+HostMirror batch_mirror(tlc_ctx* c) {
+  return HostMirror{
+      reinterpret_cast<EncResult*>(reinterpret_cast<uint8_t*>(c->rb_dev) + sizeof(Ctrl)),
+      &c->rb_dev->fault};
+}
+
+// Waits for an encode and reports its result (the stream length and M);
+// mirrored: the kernels wrote it into the readback (enc_mirror).
+int finish_compress(tlc_ctx* c, const char* fn, size_t* bytes_len, float* scale,
+                    bool mirrored = false) {
+  int st = mirrored ? sync_mirrored(c) : sync_and_read(c);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -424,6 +469,7 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
   if (e == hipSuccess)
     c->host_results =
         reinterpret_cast<EncResult*>(reinterpret_cast<uint8_t*>(c->rb) + sizeof(Ctrl));
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&c->rb_dev, c->rb, 0);
   if (e == hipSuccess)
     e = hipHostMalloc((void**)&c->staging, kStagingSlots * max_tensors * 64,
                       hipHostMallocDefault);
@@ -444,6 +490,8 @@ TLC_API int tlc_ctx_create_batch(tlc_ctx** out, size_t max_n, size_t max_tensors
     c->dec_host.reserve(max_tensors);
     c->which.reserve(max_tensors);
     c->spans.reserve(3 * max_tensors);
+    c->enc_spans_ok.reserve(3 * max_tensors);
+    c->dec_spans_ok.reserve(3 * max_tensors);
   } catch (...) {
     tlc_ctx_destroy(c);
     return fail(TLC_E_DEVICE, "tlc_ctx_create: out of host memory");
@@ -573,11 +621,12 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
     st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE_CHAINED, [&] {
       return launch_quant_encode_chained(in_place ? nullptr : tensor, residual, n, (uint32_t)m,
                                          s, partials, np, bytes, c->enc_status, ntiles,
-                                         c->enc_ticket_base, epoch, c->ctrl, c->stream);
+                                         c->enc_ticket_base, epoch, c->ctrl, enc_mirror(c),
+                                         c->stream);
     });
     if (st) return st;
     c->enc_ticket_base += ntiles;
-    return finish_compress(c, "tlc_compress", bytes_len, scale);
+    return finish_compress(c, "tlc_compress", bytes_len, scale, true);
   }
   uint32_t np = 0;
   bool trit = false;
@@ -585,7 +634,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_QUANT_ENCODE, [&] {
     return launch_quant_encode(residual, n, (uint32_t)m, s, c->partials, np, c->slots, c->recs,
-                               c->fix, summ, trit, c->ctrl, c->stream);
+                               c->fix, summ, trit, c->ctrl, enc_mirror(c), c->stream);
   });
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_CHUNKS, [&] {
@@ -594,10 +643,10 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_COMPACT, [&] {
     return launch_zre_compact(c->recs, c->chunk_agg, c->local_pre, c->slots, (uint32_t)m, bytes,
-                              c->fix, residual, n, c->ctrl, c->stream);
+                              c->fix, residual, n, c->ctrl, enc_mirror(c), c->stream);
   });
   if (st) return st;
-  return finish_compress(c, "tlc_compress", bytes_len, scale);
+  return finish_compress(c, "tlc_compress", bytes_len, scale, true);
 }
 
 namespace {
@@ -743,7 +792,7 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
     add_span(c->spans, residuals[t], ns[t] * 4, true);
     add_span(c->spans, bytes[t], quartic_len(ns[t]), true);
   }
-  if (spans_conflict(c->spans))
+  if (spans_conflict_cached(c->spans, c->enc_spans_ok))
     return fail(TLC_E_INVALID,
                 "tlc_compress_batch: a residual or byte buffer overlaps another tensor's buffer");
   std::vector<EncDesc>& d = c->enc_host;
@@ -803,11 +852,11 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
     return launch_quant_encode_batch(c->enc_descs, cnt, tiles,
                                      check ? c->partials_chk : c->partials, check,
                                      c->enc_results, c->enc_status, c->enc_ticket_base, epoch,
-                                     c->ctrl, c->stream);
+                                     c->ctrl, batch_mirror(c), c->stream);
   });
   if (st) return st;
   c->enc_ticket_base += tiles;
-  st = sync_and_read(c, cnt);
+  st = sync_mirrored(c);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -876,7 +925,8 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
   const uint32_t ntiles = (uint32_t)ceil_div(bytes_len, kZreTile);
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
     return launch_zre_index(bytes, (uint32_t)bytes_len, (uint32_t)m, c->start, c->dec_status,
-                            ntiles, c->dec_ticket_base, epoch, c->ctrl, c->stream);
+                            ntiles, c->dec_ticket_base, epoch, c->ctrl, fault_mirror(c),
+                            c->stream);
   });
   if (st) return st;
   c->dec_ticket_base += ntiles;
@@ -963,7 +1013,7 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
     add_span(c->spans, e.C, e.c, false);
     add_span(c->spans, e.out, e.n * 4, true);
   }
-  if (spans_conflict(c->spans))
+  if (spans_conflict_cached(c->spans, c->dec_spans_ok))
     return fail(TLC_E_INVALID, "tlc_decompress_batch: an output overlaps another stream's "
                                "output or bytes");
   if (tiles > c->dec_status_words || ranges > c->start_words)
@@ -980,7 +1030,8 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
-                                  c->dec_ticket_base, epoch, c->ctrl, c->stream);
+                                  c->dec_ticket_base, epoch, c->ctrl, fault_mirror(c),
+                                  c->stream);
   });
   if (st) return st;
   c->dec_ticket_base += tiles;
@@ -1042,7 +1093,8 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
-                                  c->dec_ticket_base, epoch, c->ctrl, c->stream);
+                                  c->dec_ticket_base, epoch, c->ctrl, fault_mirror(c),
+                                  c->stream);
   });
   if (st) return st;
   c->dec_ticket_base += tiles;

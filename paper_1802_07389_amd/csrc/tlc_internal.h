@@ -34,8 +34,8 @@ struct EncResult {
 };
 
 // Device control block (one per context, in the workspace).  The first 32
-// bytes are copied to pinned host memory after every encode and by
-// tlc_sync.
+// bytes are copied to pinned host memory by tlc_sync and after the encodes
+// whose kernels do not write their result there themselves (HostMirror).
 struct Ctrl {
   EncResult enc;           // single-tensor encode result
   uint32_t fault;          // sticky: a look-back wait timed out
@@ -52,6 +52,16 @@ struct HostReadback {
   uint32_t fault;
   uint32_t dec_corrupt;
   uint32_t pad[2];
+};
+
+// Device pointers into the pinned host readback that the encoders (and the
+// decoder's index scans, for the fault flag) also write a call's result to,
+// so that the host needs no copy before it reads it; null: not mirrored.
+// res: the result (one per tensor of a batch); fault: the look-back fault
+// flag.
+struct HostMirror {
+  EncResult* res = nullptr;
+  uint32_t* fault = nullptr;
 };
 
 // One tensor of a batched encode (device copy of the host's description).
@@ -149,20 +159,20 @@ hipError_t launch_accum_absmax(const float* x, float* r, uint64_t n,
 hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
                                const uint32_t* partials, uint32_t npartials, uint8_t* slots,
                                TileRec* recs, uint2* fix, const uint16_t* summ, bool trit,
-                               Ctrl* ctrl, hipStream_t st);
+                               Ctrl* ctrl, HostMirror hm, hipStream_t st);
 // x != NULL: the tiles form acc = x + r themselves from the check pass's
 // partials (r still holds the previous residual); x == NULL: r holds acc.
 hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uint32_t m,
                                        float s, const uint32_t* partials, uint32_t npartials,
                                        uint8_t* out, uint64_t* status, uint32_t ntiles,
                                        uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                                       hipStream_t st);
+                                       HostMirror hm, hipStream_t st);
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
                              uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
                               uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
-                              hipStream_t st);
+                              HostMirror hm, hipStream_t st);
 hipError_t launch_quant_pack(const float* x, float* r, uint64_t n, uint32_t m, float s,
                              int stochastic, uint64_t seed, uint64_t step,
                              const uint32_t* partials, uint32_t npartials, uint8_t* out,
@@ -182,17 +192,17 @@ hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      uint32_t total_tiles, const uint32_t* partials,
                                      bool fused, EncResult* results, uint64_t* status,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
-                                     hipStream_t st);
+                                     HostMirror hm, hipStream_t st);
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
-                            uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+                            uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st);
 hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
                                  uint64_t n, uint64_t m, float scale, float* out,
                                  int accumulate, uint32_t epoch, const Ctrl* ctrl,
                                  hipStream_t st);
 hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
                                   uint64_t* start, uint64_t* status, uint32_t ticket_base,
-                                  uint32_t epoch, Ctrl* ctrl, hipStream_t st);
+                                  uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st);
 hipError_t launch_expand_dequant_batch(const DecDesc* descs, uint32_t count,
                                        uint32_t total_ranges, const uint64_t* start,
                                        int accumulate, uint32_t epoch, const Ctrl* ctrl,

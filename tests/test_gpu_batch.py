@@ -230,6 +230,36 @@ def test_batch_overlapping_buffers_are_refused(bctx):
     assert torch.equal(o[:n], o[n:])
 
 
+def test_batch_overlap_check_after_repeated_calls(bctx):
+    """The same buffers passed again skip the overlap sort (the previous
+    call's ranges passed); a batch that differs is checked in full, a
+    refused one is not remembered, and the good batch then passes again."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    n = 7000
+    m = tlc.tlc_max_compressed_bytes(n)
+    x = torch.from_numpy(workloads.normal([991, 0], 2 * n, 1e-3)).cuda()
+    r = torch.zeros(2 * n, device="cuda")
+    b = torch.zeros(2 * m, dtype=torch.uint8, device="cuda")
+    o = torch.zeros(2 * n, device="cuda")
+    xp, rp, bp, op = x.data_ptr(), r.data_ptr(), b.data_ptr(), o.data_ptr()
+    good = ([xp, xp + 4 * n], [rp, rp + 4 * n], [n, n], [1.5, 1.5], [bp, bp + m], [m, m])
+    bad = ([xp, xp + 4 * n], [rp, rp + 4 * (n - 1)], [n, n], [1.5, 1.5], [bp, bp + m], [m, m])
+    for args in (good, good, bad, bad, good):
+        r_before = r.clone()
+        st, lens, scales, stat = tlc.tlc_compress_batch(bctx.handle, *args)
+        if args is bad:
+            assert st == tlc.TLC_E_INVALID and torch.equal(r, r_before)
+        else:
+            assert st == tlc.TLC_OK
+    for outs, ok in (([op, op + 4 * n], True), ([op, op + 4 * n], True),
+                     ([op, op + 4 * (n - 1)], False), ([op, op + 4 * (n - 1)], False),
+                     ([op, op + 4 * n], True)):
+        st = tlc.tlc_decompress_batch(bctx.handle, [bp, bp + m], lens, scales, [n, n], outs, 0)
+        assert st == (tlc.TLC_OK if ok else tlc.TLC_E_INVALID)
+        assert tlc.tlc_sync(bctx.handle) == tlc.TLC_OK
+
+
 def test_batch_decode_corrupt_writes_nothing(bctx):
     import torch
     from paper_1802_07389_amd import tlc
