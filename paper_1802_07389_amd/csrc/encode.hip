@@ -354,6 +354,7 @@ struct EncShared {
 };
 
 static_assert(kEncTile / kThreads == 16, "one uint4 of quartic bytes per thread");
+constexpr int kGroupsPerThread = kEncTile / 4 / kThreads;  // groups of 4 bytes per thread
 
 // Phase 1 of a tile (Eq. 2, residual write-back, quartic pack): the block
 // quantizes the 5 * tile_bytes accumulated values of quartic bytes
@@ -367,9 +368,32 @@ __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float
                                               uint64_t n, uint32_t m, const Scale& sc,
                                               uint64_t q0, uint32_t tile_bytes, uint8_t* q) {
   if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
-    for (uint32_t g = threadIdx.x; g * 4u < tile_bytes; g += kThreads)
+    // The thread's groups g = threadIdx.x + kThreads * it: the next group's
+    // ten loads are issued before the current group is quantized, so a
+    // tile takes about one memory round trip per thread instead of one per
+    // group (the groups' values are disjoint).  A group reaching into the
+    // padding of p4 takes the byte path.
+    auto ok = [&](uint32_t g) {
+      return g * 4u < tile_bytes && group4_full(n, m, q0 + g * 4u);
+    };
+    float4 cur[5];
+    if (ok(threadIdx.x)) load_group4<kX>(x, r, m, q0 + threadIdx.x * 4u, cur);
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it) {
+      const uint32_t g = threadIdx.x + kThreads * it;
+      if (g * 4u >= tile_bytes) break;
+      const uint64_t j = q0 + g * 4u;
+      float4 nxt[5];
+      const bool next = it + 1 < kGroupsPerThread && ok(g + kThreads);
+      if (next) load_group4<kX>(x, r, m, j + 4u * kThreads, nxt);
       *reinterpret_cast<uint32_t*>(q + g * 4u) =
-          quantize_group4<kX>(x, r, n, m, q0 + g * 4u, sc.M, sc.U);
+          ok(g) ? quantize_group4_loaded<kX>(r, m, j, cur, sc.M, sc.U)
+                : quantize_group4_bytes<kX>(x, r, n, m, j, sc.M, sc.U);
+      if (next) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k) cur[k] = nxt[k];
+      }
+    }
   } else if (kPath == kPathShift) {  // aligned float4 cells off the slice grid
     quantize_tile_shifted<kX>(x, r, n, m, q0, tile_bytes, sc.M, sc.U,
                               reinterpret_cast<uint32_t*>(q));
@@ -543,7 +567,6 @@ __device__ __forceinline__ void quantize_slice(const float4& a, uint32_t k, uint
 // A tile with at most this many float4 slices to load (of 5 * 1024) takes
 // the sparse form below.
 constexpr uint32_t kSparseSlices = 512;
-constexpr int kGroupsPerThread = kEncTile / 4 / kThreads;  // groups of 4 bytes per thread
 // Slices a thread of a sparse tile loads together (more go one at a time).
 constexpr int kSparseBatch = 4;
 
