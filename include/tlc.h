@@ -295,8 +295,10 @@ const char* tlc_last_error_string(void);
 #define TLC_KERNEL_ABSMAX 0         /* step 1 into the residual, partial max (Eq. 1) */
 #define TLC_KERNEL_QUANT_ENCODE 1   /* Eq. 1-2, residual, quartic pack, each tile's own
                                        zero-run encoding */
-#define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts */
-#define TLC_KERNEL_EXPAND_DEQUANT 3 /* zero-run expansion, quartic unpack, Eq. 3 */
+#define TLC_KERNEL_ZRE_INDEX 2      /* zero-run scan: where each output range starts
+                                       (a small stream's scan runs in the next kernel) */
+#define TLC_KERNEL_EXPAND_DEQUANT 3 /* zero-run expansion, quartic unpack, Eq. 3 (for a
+                                       small stream, with the scan in its first blocks) */
 #define TLC_KERNEL_ABSMAX_BATCH 4
 #define TLC_KERNEL_QUANT_ENCODE_BATCH 5
 #define TLC_KERNEL_ZRE_INDEX_BATCH 6

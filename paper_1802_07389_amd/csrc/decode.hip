@@ -5,7 +5,8 @@
 //       starts in the stream; checks the expanded length
 //   tlc_expand_dequant_kernel / _batch_kernel
 //       zero-run expansion into LDS, quartic unpack (Section 3.2), Eq. 3,
-//       optional accumulate
+//       optional accumulate; a small stream's decode runs the scan in the
+//       first blocks of the same launch
 //   tlc_expand_sum_kernel
 //       the same for P streams of one tensor, summed in stream order into
 //       one output in a single pass over it (server-side aggregation)
@@ -17,6 +18,27 @@
 namespace tlc {
 
 // ---------------------------------------------------------------- index scan
+// A start entry: (stream byte << 8 | how far into its expansion) with the
+// launch's epoch above it, published with an agent-scope atomic store like
+// a look-back status word, so that a reader in the same launch knows by the
+// tag alone that the entry is this launch's.  The byte index is below 2^30
+// (a stream is at most m < 2^30 bytes) and the offset below 14.
+constexpr int kStartPayloadBits = 38;
+constexpr uint64_t kStartPayloadMask = (uint64_t(1) << kStartPayloadBits) - 1u;
+static_assert(kDecEpochMax < (1u << (64 - kStartPayloadBits)), "the epoch fits above the payload");
+
+__device__ __forceinline__ uint64_t start_payload(uint64_t w) { return w & kStartPayloadMask; }
+__device__ __forceinline__ uint32_t start_epoch(uint64_t w) {
+  return (uint32_t)(w >> kStartPayloadBits);
+}
+
+// The last index tile's verdict on the stream, for the same launch's
+// expanding blocks: epoch << 1 | 1 when the expansion total is not m (or a
+// look-back gave up), epoch << 1 when it is.
+__device__ __forceinline__ uint32_t verdict_word(uint32_t epoch, bool bad) {
+  return (epoch << 1) | (bad ? 1u : 0u);
+}
+
 struct IdxShared {
   uint32_t red[kWaves];
   uint32_t fault;
@@ -86,11 +108,15 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
         host_put(hfault, 1u);
       }
       const bool last_tile = (uint64_t)(lt + 1) * kTile >= c;
-      if (last_tile && (fault || ex + agg != m)) {
+      const bool bad = fault || ex + agg != m;
+      if (last_tile && bad) {
         __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&ctrl->dec_corrupt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      if (last_tile)
+        __hip_atomic_store(&ctrl->dec_verdict, verdict_word(epoch, bad), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   __syncthreads();
@@ -119,7 +145,7 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
         rel += len;
       }
     }
-    start[k] = ((j0 + hit) << 8) | into;
+    status_publish(&start[k], ((uint64_t)epoch << kStartPayloadBits) | ((j0 + hit) << 8) | into);
   }
 }
 
@@ -150,33 +176,31 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
 }
 
 // ---------------------------------------------------------------- expansion
-// One past the last stream byte that reaches into range k (starts: the
-// stream's start entries).
-__device__ __forceinline__ uint32_t range_end(const uint64_t* __restrict__ starts, uint32_t k,
-                                              uint64_t m, uint32_t c) {
-  if ((uint64_t)(k + 1) * kDecRange < m) {
-    const uint64_t s1 = starts[k + 1];
-    return umin32((uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u), c);
-  }
-  return c;
-}
-
 // The stream bytes that expand into range k of one stream: the first one,
 // how far into its expansion the range starts, and how many (at most
 // kDecRange: the range's qn quartic bytes come from at most qn stream bytes).
+// s0, s1: the payloads of the start entries of ranges k and k + 1 (s1 is
+// not read when range k is the stream's last).
 struct Slice {
   uint32_t i0, skip, count;
 };
 
-__device__ __forceinline__ Slice slice_of(const uint64_t* __restrict__ starts, uint32_t k,
-                                          uint64_t m, uint32_t c) {
-  const uint64_t s0 = starts[k];
+__device__ __forceinline__ Slice slice_from(uint64_t s0, uint64_t s1, bool last, uint32_t c) {
   Slice r;
   r.i0 = (uint32_t)(s0 >> 8);
   r.skip = (uint32_t)(s0 & 255u);
-  const uint32_t i1 = range_end(starts, k, m, c);
+  // one past the last stream byte that reaches into the range
+  const uint32_t i1 = last ? c : umin32((uint32_t)(s1 >> 8) + ((s1 & 255u) ? 1u : 0u), c);
   r.count = i1 > r.i0 ? umin32(i1 - r.i0, kDecRange) : 0u;
   return r;
+}
+
+// The same from the start entries of a stream that an earlier launch wrote.
+__device__ __forceinline__ Slice slice_of(const uint64_t* __restrict__ starts, uint32_t k,
+                                          uint64_t m, uint32_t c) {
+  const bool last = (uint64_t)(k + 1) * kDecRange >= m;
+  return slice_from(start_payload(starts[k]), last ? 0u : start_payload(starts[k + 1]), last,
+                    c);
 }
 
 constexpr int kSliceBytes = kDecRange / kThreads;  // stream bytes per thread (at most)
@@ -428,35 +452,138 @@ __device__ __forceinline__ void dequant_range(const uint8_t* s_q, uint64_t q0, u
   }
 }
 
-// One block = quartic bytes [k*kDecRange, (k+1)*kDecRange) of one stream.
-template <int kPath, bool kAcc, bool kNT>
+// Lane 0 of an expanding block: waits for a start entry of this launch (its
+// epoch tag) and returns its payload.  Gives up (kNoStart) when the
+// launch's verdict says the stream is bad (its entries may never come) or
+// the wait runs past kSpinLimit (then the fault flag is set).
+constexpr uint64_t kNoStart = ~uint64_t(0);  // above any payload
+
+// Up to a few thousand resident blocks wait at once, so they poll gently:
+// a pause of 8 * 64 clocks between reads, and the verdict on every fourth.
+__device__ uint64_t wait_start(const uint64_t* p, uint32_t epoch, Ctrl* ctrl, uint32_t* hfault) {
+  for (uint32_t spins = 0;; ++spins) {
+    const uint64_t v = status_read(p);
+    if (start_epoch(v) == epoch) return start_payload(v);
+    if ((spins & 3u) == 3u) {
+      const uint32_t vd = __hip_atomic_load(&ctrl->dec_verdict, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+      if (vd == verdict_word(epoch, true)) return kNoStart;
+    }
+    if (spins > kSpinLimit) {
+      __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      host_put(hfault, 1u);
+      return kNoStart;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+// Lane 0 of an expanding block: waits for the launch's verdict; true when
+// the stream is good.
+__device__ bool wait_verdict(uint32_t epoch, Ctrl* ctrl, uint32_t* hfault) {
+  for (uint32_t spins = 0;; ++spins) {
+    const uint32_t vd = __hip_atomic_load(&ctrl->dec_verdict, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+    if ((vd >> 1) == epoch) return (vd & 1u) == 0u;
+    if (spins > kSpinLimit) {
+      __hip_atomic_store(&ctrl->fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      host_put(hfault, 1u);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+// One stream's expansion: range k (quartic bytes [k*kDecRange,
+// (k+1)*kDecRange)) per block.
+// kFused = false: the scan ran in its own launch before; range k =
+// blockIdx.x, the start entries are read as they are, and a corrupt stream
+// (flagged by the scan) is left alone.
+// kFused = true (small decodes, every block resident at once): blocks take
+// tickets in order; the first `ntiles` run the scan (index_tile), every
+// later one expands range k = ticket - ntiles.  An expanding block issues
+// the output loads it can, waits for its start entries (tagged with the
+// launch's epoch, written by scan tiles, which hold lower tickets and so
+// already run), expands the range into LDS, and waits for the last scan
+// tile's verdict before it stores anything: a corrupt stream leaves out
+// untouched.  The scan's latency then overlaps the expanding blocks' work
+// and no kernel boundary separates the two steps.
+template <int kPath, bool kAcc, bool kNT, bool kFused>
 __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
-    const uint8_t* __restrict__ C, uint32_t c, const uint64_t* __restrict__ start,
-    uint64_t n, uint64_t m, float M, float* __restrict__ out, uint32_t epoch,
-    const Ctrl* __restrict__ ctrl) {
+    const uint8_t* __restrict__ C, uint32_t c, uint64_t* __restrict__ start,
+    uint64_t* __restrict__ status, uint32_t ntiles, uint32_t ticket_base, uint64_t n,
+    uint64_t m, float M, float* __restrict__ out, uint32_t epoch, Ctrl* __restrict__ ctrl,
+    HostMirror hm) {
+  __shared__ IdxShared ish;
   __shared__ uint32_t red[kWaves];
   __shared__ __align__(16) uint8_t s_q[kDecRange];
-  if (ctrl->dec_bad_epoch == epoch) return;  // corrupt stream: out untouched
-  const uint32_t k = blockIdx.x;
+  __shared__ uint32_t s_t, s_ok;
+  __shared__ uint64_t s_se[2];
+  uint32_t k;
+  if constexpr (kFused) {
+    if (threadIdx.x == 0) s_t = take_ticket(&ctrl->dec_ticket) - ticket_base;
+    __syncthreads();
+    const uint32_t T = s_t;
+    if (T < ntiles) {
+      index_tile<kZreBatchBytesPerThread>(C, c, (uint32_t)m, start, status, 0, T, epoch, ctrl,
+                                          hm.fault, ish);
+      return;
+    }
+    k = T - ntiles;
+  } else {
+    if (ctrl->dec_bad_epoch == epoch) return;  // corrupt stream: out untouched
+    k = blockIdx.x;
+  }
   const uint64_t q0 = (uint64_t)k * kDecRange;
   const uint32_t qn = (uint32_t)umin64(kDecRange, m - q0);
-  if (kPath == kPathShift && kAcc && kNT) {
-    // large outputs: the first two partitions' loads overlap the expansion
-    // (on gfx950 15 us of 410 on a 2^28-value decode; outputs that fit the
-    // cache gained nothing)
-    float4 p0[kSweepCells], p1[kSweepCells];
+  const bool last = q0 + kDecRange >= m;
+  constexpr bool kPre = kPath == kPathShift && kAcc && kNT;
+  // large outputs: the first two partitions' loads go out before the
+  // expansion (on gfx950 15 us of 410 on a 2^28-value decode; outputs that
+  // fit the cache gained nothing)
+  float4 p0[kPre ? kSweepCells : 1], p1[kPre ? kSweepCells : 1];
+  if constexpr (kPre) {
     sweep_preload<0, kNT>(q0, qn, n, m, out, p0);
     sweep_preload<1, kNT>(q0, qn, n, m, out, p1);
-    const bool dense = expand_range(C, c, start, k, m, qn, s_q, red) > kDenseLiterals;
+  }
+  Slice sl;
+  if constexpr (kFused) {
+    if (threadIdx.x == 0) {
+      const uint64_t s0 = wait_start(&start[k], epoch, ctrl, hm.fault);
+      const uint64_t s1 =
+          last || s0 == kNoStart ? 0u : wait_start(&start[k + 1], epoch, ctrl, hm.fault);
+      s_se[0] = s0;
+      s_se[1] = s1;
+      s_ok = s0 != kNoStart && s1 != kNoStart ? 1u : 0u;
+    }
+    __syncthreads();
+    if (!s_ok) return;
+    sl = slice_from(s_se[0], s_se[1], last, c);
+  } else {
+    sl = slice_of(start, k, m, c);
+  }
+  const uint32_t lo = threadIdx.x * kSliceBytes;
+  const uint32_t cnt = lo < sl.count ? umin32(kSliceBytes, sl.count - lo) : 0u;
+  uint8_t b[kSliceBytes];
+#pragma unroll
+  for (int i = 0; i < kSliceBytes; ++i) b[i] = (uint32_t)i < cnt ? C[sl.i0 + lo + i] : (uint8_t)0;
+  const bool dense =
+      expand_slice([&](int i) -> uint32_t { return b[i]; }, cnt, sl.skip, qn, s_q, red) >
+      kDenseLiterals;
+  if constexpr (kFused) {
+    if (threadIdx.x == 0) s_ok = wait_verdict(epoch, ctrl, hm.fault) ? 1u : 0u;
+    __syncthreads();
+    if (!s_ok) return;  // a corrupt stream: out untouched
+  }
+  if constexpr (kPre) {
     dequant_partition_shifted<0, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, dense, p0);
     dequant_partition_shifted<1, kAcc, kNT, true>(s_q, q0, qn, n, m, M, out, dense, p1);
     dequant_partition_shifted<2, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
     dequant_partition_shifted<3, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
     dequant_partition_shifted<4, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
-    return;
+  } else {
+    dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
   }
-  const bool dense = expand_range(C, c, start, k, m, qn, s_q, red) > kDenseLiterals;
-  dequant_range<kPath, kAcc, kNT>(s_q, q0, qn, n, m, M, out, dense);
 }
 
 template <bool kAcc>
@@ -715,25 +842,32 @@ hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* 
   return hipGetLastError();
 }
 
-hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
-                                 uint64_t n, uint64_t m, float scale, float* out,
-                                 int accumulate, uint32_t epoch, const Ctrl* ctrl,
-                                 hipStream_t st) {
+hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, uint64_t* start,
+                                 uint64_t* status, uint32_t ticket_base, uint64_t n, uint64_t m,
+                                 float scale, float* out, int accumulate, uint32_t epoch,
+                                 Ctrl* ctrl, HostMirror hm, hipStream_t st) {
   const bool al = aligned16(out);
   const bool nt = al && n * sizeof(float) >= kNtMinBytes;
-  const uint32_t blocks = (uint32_t)((m + kDecRange - 1) / kDecRange);
-#define TLC_LAUNCH(V, A, N)                                                                 \
-  launch_k(tlc_expand_dequant_kernel<V, A, N>, blocks, kThreads, st, C, c, start, n, m, scale, \
-                                                                  out, epoch, ctrl)
+  const bool fused = decode_fused(c, m);
+  const uint32_t ntiles = fused ? decode_index_tiles(c, m) : 0u;
+  const uint32_t blocks = ntiles + decode_ranges(m);
+#define TLC_LAUNCH(V, A, N, F)                                                              \
+  launch_k(tlc_expand_dequant_kernel<V, A, N, F>, blocks, kThreads, st, C, c, start, status, \
+           ntiles, ticket_base, n, m, scale, out, epoch, ctrl, hm)
+#define TLC_LAUNCH2(V, A, N) \
+  if (fused) TLC_LAUNCH(V, A, N, true); else TLC_LAUNCH(V, A, N, false)
   if (nt) {
-    if (accumulate) TLC_LAUNCH(kPathShift, true, true); else TLC_LAUNCH(kPathShift, false, true);
+    // outputs of 512 MiB or more have far more blocks than a fused launch takes
+    if (accumulate) TLC_LAUNCH(kPathShift, true, true, false);
+    else TLC_LAUNCH(kPathShift, false, true, false);
   } else if (al && m % 4 == 0) {
-    if (accumulate) TLC_LAUNCH(kPathVec, true, false); else TLC_LAUNCH(kPathVec, false, false);
+    if (accumulate) { TLC_LAUNCH2(kPathVec, true, false); } else { TLC_LAUNCH2(kPathVec, false, false); }
   } else if (al) {
-    if (accumulate) TLC_LAUNCH(kPathShift, true, false); else TLC_LAUNCH(kPathShift, false, false);
+    if (accumulate) { TLC_LAUNCH2(kPathShift, true, false); } else { TLC_LAUNCH2(kPathShift, false, false); }
   } else {
-    if (accumulate) TLC_LAUNCH(kPathByte, true, false); else TLC_LAUNCH(kPathByte, false, false);
+    if (accumulate) { TLC_LAUNCH2(kPathByte, true, false); } else { TLC_LAUNCH2(kPathByte, false, false); }
   }
+#undef TLC_LAUNCH2
 #undef TLC_LAUNCH
   return hipGetLastError();
 }

@@ -276,6 +276,20 @@ int next_epoch(tlc_ctx* c, uint32_t* epoch, uint32_t max_epoch, uint64_t* status
   return TLC_OK;
 }
 
+// The decoder's epoch.  Its wrap also clears what carries a decode epoch
+// besides the status words: the corrupt-stream mark, the single-stream
+// verdict and the start entries.
+int next_dec_epoch(tlc_ctx* c, uint32_t* out) {
+  if (c->dec_epoch >= kDecEpochMax) {
+    hipError_t e = hipMemsetAsync(&c->ctrl->dec_verdict, 0, sizeof(uint32_t), c->stream);
+    if (e == hipSuccess)
+      e = hipMemsetAsync(c->start, 0, c->start_words * sizeof(uint64_t), c->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync(decoder epoch wrap)");
+  }
+  return next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
+                    &c->ctrl->dec_bad_epoch, out);
+}
+
 // Copies `bytes` of host descriptors to `dst` on the stream through a
 // pinned staging slot.  A slot is reused only after its previous copy has
 // executed, so back-to-back asynchronous calls cannot overwrite a
@@ -919,21 +933,25 @@ TLC_API int tlc_decompress(tlc_ctx* c, const uint8_t* bytes, size_t bytes_len, f
   st = dev.status();
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
-                  &c->ctrl->dec_bad_epoch, &epoch);
+  st = next_dec_epoch(c, &epoch);
   if (st) return st;
-  const uint32_t ntiles = (uint32_t)ceil_div(bytes_len, kZreTile);
-  st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
-    return launch_zre_index(bytes, (uint32_t)bytes_len, (uint32_t)m, c->start, c->dec_status,
-                            ntiles, c->dec_ticket_base, epoch, c->ctrl, fault_mirror(c),
-                            c->stream);
+  if (!decode_fused(bytes_len, m)) {  // the scan in a launch of its own
+    const uint32_t ntiles = decode_index_tiles(bytes_len, m);
+    st = timed_launch(c, TLC_KERNEL_ZRE_INDEX, [&] {
+      return launch_zre_index(bytes, (uint32_t)bytes_len, (uint32_t)m, c->start, c->dec_status,
+                              ntiles, c->dec_ticket_base, epoch, c->ctrl, fault_mirror(c),
+                              c->stream);
+    });
+    if (st) return st;
+  }
+  st = timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
+    return launch_expand_dequant(bytes, (uint32_t)bytes_len, c->start, c->dec_status,
+                                 c->dec_ticket_base, n, m, scale, out, accumulate, epoch,
+                                 c->ctrl, fault_mirror(c), c->stream);
   });
   if (st) return st;
-  c->dec_ticket_base += ntiles;
-  return timed_launch(c, TLC_KERNEL_EXPAND_DEQUANT, [&] {
-    return launch_expand_dequant(bytes, (uint32_t)bytes_len, c->start, n, m, scale, out,
-                                 accumulate, epoch, c->ctrl, c->stream);
-  });
+  c->dec_ticket_base += decode_tickets(bytes_len, m);
+  return TLC_OK;
 }
 
 TLC_API int tlc_decompress_ex(tlc_ctx* c, int mode, const uint8_t* bytes, size_t bytes_len,
@@ -1025,8 +1043,7 @@ TLC_API int tlc_decompress_batch(tlc_ctx* c, size_t count, const uint8_t* const*
   st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
-                  &c->ctrl->dec_bad_epoch, &epoch);
+  st = next_dec_epoch(c, &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,
@@ -1088,8 +1105,7 @@ TLC_API int tlc_decompress_sum(tlc_ctx* c, size_t count, const uint8_t* const* b
   st = upload(c, c->dec_descs, d.data(), cnt * sizeof(DecDesc));
   if (st) return st;
   uint32_t epoch = 0;
-  st = next_epoch(c, &c->dec_epoch, kDecEpochMax, c->dec_status, c->dec_status_words,
-                  &c->ctrl->dec_bad_epoch, &epoch);
+  st = next_dec_epoch(c, &epoch);
   if (st) return st;
   st = timed_launch(c, TLC_KERNEL_ZRE_INDEX_BATCH, [&] {
     return launch_zre_index_batch(c->dec_descs, cnt, tiles, c->start, c->dec_status,

@@ -14,8 +14,10 @@ namespace tlc {
 constexpr int kThreads = 256;             // every kernel: 4 wave64 per block
 constexpr int kZreBytesPerThread = 64;    // zero-run index scan: four uint4 per thread
 constexpr int kZreTile = kThreads * kZreBytesPerThread;  // 16384 stream bytes per tile
-// the batched scans, over many streams that mostly fit one tile, take half
-// as many bytes per thread (shorter per-thread loops on short streams)
+// the batched scans, over many streams that mostly fit one tile, and the
+// index role of the single-launch decode take half as many bytes per
+// thread (shorter per-thread loops on short streams; the fused decode
+// kernel then stays within the expanding blocks' 64 registers)
 constexpr int kZreBatchBytesPerThread = 32;
 constexpr int kZreBatchTile = kThreads * kZreBatchBytesPerThread;  // 8192
 constexpr int kEncTile = 4096;            // quartic bytes per encoder tile
@@ -43,7 +45,8 @@ struct Ctrl {
   uint32_t dec_bad_epoch;  // epoch of the last decode launch with a bad stream
   uint32_t enc_ticket;     // tile tickets of the encoder
   uint32_t dec_ticket;     // tile tickets of the zero-run index scan
-  uint32_t pad[55];
+  uint32_t dec_verdict;    // epoch << 1 | bad of the last single-stream decode's stream
+  uint32_t pad[54];
 };
 static_assert(sizeof(Ctrl) == 256, "Ctrl is one 256-byte slot");
 
@@ -193,13 +196,36 @@ hipError_t launch_quant_encode_batch(const EncDesc* descs, uint32_t count,
                                      bool fused, EncResult* results, uint64_t* status,
                                      uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
                                      HostMirror hm, hipStream_t st);
+// One stream's decode.  Small decodes (at most kFusedMaxBlocks blocks in
+// all, so every block is resident at once) run in one launch: the first
+// blocks scan the stream (kZreBatchTile bytes each), the others expand.
+// Larger ones run the scan (kZreTile bytes per block), then the expansion:
+// thousands of expanding blocks waiting inside one launch for a scan of
+// hundreds of tiles slowed it down more than the launch boundary costs.
+constexpr uint32_t kFusedMaxBlocks = 256;
+inline uint32_t decode_ranges(uint64_t m) { return (uint32_t)((m + kDecRange - 1) / kDecRange); }
+inline bool decode_fused(uint64_t c, uint64_t m) {
+  return (c + kZreBatchTile - 1) / kZreBatchTile + decode_ranges(m) <= kFusedMaxBlocks;
+}
+// The scan's tiles; the tickets a decode takes (the host advances the
+// decoder's ticket base by decode_tickets(c, m)).
+inline uint32_t decode_index_tiles(uint64_t c, uint64_t m) {
+  const uint64_t tile = decode_fused(c, m) ? kZreBatchTile : kZreTile;
+  return (uint32_t)((c + tile - 1) / tile);
+}
+inline uint32_t decode_tickets(uint64_t c, uint64_t m) {
+  return decode_index_tiles(c, m) + (decode_fused(c, m) ? decode_ranges(m) : 0u);
+}
+// The scan of one stream (not decode_fused), then its expansion; or, when
+// decode_fused, both in the expansion's launch (ticket_base then counts
+// the scan's tiles too).
 hipError_t launch_zre_index(const uint8_t* C, uint32_t c, uint32_t m, uint64_t* start,
                             uint64_t* status, uint32_t ntiles, uint32_t ticket_base,
                             uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st);
-hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, const uint64_t* start,
-                                 uint64_t n, uint64_t m, float scale, float* out,
-                                 int accumulate, uint32_t epoch, const Ctrl* ctrl,
-                                 hipStream_t st);
+hipError_t launch_expand_dequant(const uint8_t* C, uint32_t c, uint64_t* start,
+                                 uint64_t* status, uint32_t ticket_base, uint64_t n, uint64_t m,
+                                 float scale, float* out, int accumulate, uint32_t epoch,
+                                 Ctrl* ctrl, HostMirror hm, hipStream_t st);
 hipError_t launch_zre_index_batch(const DecDesc* descs, uint32_t count, uint32_t total_tiles,
                                   uint64_t* start, uint64_t* status, uint32_t ticket_base,
                                   uint32_t epoch, Ctrl* ctrl, HostMirror hm, hipStream_t st);

@@ -4,8 +4,9 @@ pseudo-random 0 to about 25 us before every status-word publish.  Each
 user of the status words runs here once against the CPU oracle, bit for
 bit: the chained single-tensor encoder, the three-pass encoder's
 tile-prefix scan, the batched encoder, and the decoder's index scan
-(single, batched and summed decodes).  Every wait is bounded; a timeout
-would surface as TLC_E_DEVICE, not a hang."""
+(single, batched and summed decodes; the single decode's blocks also wait
+for their start entries and the stream's verdict).  Every wait is bounded;
+a timeout would surface as TLC_E_DEVICE, not a hang."""
 import importlib.util
 import os
 
@@ -105,8 +106,10 @@ def test_batched_encoder(ctx):
 
 def test_decoder_index_scans(ctx):
     """Streams of synthetic quartic bytes with half of them data bytes, so
-    each stream spans about 80 index tiles of the single decode (160 of the
-    batched one); single, batched and summed decodes with accumulate."""
+    each stream spans about 160 index tiles; single, batched and summed
+    decodes with accumulate.  The single decode's expanding blocks wait for
+    start entries that are published late and out of order (the stress
+    build delays them like status words)."""
     import torch
     n = (1 << 23) + 3
     m = oracle.quartic_len(n)

@@ -116,10 +116,14 @@ def test_all_zero_tensors(ctx, n):
         assert 4 * n / C.size == 280
 
 
-@pytest.mark.parametrize("m", [16383, 16384, 16385, 2 * 16384 - 1, 2 * 16384 + 1, 3 * 16384 + 5])
+@pytest.mark.parametrize("m", [8191, 8192, 8193, 2 * 8192 - 1, 2 * 8192 + 1, 3 * 8192 + 5,
+                               16383, 16384, 16385, 2 * 16384 + 1, 200 * 4096 + 7,
+                               300 * 4096 + 1])
 def test_index_scan_tile_edges(ctx, m):
-    """Streams ending at and around the 16384-byte tiles of the zero-run
-    index scan.  All-ones tensors quantize to q = 1 everywhere (M = 1 at
+    """Streams ending at and around the tiles of the zero-run index scan:
+    8192 bytes when the scan runs in the first blocks of the decode's
+    single launch (small streams), 16384 in its own launch (the last two
+    sizes, with more than 256 blocks in all).  All-ones tensors quantize to q = 1 everywhere (M = 1 at
     s = 1), so every quartic byte is 242 and the stream is exactly m bytes,
     with range starts on tile edges; then zero groups turn random spans of
     bytes into 121, whose run codes land across the edges."""
