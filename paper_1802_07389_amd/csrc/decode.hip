@@ -674,12 +674,7 @@ __device__ __forceinline__ void wave_expand(const SumSlice& sl, const SliceWords
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       if ((uint32_t)i < cnt) len += expanded_len(slice_word_byte(w, i));
-    uint32_t incl = len;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const uint32_t o = __shfl_up(incl, d, 64);
-      if (lane >= (uint32_t)d) incl += o;
-    }
+    const uint32_t incl = wave_incl_scan(len, 0u, OpAdd());
     int pos = base + (int)(incl - len);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -689,7 +684,7 @@ __device__ __forceinline__ void wave_expand(const SumSlice& sl, const SliceWords
         pos += (int)expanded_len(x);
       }
     }
-    base += (int)__shfl(incl, 63, 64);
+    base += (int)wave_last(incl);
   }
 }
 

@@ -37,10 +37,69 @@ __device__ __forceinline__ uint32_t abs_bits(float v) {
   return __float_as_uint(v) & 0x7fffffffu;
 }
 
+// ---------------------------------------------------------------- wave scans
+// Lane moves of the data-parallel primitives (DPP) of GFX9 parts, which
+// stay in the vector ALU instead of a round trip through the LDS crossbar
+// (ds_bpermute): row_shr:k hands lane i - k of the same 16-lane row to lane
+// i, row_bcast:15 the last lane of each row to the whole next row,
+// row_bcast:31 lane 31 to rows 2 and 3, wave_shr:1 lane i - 1 to lane i.
+// A lane whose source lies outside its row (or the wave), or whose row is
+// not in the row mask, gets `old` instead.  Every lane of the wave must be
+// active.
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowShr2 = 0x112;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowShr8 = 0x118;
+constexpr int kDppWaveShr1 = 0x138;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, kCtrl, kRowMask, 0xf, false);
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_mov(uint64_t old, uint64_t v) {
+  return (uint64_t)dpp_mov<kCtrl, kRowMask>((uint32_t)old, (uint32_t)v) |
+         ((uint64_t)dpp_mov<kCtrl, kRowMask>((uint32_t)(old >> 32), (uint32_t)(v >> 32)) << 32);
+}
+
+// Inclusive scan in lane order under an associative op with identity e,
+// op(a, b) being segment a followed by segment b: doubling shifts inside
+// each row, then the rows' totals carried to the rows after them.
+template <class T, class Op>
+__device__ __forceinline__ T wave_incl_scan(T x, T e, Op op) {
+  x = op(dpp_mov<kDppRowShr1, 0xf>(e, x), x);
+  x = op(dpp_mov<kDppRowShr2, 0xf>(e, x), x);
+  x = op(dpp_mov<kDppRowShr4, 0xf>(e, x), x);
+  x = op(dpp_mov<kDppRowShr8, 0xf>(e, x), x);
+  x = op(dpp_mov<kDppRowBcast15, 0xa>(e, x), x);
+  x = op(dpp_mov<kDppRowBcast31, 0xc>(e, x), x);
+  return x;
+}
+
+// Lane i - 1's value (e in lane 0): an inclusive scan made exclusive.
+template <class T>
+__device__ __forceinline__ T wave_prev_lane(T x, T e) {
+  return dpp_mov<kDppWaveShr1, 0xf>(e, x);
+}
+
+// Lane 63's value, the same in every lane.
+__device__ __forceinline__ uint32_t wave_last(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+struct OpAdd {
+  __device__ __forceinline__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; }
+};
+struct OpMax {
+  __device__ __forceinline__ uint32_t operator()(uint32_t a, uint32_t b) const {
+    return a > b ? a : b;
+  }
+};
+
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, d, 64));
-  return v;
+  return wave_last(wave_incl_scan(v, 0u, OpMax()));
 }
 
 // Block-wide max; every thread gets the result.  Uses lds[kWaves] and one
@@ -62,12 +121,7 @@ struct ScanU32 {
 };
 __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  uint32_t incl = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t o = __shfl_up(incl, d, 64);
-    if (lane >= (uint32_t)d) incl += o;
-  }
+  const uint32_t incl = wave_incl_scan(v, 0u, OpAdd());
   if (lane == 63) lds[wid] = incl;
   __syncthreads();
   ScanU32 r;
@@ -85,14 +139,8 @@ __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
 // (all threads; ends with a barrier-protected read of lds).
 __device__ __forceinline__ ScanU32 block_scan_max_u32(uint32_t v, uint32_t* lds) {
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  uint32_t incl = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t o = __shfl_up(incl, d, 64);
-    if (lane >= (uint32_t)d) incl = max(incl, o);
-  }
-  uint32_t excl = __shfl_up(incl, 1, 64);
-  if (lane == 0) excl = 0u;
+  const uint32_t incl = wave_incl_scan(v, 0u, OpMax());
+  const uint32_t excl = wave_prev_lane(incl, 0u);
   if (lane == 63) lds[wid] = incl;
   __syncthreads();
   ScanU32 r;
@@ -373,10 +421,24 @@ __device__ __forceinline__ void unpack16(uint4 v, uint8_t* b) {
   }
 }
 
-__device__ __forceinline__ RunSum shfl_up_rs(RunSum v, int d) {
-  RunSum o;
-  o.v = __shfl_up(v.v, d, 64);
-  return o;
+// Wave scans of segment summaries (zre_scan.hpp), in lane order.
+struct OpRun {
+  __device__ __forceinline__ uint64_t operator()(uint64_t a, uint64_t b) const {
+    RunSum x, y;
+    x.v = a;
+    y.v = b;
+    return rs_combine(x, y).v;
+  }
+};
+__device__ __forceinline__ RunSum wave_incl_scan_rs(RunSum v) {
+  RunSum r;
+  r.v = wave_incl_scan(v.v, rs_identity().v, OpRun());
+  return r;
+}
+__device__ __forceinline__ RunSum wave_prev_lane_rs(RunSum v) {
+  RunSum r;
+  r.v = wave_prev_lane(v.v, rs_identity().v);
+  return r;
 }
 
 // Number of quartic bytes a stream byte stands for: data bytes (< 243) one,
@@ -434,13 +496,24 @@ __device__ __forceinline__ uint32_t nonzero_byte_mask4(uint32_t w) {
   return ((y >> 7) * 0x00204081u) >> 21 & 0xfu;
 }
 
-__device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
-                                                       uint32_t cnt) {
+__device__ __forceinline__ uint32_t nonzero_mask16(const uint4& w, uint32_t cnt) {
   static_assert(kZeroGroup == 0x79u, "the mask compares against bytes of 121");
-  const uint4 w = *reinterpret_cast<const uint4*>(q + lo);
   const uint32_t nz = nonzero_byte_mask4(w.x) | (nonzero_byte_mask4(w.y) << 4) |
                       (nonzero_byte_mask4(w.z) << 8) | (nonzero_byte_mask4(w.w) << 12);
   return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
+}
+
+__device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
+                                                       uint32_t cnt) {
+  return nonzero_mask16(*reinterpret_cast<const uint4*>(q + lo), cnt);
+}
+
+// Byte i (< 16) of four little-endian words, by selects on the values (an
+// indexed array would be placed in LDS or scratch memory).
+__device__ __forceinline__ uint32_t byte_of16(uint32_t x, uint32_t y, uint32_t z, uint32_t w,
+                                              uint32_t i) {
+  const uint32_t lo = (i & 4u) ? y : x, hi = (i & 4u) ? w : z;
+  return ((i & 8u) ? hi : lo) >> (8u * (i & 3u)) & 255u;
 }
 
 // Base-3 digits of a quartic byte, most significant first (weights 81, 27,

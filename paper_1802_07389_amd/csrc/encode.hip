@@ -436,14 +436,8 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
   const RunSum sum = rs_mask_summary(nz, cnt);
 
-  RunSum incl = sum;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    RunSum o = shfl_up_rs(incl, d);
-    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
-  }
-  RunSum excl_lane = shfl_up_rs(incl, 1);
-  if (lane == 0) excl_lane = rs_identity();
+  const RunSum incl = wave_incl_scan_rs(sum);
+  const RunSum excl_lane = wave_prev_lane_rs(incl);
   if (lane == 63) sh.wave[wid] = incl;
   __syncthreads();
   RunSum wpre = rs_identity();
@@ -751,18 +745,22 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
   }
 }
 
-// A tile whose partitions all start on a trit-byte boundary (m % 4 == 0),
-// that is whole and whose 5 * kEncTile values all lie before n: every trit
-// byte it needs exists and none needs shifting, so the loads go without
-// guards (one scalar base per partition, the group in the offset).
-__device__ __forceinline__ void load_trits_interior(const uint8_t* __restrict__ trits,
-                                                    uint32_t m, uint64_t q0,
-                                                    uint32_t (&tb)[kGroupsPerThread][5]) {
+// The same tile's trits of this thread's own 16 values in each partition
+// (values k*m + q0 + 16*tid + [0, 16), so that the thread packs the 16
+// quartic bytes it encodes): the word of trit bytes from (k*m + q0)/4 +
+// 4*tid on, taken from the aligned word at or before it and the next one
+// (alignbyte; the offset within the word is the same for the whole
+// partition).  The trits fill the first n/4 bytes of a 256-byte aligned
+// region of max_n/2 bytes, so that next word lies inside it too.
+__device__ __forceinline__ void load_trit_words(const uint8_t* __restrict__ trits, uint32_t m,
+                                                uint64_t q0, uint32_t (&d)[5]) {
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
-    const uint8_t* tp = trits + (((uint64_t)k * m + q0) >> 2);
-#pragma unroll
-    for (int it = 0; it < kGroupsPerThread; ++it) tb[it][k] = tp[threadIdx.x + kThreads * it];
+    const uint64_t b0 = ((uint64_t)k * m + q0) >> 2;
+    const uint32_t a = (uint32_t)b0 & 3u;
+    const uint32_t* wp = reinterpret_cast<const uint32_t*>(trits + (b0 - a)) + threadIdx.x;
+    const uint32_t lo = wp[0];
+    d[k] = a ? __builtin_amdgcn_alignbyte(wp[1], lo, a) : lo;
   }
 }
 
@@ -786,6 +784,19 @@ __device__ __forceinline__ void init_trit_luts(uint32_t (*lut)[256]) {
   lut[2][threadIdx.x] = 9u * sp;
   lut[3][threadIdx.x] = 3u * sp;
   lut[4][threadIdx.x] = sp;
+}
+
+// This thread's 16 quartic bytes from its trit words (load_trit_words):
+// byte g of each word holds the trits of its values 4g..4g+3.
+__device__ __forceinline__ uint4 pack_trit_words(const uint32_t (&d)[5],
+                                                 const uint32_t (*lut)[256]) {
+  uint32_t o[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    o[g] = lut[0][(d[0] >> (8 * g)) & 255u] + lut[1][(d[1] >> (8 * g)) & 255u] +
+           lut[2][(d[2] >> (8 * g)) & 255u] + lut[3][(d[3] >> (8 * g)) & 255u] +
+           lut[4][(d[4] >> (8 * g)) & 255u];
+  return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 __device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread][5], uint64_t n,
@@ -839,11 +850,16 @@ void tlc_quant_encode_kernel(
   const uint32_t t = blockIdx.x;
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
-  uint32_t h[kGroupsPerThread][5];  // bounds, or with kTrit the trit bytes
+  // an interior tile (whole, partitions on trit-byte boundaries, every
+  // value before n): each thread packs its own 16 quartic bytes in
+  // registers; other tiles pack through sh.q
+  const bool own = kTrit && m % 4u == 0u && tile_bytes == (uint32_t)kEncTile &&
+                   4ull * m + q0 + kEncTile <= n;
+  uint32_t h[kGroupsPerThread][5];  // bounds, or with kTrit the trits
   if (kTrit) {
     const uint8_t* trits = reinterpret_cast<const uint8_t*>(summ);
-    if (m % 4u == 0u && tile_bytes == (uint32_t)kEncTile && 4ull * m + q0 + kEncTile <= n)
-      load_trits_interior(trits, m, q0, h);
+    if (own)
+      load_trit_words(trits, m, q0, h[0]);
     else
       load_trits(trits, n, m, q0, tile_bytes, h);
     init_trit_luts(s_lut);
@@ -857,7 +873,12 @@ void tlc_quant_encode_kernel(
     host_put_result(hm.res, sc.bad, sc.M);
   }
   if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps acc, no stream
-  if (kTrit) {
+  const uint32_t lo = threadIdx.x * kBytes;
+  const uint32_t cnt = lo < tile_bytes ? umin32(kBytes, tile_bytes - lo) : 0u;
+  uint4 w = make_uint4(0u, 0u, 0u, 0u);  // the thread's quartic bytes [lo, lo + cnt)
+  if (own) {
+    w = pack_trit_words(h[0], s_lut);
+  } else if (kTrit) {
     pack_trits(h, n, m, q0, tile_bytes, s_lut, sh.q);
   } else if (kPath == kPathVec) {
     if (summ)
@@ -869,6 +890,7 @@ void tlc_quant_encode_kernel(
   } else {
     quantize_tile<kPath>(nullptr, r, n, m, sc, q0, tile_bytes, sh.q);
   }
+  if (!own && cnt) w = *reinterpret_cast<const uint4*>(sh.q + lo);
 
   // ---- Section 3.3 from the tile's first non-121 byte on, from the gaps
   // between non-121 bytes: a max-scan over the threads' last non-121
@@ -876,9 +898,8 @@ void tlc_quant_encode_kernel(
   // thread emits gives its output offset (zre_scan.hpp: rs_gaps_len,
   // rs_gaps_emit); the thread with the tile's last non-121 byte adds the
   // trailing run's codes 255 to its length.
-  const uint32_t lo = threadIdx.x * kBytes;
-  const uint32_t cnt = lo < tile_bytes ? umin32(kBytes, tile_bytes - lo) : 0u;
-  const uint32_t nz = cnt ? nonzero_group_mask(sh.q, lo, cnt) : 0u;
+  static_assert(kBytes == 16, "one uint4 of quartic bytes per thread");
+  const uint32_t nz = cnt ? nonzero_mask16(w, cnt) : 0u;
   const uint32_t last = nz ? lo + 31u - (uint32_t)__builtin_clz(nz) : 0u;
   const ScanU32 pm = block_scan_max_u32(nz ? last + 1u : 0u, sh.red);
   const int prev = (int)pm.excl - 1;  // the previous non-121 byte, -1 if none
@@ -898,8 +919,9 @@ void tlc_quant_encode_kernel(
     if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
     ++o;
   };
-  rs_gaps_emit(nz, lo, prev, [&](uint32_t i) { return (uint32_t)sh.q[lo + i]; }, put,
-               [&](uint32_t k) { o += k; });
+  const uint32_t w0 = w.x, w1 = w.y, w2 = w.z, w3 = w.w;
+  rs_gaps_emit(nz, lo, prev, [w0, w1, w2, w3](uint32_t i) { return byte_of16(w0, w1, w2, w3, i); },
+               put, [&](uint32_t k) { o += k; });
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
   const uint32_t len = umin32(off.total, tile_bytes);
@@ -938,14 +960,8 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_chunk_kernel(
   const uint32_t i = c * kChunkTiles + lane;
   RunSum a = rs_identity();
   if (i < ntiles) a.v = recs[i].agg;
-  RunSum incl = a;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    RunSum o = shfl_up_rs(incl, d);
-    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
-  }
-  RunSum ex = shfl_up_rs(incl, 1);
-  if (lane == 0) ex = rs_identity();
+  const RunSum incl = wave_incl_scan_rs(a);
+  const RunSum ex = wave_prev_lane_rs(incl);
   if (i < ntiles) local_pre[i] = ex.v;
   if (lane == 63) chunk_agg[c] = incl.v;
 }
@@ -967,14 +983,8 @@ __global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
     a.v = chunk_agg[j];
     mine = rs_combine(mine, a);
   }
-  RunSum incl = mine;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    RunSum o = shfl_up_rs(incl, d);
-    if (lane >= (uint32_t)d) incl = rs_combine(o, incl);
-  }
-  RunSum ex = shfl_up_rs(incl, 1);
-  if (lane == 0) ex = rs_identity();
+  const RunSum incl = wave_incl_scan_rs(mine);
+  const RunSum ex = wave_prev_lane_rs(incl);
   if (lane == 63) s_wave[wid] = incl;
   __syncthreads();
   RunSum p = rs_identity();

@@ -199,16 +199,16 @@ TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byt
 // non-121 byte emits its floor(g/14) codes 255 separately.
 TLC_HD uint32_t rs_gap_len(uint32_t g) { return g / kRunMax + (g % kRunMax != 0u ? 1u : 0u); }
 
+// With nz inside 16 bits, a gap between two of the thread's own bytes is
+// at most 14 bytes and costs exactly one code if non-empty: besides the
+// gap from prev, the count is one per non-121 byte plus one per maximal run
+// of set bits after the first.
 TLC_HD uint32_t rs_gaps_len(uint32_t nz, uint32_t lo, int prev) {
-  uint32_t len = 0u;
-  while (nz) {
-    const uint32_t p = lo + (uint32_t)__builtin_ctz(nz);
-    nz &= nz - 1u;
-    if (prev >= 0) len += rs_gap_len(p - (uint32_t)prev - 1u);
-    len += 1u;
-    prev = (int)p;
-  }
-  return len;
+  if (nz == 0u) return 0u;
+  const uint32_t first = lo + (uint32_t)__builtin_ctz(nz);
+  const uint32_t runs = (uint32_t)__builtin_popcount(nz & ~(nz << 1));
+  return (prev >= 0 ? rs_gap_len(first - (uint32_t)prev - 1u) : 0u) +
+         (uint32_t)__builtin_popcount(nz) + runs - 1u;
 }
 
 template <class Byte, class Put, class Fill>
