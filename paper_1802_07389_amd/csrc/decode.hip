@@ -58,7 +58,8 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
                                            uint64_t* __restrict__ start,
                                            uint64_t* __restrict__ status, uint32_t floor,
                                            uint32_t lt, uint32_t epoch, Ctrl* __restrict__ ctrl,
-                                           uint32_t* hfault, IdxShared& sh) {
+                                           uint32_t* hfault, uint32_t* hcorrupt,
+                                           IdxShared& sh) {
   constexpr uint32_t kTile = kThreads * kBytes;
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint64_t j0 = (uint64_t)lt * kTile + threadIdx.x * kBytes;
@@ -113,6 +114,7 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
         __hip_atomic_store(&ctrl->dec_bad_epoch, epoch, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&ctrl->dec_corrupt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        host_put(hcorrupt, 1u);
       }
       if (last_tile)
         __hip_atomic_store(&ctrl->dec_verdict, verdict_word(epoch, bad), __ATOMIC_RELAXED,
@@ -157,7 +159,8 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_kernel(
   __shared__ uint32_t s_tile;
   if (threadIdx.x == 0) s_tile = take_ticket(&ctrl->dec_ticket) - ticket_base;
   __syncthreads();
-  index_tile<kZreBytesPerThread>(C, c, m, start, status, 0, s_tile, epoch, ctrl, hm.fault, sh);
+  index_tile<kZreBytesPerThread>(C, c, m, start, status, 0, s_tile, epoch, ctrl, hm.fault,
+                                 hm.corrupt, sh);
 }
 
 __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
@@ -172,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void tlc_zre_index_batch_kernel(
   const uint32_t t = find_desc(descs, count, T, [](const DecDesc& d) { return d.tile0; });
   const DecDesc d = descs[t];
   index_tile<kZreBatchBytesPerThread>(d.C, d.c, d.m, start + d.range0, status, d.tile0,
-                                      T - d.tile0, epoch, ctrl, hm.fault, sh);
+                                      T - d.tile0, epoch, ctrl, hm.fault, hm.corrupt, sh);
 }
 
 // ---------------------------------------------------------------- expansion
@@ -526,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void tlc_expand_dequant_kernel(
     const uint32_t T = s_t;
     if (T < ntiles) {
       index_tile<kZreBatchBytesPerThread>(C, c, (uint32_t)m, start, status, 0, T, epoch, ctrl,
-                                          hm.fault, ish);
+                                          hm.fault, hm.corrupt, ish);
       return;
     }
     k = T - ntiles;

@@ -506,9 +506,9 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
 //     run before it, so the encoder is at phase 0 there.  Each tile records
 //     its summary (RunSum), the length of its leading 121 run and the slot
 //     length.
-//   pass B (tlc_zre_chunk_kernel, tlc_zre_chunk_scan_kernel): every tile's
-//     prefix within its chunk of 64 tiles and the chunk summaries, then one
-//     block scans the chunk summaries.
+//   pass B (tlc_zre_chunk_kernel): every tile's prefix within its chunk of
+//     64 tiles and the chunk summaries; the pass's last block scans the
+//     chunk summaries.
 //   pass C (tlc_zre_compact_kernel, one wave per tile): the tile's prefix
 //     (its output offset and incoming run phase) from its chunk's prefix
 //     and its own within the chunk, then the leading run's codes, which
@@ -944,39 +944,43 @@ void tlc_quant_encode_kernel(
   }
 }
 
-// Pass B1: one wave per chunk of 64 tiles: every tile's prefix within its
-// chunk (an ordered wave scan) and the chunk's summary.
+// Pass B: one wave per chunk of 64 tiles: every tile's prefix within its
+// chunk (an ordered wave scan) and the chunk's summary.  The last block to
+// finish (a count of finished blocks, each block's summaries released
+// before its count) then scans the chunk summaries in place, each entry
+// becoming its chunk's exclusive prefix, and clears the count for the next
+// call.
 constexpr uint32_t kChunkTiles = 64;
-constexpr uint32_t kChunkScanThreads = 1024;
 
 __global__ __launch_bounds__(kThreads) void tlc_zre_chunk_kernel(
     const TileRec* __restrict__ recs, uint32_t ntiles, uint64_t* __restrict__ local_pre,
-    uint64_t* __restrict__ chunk_agg, const Ctrl* __restrict__ ctrl) {
-  if (ctrl->enc.err) return;  // pass A refused the tensor
+    uint64_t* __restrict__ chunk_agg, Ctrl* __restrict__ ctrl) {
+  __shared__ RunSum s_wave[kWaves];
+  __shared__ uint32_t s_last;
+  if (ctrl->enc.err) return;  // pass A refused the tensor (every block returns)
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t nchunks = (ntiles + kChunkTiles - 1) / kChunkTiles;
   const uint32_t c = blockIdx.x * kWaves + wid;
-  if (c >= nchunks) return;  // whole waves only: no barrier follows
-  const uint32_t i = c * kChunkTiles + lane;
-  RunSum a = rs_identity();
-  if (i < ntiles) a.v = recs[i].agg;
-  const RunSum incl = wave_incl_scan_rs(a);
-  const RunSum ex = wave_prev_lane_rs(incl);
-  if (i < ntiles) local_pre[i] = ex.v;
-  if (lane == 63) chunk_agg[c] = incl.v;
-}
-
-// Pass B2: one block scans the chunk summaries in place (each entry becomes
-// the chunk's exclusive prefix); thread j takes a run of consecutive
-// chunks.
-__global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
-    uint32_t nchunks, uint64_t* __restrict__ chunk_agg, const Ctrl* __restrict__ ctrl) {
-  constexpr int kScanWaves = kChunkScanThreads / 64;
-  __shared__ RunSum s_wave[kScanWaves];
-  if (ctrl->enc.err) return;
-  const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
-  const uint32_t per = (nchunks + kChunkScanThreads - 1) / kChunkScanThreads;
-  const uint32_t j0 = threadIdx.x * per, j1 = min(j0 + per, nchunks);
+  if (c < nchunks) {  // whole waves
+    const uint32_t i = c * kChunkTiles + lane;
+    RunSum a = rs_identity();
+    if (i < ntiles) a.v = recs[i].agg;
+    const RunSum incl = wave_incl_scan_rs(a);
+    const RunSum ex = wave_prev_lane_rs(incl);
+    if (i < ntiles) local_pre[i] = ex.v;
+    if (lane == 63) chunk_agg[c] = incl.v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    s_last = atomicAdd(&ctrl->chunk_done, 1u) == gridDim.x - 1u ? 1u : 0u;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  // thread j scans a run of consecutive chunks
+  const uint32_t per = (nchunks + kThreads - 1) / kThreads;
+  const uint32_t j0 = umin32(threadIdx.x * per, nchunks), j1 = umin32(j0 + per, nchunks);
   RunSum mine = rs_identity();
   for (uint32_t j = j0; j < j1; ++j) {
     RunSum a;
@@ -996,6 +1000,8 @@ __global__ __launch_bounds__(kChunkScanThreads) void tlc_zre_chunk_scan_kernel(
     chunk_agg[j] = p.v;
     p = rs_combine(p, a);
   }
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&ctrl->chunk_done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Pass C, the compaction: one wave per tile.  Prefix = the chunk's prefix
@@ -1297,13 +1303,10 @@ hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uin
 }
 
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
-                             uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st) {
+                             uint64_t* chunk_agg, Ctrl* ctrl, hipStream_t st) {
   const uint32_t nchunks = (ntiles + kChunkTiles - 1) / kChunkTiles;
   launch_k(tlc_zre_chunk_kernel, (nchunks + kWaves - 1) / kWaves, kThreads, st,
       recs, ntiles, local_pre, chunk_agg, ctrl);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  launch_k(tlc_zre_chunk_scan_kernel, 1, kChunkScanThreads, st, nchunks, chunk_agg, ctrl);
   return hipGetLastError();
 }
 

@@ -340,7 +340,7 @@ HostMirror enc_mirror(tlc_ctx* c) {
   return HostMirror{&c->rb_dev->enc, &c->rb_dev->fault};
 }
 HostMirror fault_mirror(tlc_ctx* c) {
-  return HostMirror{nullptr, &c->rb_dev->fault};
+  return HostMirror{nullptr, &c->rb_dev->fault, &c->rb_dev->dec_corrupt};
 }
 // A batch: the per-tensor results follow the control block's slot in the
 // readback (as host_results does on the host).
@@ -1126,7 +1126,9 @@ TLC_API int tlc_sync(tlc_ctx* c) {
   DeviceScope dev(c->device);
   int st = dev.status();
   if (st) return st;
-  st = sync_and_read(c);
+  // every kernel that sets the fault or bad-stream flag also writes it
+  // into the pinned readback
+  st = sync_mirrored(c);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -1136,6 +1138,7 @@ TLC_API int tlc_sync(tlc_ctx* c) {
     hipError_t e = hipMemsetAsync(&c->ctrl->dec_corrupt, 0, sizeof(uint32_t), c->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) return hip_fail(e, "tlc_sync: clearing status");
+    c->rb->dec_corrupt = 0u;
     return fail(TLC_E_CORRUPT, "a decoded stream did not expand to ceil(n/5) bytes");
   }
   return TLC_OK;

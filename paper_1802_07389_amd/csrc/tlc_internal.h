@@ -46,7 +46,8 @@ struct Ctrl {
   uint32_t enc_ticket;     // tile tickets of the encoder
   uint32_t dec_ticket;     // tile tickets of the zero-run index scan
   uint32_t dec_verdict;    // epoch << 1 | bad of the last single-stream decode's stream
-  uint32_t pad[54];
+  uint32_t chunk_done;     // blocks of the tile-chunk pass done (0 between calls)
+  uint32_t pad[53];
 };
 static_assert(sizeof(Ctrl) == 256, "Ctrl is one 256-byte slot");
 
@@ -58,13 +59,14 @@ struct HostReadback {
 };
 
 // Device pointers into the pinned host readback that the encoders (and the
-// decoder's index scans, for the fault flag) also write a call's result to,
+// decoders, for the fault and bad-stream flags) also write a call's result to,
 // so that the host needs no copy before it reads it; null: not mirrored.
 // res: the result (one per tensor of a batch); fault: the look-back fault
-// flag.
+// flag; corrupt: the decoder's sticky bad-stream flag.
 struct HostMirror {
   EncResult* res = nullptr;
   uint32_t* fault = nullptr;
+  uint32_t* corrupt = nullptr;
 };
 
 // One tensor of a batched encode (device copy of the host's description).
@@ -171,7 +173,7 @@ hipError_t launch_quant_encode_chained(const float* x, float* r, uint64_t n, uin
                                        uint32_t ticket_base, uint32_t epoch, Ctrl* ctrl,
                                        HostMirror hm, hipStream_t st);
 hipError_t launch_zre_chunks(const TileRec* recs, uint32_t ntiles, uint64_t* local_pre,
-                             uint64_t* chunk_agg, const Ctrl* ctrl, hipStream_t st);
+                             uint64_t* chunk_agg, Ctrl* ctrl, hipStream_t st);
 hipError_t launch_zre_compact(const TileRec* recs, const uint64_t* chunk_pre,
                               const uint64_t* local_pre, const uint8_t* slots, uint32_t m,
                               uint8_t* out, const uint2* fix, float* r, uint64_t n, Ctrl* ctrl,
