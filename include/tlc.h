@@ -104,7 +104,11 @@ int tlc_ctx_destroy(tlc_ctx* ctx);
  *   bytes_cap must be >= tlc_max_compressed_bytes(n).
  *   bytes_len host out: stream length (0 on error).
  *   scale     host out: M (0 when n == 0).
- * Synchronous: returns after the stream length is known.  On
+ * Synchronous: returns after the stream length is known, which the encode
+ * hands to the host a little before its last kernels end: the stream bytes
+ * and the residual are complete in the order of the context's stream (work
+ * issued there afterwards sees them; the host or another stream waits for
+ * that stream, e.g. with tlc_sync, before reading them).  On
  * TLC_E_NONFINITE the residual and the bytes are left unchanged (with
  * TLC_OPT_IN_PLACE_FEEDBACK the residual holds acc instead). */
 int tlc_compress(tlc_ctx* ctx, const float* tensor, float* residual, size_t n,

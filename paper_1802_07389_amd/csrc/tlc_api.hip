@@ -2,6 +2,7 @@
 // checks, the per-context device workspace, kernel launches on the
 // context's stream, status readback and optional per-kernel event timing.
 #include <math.h>
+#include <stddef.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -209,17 +210,26 @@ hipEvent_t take_event(tlc_ctx* c) {
 }
 
 // Resolve recorded event pairs; call only after the stream is idle.
+// Adds the finished timed launches to the totals; a pair whose kernels are
+// still running (an encode returns once its result has arrived) stays
+// pending for the next call.
 void collect_timings(tlc_ctx* c) {
+  size_t keep = 0;
   for (const PendingTiming& p : c->pending) {
     float ms = 0.0f;
-    if (hipEventElapsedTime(&ms, p.start, p.stop) == hipSuccess) {
+    const hipError_t e = hipEventElapsedTime(&ms, p.start, p.stop);
+    if (e == hipErrorNotReady) {
+      c->pending[keep++] = p;
+      continue;
+    }
+    if (e == hipSuccess) {
       c->total_ms[p.kernel] += ms;
       c->launches[p.kernel] += 1;
     }
     c->free_events.push_back(p.start);
     c->free_events.push_back(p.stop);
   }
-  c->pending.clear();
+  c->pending.resize(keep);
 }
 
 // Launch helper: brackets the launch with events when profiling is on.
@@ -350,11 +360,63 @@ HostMirror batch_mirror(tlc_ctx* c) {
       &c->rb_dev->fault};
 }
 
+// A single-tensor encode whose kernels mirror their result (enc_mirror):
+// before its launches the host fills the readback's err, len and scale
+// words with kPending, which none of their values takes (err is 0 or 1, a
+// length is below 2^31, a scale is finite), and then waits for the words
+// to change rather than for the stream: the first encode pass writes err
+// and the scale from its first tile, the last pass the length from its last
+// tile, a little before the kernels end.
+constexpr uint32_t kPending = 0xffffffffu;
+
+void arm_result(tlc_ctx* c) {
+  volatile uint32_t* w = reinterpret_cast<volatile uint32_t*>(&c->rb->enc);
+  static_assert(offsetof(EncResult, err) == 0 && offsetof(EncResult, len) == 4 &&
+                    offsetof(EncResult, scale) == 8,
+                "err, len and scale are the result's first three words");
+  w[0] = kPending;
+  w[1] = kPending;
+  w[2] = kPending;
+}
+
+bool result_pending(const tlc_ctx* c) {
+  const volatile uint32_t* w = reinterpret_cast<const volatile uint32_t*>(&c->rb->enc);
+  const uint32_t err = w[0];
+  return err == kPending || w[2] == kPending || (err == 0u && w[1] == kPending);
+}
+
+// Polls the armed result; falls back to waiting for the stream once the
+// stream has finished (or a look-back fault was flagged) without it.
+int wait_result(tlc_ctx* c) {
+  const volatile uint32_t* fault = &c->rb->fault;
+  for (uint32_t spin = 1;; ++spin) {
+    if (*fault) break;
+    if (!result_pending(c)) {
+      collect_timings(c);
+      return TLC_OK;
+    }
+    if ((spin & 255u) == 0u) {
+      const hipError_t q = hipStreamQuery(c->stream);
+      if (q == hipSuccess) break;
+      if (q != hipErrorNotReady) return hip_fail(q, "hipStreamQuery");
+    }
+    __builtin_ia32_pause();
+  }
+  int st = sync_mirrored(c);
+  if (st) return st;
+  if (!*fault && result_pending(c)) {
+    c->broken = true;
+    return fail(TLC_E_DEVICE, "the encode wrote no result");
+  }
+  return TLC_OK;
+}
+
 // Waits for an encode and reports its result (the stream length and M);
-// mirrored: the kernels wrote it into the readback (enc_mirror).
+// mirrored: the kernels wrote it into the readback (enc_mirror), which
+// arm_result prepared.
 int finish_compress(tlc_ctx* c, const char* fn, size_t* bytes_len, float* scale,
                     bool mirrored = false) {
-  int st = mirrored ? sync_mirrored(c) : sync_and_read(c);
+  int st = mirrored ? wait_result(c) : sync_and_read(c);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -602,6 +664,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   st = dev.status();
   if (st) return st;
 
+  arm_result(c);
   const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   // The three passes' float4 path: after the check pass the max pass
   // quantizes every value and keeps 2-bit trits per value in summ; in place
