@@ -28,8 +28,8 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E
 METRIC = "3LC encode/decode GB/s of fp32 input on 1 MI355X; % HBM peak; compression ratio"
 KERNEL_SRC = [os.path.join(ROOT, "paper_1802_07389_amd", "csrc", f)
-              for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "zre_scan.hpp",
-                        "tlc_internal.h")]
+              for f in ("encode.hip", "device_common.hpp", "lookback.hpp", "wave_scan.hpp",
+                        "zre_scan.hpp", "tlc_internal.h")]
 DOMINANT = "tlc_accum_quantize_kernel"  # the longest kernel of a step
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", DOMINANT + "_c4_traffic.md")
 
@@ -47,8 +47,8 @@ def algorithmic_bytes(n, c, nnz):
         # read the trits; write each tile's own stream bytes (c in all) and
         # its 16-byte record
         "tlc_quant_encode_kernel": n // 4 + c + 16 * tiles,
-        # tile records in, tile prefixes and chunk summaries out (the
-        # chunk summaries' scan, a second launch, rides on the same id)
+        # tile records in, tile prefixes and chunk summaries out (the last
+        # block then scans the chunk summaries in place)
         "tlc_zre_chunk_kernel": 24 * tiles,
         # records and prefixes in, slot bytes in, the stream out
         "tlc_zre_compact_kernel": 2 * c + 32 * tiles,

@@ -12,7 +12,7 @@ LIB = os.path.join(PKG, "libtlc.so")
 # tests/test_gpu_lookback_delays.py.
 LIB_DELAY = os.path.join(PKG, "libtlc_delay.so")
 SOURCES = ["encode.hip", "decode.hip", "int8.hip", "tlc_api.hip", "noalloc.hip"]
-HEADERS = ["tlc_internal.h", "device_common.hpp", "lookback.hpp", "zre_scan.hpp"]
+HEADERS = ["tlc_internal.h", "device_common.hpp", "lookback.hpp", "wave_scan.hpp", "zre_scan.hpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

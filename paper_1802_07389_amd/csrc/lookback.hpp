@@ -18,6 +18,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "wave_scan.hpp"
+
 namespace tlc {
 
 constexpr uint32_t kFlagAgg = 1u;
@@ -75,12 +77,26 @@ __device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
 // one wave, over an associative operator op(earlier, later).  Tiles
 // [floor, tile) belong to the same scan (a batch keeps several scans in one
 // status array); tile `floor` always publishes its inclusive prefix.  Lane l
-// polls the word of tile (base - l), so one poll covers 64 predecessors.  The words
-// from the nearest inclusive prefix up to tile - 1 are folded in order with
-// a shuffle reduction (a higher lane holds an earlier tile).  Publishes the
-// tile's aggregate first and its inclusive prefix last; returns the
-// exclusive prefix in every lane.  A bounded wait or a predecessor fault
-// publishes a fault word and sets *fault.
+// polls the word of tile (base - l), so one poll covers 64 predecessors (a
+// higher lane holds an earlier tile).  The words from the nearest inclusive
+// prefix up to tile - 1 are folded in order by a DPP scan of the lanes under
+// op with its arguments swapped, which leaves the fold in lane 63.
+// Publishes the tile's aggregate first and its inclusive prefix last;
+// returns the exclusive prefix in every lane.  A bounded wait or a
+// predecessor fault publishes a fault word and sets *fault.
+template <class Op>
+struct OpLaterFirst {
+  Op op;
+  __device__ __forceinline__ uint64_t operator()(uint64_t later, uint64_t earlier) const {
+    return op(earlier, later);
+  }
+};
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+  return (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane) |
+         ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane) << 32);
+}
+
 template <class SW, class Op>
 __device__ uint64_t lookback_wave(uint64_t* status, uint32_t floor, uint32_t tile,
                                   uint64_t agg, uint64_t identity, uint32_t epoch, Op op,
@@ -105,12 +121,12 @@ __device__ uint64_t lookback_wave(uint64_t* status, uint32_t floor, uint32_t til
     }
     const uint64_t pmask = __ballot(is_prefix);
     const uint32_t p = pmask ? (uint32_t)(__ffsll((unsigned long long)pmask) - 1) : 64u;
-    const uint64_t need = p >= 63u ? ~0ull : ((2ull << p) - 1ull);  // lanes 0..p
-    if (__ballot(is_fault) & need) {
+    const bool need = lane <= p;  // the nearest prefix and the tiles after it
+    if (__ballot(is_fault && need)) {
       failed = true;
       break;
     }
-    if (__ballot(!ready) & need) {
+    if (__ballot(!ready && need)) {
       if (++spins > kSpinLimit) {
         failed = true;
         break;
@@ -118,13 +134,8 @@ __device__ uint64_t lookback_wave(uint64_t* status, uint32_t floor, uint32_t til
       __builtin_amdgcn_s_sleep(1);
       continue;
     }
-    uint64_t v = lane <= p ? val : identity;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const uint64_t o = __shfl_down(v, d, 64);
-      if (lane + d < 64u) v = op(o, v);
-    }
-    run = op(__shfl(v, 0, 64), run);
+    const uint64_t fold = wave_incl_scan(need ? val : identity, identity, OpLaterFirst<Op>{op});
+    run = op(readlane64(fold, 63), run);
     if (p < 64u) break;
     base -= 64;
   }
