@@ -360,38 +360,44 @@ HostMirror batch_mirror(tlc_ctx* c) {
       &c->rb_dev->fault};
 }
 
-// A single-tensor encode whose kernels mirror their result (enc_mirror):
-// before its launches the host fills the readback's err, len and scale
-// words with kPending, which none of their values takes (err is 0 or 1, a
-// length is below 2^31, a scale is finite), and then waits for the words
-// to change rather than for the stream: the first encode pass writes err
-// and the scale from its first tile, the last pass the length from its last
-// tile, a little before the kernels end.
+// An encode whose kernels mirror their results (enc_mirror, batch_mirror):
+// before its launches the host fills each result's err, len and scale words
+// with kPending, which none of their values takes (err is 0 or 1, a length
+// is below 2^31, a scale is finite), and then waits for the words to change
+// rather than for the stream: a tensor's first tile writes err and the
+// scale (and a zero length on error), its last tile, or the compaction's
+// last, the length, a little before the kernels end.
 constexpr uint32_t kPending = 0xffffffffu;
 
-void arm_result(tlc_ctx* c) {
-  volatile uint32_t* w = reinterpret_cast<volatile uint32_t*>(&c->rb->enc);
-  static_assert(offsetof(EncResult, err) == 0 && offsetof(EncResult, len) == 4 &&
-                    offsetof(EncResult, scale) == 8,
-                "err, len and scale are the result's first three words");
-  w[0] = kPending;
-  w[1] = kPending;
-  w[2] = kPending;
+static_assert(offsetof(EncResult, err) == 0 && offsetof(EncResult, len) == 4 &&
+                  offsetof(EncResult, scale) == 8 && sizeof(EncResult) == 16,
+              "err, len and scale are the first three of a result's four words");
+
+void arm_results(EncResult* r, uint32_t count) {
+  volatile uint32_t* w = reinterpret_cast<volatile uint32_t*>(r);
+  for (uint32_t i = 0; i < count; ++i) {
+    w[4 * i] = kPending;
+    w[4 * i + 1] = kPending;
+    w[4 * i + 2] = kPending;
+  }
 }
 
-bool result_pending(const tlc_ctx* c) {
-  const volatile uint32_t* w = reinterpret_cast<const volatile uint32_t*>(&c->rb->enc);
+bool result_pending(const EncResult* r) {
+  const volatile uint32_t* w = reinterpret_cast<const volatile uint32_t*>(r);
   const uint32_t err = w[0];
   return err == kPending || w[2] == kPending || (err == 0u && w[1] == kPending);
 }
 
-// Polls the armed result; falls back to waiting for the stream once the
-// stream has finished (or a look-back fault was flagged) without it.
-int wait_result(tlc_ctx* c) {
+// Polls the armed results; falls back to waiting for the stream once the
+// stream has finished (or a look-back fault was flagged) without them.
+int wait_results(tlc_ctx* c, const EncResult* r, uint32_t count) {
   const volatile uint32_t* fault = &c->rb->fault;
+  uint32_t i = 0;  // results before i have arrived
   for (uint32_t spin = 1;; ++spin) {
     if (*fault) break;
-    if (!result_pending(c)) {
+    while (i < count && !result_pending(&r[i])) ++i;
+    if (i == count) {
+      __atomic_thread_fence(__ATOMIC_ACQUIRE);  // the results' plain reads come after
       collect_timings(c);
       return TLC_OK;
     }
@@ -404,10 +410,12 @@ int wait_result(tlc_ctx* c) {
   }
   int st = sync_mirrored(c);
   if (st) return st;
-  if (!*fault && result_pending(c)) {
-    c->broken = true;
-    return fail(TLC_E_DEVICE, "the encode wrote no result");
-  }
+  if (!*fault)
+    for (; i < count; ++i)
+      if (result_pending(&r[i])) {
+        c->broken = true;
+        return fail(TLC_E_DEVICE, "the encode wrote no result for a tensor");
+      }
   return TLC_OK;
 }
 
@@ -416,7 +424,7 @@ int wait_result(tlc_ctx* c) {
 // arm_result prepared.
 int finish_compress(tlc_ctx* c, const char* fn, size_t* bytes_len, float* scale,
                     bool mirrored = false) {
-  int st = mirrored ? wait_result(c) : sync_and_read(c);
+  int st = mirrored ? wait_results(c, &c->rb->enc, 1) : sync_and_read(c);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
@@ -664,7 +672,7 @@ TLC_API int tlc_compress(tlc_ctx* c, const float* tensor, float* residual, size_
   st = dev.status();
   if (st) return st;
 
-  arm_result(c);
+  arm_results(&c->rb->enc, 1);
   const uint32_t ntiles = (uint32_t)ceil_div(m, kEncTile);
   // The three passes' float4 path: after the check pass the max pass
   // quantizes every value and keeps 2-bit trits per value in summ; in place
@@ -906,6 +914,7 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   const uint32_t cnt = (uint32_t)d.size();
   st = upload(c, c->enc_descs, d.data(), cnt * sizeof(EncDesc));
   if (st) return st;
+  arm_results(c->host_results, cnt);
   // default policy: the check pass, then every tile forms acc = x + r itself
   // from its tensor (no writing max pass); in place: step 1 into the buffers
   // with the partial maxima of the sums, then the tiles quantize the buffers
@@ -933,7 +942,7 @@ TLC_API int tlc_compress_batch(tlc_ctx* c, size_t count, const float* const* ten
   });
   if (st) return st;
   c->enc_ticket_base += tiles;
-  st = sync_mirrored(c);
+  st = wait_results(c, c->host_results, cnt);
   if (st) return st;
   if (c->rb->fault) {
     c->broken = true;
