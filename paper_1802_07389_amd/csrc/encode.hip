@@ -361,13 +361,29 @@ constexpr int kGroupsPerThread = kEncTile / 4 / kThreads;  // groups of 4 bytes 
 // [q0, q0 + tile_bytes), held in the buffer r, and leaves the bytes in q
 // (LDS).  kPath: threads take groups of 4 bytes,
 // aligned float4 cells of one partition at a time, or single bytes,
-// interleaved so every load and store instruction is coalesced.  Ends with
-// a barrier.
-template <int kPath, bool kX = false>
+// interleaved so every load and store instruction is coalesced.  kDeep
+// (float4 path): in a whole tile whose every group lies before n, all of a
+// thread's groups are loaded, without branches between them, before the
+// first is quantized: one memory round trip per tile instead of one per
+// group, at the cost of registers, for grids small enough to stay resident
+// (the chained and batched encoders).  Ends with a barrier.
+template <int kPath, bool kX = false, bool kDeep = false>
 __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, float* __restrict__ r,
                                               uint64_t n, uint32_t m, const Scale& sc,
                                               uint64_t q0, uint32_t tile_bytes, uint8_t* q) {
-  if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
+  if (kPath == kPathVec && kDeep && tile_bytes == (uint32_t)kEncTile &&
+      group4_full(n, m, q0 + kEncTile - 4u)) {
+    float4 v[kGroupsPerThread][5];
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it)
+      load_group4<kX>(x, r, m, q0 + (threadIdx.x + kThreads * it) * 4u, v[it]);
+#pragma unroll
+    for (int it = 0; it < kGroupsPerThread; ++it) {
+      const uint32_t g = threadIdx.x + kThreads * it;
+      *reinterpret_cast<uint32_t*>(q + g * 4u) =
+          quantize_group4_loaded<kX>(r, m, q0 + g * 4u, v[it], sc.M, sc.U);
+    }
+  } else if (kPath == kPathVec) {  // 4 bytes per thread: float4 loads and stores
     // The thread's groups g = threadIdx.x + kThreads * it: the next group's
     // ten loads are issued before the current group is quantized, so a
     // tile takes about one memory round trip per thread instead of one per
@@ -427,7 +443,7 @@ __device__ __forceinline__ void encode_tile(const float* __restrict__ x, float* 
   // ---- phase 1: Eq. 1-2, residual write-back, quartic pack
   const uint64_t q0 = (uint64_t)lt * kEncTile;
   const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
-  quantize_tile<kPath, kX>(x, r, n, m, sc, q0, tile_bytes, sh.q);
+  quantize_tile<kPath, kX, true>(x, r, n, m, sc, q0, tile_bytes, sh.q);
 
   // ---- phase 2: Section 3.3
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
