@@ -279,12 +279,14 @@ int tlc_sync(tlc_ctx* ctx);
  * per-context counter (encode 1 .. TLC_ENC_EPOCH_MAX, decode 1 ..
  * TLC_DEC_EPOCH_MAX), so the words need no clearing between launches;
  * when a counter wraps, its status words are cleared first (and for the
- * decode counter the mark that flags a corrupt stream's launch). */
+ * decode counter the range starts, the verdict and the mark that flags a
+ * corrupt stream's launch). */
 #define TLC_ENC_EPOCH_MAX 8388607  /* 2^23 - 1 */
 #define TLC_DEC_EPOCH_MAX 67108863 /* 2^26 - 1 */
 
-/* For tests of the wrap: wait for the context's work, clear the status
- * words of both scans (no word of an earlier launch can then carry a
+/* For tests of the wrap: wait for the context's work, clear the
+ * epoch-tagged words of both scans (status words, the decoder's range
+ * starts and its verdict: no word of an earlier launch can then carry a
  * future epoch) and set the counters to the last epochs used, enc_epoch
  * <= TLC_ENC_EPOCH_MAX and dec_epoch <= TLC_DEC_EPOCH_MAX (else
  * TLC_E_INVALID).  The corrupt-stream mark is left as it is: only the wrap

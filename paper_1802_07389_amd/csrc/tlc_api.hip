@@ -1225,10 +1225,16 @@ TLC_API int tlc_ctx_set_epochs(tlc_ctx* c, uint32_t enc_epoch, uint32_t dec_epoc
   DeviceScope dev(c->device);
   st = dev.status();
   if (st) return st;
+  // every epoch-tagged word: status words, range starts and the
+  // single-stream verdict (a word from an earlier use of an epoch must not
+  // match)
   hipError_t e = hipMemsetAsync(c->enc_status, 0, c->enc_status_words * sizeof(uint64_t),
                                 c->stream);
   if (e == hipSuccess)
     e = hipMemsetAsync(c->dec_status, 0, c->dec_status_words * sizeof(uint64_t), c->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(c->start, 0, c->start_words * sizeof(uint64_t), c->stream);
+  if (e == hipSuccess)
+    e = hipMemsetAsync(&c->ctrl->dec_verdict, 0, sizeof(uint32_t), c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e != hipSuccess) return hip_fail(e, "tlc_ctx_set_epochs");
   c->enc_epoch = enc_epoch;

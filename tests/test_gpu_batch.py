@@ -397,3 +397,52 @@ def test_shared_pull_one_payload_many_receivers(bctx):
     for w, (o, r0) in enumerate(zip(outs, replicas0)):
         st, ref = oracle.decompress(C, M, n, r0.copy(), accumulate=True)
         assert st == 0 and np.array_equal(g.bits(o.cpu().numpy()), g.bits(ref)), w
+
+
+@pytest.mark.parametrize("big", [False, True])
+@pytest.mark.parametrize("corrupt", [False, True])
+def test_batch_decode_short_and_long_streams(bctx, big, corrupt):
+    """A batch of short streams (one or two 8 KiB scan tiles each), and one
+    that also holds a stream of several scan tiles: both give the oracle's
+    decode-accumulate bit for bit, and a corrupt stream in either (here the
+    last, the long one in the second batch) leaves every output untouched.
+    The kernel timers show one scan launch and one expansion launch."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+    sizes = [300, 20481, 4096 * 5 + 3, 7] + ([1 << 20] if big else [])
+    xs = [workloads.normal([740, t], n, 1.0) if n == 1 << 20 else
+          workloads.runs_tensor([740, t], n) for t, n in enumerate(sizes)]
+    pays = []
+    for x in xs:
+        st, C, M = oracle.compress(x, np.zeros(x.size, F32), 1.0)
+        assert st == 0
+        pays.append((C, M))
+    longest = max(C.size for C, _ in pays)
+    assert (longest > 2 * 8192) == big, longest
+    streams = [C for C, _ in pays]
+    if corrupt:
+        bad = streams[-1].copy()
+        bad[len(bad) // 2] = 7 if bad[len(bad) // 2] >= 243 else 255
+        streams[-1] = bad
+    outs0 = [workloads.normal([741, t], n) for t, n in enumerate(sizes)]
+    outs = [torch.from_numpy(o.copy()).cuda() for o in outs0]
+    bctx.profile(True, kernels=[tlc.TLC_KERNEL_ZRE_INDEX_BATCH,
+                                tlc.TLC_KERNEL_EXPAND_DEQUANT_BATCH])
+    bctx.profile_reset()
+    bctx.decompress_batch([torch.from_numpy(C).cuda() for C in streams],
+                          [M for _, M in pays], outs, accumulate=True)
+    st = tlc.tlc_sync(bctx.handle)
+    scans = bctx.profile_get(tlc.TLC_KERNEL_ZRE_INDEX_BATCH)[1]
+    expands = bctx.profile_get(tlc.TLC_KERNEL_EXPAND_DEQUANT_BATCH)[1]
+    bctx.profile(False)
+    assert (scans, expands) == (1, 1)
+    if corrupt:
+        assert st == tlc.TLC_E_CORRUPT
+        for o, o0 in zip(outs, outs0):
+            assert np.array_equal(g.bits(o.cpu().numpy()), g.bits(o0))
+        return
+    assert st == tlc.TLC_OK
+    for t, (o, o0) in enumerate(zip(outs, outs0)):
+        st, ref = oracle.decompress(pays[t][0], pays[t][1], sizes[t], o0.copy(), True)
+        assert st == 0 and np.array_equal(g.bits(o.cpu().numpy()), g.bits(ref)), t

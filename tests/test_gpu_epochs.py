@@ -128,3 +128,35 @@ def test_decode_epochs_wrap_and_corrupt_mark(ctx):
     batch()                                         # wrap: 1
     single(*streams[1], 0)                          # 2
     g.log("corrupt stream in the last epoch, good streams after the wrap ok")
+
+    # batches of short streams, corrupt in the last epoch before the wrap
+    sizes = [20481, 300, 4096 * 5 + 3]
+    short = []
+    for t, m in enumerate(sizes):
+        st, C, M = oracle.compress(workloads.runs_tensor([90, t], m), np.zeros(m, F32), 1.0)
+        assert st == 0 and C.size <= 2 * 8192
+        short.append((C, M))
+    outs0 = [workloads.normal([91, t], m) for t, m in enumerate(sizes)]
+
+    def short_batch(corrupt):
+        streams_ = [C for C, _ in short]
+        if corrupt:
+            streams_[0] = np.append(streams_[0], streams_[0][-1:])
+        outs = [torch.from_numpy(o.copy()).cuda() for o in outs0]
+        ctx.decompress_batch([torch.from_numpy(C).cuda() for C in streams_],
+                             [M for _, M in short], outs, accumulate=True)
+        st = tlc.tlc_sync(ctx.handle)
+        for t, (o, o0) in enumerate(zip(outs, outs0)):
+            if corrupt:
+                assert np.array_equal(g.bits(o.cpu().numpy()), g.bits(o0)), t
+            else:
+                _, ref = oracle.decompress(short[t][0], short[t][1], sizes[t], o0.copy(), True)
+                assert np.array_equal(g.bits(o.cpu().numpy()), g.bits(ref)), t
+        assert st == (tlc.TLC_E_CORRUPT if corrupt else tlc.TLC_OK)
+
+    assert tlc.tlc_ctx_set_epochs(ctx.handle, 0, D - 2) == tlc.TLC_OK
+    short_batch(False)  # D - 1
+    short_batch(True)   # D: the last epoch before the wrap
+    short_batch(False)  # wrap: 1
+    short_batch(False)  # 2
+    g.log("short-stream batches across the wrap ok")
