@@ -761,22 +761,24 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
   }
 }
 
-// The same tile's trits of this thread's own 16 values in each partition
+// The trits of this thread's own 16 values in each partition of a tile
 // (values k*m + q0 + 16*tid + [0, 16), so that the thread packs the 16
-// quartic bytes it encodes): the word of trit bytes from (k*m + q0)/4 +
-// 4*tid on, taken from the aligned word at or before it and the next one
-// (alignbyte; the offset within the word is the same for the whole
-// partition).  The trits fill the first n/4 bytes of a 256-byte aligned
-// region of max_n/2 bytes, so that next word lies inside it too.
+// quartic bytes it encodes): 32 consecutive bits of the trit array from bit
+// 2*(k*m + q0) + 32*tid on, taken from the aligned word at or before them
+// and the next one (alignbit; the bit offset within the word is the same
+// for the whole partition, so any m works).  The trits fill the first n/4
+// bytes of a 256-byte aligned region of max_n/2 bytes, so that next word
+// lies inside it too.
 __device__ __forceinline__ void load_trit_words(const uint8_t* __restrict__ trits, uint32_t m,
                                                 uint64_t q0, uint32_t (&d)[5]) {
+  const uint32_t* tw = reinterpret_cast<const uint32_t*>(trits);
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
-    const uint64_t b0 = ((uint64_t)k * m + q0) >> 2;
-    const uint32_t a = (uint32_t)b0 & 3u;
-    const uint32_t* wp = reinterpret_cast<const uint32_t*>(trits + (b0 - a)) + threadIdx.x;
+    const uint64_t e0 = (uint64_t)k * m + q0;  // the partition's first value in the tile
+    const uint32_t sh = 2u * (uint32_t)(e0 & 15u);
+    const uint32_t* wp = tw + (e0 >> 4) + threadIdx.x;
     const uint32_t lo = wp[0];
-    d[k] = a ? __builtin_amdgcn_alignbyte(wp[1], lo, a) : lo;
+    d[k] = sh ? __builtin_amdgcn_alignbit(wp[1], lo, sh) : lo;
   }
 }
 
@@ -866,11 +868,9 @@ void tlc_quant_encode_kernel(
   const uint32_t t = blockIdx.x;
   const uint64_t q0 = (uint64_t)t * kEncTile;
   const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
-  // an interior tile (whole, partitions on trit-byte boundaries, every
-  // value before n): each thread packs its own 16 quartic bytes in
-  // registers; other tiles pack through sh.q
-  const bool own = kTrit && m % 4u == 0u && tile_bytes == (uint32_t)kEncTile &&
-                   4ull * m + q0 + kEncTile <= n;
+  // an interior tile (whole, every value before n): each thread packs its
+  // own 16 quartic bytes in registers; other tiles pack through sh.q
+  const bool own = kTrit && tile_bytes == (uint32_t)kEncTile && 4ull * m + q0 + kEncTile <= n;
   uint32_t h[kGroupsPerThread][5];  // bounds, or with kTrit the trits
   if (kTrit) {
     const uint8_t* trits = reinterpret_cast<const uint8_t*>(summ);
