@@ -619,3 +619,43 @@ def test_c5_aggregation_and_reencode(ctx):
     g.log("C5 aggregate ok")
     res = check_encode_decode(ctx, sum_ref, np.zeros(n, F32), workloads.C5_S, tag="C5 re-encode")
     g.log(f"C5 re-encode ok: len={res[0].size}")
+
+
+# ------------------------------------------------------------------ seeded shapes
+def _seeded_cases(count=40, seed=20261202):
+    """(index, kind, n, offset, s, accumulate) draws: n log-uniform up to 3M
+    values, every tenth past the three-pass threshold (512 tiles of 4096
+    quartic bytes); offsets 0-4 values (alignment); s in [1, 2) as fp32."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        kind = ("normal", "runs", "spikes", "wide")[i % 4]
+        if i % 10 == 9:
+            n = int(5 * 4096 * 512 + rng.integers(0, 5 * 4096 * 4))
+        else:
+            n = int(np.exp(rng.uniform(0.0, np.log(3 << 20))))
+        s = float(F32(1.0 + rng.uniform(0.0, 0.999)))
+        cases.append((i, kind, n, int(rng.integers(0, 5)), s, bool(rng.integers(0, 2))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _seeded_cases(), ids=lambda c: f"{c[0]}-{c[1]}-n{c[2]}")
+def test_seeded_random_shapes(ctx, case):
+    """Forty seeded draws of size, alignment, s, input kind (small normal
+    values, zero runs, isolated spikes, unit-scale values) and accumulate:
+    stream, M, residual and decoded output bit-exact against the oracle."""
+    i, kind, n, offset, s, acc = case
+    if kind == "normal":
+        x = workloads.normal([760, i], n, 1e-3)
+    elif kind == "runs":
+        x = workloads.runs_tensor([760, i], n)
+    elif kind == "wide":
+        x = workloads.normal([760, i], n, 1.0)
+    else:
+        x = np.zeros(n, F32)
+        js = np.random.default_rng([760, i]).integers(0, n, max(1, n // 5000))
+        x[js] = workloads.normal([763, i], js.size, 1.0)
+    r = workloads.normal([761, i], n, 1e-4) if i % 3 else np.zeros(n, F32)
+    out0 = workloads.normal([762, i], n, 1e-3) if acc else None
+    check_encode_decode(ctx, x, r, s, out0=out0, accumulate=acc, offset=offset,
+                        tag=f"case {i} {kind} n={n} offset={offset} s={s}")
