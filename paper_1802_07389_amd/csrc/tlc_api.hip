@@ -406,7 +406,9 @@ int wait_results(tlc_ctx* c, const EncResult* r, uint32_t count) {
       if (q == hipSuccess) break;
       if (q != hipErrorNotReady) return hip_fail(q, "hipStreamQuery");
     }
-    __builtin_ia32_pause();
+#if defined(__x86_64__) || defined(__i386__)
+    __builtin_ia32_pause();  // a spin-wait hint to the core
+#endif
   }
   int st = sync_mirrored(c);
   if (st) return st;
@@ -593,6 +595,10 @@ TLC_API int tlc_ctx_destroy(tlc_ctx* c) {
   DeviceScope dev(c->device);
   (void)hipStreamSynchronize(c->stream);
   collect_timings(c);
+  for (const PendingTiming& p : c->pending) {  // left only if the stream failed
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
   for (hipEvent_t ev : c->free_events) (void)hipEventDestroy(ev);
   for (int i = 0; i < kStagingSlots; ++i)
     if (c->staging_done[i]) (void)hipEventDestroy(c->staging_done[i]);
