@@ -520,6 +520,9 @@ def main():
     ctx.profile(True, kernels=[dom_id])
     ctx.profile_reset()
     lens.clear()
+    # the state the timed steps start from, so that the per-kernel timing and
+    # the in-place comparison below replay exactly these steps
+    resid0, model0 = resid.clone(), model.clone()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -532,51 +535,63 @@ def main():
     dom_ms_timed /= max(dom_cnt, 1)
     timed_lens = list(lens)
 
-    # Further untimed steps time every kernel of a step, one kernel at a
-    # time: a single event pair per step, as for the roofline kernel (an
-    # event pair on every kernel would cost tens of microseconds per step).
-    kern_steps = 3
-    names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
-    enc_k = ["tlc_absmax_check_kernel", "tlc_accum_quantize_kernel", "tlc_quant_encode_kernel",
-             "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
-    dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
-    kern = {}
-    base = args.warmup + args.steps
-    for name in enc_k + dec_k:
-        kid = names.index(name)
-        ctx.profile(True, kernels=[kid])
-        ctx.profile_reset()
-        for k in range(kern_steps):
-            step(base + k)
-        ctx.sync()
-        ctx.profile(False)
-        ms, cnt = ctx.profile_get(kid)
-        kern[name] = (ms / cnt if cnt else 0.0, cnt)
-        base += kern_steps
-
-    # The same steps with TLC_OPT_IN_PLACE_FEEDBACK (no check pass before the
-    # in-place max pass; only the residual after NaN/Inf differs), timed the
-    # same way without any events.
-    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
-    for k in range(2):
-        step(base + k)
-    ctx.sync()
-    torch.cuda.synchronize()
-    t0_ip = time.perf_counter()
-    for k in range(args.steps):
-        step(base + 2 + k)
-    ctx.sync()
-    torch.cuda.synchronize()
-    t1_ip = time.perf_counter()
-    ctx.set_options(0)
-
-    # Values with q != 0 in the last step's stream: its decode into zeros is
-    # non-zero exactly there (M > 0).
+    # Values with q != 0 in the last timed step's stream: its decode into
+    # zeros is non-zero exactly there (M > 0).
     probe = torch.zeros(n, dtype=torch.float32, device=dev)
     ctx.decompress(payload[:lens[-1]], scales[-1], n, probe, accumulate=False)
     ctx.sync()
     nnz = int(torch.count_nonzero(probe).item())
     del probe
+
+    def replay():
+        """The timed steps again, from the state they started from; the
+        streams come out the same (the library is deterministic)."""
+        resid.copy_(resid0)
+        model.copy_(model0)
+        lens.clear()
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            step(args.warmup + k)
+        ctx.sync()
+        assert lens == timed_lens, "a replayed step gave another stream length"
+
+    # Every kernel timed over the same steps, one kernel at a time: a single
+    # event pair per step, as for the roofline kernel (an event pair on every
+    # kernel would cost tens of microseconds per step).
+    names = [tlc.tlc_kernel_name(k) for k in range(tlc.TLC_KERNEL_COUNT)]
+    enc_k = ["tlc_absmax_check_kernel", "tlc_accum_quantize_kernel", "tlc_quant_encode_kernel",
+             "tlc_zre_chunk_kernel", "tlc_zre_compact_kernel"]
+    dec_k = ["tlc_zre_index_kernel", "tlc_expand_dequant_kernel"]
+    kern = {}
+    for name in enc_k + dec_k:
+        kid = names.index(name)
+        ctx.profile(True, kernels=[kid])
+        ctx.profile_reset()
+        replay()
+        ctx.profile(False)
+        ms, cnt = ctx.profile_get(kid)
+        kern[name] = (ms / cnt if cnt else 0.0, cnt)
+
+    # The same steps with TLC_OPT_IN_PLACE_FEEDBACK (no check pass before the
+    # in-place max pass; only the residual after NaN/Inf differs), timed the
+    # same way without any events, after two steps that load its kernels.
+    ctx.set_options(tlc.TLC_OPT_IN_PLACE_FEEDBACK)
+    for k in range(2):
+        step(args.warmup + k)
+    ctx.sync()
+    resid.copy_(resid0)
+    model.copy_(model0)
+    lens.clear()
+    torch.cuda.synchronize()
+    t0_ip = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k)
+    ctx.sync()
+    torch.cuda.synchronize()
+    t1_ip = time.perf_counter()
+    ctx.set_options(0)
+    assert lens == timed_lens, "the in-place option gave another stream length"
+    del resid0, model0
 
     elapsed = t1 - t0
     ms_per_step = elapsed / args.steps * 1e3
@@ -638,9 +653,9 @@ def main():
         "decode_dense_equiv_hbm_frac": round((c_avg + 8 * n) / (dec_kernel_ms * 1e-3) / 1e9
                                              / PEAK_HBM_GBPS, 4),
         "kernels_avg_ms": {k: round(v[0], 5) for k, v in kern.items() if v[1]},
-        "kernels_avg_ms_note": "each kernel timed alone (one event pair per step) over %d "
-                               "further steps after the timed region; the roofline kernel "
-                               "is timed inside it" % kern_steps,
+        "kernels_avg_ms_note": "each kernel timed alone (one event pair per step) over a "
+                               "replay of the timed steps from their starting state; the "
+                               "roofline kernel is timed inside the timed region",
         "in_place_feedback": {
             "value": round(4 * n * args.steps / (t1_ip - t0_ip) / 1e9, 2),
             "ms_per_step": round((t1_ip - t0_ip) / args.steps * 1e3, 4),
