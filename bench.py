@@ -457,8 +457,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the 3LC path is per tensor and this build "
-              "has no multi-GPU leg (run with --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only: the 3LC path is per tensor and the "
+              "library has no multi-GPU leg (run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch

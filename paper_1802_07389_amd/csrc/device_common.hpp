@@ -443,6 +443,33 @@ __device__ __forceinline__ uint32_t nonzero_mask16(const uint4& w, uint32_t cnt)
   return cnt >= 16u ? nz : nz & ((1u << cnt) - 1u);
 }
 
+// The same mask in spread form, bit 2i for byte lo + i (rs_gaps_len<2>):
+// the multiply places the four bit-7 flags, shifted to bits 0, 8, 16, 24,
+// at bits 18, 20, 22, 24 (again no two partial products share a bit).
+__device__ __forceinline__ uint32_t nonzero_byte_mask4_spread(uint32_t w) {
+  const uint32_t x = w ^ 0x79797979u;
+  const uint32_t y = (x | ((x & 0x7f7f7f7fu) + 0x7f7f7f7fu)) & 0x80808080u;
+  return ((y >> 7) * 0x00041041u) >> 18 & 0x55u;
+}
+
+__device__ __forceinline__ uint32_t nonzero_mask16_spread(const uint4& w, uint32_t cnt) {
+  const uint32_t nz = nonzero_byte_mask4_spread(w.x) | (nonzero_byte_mask4_spread(w.y) << 8) |
+                      (nonzero_byte_mask4_spread(w.z) << 16) |
+                      (nonzero_byte_mask4_spread(w.w) << 24);
+  return cnt >= 16u ? nz : nz & ((1u << (2u * cnt)) - 1u);
+}
+
+// The spread mask of the 16 quartic bytes that five trit words pack (word
+// k holds partition k's trits, trit i in bits 2i and 2i + 1, as q + 1):
+// byte i is 121 exactly when all five of its trits are 1 (Section 3.2: 121
+// is 11111 in base 3), i.e. when bits 2i, 2i + 1 read 01 in every word.
+__device__ __forceinline__ uint32_t nonzero_mask_trits(const uint32_t (&d)[5]) {
+  constexpr uint32_t kOnes = 0x55555555u;  // trit 1 in every field
+  const uint32_t z = (d[0] ^ kOnes) | (d[1] ^ kOnes) | (d[2] ^ kOnes) | (d[3] ^ kOnes) |
+                     (d[4] ^ kOnes);
+  return (z | (z >> 1)) & kOnes;
+}
+
 __device__ __forceinline__ uint32_t nonzero_group_mask(const uint8_t* q, uint32_t lo,
                                                        uint32_t cnt) {
   return nonzero_mask16(*reinterpret_cast<const uint4*>(q + lo), cnt);

@@ -882,7 +882,18 @@ void tlc_quant_encode_kernel(
   } else if (kPath == kPathVec && summ) {
     load_bounds(summ, n, m, q0, tile_bytes, h);
   }
-  const Scale sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+  Scale sc;
+  if (kTrit && t != 0) {
+    // with trits only block 0 needs M (for the result); the others need the
+    // verdict, which the writing pass left in every partial: all 0xffffffff
+    // for a refused tensor, otherwise the check pass's finite maxima
+    __syncthreads();  // the tables
+    sc.M = 0.0f;
+    sc.U = 0.0f;
+    sc.bad = partials[0] >= 0x7f800000u ? 1u : 0u;
+  } else {
+    sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+  }
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
     ctrl->enc.scale = sc.M;
@@ -914,15 +925,17 @@ void tlc_quant_encode_kernel(
   // thread emits gives its output offset (zre_scan.hpp: rs_gaps_len,
   // rs_gaps_emit); the thread with the tile's last non-121 byte adds the
   // trailing run's codes 255 to its length.
+  // The mask of the thread's non-121 bytes is kept spread, bit 2i for byte
+  // lo + i, the form the trits of a register-packed tile give directly.
   static_assert(kBytes == 16, "one uint4 of quartic bytes per thread");
-  const uint32_t nz = cnt ? nonzero_mask16(w, cnt) : 0u;
-  const uint32_t last = nz ? lo + 31u - (uint32_t)__builtin_clz(nz) : 0u;
+  const uint32_t nz = own ? nonzero_mask_trits(h[0]) : (cnt ? nonzero_mask16_spread(w, cnt) : 0u);
+  const uint32_t last = nz ? lo + (31u - (uint32_t)__builtin_clz(nz)) / 2u : 0u;
   const ScanU32 pm = block_scan_max_u32(nz ? last + 1u : 0u, sh.red);
   const int prev = (int)pm.excl - 1;  // the previous non-121 byte, -1 if none
   const bool tail = nz != 0u && last + 1u == pm.total;
-  if (nz != 0u && prev < 0) sh.lead = lo + (uint32_t)__builtin_ctz(nz);
+  if (nz != 0u && prev < 0) sh.lead = lo + (uint32_t)__builtin_ctz(nz) / 2u;
   const uint32_t trail = tile_bytes - pm.total;  // 121s after the last non-121 byte
-  const uint32_t mine = rs_gaps_len(nz, lo, prev) + (tail ? trail / kRunMax : 0u);
+  const uint32_t mine = rs_gaps_len<2>(nz, lo, prev) + (tail ? trail / kRunMax : 0u);
   // every output byte that is not a remainder code or a non-121 byte is a
   // 255: fill the whole output with 255 first (the scan's barrier orders
   // it before the writes below), so runs only advance the offset
@@ -936,8 +949,9 @@ void tlc_quant_encode_kernel(
     ++o;
   };
   const uint32_t w0 = w.x, w1 = w.y, w2 = w.z, w3 = w.w;
-  rs_gaps_emit(nz, lo, prev, [w0, w1, w2, w3](uint32_t i) { return byte_of16(w0, w1, w2, w3, i); },
-               put, [&](uint32_t k) { o += k; });
+  rs_gaps_emit<2>(nz, lo, prev,
+                  [w0, w1, w2, w3](uint32_t i) { return byte_of16(w0, w1, w2, w3, i); }, put,
+                  [&](uint32_t k) { o += k; });
   // the slot holds at most the tile's own bytes; the clamp only keeps a
   // logic error inside the slot
   const uint32_t len = umin32(off.total, tile_bytes);

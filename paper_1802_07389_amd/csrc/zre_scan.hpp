@@ -189,8 +189,9 @@ TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byt
 // A segment that starts at a non-121 byte (phase 0) in terms of the gaps
 // between its non-121 bytes: a gap of g bytes of 121 costs floor(g/14)
 // codes 255 and, if g mod 14 != 0, one remainder code; each non-121 byte
-// costs itself.  For the non-121 bytes of one thread (mask nz, bit i at
-// position lo + i) after the segment's previous non-121 byte at prev
+// costs itself.  For the non-121 bytes of one thread (mask nz, bit
+// kStep * i for position lo + i; kStep 2 is the spread form that 2-bit
+// trits give directly) after the segment's previous non-121 byte at prev
 // (prev < 0: none; the thread's first byte then opens the segment),
 // rs_gaps_len counts the bytes they emit with their gaps and rs_gaps_emit
 // emits them, handing each gap's k codes 255 to fill(k) and every other
@@ -199,23 +200,25 @@ TLC_HD uint32_t rs_mask_walk(uint32_t nz, uint32_t len, uint32_t phi, Byte&& byt
 // non-121 byte emits its floor(g/14) codes 255 separately.
 TLC_HD uint32_t rs_gap_len(uint32_t g) { return g / kRunMax + (g % kRunMax != 0u ? 1u : 0u); }
 
-// With nz inside 16 bits, a gap between two of the thread's own bytes is
-// at most 14 bytes and costs exactly one code if non-empty: besides the
-// gap from prev, the count is one per non-121 byte plus one per maximal run
-// of set bits after the first.
+// With nz covering at most 16 bytes, a gap between two of the thread's own
+// bytes is at most 14 bytes and costs exactly one code if non-empty:
+// besides the gap from prev, the count is one per non-121 byte plus one per
+// maximal run of marked bytes after the first.
+template <uint32_t kStep = 1>
 TLC_HD uint32_t rs_gaps_len(uint32_t nz, uint32_t lo, int prev) {
+  static_assert(kStep == 1 || kStep == 2, "one or two mask bits per byte");
   if (nz == 0u) return 0u;
-  const uint32_t first = lo + (uint32_t)__builtin_ctz(nz);
-  const uint32_t runs = (uint32_t)__builtin_popcount(nz & ~(nz << 1));
+  const uint32_t first = lo + (uint32_t)__builtin_ctz(nz) / kStep;
+  const uint32_t runs = (uint32_t)__builtin_popcount(nz & ~(nz << kStep));
   return (prev >= 0 ? rs_gap_len(first - (uint32_t)prev - 1u) : 0u) +
          (uint32_t)__builtin_popcount(nz) + runs - 1u;
 }
 
-template <class Byte, class Put, class Fill>
+template <uint32_t kStep = 1, class Byte, class Put, class Fill>
 TLC_HD void rs_gaps_emit(uint32_t nz, uint32_t lo, int prev, Byte&& byte, Put&& put,
                          Fill&& fill) {
   while (nz) {
-    const uint32_t i = (uint32_t)__builtin_ctz(nz);
+    const uint32_t i = (uint32_t)__builtin_ctz(nz) / kStep;
     const uint32_t p = lo + i;
     nz &= nz - 1u;
     if (prev >= 0) {

@@ -16,9 +16,11 @@
 // agree with the byte-by-byte forms (exit 4, 5, 6 otherwise), and every
 // tile is also encoded in the gap form (rs_gaps_len, rs_gaps_emit: output
 // offsets from a sum over threads, the previous non-121 byte from a max),
-// which must give the same slot and record (exit 7-10 otherwise).
+// which must give the same slot and record (exit 7-10 otherwise), with the
+// mask in its compact and its spread form alike (exit 11, 12 otherwise).
 // Reads raw bytes on stdin, writes the encoded stream on stdout.
 // Usage: zre_deferred_sim TILE PER < in > out
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
@@ -107,14 +109,26 @@ int main(int argc, char** argv) {
         const uint32_t lo = (uint32_t)(ti * per), nz = nzs[ti];
         const int last = nz ? (int)(lo + 31 - __builtin_clz(nz)) : -1;
         uint32_t len = rs_gaps_len(nz, lo, prev);
+        // the spread form (bit 2i for byte lo + i) must agree
+        uint32_t nz2 = 0u;
+        for (uint32_t i = 0; i < 16u; ++i) nz2 |= ((nz >> i) & 1u) << (2u * i);
+        if (rs_gaps_len<2>(nz2, lo, prev) != len) return 11;
         if (nz && last == last_all) len += (uint32_t)(tb - 1 - last) / kRunMax;
         const size_t before = gslot.size();
         auto fill = [&](uint32_t k) {
           for (uint32_t e = 0; e < k; ++e) gslot.push_back((uint8_t)kFullChunk);
         };
+        std::vector<uint8_t> spread_out;
+        rs_gaps_emit<2>(
+            nz2, lo, prev, [&](uint32_t i) { return (uint32_t)q[q0 + lo + i]; },
+            [&](uint32_t b) { spread_out.push_back((uint8_t)b); },
+            [&](uint32_t k) { spread_out.insert(spread_out.end(), k, (uint8_t)kFullChunk); });
         rs_gaps_emit(
             nz, lo, prev, [&](uint32_t i) { return (uint32_t)q[q0 + lo + i]; },
             [&](uint32_t b) { gslot.push_back((uint8_t)b); }, fill);
+        if (spread_out.size() != gslot.size() - before ||
+            !std::equal(spread_out.begin(), spread_out.end(), gslot.begin() + before))
+          return 12;
         if (nz && last == last_all) fill((uint32_t)(tb - 1 - last) / kRunMax);
         if (gslot.size() - before != len) return 7;
         total += len;
