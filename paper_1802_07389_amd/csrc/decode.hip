@@ -86,10 +86,15 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
       w[q] = x;
     }
   }
-  uint32_t sum = 0;
+  // one quartic byte per stream byte and the runs' extra bytes word by
+  // word (the zero bytes past cnt add nothing)
+  uint32_t wx[kBytes / 4];
+  uint32_t sum = cnt;
 #pragma unroll
-  for (int i = 0; i < kBytes; ++i)
-    if ((uint32_t)i < cnt) sum += expanded_len((w[i >> 2] >> (8 * (i & 3))) & 255u);
+  for (int q = 0; q < kBytes / 4; ++q) {
+    wx[q] = run_extra4(w[q]);
+    sum += wx[q];
+  }
   const ScanU32 sc = block_scan_u32(sum, sh.red);
   const uint32_t agg = sc.total;
 
@@ -133,19 +138,28 @@ __device__ __forceinline__ void index_tile(const uint8_t* __restrict__ C, uint32
   const uint64_t at = k * kDecRange;
   if (at < m && at < o + sum) {
     const uint32_t d = (uint32_t)(at - o);  // the start's distance into the thread's expansion
-    uint32_t rel = 0, hit = 0, into = 0;
-    bool found = false;
+    // The word whose expansion holds position d (the words' expansions tile
+    // [0, sum), so exactly one has d - rel < its length), then the byte in
+    // it.  Every word before it holds four of the thread's bytes; the zero
+    // bytes past cnt come after the start's byte and are never reached.
+    uint32_t rel = 0, hq = 0, hw = 0, hrel = 0;
 #pragma unroll
-    for (int i = 0; i < kBytes; ++i) {
-      if ((uint32_t)i < cnt) {
-        const uint32_t len = expanded_len((w[i >> 2] >> (8 * (i & 3))) & 255u);
-        if (!found && d < rel + len) {
-          hit = (uint32_t)i;
-          into = d - rel;
-          found = true;
-        }
-        rel += len;
-      }
+    for (int q = 0; q < kBytes / 4; ++q) {
+      const uint32_t wl = 4u + wx[q];
+      const bool here = d - rel < wl;  // d < rel wraps to a large difference
+      hq = here ? (uint32_t)q : hq;
+      hw = here ? w[q] : hw;
+      hrel = here ? rel : hrel;
+      rel += wl;
+    }
+    uint32_t hit = 4u * hq, into = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t len = expanded_len((hw >> (8 * c)) & 255u);
+      const bool here = d - hrel < len;
+      hit = here ? 4u * hq + (uint32_t)c : hit;
+      into = here ? d - hrel : into;
+      hrel += len;
     }
     status_publish(&start[k], ((uint64_t)epoch << kStartPayloadBits) | ((j0 + hit) << 8) | into);
   }

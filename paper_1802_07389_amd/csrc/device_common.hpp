@@ -387,6 +387,17 @@ __device__ __forceinline__ uint32_t expanded_len(uint32_t b) {
   return b < kRunBase ? 1u : b - (kRunBase - 2u);
 }
 
+// What the four stream bytes of w expand to beyond one quartic byte each:
+// byte b adds max(b - 242, 0) (expanded_len less one), which is
+// (|b - 242| + b - 242) / 2, and two sums of absolute byte differences
+// (v_sad_u8) give that for the four bytes at once.  A zero byte adds 0.
+__device__ __forceinline__ uint32_t run_extra4(uint32_t w) {
+  constexpr uint32_t kPivot = kRunBase - 1u;  // 242 in every byte below
+  const uint32_t s =
+      __builtin_amdgcn_sad_u8(w, kPivot * 0x01010101u, __builtin_amdgcn_sad_u8(w, 0u, 0u));
+  return (s - 4u * kPivot) >> 1;
+}
+
 // ---------------------------------------------------------------- Eq. 3
 // The dequantized value M*q for trit t = q + 1 is -M, M*0 or M (M*(-1) is
 // the exact negation; M*0 is +0, or -0 for a scale of -0.0, which the
