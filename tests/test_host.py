@@ -185,3 +185,33 @@ def test_quantization_threshold_matches_oracle():
         assert Mo == M
         expect = [1] + [1, 0, 0, 0] + [-1, 0, 0, 0]
         assert q.tolist() == expect
+
+
+def test_byte_tricks_of_the_zero_run_kernels():
+    """The word-level shortcuts the zero-run kernels take, exhaustively.
+
+    * The index scan counts a stream byte's expansion beyond one quartic
+      byte as (|b - 242| + b - 242) / 2, from two sums of absolute byte
+      differences: it must equal expanded length - 1 (codes 243..255 stand
+      for runs of 2..14 bytes of 121, every other byte for itself).
+    * The first encode pass marks quartic byte i as non-121 from its five
+      trits (q + 1): a byte is 121 exactly when all five trits are 1.
+    * The spread byte mask gathers the four bytes' flags with one multiply
+      (constant with bits 0, 6, 12, 18), whose partial products must not
+      overlap.
+    """
+    b = np.arange(256, dtype=np.int64)
+    expanded = np.where(b < 243, 1, b - 241)
+    assert np.array_equal((np.abs(b - 242) + b - 242) // 2, expanded - 1)
+    # five trits per byte, weights 81, 27, 9, 3, 1: only 11111 (base 3) is 121
+    t = np.array(np.meshgrid(*[np.arange(3)] * 5, indexing="ij")).reshape(5, -1)
+    byte = (t * np.array([81, 27, 9, 3, 1])[:, None]).sum(0)
+    assert np.array_equal(byte == 121, (t == 1).all(0))
+    # flags at bits 0, 8, 16, 24 times 0x41041: every partial product on its
+    # own bit, and the four flags land on bits 18, 20, 22, 24
+    bits = sorted(8 * f + k for f in range(4) for k in (0, 6, 12, 18) if 8 * f + k < 32)
+    assert len(bits) == len(set(bits))
+    for flags in range(16):
+        y = sum(((flags >> f) & 1) << (8 * f) for f in range(4))
+        spread = ((y * 0x00041041) & 0xFFFFFFFF) >> 18 & 0x55
+        assert spread == sum(((flags >> f) & 1) << (2 * f) for f in range(4))
