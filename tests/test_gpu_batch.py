@@ -446,3 +446,44 @@ def test_batch_decode_short_and_long_streams(bctx, big, corrupt):
     for t, (o, o0) in enumerate(zip(outs, outs0)):
         st, ref = oracle.decompress(pays[t][0], pays[t][1], sizes[t], o0.copy(), True)
         assert st == 0 and np.array_equal(g.bits(o.cpu().numpy()), g.bits(ref)), t
+
+
+def test_batch_calls_alternating_buffer_sets(bctx):
+    """Batched encodes on one context that alternate between two sets of
+    buffers, and repeat one, all match the oracle (the residuals carried
+    from call to call): nothing of one call's descriptors leaks into the
+    next."""
+    import torch
+    from paper_1802_07389_amd import tlc
+    g = G()
+
+    def make(sizes, seed):
+        xs = [torch.empty(n, dtype=torch.float32, device="cuda") for n in sizes]
+        rs = [torch.zeros(n, dtype=torch.float32, device="cuda") for n in sizes]
+        outs = [torch.empty(tlc.tlc_max_compressed_bytes(n), dtype=torch.uint8, device="cuda")
+                for n in sizes]
+        return dict(sizes=sizes, xs=xs, rs=rs, outs=outs, r_ref=[np.zeros(n, F32) for n in sizes],
+                    seed=seed)
+
+    def run(b, step):
+        xh = [workloads.normal([760, b["seed"], step, t], n, 1.0)
+              for t, n in enumerate(b["sizes"])]
+        for x, xd in zip(xh, b["xs"]):
+            xd.copy_(torch.from_numpy(x))
+        ss = [1.75] * len(xh)
+        st, lens, scales, stat = tlc.tlc_compress_batch(
+            bctx.handle, [t.data_ptr() for t in b["xs"]], [t.data_ptr() for t in b["rs"]],
+            b["sizes"], ss, [o.data_ptr() for o in b["outs"]], [o.numel() for o in b["outs"]])
+        torch.cuda.synchronize()
+        assert st == 0 and all(v == 0 for v in stat), (b["seed"], step)
+        for t, x in enumerate(xh):
+            st_ref, C_ref, M_ref = oracle.compress(x, b["r_ref"][t], 1.75)
+            assert st_ref == 0 and scales[t] == M_ref, (b["seed"], step, t)
+            assert np.array_equal(b["outs"][t][:lens[t]].cpu().numpy(), C_ref), (b["seed"], step, t)
+            assert np.array_equal(g.bits(b["rs"][t].cpu().numpy()), g.bits(b["r_ref"][t])), \
+                (b["seed"], step, t)
+
+    A = make([2 * 20480 + 7, 1000, 5], 1)
+    B = make([333, 20480 + 1], 2)
+    for step, b in enumerate([A, A, B, A, B, B, A]):
+        run(b, step)
