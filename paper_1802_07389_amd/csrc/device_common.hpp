@@ -42,23 +42,27 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   return wave_last(wave_incl_scan(v, 0u, OpMax()));
 }
 
-// Block-wide max; every thread gets the result.  Uses lds[kWaves] and one
-// barrier; callers that reuse lds must barrier again first.
+// Block-wide max over a block of kW waves; every thread gets the result.
+// Uses lds[kW] and one barrier; callers that reuse lds must barrier again
+// first.
+template <int kW = kWaves>
 __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* lds) {
   v = wave_max(v);
   if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = v;
   __syncthreads();
   uint32_t r = lds[0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) r = max(r, lds[w]);
+  for (int w = 1; w < kW; ++w) r = max(r, lds[w]);
   return r;
 }
 
-// Block-wide exclusive prefix of u32 values: returns (exclusive prefix of
-// this thread, block total).  Uses lds[kWaves] and one barrier.
+// Block-wide exclusive prefix of u32 values over a block of kW waves:
+// returns (exclusive prefix of this thread, block total).  Uses lds[kW] and
+// one barrier.
 struct ScanU32 {
   uint32_t excl, total;
 };
+template <int kW = kWaves>
 __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t incl = wave_incl_scan(v, 0u, OpAdd());
@@ -68,15 +72,16 @@ __device__ __forceinline__ ScanU32 block_scan_u32(uint32_t v, uint32_t* lds) {
   r.excl = incl - v;
   r.total = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < kW; ++w) {
     if ((uint32_t)w < wid) r.excl += lds[w];
     r.total += lds[w];
   }
   return r;
 }
 
-// Exclusive max-scan over the block (0 for thread 0) and the block's max
-// (all threads; ends with a barrier-protected read of lds).
+// Exclusive max-scan over a block of kW waves (0 for thread 0) and the
+// block's max (all threads; ends with a barrier-protected read of lds).
+template <int kW = kWaves>
 __device__ __forceinline__ ScanU32 block_scan_max_u32(uint32_t v, uint32_t* lds) {
   const uint32_t lane = threadIdx.x & 63u, wid = threadIdx.x >> 6;
   const uint32_t incl = wave_incl_scan(v, 0u, OpMax());
@@ -87,7 +92,7 @@ __device__ __forceinline__ ScanU32 block_scan_max_u32(uint32_t v, uint32_t* lds)
   r.excl = excl;
   r.total = 0u;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < kW; ++w) {
     if ((uint32_t)w < wid) r.excl = max(r.excl, lds[w]);
     r.total = max(r.total, lds[w]);
   }
@@ -154,12 +159,15 @@ __device__ __forceinline__ float quant_threshold(float M) {
   return f;
 }
 
-// M and U from the partial maxima of one tensor (all threads of the block).
+// M and U from the partial maxima of one tensor (all kT threads of the
+// block).
+template <int kT = kThreads>
 __device__ __forceinline__ Scale finish_scale(const uint32_t* __restrict__ partials,
                                               uint32_t np, float s, uint32_t* lds) {
+  static_assert(kT % 64 == 0, "whole waves");
   uint32_t v = 0;
-  for (uint32_t i = threadIdx.x; i < np; i += kThreads) v = max(v, partials[i]);
-  const uint32_t A = block_max(v, lds);
+  for (uint32_t i = threadIdx.x; i < np; i += kT) v = max(v, partials[i]);
+  const uint32_t A = block_max<kT / 64>(v, lds);
   Scale sc;
   sc.M = 0.0f;
   sc.U = 0.0f;

@@ -729,9 +729,10 @@ __device__ __forceinline__ void quantize_tile_vec_deferred(
 // are issued before the block reduces it.  pack_trits then forms the
 // quartic bytes (Section 3.2), with the values past n as the zero padding
 // (trit 0), and ends with a barrier.
+template <int kT = kThreads>
 __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, uint64_t n,
                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
-                                           uint32_t (&tb)[kGroupsPerThread][5]) {
+                                           uint32_t (&tb)[kEncTile / 4 / kT][5]) {
 #pragma unroll
   for (int k = 0; k < 5; ++k) {
     // group g's first value is e = base + 4g; q0 is a multiple of 4, so
@@ -744,8 +745,8 @@ __device__ __forceinline__ void load_trits(const uint8_t* __restrict__ trits, ui
     const uint32_t lim = (uint32_t)umin64(left, tile_bytes);
     const uint32_t cap = (uint32_t)umin64(left + a, 2u * kEncTile);
 #pragma unroll
-    for (int it = 0; it < kGroupsPerThread; ++it) {
-      const uint32_t g = threadIdx.x + kThreads * it;
+    for (int it = 0; it < kEncTile / 4 / kT; ++it) {
+      const uint32_t g = threadIdx.x + kT * it;
       uint32_t v = 0u;
       if (g * 4u < lim) {
         v = tp[g];
@@ -794,14 +795,18 @@ __device__ __forceinline__ uint32_t spread_trits(uint32_t tb) {
 // a group (each at most 242, so no carry crosses a lane): five LDS reads
 // and four adds instead of five spreads and four multiply-adds.  Written
 // before a barrier of the caller.
+template <int kT = kThreads>
 __device__ __forceinline__ void init_trit_luts(uint32_t (*lut)[256]) {
-  static_assert(kThreads == 256, "one table entry per thread and partition");
-  const uint32_t sp = spread_trits(threadIdx.x);
-  lut[0][threadIdx.x] = 81u * sp;
-  lut[1][threadIdx.x] = 27u * sp;
-  lut[2][threadIdx.x] = 9u * sp;
-  lut[3][threadIdx.x] = 3u * sp;
-  lut[4][threadIdx.x] = sp;
+  static_assert(256 % kT == 0, "whole rounds of table entries");
+#pragma unroll
+  for (uint32_t b = threadIdx.x; b < 256u; b += kT) {
+    const uint32_t sp = spread_trits(b);
+    lut[0][b] = 81u * sp;
+    lut[1][b] = 27u * sp;
+    lut[2][b] = 9u * sp;
+    lut[3][b] = 3u * sp;
+    lut[4][b] = sp;
+  }
 }
 
 // This thread's 16 quartic bytes from its trit words (load_trit_words):
@@ -817,13 +822,14 @@ __device__ __forceinline__ uint4 pack_trit_words(const uint32_t (&d)[5],
   return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
-__device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kGroupsPerThread][5], uint64_t n,
+template <int kT = kThreads>
+__device__ __forceinline__ void pack_trits(const uint32_t (&tb)[kEncTile / 4 / kT][5], uint64_t n,
                                            uint32_t m, uint64_t q0, uint32_t tile_bytes,
                                            const uint32_t (*lut)[256], uint8_t* q) {
   uint32_t* qw = reinterpret_cast<uint32_t*>(q);
 #pragma unroll
-  for (int it = 0; it < kGroupsPerThread; ++it) {
-    const uint32_t g = threadIdx.x + kThreads * it;
+  for (int it = 0; it < kEncTile / 4 / kT; ++it) {
+    const uint32_t g = threadIdx.x + kT * it;
     if (g * 4u >= tile_bytes) break;
     const uint64_t j = q0 + g * 4u;
     if (4ull * m + j + 4u <= n) {
@@ -861,6 +867,7 @@ void tlc_quant_encode_kernel(
   __shared__ EncShared sh;
   __shared__ uint2 s_fix[(kPath == kPathVec && !kTrit) ? kFixCap : 1];
   __shared__ uint32_t s_lut[kTrit ? 5 : 1][256];
+  __shared__ uint32_t s_scale[kWaves];  // M's reduction: the scans below reuse sh.red
   if (threadIdx.x == 0) {
     sh.nfix = 0u;
     sh.nneed = 0u;
@@ -892,7 +899,7 @@ void tlc_quant_encode_kernel(
     sc.U = 0.0f;
     sc.bad = partials[0] >= 0x7f800000u ? 1u : 0u;
   } else {
-    sc = finish_scale(partials, np, s, sh.red);  // includes a barrier
+    sc = finish_scale(partials, np, s, s_scale);  // includes a barrier
   }
   if (t == 0 && threadIdx.x == 0) {
     ctrl->enc.err = sc.bad;
@@ -970,6 +977,154 @@ void tlc_quant_encode_kernel(
       rec.len = (uint16_t)len;
     }
     rec.nfix = umin32(sh.nfix, kFixCap);
+    recs[t] = rec;
+  }
+}
+
+// The first pass from trits with two waves per tile: each thread takes 32
+// quartic bytes, twice what tlc_quant_encode_kernel's threads take, so the
+// block scans, the scale's verdict and the record, which cost the same per
+// thread, are spread over twice the bytes (this pass is bound by its vector
+// instructions).  The same stream and records as tlc_quant_encode_kernel
+// with trits: the thread's bytes are two halves of 16, each packed and
+// masked as there, and the emitted-byte count and the emission take the
+// halves in turn (a gap inside a half costs exactly one code).
+constexpr int kTritThreads = 128;
+constexpr int kTritWaves = kTritThreads / 64;
+// Below this many tiles the grid is too small to hide the longer work per
+// block, and four waves per tile are faster (on gfx950: 13,108 tiles 19.3
+// against 23.0 us; a mix of 3,277- and 1,250-tile tensors 10.8 against 9.6).
+constexpr uint32_t kTritTwoWaveMinTiles = 8192;
+static_assert(kEncTile / kTritThreads == 32, "two uint4 of quartic bytes per thread");
+
+__global__ __launch_bounds__(kTritThreads) void tlc_quant_encode_trits_kernel(
+    uint64_t n, uint32_t m, float s, const uint32_t* __restrict__ partials, uint32_t np,
+    uint8_t* __restrict__ slots, TileRec* __restrict__ recs, const uint8_t* __restrict__ trits,
+    Ctrl* __restrict__ ctrl, HostMirror hm) {
+  __shared__ EncShared sh;
+  __shared__ uint32_t s_lut[5][256];
+  __shared__ uint32_t s_scale[kTritWaves];  // block 0's reduction of M, read after its barrier
+  const uint32_t t = blockIdx.x;
+  const uint64_t q0 = (uint64_t)t * kEncTile;
+  const uint32_t tile_bytes = (uint32_t)umin64(kEncTile, (uint64_t)m - q0);
+  // an interior tile (whole, every value before n): each thread packs its
+  // own 32 quartic bytes in registers; other tiles pack through sh.q
+  const bool own = tile_bytes == (uint32_t)kEncTile && 4ull * m + q0 + kEncTile <= n;
+  const uint32_t lo = threadIdx.x * 32u;
+  uint32_t d[2][5];  // own tile: the trits of the thread's values, 16 per word
+  uint32_t h[kEncTile / 4 / kTritThreads][5];
+  if (own) {
+    // 64 consecutive bits of the trit array per partition from bit
+    // 2*(k*m + q0) + 64*tid on, from the aligned words at or after the one
+    // holding the first; as in load_trit_words, the word past the last one
+    // lies inside the trit area
+    const uint32_t* tw = reinterpret_cast<const uint32_t*>(trits);
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      const uint64_t e0 = (uint64_t)k * m + q0;
+      const uint32_t sh2 = 2u * (uint32_t)(e0 & 15u);
+      const uint32_t* wp = tw + (e0 >> 4) + 2u * threadIdx.x;
+      const uint32_t w0 = wp[0], w1 = wp[1], w2 = wp[2];
+      d[0][k] = sh2 ? __builtin_amdgcn_alignbit(w1, w0, sh2) : w0;
+      d[1][k] = sh2 ? __builtin_amdgcn_alignbit(w2, w1, sh2) : w1;
+    }
+  } else {
+    load_trits<kTritThreads>(trits, n, m, q0, tile_bytes, h);
+  }
+  init_trit_luts<kTritThreads>(s_lut);
+  Scale sc;
+  if (t != 0) {
+    // only block 0 needs M (for the result); the others need the verdict,
+    // which the writing pass left in every partial: all 0xffffffff for a
+    // refused tensor, otherwise the check pass's finite maxima
+    __syncthreads();  // the tables
+    sc.M = 0.0f;
+    sc.U = 0.0f;
+    sc.bad = partials[0] >= 0x7f800000u ? 1u : 0u;
+  } else {
+    // its own LDS words: the scans below reuse sh.red with no barrier between
+    sc = finish_scale<kTritThreads>(partials, np, s, s_scale);  // includes a barrier
+    if (threadIdx.x == 0) {
+      ctrl->enc.err = sc.bad;
+      ctrl->enc.scale = sc.M;
+      host_put_result(hm.res, sc.bad, sc.M);
+    }
+  }
+  if (sc.bad) return;  // NaN/Inf or overflow: the buffer keeps its values, no stream
+  const uint32_t cnt = lo < tile_bytes ? umin32(32u, tile_bytes - lo) : 0u;
+  uint4 w[2];
+  uint32_t nz[2];  // non-121 bytes of each half, spread: bit 2i for byte i of the half
+  if (own) {
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      w[hf] = pack_trit_words(d[hf], s_lut);
+      nz[hf] = nonzero_mask_trits(d[hf]);
+    }
+  } else {
+    pack_trits<kTritThreads>(h, n, m, q0, tile_bytes, s_lut, sh.q);
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const uint32_t c = cnt > 16u * hf ? umin32(cnt - 16u * hf, 16u) : 0u;
+      w[hf] = c ? *reinterpret_cast<const uint4*>(sh.q + lo + 16u * hf) : make_uint4(0, 0, 0, 0);
+      nz[hf] = c ? nonzero_mask16_spread(w[hf], c) : 0u;
+    }
+  }
+
+  // ---- Section 3.3 as in tlc_quant_encode_kernel, over the two halves
+  const uint32_t last0 = nz[0] ? lo + (31u - (uint32_t)__builtin_clz(nz[0])) / 2u : 0u;
+  const uint32_t last1 = nz[1] ? lo + 16u + (31u - (uint32_t)__builtin_clz(nz[1])) / 2u : 0u;
+  const bool any = (nz[0] | nz[1]) != 0u;
+  const uint32_t last = nz[1] ? last1 : last0;
+  const ScanU32 pm = block_scan_max_u32<kTritWaves>(any ? last + 1u : 0u, sh.red);
+  const int prev = (int)pm.excl - 1;  // the previous non-121 byte, -1 if none
+  const int prev1 = nz[0] ? (int)last0 : prev;  // the same before the second half
+  const bool tail = any && last + 1u == pm.total;
+  if (any && prev < 0)
+    sh.lead = nz[0] ? lo + (uint32_t)__builtin_ctz(nz[0]) / 2u
+                    : lo + 16u + (uint32_t)__builtin_ctz(nz[1]) / 2u;
+  const uint32_t trail = tile_bytes - pm.total;  // 121s after the last non-121 byte
+  const uint32_t mine = rs_gaps_len<2>(nz[0], lo, prev) + rs_gaps_len<2>(nz[1], lo + 16u, prev1) +
+                        (tail ? trail / kRunMax : 0u);
+  static_assert(sizeof(sh.out) == 32 * kTritThreads + 16, "two uint4 of output per thread, +1");
+  reinterpret_cast<uint4*>(sh.out)[2 * threadIdx.x] = make_uint4(~0u, ~0u, ~0u, ~0u);
+  reinterpret_cast<uint4*>(sh.out)[2 * threadIdx.x + 1] = make_uint4(~0u, ~0u, ~0u, ~0u);
+  if (threadIdx.x == 0)
+    reinterpret_cast<uint4*>(sh.out)[2 * kTritThreads] = make_uint4(~0u, ~0u, ~0u, ~0u);
+  const ScanU32 off = block_scan_u32<kTritWaves>(mine, sh.red2);
+  uint32_t o = off.excl;
+  auto put = [&](uint32_t c) {
+    if (o < sizeof(sh.out)) sh.out[o] = (uint8_t)c;
+    ++o;
+  };
+  auto fill = [&](uint32_t k) { o += k; };
+  {
+    const uint32_t a0 = w[0].x, a1 = w[0].y, a2 = w[0].z, a3 = w[0].w;
+    rs_gaps_emit<2>(nz[0], lo, prev,
+                    [a0, a1, a2, a3](uint32_t i) { return byte_of16(a0, a1, a2, a3, i); }, put,
+                    fill);
+    const uint32_t b0 = w[1].x, b1 = w[1].y, b2 = w[1].z, b3 = w[1].w;
+    rs_gaps_emit<2>(nz[1], lo + 16u, prev1,
+                    [b0, b1, b2, b3](uint32_t i) { return byte_of16(b0, b1, b2, b3, i); }, put,
+                    fill);
+  }
+  // the slot holds at most the tile's own bytes; the clamp only keeps a
+  // logic error inside the slot
+  const uint32_t len = umin32(off.total, tile_bytes);
+  __syncthreads();
+  for (uint32_t i = 16u * threadIdx.x; i < len; i += 16u * kTritThreads)
+    *reinterpret_cast<uint4*>(slots + q0 + i) = *reinterpret_cast<const uint4*>(sh.out + i);
+  if (threadIdx.x == 0) {
+    TileRec rec;
+    if (pm.total == 0u) {  // all 121: one run
+      rec.agg = rs_zero_run(tile_bytes).v;
+      rec.lead = (uint16_t)tile_bytes;
+      rec.len = 0u;
+    } else {
+      rec.agg = rs_combine(rs_zero_run(sh.lead), rs_make(0u, 0u, trail % kRunMax, off.total)).v;
+      rec.lead = (uint16_t)sh.lead;
+      rec.len = (uint16_t)len;
+    }
+    rec.nfix = 0u;
     recs[t] = rec;
   }
 }
@@ -1297,7 +1452,11 @@ hipError_t launch_quant_encode(float* r, uint64_t n, uint32_t m, float s,
 #define TLC_ARGS r, n, m, s, partials, npartials, slots, recs, fix, summ, ctrl, hm
   if (trit) {
     if (!summ) return hipErrorInvalidValue;
-    launch_k(tlc_quant_encode_kernel<kPathVec, true>, ntiles, kThreads, st, TLC_ARGS);
+    if (ntiles >= kTritTwoWaveMinTiles)
+      launch_k(tlc_quant_encode_trits_kernel, ntiles, kTritThreads, st, n, m, s, partials,
+          npartials, slots, recs, reinterpret_cast<const uint8_t*>(summ), ctrl, hm);
+    else
+      launch_k(tlc_quant_encode_kernel<kPathVec, true>, ntiles, kThreads, st, TLC_ARGS);
   } else if (al && m % 4 == 0) {
     launch_k(tlc_quant_encode_kernel<kPathVec>, ntiles, kThreads, st, TLC_ARGS);
   } else {

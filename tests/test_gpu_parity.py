@@ -210,6 +210,35 @@ def test_three_pass_encoder_patterns(ctx, n):
     g.log(f"three-pass patterns n={n} ok")
 
 
+# at least 8192 encode tiles (the first pass then runs two waves per tile,
+# 32 quartic bytes per thread): m % 4 = 1, 3 and 2, partial last tiles,
+# padding of 2 and 4 values and none
+TWO_WAVE_N = [5 * (4096 * 8192 + 1) - 2, 5 * (4096 * 8200 + 3) - 4, 5 * (4096 * 8192 + 2)]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n", TWO_WAVE_N)
+def test_first_pass_two_waves_per_tile(ctx, n):
+    m = (n + 4) // 5
+    g = G()
+    # non-zero groups at tile edges and at the edges of each thread's two
+    # 16-byte halves, in every partition
+    rng = np.random.default_rng(n % 997)
+    x = np.zeros(n, F32)
+    js = [4096 * t + d for t in range(0, m // 4096, 97) for d in (0, 15, 16, 17, 31, 32, 4095)]
+    js += list(rng.integers(0, m, 2000))
+    js = np.unique([j for j in js if 0 <= j < m])
+    for k in range(5):
+        e = k * m + js
+        x[e[e < n]] = F32(1.0 if k % 2 else -1.0)
+    check_encode_decode(ctx, x, np.zeros(n, F32), 1.0, tag=f"two-wave spikes n={n}")
+    x = workloads.runs_tensor([54, n], n)
+    r = workloads.normal([55, n], n, 1e-4)
+    check_encode_decode(ctx, x, r, 1.5, out0=workloads.normal([56, n], n), accumulate=True,
+                        tag=f"two-wave runs n={n}")
+    g.log(f"two-wave first pass n={n} ok")
+
+
 @pytest.mark.parametrize("offset", [1, 2, 3])
 def test_unaligned_pointers(ctx, offset):
     """Tensors that are not 16-byte aligned take the scalar kernels."""
