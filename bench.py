@@ -44,6 +44,7 @@ def algorithmic_bytes(n, c, nnz):
         # read x, r; write the residual r = acc - M*q and one byte of 2-bit
         # trits (q + 1) per float4 for the quartic pack
         "tlc_accum_quantize_kernel": 12 * n + n // 4,
+        # the first pass (tlc_quant_encode_trits_kernel from 8192 tiles on):
         # read the trits; write each tile's own stream bytes (c in all) and
         # its 16-byte record
         "tlc_quant_encode_kernel": n // 4 + c + 16 * tiles,
